@@ -1,0 +1,310 @@
+"""Plain fp64 CPU oracle for one Simple Recurrent Unit (SRU) layer.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this module: only the test suite, the smoke check and the CPU-baseline
+leg of the benchmark use it.  It shares no code with the HIP library and
+imports nothing from the product package.
+
+What it computes (Lei et al., "Simple Recurrent Units for Highly
+Parallelizable Recurrence", Sec. 2, Eq. 1-4):
+
+    f_t = sigma(W_f x_t + v_f * c_{t-1} + b_f)          (Eq. 1)
+    c_t = f_t * c_{t-1} + (1 - f_t) * (W x_t)            (Eq. 2)
+    r_t = sigma(W_r x_t + v_r * c_{t-1} + b_r)          (Eq. 3)
+    h_t = r_t * c_t + (1 - r_t) * x_t                    (Eq. 4)
+
+The forward pass is the plain per-step definition (the "naive
+implementation" of Sec. 2.1 that evaluates Eq. 1-4 one step at a time, with
+the projections x_t W^T computed inside the time loop).  The batched
+reorganisation of Sec. 2.1 (one matrix product for all steps, then the fused
+element-wise loop of Algorithm 1) is what the GPU path implements; the oracle
+does NOT assume it, and the test suite checks the two organisations agree.
+
+Readings of the paper taken here (each is also listed in the design notes):
+  * The reset gate uses c_{t-1}, as Eq. 3 writes it (Algorithm 1 evaluates r
+    after updating c; Eq. 3 is taken as the definition).
+  * Highway scaling alpha = 1 (Eq. 4 as printed, no scaling correction).
+  * "b_v" after Eq. 4 is read as b_r.
+  * When d_in != d, Eq. 4 has no x_t of width d; the highway term uses a
+    fourth learned block W_h (x_hat = W_h x_t), stored as projection block 3.
+    With d_in == d, x_hat = x_t and there are k = 3 blocks.
+  * Padding: a padded step (t, b) leaves c unchanged and outputs h = 0; its
+    upstream gradient is ignored and it contributes no parameter gradient.
+  * Bidirectional: the two directions are independent layers (own W, v, b,
+    c0); the reverse one visits t = L-1 .. 0.  Features are concatenated
+    [forward | reverse].
+  * bf16 GEMM mode rounds the operands of the three matrix products (and only
+    those) to bfloat16, round-to-nearest-even; state and gates stay wide.
+
+The backward pass is not in the paper (training by back-propagation is
+implied by the optimisers of Sec. 4).  It is the chain rule of Eq. 1-4 taken
+in reverse step order; the formulas are derived in the design notes and
+pinned by finite differences in the tests.
+
+Shapes (row-major, same as the C ABI):
+  X   [L, B, d_in]           W  [ndir, k, d, d_in]
+  v_f, v_r, b_f, b_r [ndir, d]
+  c0, c_last, dc0, dc_last [B, ndir*d]
+  U   [L, B, ndir, k, d]     H, C, dH [L, B, ndir*d]
+  pad_mask [L, B] (nonzero = padded) or None
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+DIR_FWD, DIR_REV, DIR_BI = 0, 1, 2
+GEMM_FP32, GEMM_BF16 = 0, 1
+
+
+def _f64(a):
+    return None if a is None else np.asarray(a, dtype=np.float64)
+
+
+def bf16_round(a):
+    """Round to the nearest bfloat16 value (ties to even), returned as fp64.
+
+    A bfloat16 keeps the top 16 bits of an IEEE binary32.  The value is first
+    rounded to binary32 (the GPU rounds fp32 values), then the low 16 bits are
+    rounded away: add 0x7FFF plus the lowest kept bit, truncate.  NaN inputs
+    stay NaN; +-Inf stay Inf.
+    """
+    a32 = np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+    bits = a32.view(np.uint32).astype(np.uint64)
+    lsb = (bits >> 16) & 1
+    rounded = ((bits + 0x7FFF + lsb) >> 16) << 16
+    nan = np.isnan(a32)
+    rounded = np.where(nan, bits | 0x00400000, rounded)  # keep NaN quiet NaN
+    out = (rounded & 0xFFFFFFFF).astype(np.uint32).view(np.float32)
+    return out.astype(np.float64)
+
+
+def sigmoid(z):
+    """Logistic function 1 / (1 + e^{-z}) in fp64 (Eq. 1 and 3)."""
+    with np.errstate(over="ignore"):
+        return 1.0 / (1.0 + np.exp(-z))
+
+
+def _ndir(direction):
+    if direction not in (DIR_FWD, DIR_REV, DIR_BI):
+        raise ValueError(f"unknown direction {direction}")
+    return 2 if direction == DIR_BI else 1
+
+
+def _is_reverse(direction, dirn):
+    return direction == DIR_REV or (direction == DIR_BI and dirn == 1)
+
+
+def _check_shapes(X, W, direction):
+    L, B, d_in = X.shape
+    ndir, k, d, d_in_w = W.shape
+    if ndir != _ndir(direction):
+        raise ValueError("W's first axis must be the number of directions")
+    if d_in_w != d_in:
+        raise ValueError("W's last axis must be d_in")
+    want_k = 3 if d_in == d else 4
+    if k != want_k:
+        raise ValueError(f"k must be {want_k} for d_in={d_in}, d={d}")
+    return L, B, d_in, ndir, k, d
+
+
+def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
+            pad_mask=None, gemm_dtype=GEMM_FP32):
+    """Eq. 1-4 evaluated step by step; returns dict(U, H, C, c_last).
+
+    U holds the per-step projections x_t W^T (one block per gate), assembled
+    in the [L, B, ndir, k, d] layout so that it can be compared with the
+    batched projection.
+    """
+    X = _f64(X)
+    W = _f64(W)
+    L, B, d_in, ndir, k, d = _check_shapes(X, W, direction)
+    v_f, v_r, b_f, b_r = (_f64(a).reshape(ndir, d) for a in (v_f, v_r, b_f, b_r))
+    c0 = np.zeros((B, ndir, d)) if c0 is None else _f64(c0).reshape(B, ndir, d)
+    pad = np.zeros((L, B), bool) if pad_mask is None else (np.asarray(pad_mask) != 0)
+    bf16 = gemm_dtype == GEMM_BF16
+    Wp = bf16_round(W) if bf16 else W
+
+    U = np.zeros((L, B, ndir, k, d))
+    H = np.zeros((L, B, ndir, d))
+    C = np.zeros((L, B, ndir, d))
+    c_last = np.zeros((B, ndir, d))
+    for dirn in range(ndir):
+        steps = range(L - 1, -1, -1) if _is_reverse(direction, dirn) else range(L)
+        c = c0[:, dirn].copy()
+        for t in steps:
+            x_t = X[t]
+            xp = bf16_round(x_t) if bf16 else x_t
+            u = [xp @ Wp[dirn, q].T for q in range(k)]          # W x_t, W_f x_t, ...
+            x_hat = x_t if k == 3 else u[3]
+            f = sigmoid(u[1] + v_f[dirn] * c + b_f[dirn])        # Eq. 1
+            r = sigmoid(u[2] + v_r[dirn] * c + b_r[dirn])        # Eq. 3 (old c)
+            c_new = f * c + (1.0 - f) * u[0]                      # Eq. 2
+            h = r * c_new + (1.0 - r) * x_hat                     # Eq. 4
+            valid = ~pad[t][:, None]
+            c = np.where(valid, c_new, c)
+            H[t, :, dirn] = np.where(valid, h, 0.0)
+            C[t, :, dirn] = c
+            U[t, :, dirn] = np.stack(u, axis=1)
+        c_last[:, dirn] = c
+    return dict(U=U, H=H.reshape(L, B, ndir * d), C=C.reshape(L, B, ndir * d),
+                c_last=c_last.reshape(B, ndir * d))
+
+
+def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
+             pad_mask=None, gemm_dtype=GEMM_FP32, dc_last=None):
+    """Reverse-step chain rule of Eq. 1-4.
+
+    Returns dict(dX, dW, dv_f, dv_r, db_f, db_r, dc0, dU, dxh) where dU is
+    the gradient with respect to the projections ([L, B, ndir, k, d]) and dxh
+    the gradient reaching x_hat through the highway skip term (zeros when
+    k = 4, where it is part of dU block 3).  The forward states are
+    recomputed here by `forward` on the same inputs.
+    """
+    X = _f64(X)
+    W = _f64(W)
+    L, B, d_in, ndir, k, d = _check_shapes(X, W, direction)
+    v_f, v_r, b_f, b_r = (_f64(a).reshape(ndir, d) for a in (v_f, v_r, b_f, b_r))
+    c0_ = np.zeros((B, ndir, d)) if c0 is None else _f64(c0).reshape(B, ndir, d)
+    pad = np.zeros((L, B), bool) if pad_mask is None else (np.asarray(pad_mask) != 0)
+    dH = _f64(dH).reshape(L, B, ndir, d)
+    g_init = np.zeros((B, ndir, d)) if dc_last is None else _f64(dc_last).reshape(B, ndir, d)
+    bf16 = gemm_dtype == GEMM_BF16
+
+    fw = forward(X, W, v_f, v_r, b_f, b_r, c0_.reshape(B, ndir * d), direction,
+                 pad_mask, gemm_dtype)
+    U = fw["U"]
+    C = fw["C"].reshape(L, B, ndir, d)
+    Wp = bf16_round(W) if bf16 else W
+
+    dU = np.zeros((L, B, ndir, k, d))
+    dxh = np.zeros((L, B, ndir, d))
+    dX = np.zeros((L, B, d_in))
+    dW = np.zeros((ndir, k, d, d_in))
+    dv_f = np.zeros((ndir, d))
+    dv_r = np.zeros((ndir, d))
+    db_f = np.zeros((ndir, d))
+    db_r = np.zeros((ndir, d))
+    dc0 = np.zeros((B, ndir, d))
+
+    for dirn in range(ndir):
+        rev = _is_reverse(direction, dirn)
+        fwd_steps = list(range(L - 1, -1, -1)) if rev else list(range(L))
+        g = g_init[:, dirn].copy()                     # dloss/dc_t from later steps
+        for pos in range(L - 1, -1, -1):               # reverse of the forward order
+            t = fwd_steps[pos]
+            c_p = C[fwd_steps[pos - 1], :, dirn] if pos > 0 else c0_[:, dirn]
+            c_t = C[t, :, dirn]
+            u0, u1, u2 = U[t, :, dirn, 0], U[t, :, dirn, 1], U[t, :, dirn, 2]
+            x_hat = X[t] if k == 3 else U[t, :, dirn, 3]
+            valid = ~pad[t][:, None]
+            dh = np.where(valid, dH[t, :, dirn], 0.0)
+
+            f = sigmoid(u1 + v_f[dirn] * c_p + b_f[dirn])
+            r = sigmoid(u2 + v_r[dirn] * c_p + b_r[dirn])
+            gc = g + dh * r                            # dh/dc_t = r
+            dr = dh * (c_t - x_hat) * r * (1.0 - r)    # through r's pre-activation
+            df = gc * (c_p - u0) * f * (1.0 - f)       # through f's pre-activation
+            du0 = gc * (1.0 - f)
+            dxhat = dh * (1.0 - r)
+            df = np.where(valid, df, 0.0)
+            dr = np.where(valid, dr, 0.0)
+            du0 = np.where(valid, du0, 0.0)
+            dxhat = np.where(valid, dxhat, 0.0)
+
+            dU[t, :, dirn, 0] = du0
+            dU[t, :, dirn, 1] = df
+            dU[t, :, dirn, 2] = dr
+            if k == 3:
+                dxh[t, :, dirn] = dxhat
+            else:
+                dU[t, :, dirn, 3] = dxhat
+            dv_f[dirn] += (df * c_p).sum(axis=0)
+            dv_r[dirn] += (dr * c_p).sum(axis=0)
+            db_f[dirn] += df.sum(axis=0)
+            db_r[dirn] += dr.sum(axis=0)
+            g_prev = gc * f + df * v_f[dirn] + dr * v_r[dirn]
+            g = np.where(valid, g_prev, g)             # padded step: identity on c
+
+            # Projections: dX gets dU_t W, dW gets dU_t^T x_t (per step).
+            x_t = X[t]
+            du_t = dU[t, :, dirn]                      # [B, k, d]
+            du_p = bf16_round(du_t) if bf16 else du_t
+            xp = bf16_round(x_t) if bf16 else x_t
+            for q in range(k):
+                dX[t] += du_p[:, q] @ Wp[dirn, q]
+                dW[dirn, q] += du_p[:, q].T @ xp
+            if k == 3:
+                dX[t] += dxh[t, :, dirn]
+        dc0[:, dirn] = g
+    return dict(dX=dX, dW=dW, dv_f=dv_f, dv_r=dv_r, db_f=db_f, db_r=db_r,
+                dc0=dc0.reshape(B, ndir * d), dU=dU, dxh=dxh)
+
+
+def forward_alg1_scalar(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
+                        pad_mask=None):
+    """Tiny-shape cross-check in the shape of Algorithm 1 (fp32 GEMM mode).
+
+    The projections for all steps come first as one batched product (Sec. 2.1),
+    then independent scalar recurrences run per (example i, dimension j),
+    reading the gate columns at offsets j, j+d, j+2d of the batched tensor.
+    The reset gate uses the previous state (Eq. 3 reading).  Pure Python loops:
+    only for tiny shapes.
+    """
+    X = _f64(X)
+    W = _f64(W)
+    L, B, d_in, ndir, k, d = _check_shapes(X, W, direction)
+    v_f, v_r, b_f, b_r = (_f64(a).reshape(ndir, d) for a in (v_f, v_r, b_f, b_r))
+    c0 = np.zeros((B, ndir, d)) if c0 is None else _f64(c0).reshape(B, ndir, d)
+    pad = np.zeros((L, B), bool) if pad_mask is None else (np.asarray(pad_mask) != 0)
+    # Batched projection: rows (dir, block, j) of the stacked weight.
+    Wcat = W.reshape(ndir * k * d, d_in)
+    Ub = (X.reshape(L * B, d_in) @ Wcat.T).reshape(L, B, ndir, k * d)
+    H = np.zeros((L, B, ndir, d))
+    C = np.zeros((L, B, ndir, d))
+    for dirn in range(ndir):
+        steps = range(L - 1, -1, -1) if _is_reverse(direction, dirn) else range(L)
+        for i in range(B):
+            for j in range(d):
+                c = float(c0[i, dirn, j])
+                for l in steps:
+                    if pad[l, i]:
+                        C[l, i, dirn, j] = c
+                        continue
+                    u = Ub[l, i, dirn]
+                    f = float(sigmoid(u[j + d] + v_f[dirn, j] * c + b_f[dirn, j]))
+                    r = float(sigmoid(u[j + 2 * d] + v_r[dirn, j] * c + b_r[dirn, j]))
+                    c = f * c + (1.0 - f) * u[j]
+                    xh = X[l, i, j] if k == 3 else u[j + 3 * d]
+                    H[l, i, dirn, j] = r * c + (1.0 - r) * xh
+                    C[l, i, dirn, j] = c
+    return dict(H=H.reshape(L, B, ndir * d), C=C.reshape(L, B, ndir * d))
+
+
+def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
+                           need_backward=True):
+    """Stacked layers: layer l+1 takes layer l's H as its X.
+
+    `layers` is a list of dicts with W, v_f, v_r, b_f, b_r (c0 = 0).
+    Returns dict(Hs=[H per layer], Cs=[...], Us=[...], grads=[per-layer
+    backward dicts, bottom first]) ; grads is empty without backward.
+    """
+    xs = [np.asarray(X, np.float64)]
+    fws = []
+    for p in layers:
+        fw = forward(xs[-1], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], None,
+                     direction, pad_mask, gemm_dtype)
+        fws.append(fw)
+        xs.append(fw["H"])
+    grads = []
+    if need_backward:
+        g = np.asarray(dH_top, np.float64)
+        for li in range(len(layers) - 1, -1, -1):
+            p = layers[li]
+            bw = backward(xs[li], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], g,
+                          None, direction, pad_mask, gemm_dtype)
+            grads.append(bw)
+            g = bw["dX"]
+        grads.reverse()
+    return dict(Hs=[fw["H"] for fw in fws], Cs=[fw["C"] for fw in fws],
+                Us=[fw["U"] for fw in fws], grads=grads, xs=xs)
