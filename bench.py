@@ -1,0 +1,291 @@
+#!/usr/bin/env python3
+"""Throughput of the SRU layer stack (forward + backward) on one MI355X.
+
+Workload: 6 stacked unidirectional SRU layers, L = 256 steps, B = 64
+sequences, d_in = d = 1024, bf16-input / fp32-accumulate matrix products,
+fp32 scans, synthetic inputs (seeded; the paper's datasets are not used).
+One step = forward through all 6 layers, then backward through all 6
+(including dX of the first layer).  Metric: tokens/s = L*B / step time.
+
+Besides the headline number the JSON line carries
+  * roofline: the kernel that takes the most time per step, its algorithmic
+    bytes or flops per launch over its average duration (HIP events recorded
+    by the library around every launch, on the launch stream), against the
+    MI355X peak;
+  * scan_hbm: the same for both scan kernels (the metric's second half);
+  * cpu_baseline: the fp64 CPU oracle timed on a bounded sample of the same
+    workload on this host.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+
+from __future__ import annotations
+
+import argparse
+import ctypes
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------ HIP events
+class HipEvents:
+    """A pool of HIP events created through the HIP runtime torch has loaded."""
+
+    def __init__(self, n):
+        path = None
+        for line in open("/proc/self/maps"):
+            if "libamdhip64" in line:
+                path = line.split()[-1]
+                break
+        if path is None:
+            raise RuntimeError("HIP runtime not loaded")
+        h = ctypes.CDLL(path)
+        h.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                          ctypes.c_void_p]
+        h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.h = h
+        self.events = (ctypes.c_void_p * n)()
+        for i in range(n):
+            ev = ctypes.c_void_p()
+            if h.hipEventCreate(ctypes.byref(ev)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.events[i] = ev
+        self.n = n
+
+    def elapsed_ms(self, i, j):
+        ms = ctypes.c_float()
+        rc = self.h.hipEventElapsedTime(ctypes.byref(ms), self.events[i], self.events[j])
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return ms.value
+
+    def close(self):
+        for i in range(self.n):
+            self.h.hipEventDestroy(self.events[i])
+
+
+# ------------------------------------------------------------------ work model
+def kernel_work(w, splits):
+    """Algorithmic bytes / flops per launch of each kernel at workload w
+    (first layer shape; all layers of a unidirectional d_in = d stack match).
+    Bytes count each element read or written once (4 B fp32)."""
+    M = w.L * w.B
+    nfeat = w.ndir * w.d
+    k = 3
+    N = w.ndir * k * w.d
+    K = w.d_in
+    elems = M * nfeat
+    return {
+        "gemm_nt": dict(flops=2.0 * M * N * K),
+        "gemm_nn": dict(flops=2.0 * M * K * N),
+        "gemm_tn": dict(flops=2.0 * N * K * M),
+        # read U (3 blocks) and x, write h and c: 24 B per (t, b, j)
+        "scan_fwd": dict(bytes=elems * 4.0 * (k + 1 + 2)),
+        # read U (3 blocks), x, c, dh; write dU (3 blocks), dx_hat: 40 B
+        "scan_bwd": dict(bytes=elems * 4.0 * (k + 3 + k + 1)),
+        "reduce_vb": dict(bytes=4.0 * (4 * w.B * nfeat + 4 * nfeat)),
+        "splitk_reduce": dict(bytes=4.0 * (splits + 1) * N * K),
+    }
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_1709_02755_amd", "csrc", "*"))):
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def pmc_traffic(label):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    it was taken on the current kernel sources; else None."""
+    p = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+    if not os.path.exists(p):
+        return None
+    d = json.load(open(p))
+    if d.get("source_hash") != source_hash():
+        return None
+    k = d.get("kernels", {}).get(label)
+    return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+# ------------------------------------------------------------------ CPU oracle
+def cpu_baseline(w, inp, nseq):
+    """The fp64 oracle (test infrastructure, never the product path) on the
+    first `nseq` sequences of the same inputs: full stack forward + backward."""
+    from oracle import sru_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info()
+                       if i.get("user_api") == "blas"), default=1)
+    except Exception:  # threadpoolctl missing: report the affinity set
+        threads = len(os.sched_getaffinity(0))
+    sl = slice(0, nseq)
+    X = inp["X"][:, sl]
+    mask = None if inp["mask"] is None else inp["mask"][:, sl]
+    t0 = time.perf_counter()
+    O.stack_forward_backward(X, inp["layers"], w.direction, mask, w.gemm_dtype,
+                             inp["dH"][:, sl], need_backward=True)
+    secs = time.perf_counter() - t0
+    tokens = w.L * nseq
+    return {"value": tokens / secs, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "seconds": secs,
+            "sample": f"{w.layers}-layer fwd+bwd stack on {nseq} of {w.B} sequences "
+                      f"({tokens} tokens), fp64 NumPy, per-step projections"}
+
+
+# ------------------------------------------------------------------ main
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=3, help="index into the workload table")
+    ap.add_argument("--profile-steps", type=int, default=5,
+                    help="steps run with per-kernel event brackets")
+    ap.add_argument("--cpu-seqs", type=int, default=2,
+                    help="sequences in the CPU-oracle sample (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1709_02755_amd import sru
+    from paper_1709_02755_amd.workloads import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    log(f"workload {w.name}: L={w.L} B={w.B} d_in={w.d_in} d={w.d} layers={w.layers}")
+    inp = make_inputs(w)
+    dev = torch.device("cuda:0")
+    to = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    layers = [{k: to(v) for k, v in p.items()} for p in inp["layers"]]
+    X, dH, mask = to(inp["X"]), to(inp["dH"]), to(inp["mask"])
+    st = sru.Stack(layers, w.L, w.B, w.d_in, w.d, w.direction, w.gemm_dtype, dev,
+                   backward=w.backward)
+
+    def step():
+        st.forward(X, mask)
+        st.backward(X, dH, mask)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} done")
+
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    secs = time.perf_counter() - t0
+    ms_per_step = 1e3 * secs / args.steps
+    tokens_per_s = w.tokens * args.steps / secs
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {tokens_per_s:.4g} tokens/s")
+
+    # --- per-kernel durations: the library brackets each launch with events
+    per_step = w.layers * (2 + 5)
+    ev = HipEvents(2 * per_step * args.profile_steps + 2)
+    lib = sru.lib()
+    lib.sru_timing_begin(ev.events, ev.n)
+    try:
+        for _ in range(args.profile_steps):
+            step()
+    finally:
+        nk = lib.sru_timing_end()
+    torch.cuda.synchronize()
+    agg = {}
+    for i in range(nk):
+        lab = lib.sru_timing_label(i).decode()
+        ms = ev.elapsed_ms(2 * i, 2 * i + 1)
+        a = agg.setdefault(lab, [0.0, 0])
+        a[0] += ms
+        a[1] += 1
+    ev.close()
+    splits = 1
+    if w.backward:
+        ws_k = lib.sru_gemm_workspace_bytes(sru.OP_TN, w.ndir * 3 * w.d, w.d_in, w.tokens,
+                                            w.gemm_dtype)
+        splits = max(1, ws_k // (4 * w.ndir * 3 * w.d * w.d_in))
+    work = kernel_work(w, splits)
+    gemm_peak = MFMA_PEAK_TFLOPS["bf16" if w.gemm_dtype == sru.GEMM_BF16 else "fp32"]
+    kernels = {}
+    for lab, (tot, cnt) in agg.items():
+        avg_ms = tot / cnt
+        wk = work.get(lab, {})
+        row = {"avg_us": round(avg_ms * 1e3, 2), "launches_per_step": cnt // args.profile_steps,
+               "ms_per_step": round(tot / args.profile_steps, 4)}
+        if "flops" in wk:
+            tf = wk["flops"] / (avg_ms * 1e-3) / 1e12
+            row.update(bound="mfma", achieved=round(tf, 1), unit="TFLOP/s", peak=gemm_peak,
+                       frac=round(tf / gemm_peak, 4), algorithmic=wk["flops"])
+        elif "bytes" in wk:
+            gbps = wk["bytes"] / (avg_ms * 1e-3) / 1e9
+            row.update(bound="hbm", achieved=round(gbps, 1), unit="GB/s", peak=HBM_PEAK_GBPS,
+                       frac=round(gbps / HBM_PEAK_GBPS, 4), algorithmic=wk["bytes"])
+        kernels[lab] = row
+    dominant = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    d = kernels[dominant]
+    roofline = {"kernel": dominant, "bound": d.get("bound"), "achieved": d.get("achieved"),
+                "peak": d.get("peak"), "unit": d.get("unit"), "frac": d.get("frac"),
+                "avg_us": d["avg_us"], "traffic": pmc_traffic(dominant)}
+    scan_hbm = {k: {"GBps": kernels[k]["achieved"], "frac": kernels[k]["frac"],
+                    "avg_us": kernels[k]["avg_us"], "traffic": pmc_traffic(k)}
+                for k in ("scan_fwd", "scan_bwd") if k in kernels}
+    for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
+        log(f"  {k:14s} {v['avg_us']:9.2f} us x{v['launches_per_step']}  "
+            f"{v.get('achieved', '-')} {v.get('unit', '')} ({v.get('frac', '-')})")
+
+    cpu = None
+    if args.cpu_seqs > 0:
+        log(f"cpu oracle on {args.cpu_seqs} sequences ...")
+        cpu = cpu_baseline(w, inp, args.cpu_seqs)
+        log(f"cpu oracle: {cpu['value']:.4g} tokens/s in {cpu['seconds']:.1f} s "
+            f"({cpu['cores']} threads)")
+
+    out = {
+        "metric": "SRU fwd+bwd tokens/s at L256 B64 d1024; scan-kernel HBM GB/s % of peak",
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": w.layers, "L": w.L, "B": w.B,
+                   "d_in": w.d_in, "d": w.d,
+                   "direction": ["forward", "reverse", "bidirectional"][w.direction],
+                   "passes": "fwd+bwd" if w.backward else "fwd",
+                   "gemm": "bf16 operands, fp32 accumulate" if w.gemm_dtype else "fp32",
+                   "scan": "fp32", "tokens_per_step": w.tokens, "global_batch": w.B,
+                   "seq_len": w.L, "parallelism": "single GPU"},
+        "roofline": roofline,
+        "scan_hbm": scan_hbm,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

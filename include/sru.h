@@ -1,0 +1,198 @@
+/*
+ * sru.h -- C ABI of libsru.so, an MI355X (gfx950) implementation of one
+ * Simple Recurrent Unit layer (Lei et al., "Simple Recurrent Units for Highly
+ * Parallelizable Recurrence", EMNLP 2018).
+ *
+ * The layer (Sec. 2, Eq. 1-4), per direction, for t in the direction's order:
+ *   f_t = sigma(W_f x_t + v_f * c_{t-1} + b_f)
+ *   c_t = f_t * c_{t-1} + (1 - f_t) * (W x_t)
+ *   r_t = sigma(W_r x_t + v_r * c_{t-1} + b_r)
+ *   h_t = r_t * c_t + (1 - r_t) * x_hat_t
+ * computed as in Sec. 2.1: one matrix product U = X [W; W_f; W_r]^T over all
+ * L*B tokens, then one fused element-wise scan, parallel over (batch, hidden
+ * unit, direction) and sequential over t (Algorithm 1).  The reset gate reads
+ * c_{t-1} as Eq. 3 writes it.
+ *
+ * x_hat: when d_in == d there are k = 3 weight blocks and x_hat_t = x_t
+ * (Eq. 4).  When d_in != d, Eq. 4 is undefined; a fourth block W_h supplies
+ * x_hat_t = W_h x_t (k = 4).  k is implied by (d_in, d).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Layout: row-major, contiguous, fp32 unless stated.  ndir = 2 for
+ *   SRU_DIR_BI, else 1.  M = L*B tokens, N = ndir*k*d projection columns.
+ *     X        [L, B, d_in]
+ *     W        [ndir, k, d, d_in]   (block order W, W_f, W_r[, W_h])
+ *     v_f, v_r, b_f, b_r            [ndir, d]
+ *     c0, c_last, dc0, dc_last      [B, ndir*d]
+ *     U        [L, B, ndir, k, d]   (= [M, N], the batched projection)
+ *     H, C, dH [L, B, ndir*d]       (features: forward direction first)
+ *     pad_mask [L, B] uint8, nonzero = padded position, or NULL (no padding)
+ *   A padded (t, b) leaves c unchanged and writes h = 0 (C holds the carried
+ *   state there); its dH is ignored and it adds nothing to any gradient.
+ *   SRU_DIR_REV and the second half of SRU_DIR_BI visit t = L-1 .. 0.
+ * Memory: every pointer is caller-owned DEVICE memory except where stated;
+ *   inputs and outputs must not alias.  The library never allocates, frees
+ *   or synchronises; the caller supplies a workspace of at least the queried
+ *   size (device memory, any contents, 256-byte aligned) and a stream.
+ * Precision: the ABI is fp32.  SRU_GEMM_BF16 rounds the operands of the
+ *   matrix products (X and W for U; dU and W for dX; dU and X for dW) to
+ *   bfloat16, round-to-nearest-even, accumulating in fp32.  The scan (state,
+ *   gates, highway term) is fp32 in both modes.
+ * Errors: every function returns an sru_status.  All arguments are checked
+ *   before anything is enqueued; on error nothing is enqueued and no output
+ *   is touched.  SRU_OK means "enqueued on `stream`": execution errors
+ *   surface at the caller's next synchronisation.  After SRU_E_HIP,
+ *   sru_last_hip_error() returns the hipError_t (per calling thread).
+ * Gradients are overwritten, never accumulated.  Results are deterministic:
+ *   the same inputs give bit-identical outputs (no floating-point atomics).
+ */
+#ifndef SRU_H_
+#define SRU_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#if defined(__GNUC__)
+#define SRU_API __attribute__((visibility("default")))
+#else
+#define SRU_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SRU_OK = 0,
+  SRU_E_NULLPTR = 1,   /* a required pointer is NULL                         */
+  SRU_E_SHAPE = 2,     /* a size is <= 0, too large, or inconsistent         */
+  SRU_E_FLAG = 3,      /* unknown direction / gemm dtype / gemm op           */
+  SRU_E_WORKSPACE = 4, /* workspace NULL or smaller than the queried size    */
+  SRU_E_HIP = 5,       /* a HIP launch failed; see sru_last_hip_error()      */
+  SRU_E_ALIGN = 6      /* a pointer is not 4-byte (fp32) / 256-byte aligned  */
+} sru_status;
+
+typedef enum { SRU_DIR_FWD = 0, SRU_DIR_REV = 1, SRU_DIR_BI = 2 } sru_direction;
+typedef enum { SRU_GEMM_FP32 = 0, SRU_GEMM_BF16 = 1 } sru_gemm_dtype;
+
+/* Human-readable name of a status code (static string, never NULL). */
+SRU_API const char* sru_status_string(int status);
+
+/* hipError_t of the last SRU_E_HIP returned to the calling thread. */
+SRU_API int sru_last_hip_error(void);
+
+/* ABI version: (major << 16) | minor. */
+SRU_API int sru_version(void);
+
+/* Workspace bytes sru_forward / sru_backward need for these sizes (0 means
+ * none; NULL may then be passed).  Returns 0 for invalid arguments as well;
+ * the compute call reports those. */
+SRU_API size_t sru_forward_workspace_bytes(int L, int B, int d_in, int d, int direction,
+                                   int gemm_dtype);
+SRU_API size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int direction,
+                                    int gemm_dtype);
+
+/*
+ * Forward pass of one layer (Sec. 2 Eq. 1-4, organised as Sec. 2.1 /
+ * Algorithm 1).
+ *   in : X, W, v_f, v_r, b_f, b_r; c0 (NULL = zeros); pad_mask (NULL = none)
+ *   out: U [M, N] -- the batched projection, kept by the caller for
+ *        sru_backward;
+ *        H [L, B, ndir*d];
+ *        C [L, B, ndir*d] -- every state c_t, needed by sru_backward
+ *        (NULL = do not store: inference);
+ *        c_last [B, ndir*d] -- state after each sequence's last valid step
+ *        (NULL = do not store).
+ */
+SRU_API int sru_forward(const float* X, const float* W,
+                const float* v_f, const float* v_r, const float* b_f, const float* b_r,
+                const float* c0, int L, int B, int d_in, int d, int direction,
+                const uint8_t* pad_mask, int gemm_dtype,
+                float* U, float* H, float* C, float* c_last,
+                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Backward pass of one layer: the chain rule of Eq. 1-4 taken in reverse
+ * step order (the paper trains by back-propagation but does not state it).
+ *   in : the forward inputs, U and C from sru_forward on those inputs,
+ *        dH [L, B, ndir*d] (gradient of the loss w.r.t. H), dc_last
+ *        [B, ndir*d] (w.r.t. c_last; NULL = zeros).
+ *   out: dX [L, B, d_in], dW [ndir, k, d, d_in], dv_f, dv_r, db_f, db_r
+ *        [ndir, d], dc0 [B, ndir*d] (NULL = do not compute).
+ */
+SRU_API int sru_backward(const float* X, const float* W,
+                 const float* v_f, const float* v_r, const float* b_f, const float* b_r,
+                 const float* c0, int L, int B, int d_in, int d, int direction,
+                 const uint8_t* pad_mask, int gemm_dtype,
+                 const float* U, const float* C, const float* dH, const float* dc_last,
+                 float* dX, float* dW, float* dv_f, float* dv_r, float* db_f, float* db_r,
+                 float* dc0, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Component entry points: the individual steps of the two calls above, with
+ * the same conventions, for testing and per-kernel measurement.
+ * ------------------------------------------------------------------------- */
+
+typedef enum {
+  SRU_OP_NT = 0, /* C[M,N] = A[M,K] * B[N,K]^T   (U = X W^T)     */
+  SRU_OP_NN = 1, /* C[M,N] = A[M,K] * B[K,N]     (dX = dU W)     */
+  SRU_OP_TN = 2  /* C[M,N] = A[K,M]^T * B[K,N]   (dW = dU^T X)   */
+} sru_gemm_op;
+
+/* Matrix product on the MFMA units (the batched projection of Sec. 2.1 and
+ * its two backward products).  Row-major operands with leading dimensions
+ * lda, ldb, ldc (elements).  gemm_dtype as above.  TN may split the
+ * reduction; it then needs sru_gemm_workspace_bytes of workspace. */
+SRU_API size_t sru_gemm_workspace_bytes(int op, int M, int N, int K, int gemm_dtype);
+SRU_API int sru_gemm(int op, int gemm_dtype, int M, int N, int K,
+             const float* A, int lda, const float* B, int ldb, float* C, int ldc,
+             void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* The fused forward scan (Algorithm 1 with the Eq. 3 reading) on a given U.
+ * X is read only when k = 3 (d_in == d).  C and c_last may be NULL. */
+SRU_API int sru_scan_forward(const float* U, const float* X,
+                     const float* v_f, const float* v_r, const float* b_f, const float* b_r,
+                     const float* c0, int L, int B, int d_in, int d, int direction,
+                     const uint8_t* pad_mask, float* H, float* C, float* c_last,
+                     hipStream_t stream);
+
+/* The reverse-time gradient scan on a given U, C, dH.
+ *   out: dU [L, B, ndir, k, d] (gradient w.r.t. the projections; when k = 4
+ *        block 3 holds the highway gradient), dxh [L, B, ndir, d] (highway
+ *        gradient w.r.t. x_t when k = 3; must be NULL when k = 4), dv_f,
+ *        dv_r, db_f, db_r [ndir, d], dc0 (NULL = skip).
+ * Workspace: sru_scan_backward_workspace_bytes. */
+SRU_API size_t sru_scan_backward_workspace_bytes(int L, int B, int d_in, int d, int direction);
+SRU_API int sru_scan_backward(const float* U, const float* X, const float* C, const float* dH,
+                      const float* dc_last,
+                      const float* v_f, const float* v_r, const float* b_f, const float* b_r,
+                      const float* c0, int L, int B, int d_in, int d, int direction,
+                      const uint8_t* pad_mask,
+                      float* dU, float* dxh, float* dv_f, float* dv_r, float* db_f,
+                      float* db_r, float* dc0,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Measurement hook, per calling thread.  sru_timing_begin arms it with
+ * `capacity` events the caller created (hipEventCreate, timing enabled).
+ * Every kernel this thread then enqueues through the calls above is
+ * bracketed by two of them, recorded on the kernel's stream in launch order:
+ * kernel i runs between events[2i] and events[2i+1].  When the events run
+ * out, further kernels are not bracketed.  sru_timing_end disarms the hook
+ * and returns the number of kernels bracketed; sru_timing_label(i) names
+ * kernel i ("gemm_nt", "gemm_nn", "gemm_tn", "splitk_reduce", "scan_fwd",
+ * "scan_bwd", "reduce_vb"; "" out of range) until the next
+ * sru_timing_begin.  The caller owns the events and reads them after
+ * synchronising.  Disarmed (the default), launches record nothing.
+ * ------------------------------------------------------------------------- */
+SRU_API int sru_timing_begin(hipEvent_t* events, int capacity);
+SRU_API int sru_timing_end(void);
+SRU_API const char* sru_timing_label(int i);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SRU_H_ */

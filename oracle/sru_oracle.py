@@ -152,14 +152,14 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
 
 
 def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
-             pad_mask=None, gemm_dtype=GEMM_FP32, dc_last=None):
+             pad_mask=None, gemm_dtype=GEMM_FP32, dc_last=None, fw=None):
     """Reverse-step chain rule of Eq. 1-4.
 
     Returns dict(dX, dW, dv_f, dv_r, db_f, db_r, dc0, dU, dxh) where dU is
     the gradient with respect to the projections ([L, B, ndir, k, d]) and dxh
     the gradient reaching x_hat through the highway skip term (zeros when
-    k = 4, where it is part of dU block 3).  The forward states are
-    recomputed here by `forward` on the same inputs.
+    k = 4, where it is part of dU block 3).  The forward states come from
+    `fw` (the result of `forward` on the same inputs) or are recomputed.
     """
     X = _f64(X)
     W = _f64(W)
@@ -171,8 +171,9 @@ def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
     g_init = np.zeros((B, ndir, d)) if dc_last is None else _f64(dc_last).reshape(B, ndir, d)
     bf16 = gemm_dtype == GEMM_BF16
 
-    fw = forward(X, W, v_f, v_r, b_f, b_r, c0_.reshape(B, ndir * d), direction,
-                 pad_mask, gemm_dtype)
+    if fw is None:
+        fw = forward(X, W, v_f, v_r, b_f, b_r, c0_.reshape(B, ndir * d), direction,
+                     pad_mask, gemm_dtype)
     U = fw["U"]
     C = fw["C"].reshape(L, B, ndir, d)
     Wp = bf16_round(W) if bf16 else W
@@ -302,7 +303,7 @@ def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
         for li in range(len(layers) - 1, -1, -1):
             p = layers[li]
             bw = backward(xs[li], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], g,
-                          None, direction, pad_mask, gemm_dtype)
+                          None, direction, pad_mask, gemm_dtype, fw=fws[li])
             grads.append(bw)
             g = bw["dX"]
         grads.reverse()

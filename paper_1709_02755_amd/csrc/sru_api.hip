@@ -1,0 +1,340 @@
+// C ABI of libsru.so: argument validation, workspace layout and dispatch.
+// Every check runs before anything is enqueued; nothing here allocates,
+// frees or synchronises.
+#include <limits.h>
+
+#include <vector>
+
+#include "../../include/sru.h"
+#include "sru_internal.h"
+
+namespace {
+
+// Per-thread state of the measurement hook.
+struct TimingState {
+  hipEvent_t* events = nullptr;
+  int capacity = 0;  // events available
+  int used = 0;      // events recorded
+  std::vector<const char*> labels;
+};
+thread_local TimingState g_timing;
+
+thread_local int g_last_hip_error = 0;
+
+constexpr size_t kAlign = 256;
+constexpr long long kMaxElems = 1LL << 40;  // per tensor, far beyond any HBM size
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool valid_direction(int d) { return d == SRU_DIR_FWD || d == SRU_DIR_REV || d == SRU_DIR_BI; }
+bool valid_dtype(int t) { return t == SRU_GEMM_FP32 || t == SRU_GEMM_BF16; }
+
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3) == 0; }
+
+struct Dims {
+  int L, B, d_in, d, ndir, k;
+  long long M, N, nfeat;
+};
+
+// Shape checks shared by every layer entry point.  Sizes must be positive,
+// products must fit the 32-bit indices the kernels use for tokens, columns
+// and lanes, and no tensor may exceed kMaxElems elements.
+int make_dims(int L, int B, int d_in, int d, int direction, Dims& s) {
+  if (!valid_direction(direction)) return SRU_E_FLAG;
+  if (L <= 0 || B <= 0 || d_in <= 0 || d <= 0) return SRU_E_SHAPE;
+  s.L = L;
+  s.B = B;
+  s.d_in = d_in;
+  s.d = d;
+  s.ndir = direction == SRU_DIR_BI ? 2 : 1;
+  s.k = d_in == d ? 3 : 4;
+  s.M = (long long)L * B;
+  s.N = (long long)s.ndir * s.k * d;
+  s.nfeat = (long long)s.ndir * d;
+  if (s.M > INT_MAX || s.N > INT_MAX || (long long)B * s.nfeat > INT_MAX) return SRU_E_SHAPE;
+  if (s.M * s.N > kMaxElems || s.M * d_in > kMaxElems) return SRU_E_SHAPE;
+  return SRU_OK;
+}
+
+sru::ScanShape scan_shape(const Dims& s, int direction) {
+  return sru::ScanShape{s.L, s.B, s.d_in, s.d, s.ndir, s.k, direction};
+}
+
+int hip_status(hipError_t e) {
+  if (e == hipSuccess) return SRU_OK;
+  g_last_hip_error = (int)e;
+  return SRU_E_HIP;
+}
+
+sru::GemmDesc gemm_desc(int op, bool bf16, int M, int N, int K, const float* A, long long lda,
+                        const float* B, long long ldb, float* C, long long ldc) {
+  sru::GemmDesc g{};
+  g.A = A;
+  g.B = B;
+  g.C = C;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = ldc;
+  g.a_kc = op != SRU_OP_TN;
+  g.b_kc = op == SRU_OP_NT;
+  g.bf16 = bf16;
+  g.splits = 1;
+  return g;
+}
+
+// Backward workspace layout: [dU | dxh (k = 3) | v/b partials | dW split partials]
+struct BwdLayout {
+  size_t dU, dxh, partial, splitk, total;
+  int splits;
+};
+
+BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
+  BwdLayout w{};
+  size_t off = 0;
+  w.dU = off;
+  off += align_up(sizeof(float) * (size_t)s.M * (size_t)s.N);
+  w.dxh = off;
+  if (s.k == 3) off += align_up(sizeof(float) * (size_t)s.M * (size_t)s.nfeat);
+  w.partial = off;
+  off += align_up(sizeof(float) * 4 * (size_t)s.B * (size_t)s.nfeat);
+  sru::GemmDesc dw = gemm_desc(SRU_OP_TN, gemm_dtype == SRU_GEMM_BF16, (int)s.N, s.d_in, (int)s.M,
+                               nullptr, s.N, nullptr, s.d_in, nullptr, s.d_in);
+  w.splits = sru::gemm_splits(dw);
+  w.splitk = off;
+  off += align_up(sru::gemm_partial_bytes((int)s.N, s.d_in, w.splits));
+  w.total = off;
+  return w;
+}
+
+}  // namespace
+
+namespace sru {
+
+void timing_before(const char* label, hipStream_t stream) {
+  TimingState& t = g_timing;
+  if (!t.events || t.used + 2 > t.capacity) return;
+  hipEventRecord(t.events[t.used++], stream);
+  t.labels.push_back(label);
+}
+
+void timing_after(hipStream_t stream) {
+  TimingState& t = g_timing;
+  // pairs with a timing_before that recorded (used is then odd)
+  if (!t.events || (t.used & 1) == 0) return;
+  hipEventRecord(t.events[t.used++], stream);
+}
+
+}  // namespace sru
+
+extern "C" {
+
+int sru_timing_begin(hipEvent_t* events, int capacity) {
+  if (!events || capacity < 2) return SRU_E_NULLPTR;
+  g_timing.events = events;
+  g_timing.capacity = capacity;
+  g_timing.used = 0;
+  g_timing.labels.clear();
+  return SRU_OK;
+}
+
+int sru_timing_end(void) {
+  const int n = g_timing.used / 2;
+  g_timing.events = nullptr;
+  g_timing.capacity = 0;
+  return n;
+}
+
+const char* sru_timing_label(int i) {
+  if (i < 0 || i >= (int)g_timing.labels.size()) return "";
+  return g_timing.labels[i];
+}
+
+const char* sru_status_string(int status) {
+  switch (status) {
+    case SRU_OK: return "SRU_OK";
+    case SRU_E_NULLPTR: return "SRU_E_NULLPTR: a required pointer is NULL";
+    case SRU_E_SHAPE: return "SRU_E_SHAPE: invalid or inconsistent size";
+    case SRU_E_FLAG: return "SRU_E_FLAG: unknown direction, gemm dtype or gemm op";
+    case SRU_E_WORKSPACE: return "SRU_E_WORKSPACE: workspace missing or too small";
+    case SRU_E_HIP: return "SRU_E_HIP: a HIP launch failed";
+    case SRU_E_ALIGN: return "SRU_E_ALIGN: misaligned pointer";
+    default: return "unknown sru_status";
+  }
+}
+
+int sru_last_hip_error(void) { return g_last_hip_error; }
+
+int sru_version(void) { return (1 << 16) | 0; }
+
+size_t sru_forward_workspace_bytes(int L, int B, int d_in, int d, int direction, int gemm_dtype) {
+  Dims s;
+  if (make_dims(L, B, d_in, d, direction, s) != SRU_OK || !valid_dtype(gemm_dtype)) return 0;
+  return 0;  // the projection writes U directly; the scan needs no scratch
+}
+
+size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int direction,
+                                    int gemm_dtype) {
+  Dims s;
+  if (make_dims(L, B, d_in, d, direction, s) != SRU_OK || !valid_dtype(gemm_dtype)) return 0;
+  return bwd_layout(s, gemm_dtype).total;
+}
+
+int sru_forward(const float* X, const float* W, const float* v_f, const float* v_r,
+                const float* b_f, const float* b_r, const float* c0, int L, int B, int d_in,
+                int d, int direction, const uint8_t* pad_mask, int gemm_dtype, float* U,
+                float* H, float* C, float* c_last, void* workspace, size_t workspace_bytes,
+                hipStream_t stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  Dims s;
+  int st = make_dims(L, B, d_in, d, direction, s);
+  if (st != SRU_OK) return st;
+  if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
+  if (!X || !W || !v_f || !v_r || !b_f || !b_r || !U || !H) return SRU_E_NULLPTR;
+  const void* ptrs[] = {X, W, v_f, v_r, b_f, b_r, c0, U, H, C, c_last};
+  for (const void* p : ptrs)
+    if (p && !aligned4(p)) return SRU_E_ALIGN;
+
+  sru::GemmDesc g = gemm_desc(SRU_OP_NT, gemm_dtype == SRU_GEMM_BF16, (int)s.M, (int)s.N, d_in, X,
+                              d_in, W, d_in, U, s.N);
+  if (int e = hip_status(sru::gemm_launch(g, stream))) return e;
+
+  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last};
+  return hip_status(sru::scan_forward_launch(scan_shape(s, direction), a, stream));
+}
+
+int sru_backward(const float* X, const float* W, const float* v_f, const float* v_r,
+                 const float* b_f, const float* b_r, const float* c0, int L, int B, int d_in,
+                 int d, int direction, const uint8_t* pad_mask, int gemm_dtype, const float* U,
+                 const float* C, const float* dH, const float* dc_last, float* dX, float* dW,
+                 float* dv_f, float* dv_r, float* db_f, float* db_r, float* dc0,
+                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  Dims s;
+  int st = make_dims(L, B, d_in, d, direction, s);
+  if (st != SRU_OK) return st;
+  if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
+  if (!X || !W || !v_f || !v_r || !b_f || !b_r || !U || !C || !dH || !dX || !dW || !dv_f ||
+      !dv_r || !db_f || !db_r)
+    return SRU_E_NULLPTR;
+  const void* ptrs[] = {X, W, v_f, v_r, b_f, b_r, c0, U, C, dH, dc_last, dX, dW, dv_f, dv_r,
+                        db_f, db_r, dc0};
+  for (const void* p : ptrs)
+    if (p && !aligned4(p)) return SRU_E_ALIGN;
+  const BwdLayout lay = bwd_layout(s, gemm_dtype);
+  if (!workspace || workspace_bytes < lay.total) return SRU_E_WORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
+
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  float* dU = reinterpret_cast<float*>(ws + lay.dU);
+  float* dxh = s.k == 3 ? reinterpret_cast<float*>(ws + lay.dxh) : nullptr;
+  float* partial = reinterpret_cast<float*>(ws + lay.partial);
+  float* splitk = reinterpret_cast<float*>(ws + lay.splitk);
+
+  // 1. reverse gradient scan and the v/b sums
+  sru::ScanBwdArgs a{U,   X,       C,   dH,    dc_last, v_f,  v_r,  b_f,  b_r, c0,
+                     pad_mask, dU, dxh, partial, dc0,  dv_f, dv_r, db_f, db_r};
+  if (int e = hip_status(sru::scan_backward_launch(scan_shape(s, direction), a, stream))) return e;
+
+  const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
+  // 2. dX = dU W (+ the highway gradient of every direction when k = 3)
+  sru::GemmDesc gx = gemm_desc(SRU_OP_NN, bf16, (int)s.M, d_in, (int)s.N, dU, s.N, W, d_in, dX,
+                               d_in);
+  if (s.k == 3) {
+    gx.add = dxh;
+    gx.add_ld = s.nfeat;
+    gx.add_off = d;
+    gx.add_count = s.ndir;
+  }
+  if (int e = hip_status(sru::gemm_launch(gx, stream))) return e;
+
+  // 3. dW = dU^T X (reduction over all tokens, split over K)
+  sru::GemmDesc gw = gemm_desc(SRU_OP_TN, bf16, (int)s.N, d_in, (int)s.M, dU, s.N, X, d_in, dW,
+                               d_in);
+  gw.partials = splitk;
+  return hip_status(sru::gemm_launch(gw, stream));
+}
+
+size_t sru_gemm_workspace_bytes(int op, int M, int N, int K, int gemm_dtype) {
+  if (op < SRU_OP_NT || op > SRU_OP_TN || !valid_dtype(gemm_dtype)) return 0;
+  if (M <= 0 || N <= 0 || K <= 0) return 0;
+  sru::GemmDesc g = gemm_desc(op, gemm_dtype == SRU_GEMM_BF16, M, N, K, nullptr, 0, nullptr, 0,
+                              nullptr, 0);
+  return align_up(sru::gemm_partial_bytes(M, N, sru::gemm_splits(g)));
+}
+
+int sru_gemm(int op, int gemm_dtype, int M, int N, int K, const float* A, int lda,
+             const float* B, int ldb, float* C, int ldc, void* workspace,
+             size_t workspace_bytes, hipStream_t stream) {
+  if (op < SRU_OP_NT || op > SRU_OP_TN || !valid_dtype(gemm_dtype)) return SRU_E_FLAG;
+  if (M <= 0 || N <= 0 || K <= 0) return SRU_E_SHAPE;
+  if (!A || !B || !C) return SRU_E_NULLPTR;
+  // leading dimensions cover a row of the stored layout
+  const int a_row = op == SRU_OP_TN ? M : K;
+  const int b_row = op == SRU_OP_NT ? K : N;
+  if (lda < a_row || ldb < b_row || ldc < N) return SRU_E_SHAPE;
+  if ((long long)M * N > kMaxElems) return SRU_E_SHAPE;
+  if (!aligned4(A) || !aligned4(B) || !aligned4(C)) return SRU_E_ALIGN;
+  sru::GemmDesc g = gemm_desc(op, gemm_dtype == SRU_GEMM_BF16, M, N, K, A, lda, B, ldb, C, ldc);
+  const size_t need = align_up(sru::gemm_partial_bytes(M, N, sru::gemm_splits(g)));
+  if (need > 0) {
+    if (!workspace || workspace_bytes < need) return SRU_E_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
+    g.partials = static_cast<float*>(workspace);
+  }
+  return hip_status(sru::gemm_launch(g, stream));
+}
+
+int sru_scan_forward(const float* U, const float* X, const float* v_f, const float* v_r,
+                     const float* b_f, const float* b_r, const float* c0, int L, int B, int d_in,
+                     int d, int direction, const uint8_t* pad_mask, float* H, float* C,
+                     float* c_last, hipStream_t stream) {
+  Dims s;
+  int st = make_dims(L, B, d_in, d, direction, s);
+  if (st != SRU_OK) return st;
+  if (!U || !v_f || !v_r || !b_f || !b_r || !H) return SRU_E_NULLPTR;
+  if (s.k == 3 && !X) return SRU_E_NULLPTR;
+  const void* ptrs[] = {U, X, v_f, v_r, b_f, b_r, c0, H, C, c_last};
+  for (const void* p : ptrs)
+    if (p && !aligned4(p)) return SRU_E_ALIGN;
+  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last};
+  return hip_status(sru::scan_forward_launch(scan_shape(s, direction), a, stream));
+}
+
+size_t sru_scan_backward_workspace_bytes(int L, int B, int d_in, int d, int direction) {
+  Dims s;
+  if (make_dims(L, B, d_in, d, direction, s) != SRU_OK) return 0;
+  return align_up(sru::scan_backward_partial_bytes(scan_shape(s, direction)));
+}
+
+int sru_scan_backward(const float* U, const float* X, const float* C, const float* dH,
+                      const float* dc_last, const float* v_f, const float* v_r, const float* b_f,
+                      const float* b_r, const float* c0, int L, int B, int d_in, int d,
+                      int direction, const uint8_t* pad_mask, float* dU, float* dxh,
+                      float* dv_f, float* dv_r, float* db_f, float* db_r, float* dc0,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  Dims s;
+  int st = make_dims(L, B, d_in, d, direction, s);
+  if (st != SRU_OK) return st;
+  if (!U || !C || !dH || !v_f || !v_r || !b_f || !b_r || !dU || !dv_f || !dv_r || !db_f || !db_r)
+    return SRU_E_NULLPTR;
+  if (s.k == 3 && (!X || !dxh)) return SRU_E_NULLPTR;
+  if (s.k == 4 && dxh) return SRU_E_SHAPE;
+  const void* ptrs[] = {U, X, C, dH, dc_last, v_f, v_r, b_f, b_r, c0, dU, dxh, dv_f, dv_r,
+                        db_f, db_r, dc0};
+  for (const void* p : ptrs)
+    if (p && !aligned4(p)) return SRU_E_ALIGN;
+  const sru::ScanShape sh = scan_shape(s, direction);
+  const size_t need = align_up(sru::scan_backward_partial_bytes(sh));
+  if (!workspace || workspace_bytes < need) return SRU_E_WORKSPACE;
+  sru::ScanBwdArgs a{U,        X,  C,   dH,
+                     dc_last,  v_f, v_r, b_f,
+                     b_r,      c0, pad_mask, dU,
+                     dxh,      static_cast<float*>(workspace), dc0, dv_f,
+                     dv_r,     db_f, db_r};
+  return hip_status(sru::scan_backward_launch(sh, a, stream));
+}
+
+}  // extern "C"

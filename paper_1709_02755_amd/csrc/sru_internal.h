@@ -1,0 +1,94 @@
+// Internal launch interface between the C ABI (sru_api.hip) and the kernels.
+// Launchers assume validated arguments and only enqueue work.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sru {
+
+// ----------------------------------------------------------------- GEMM
+// C[M,N] = sum_k A(m,k) B(n,k), fp32 in memory, MFMA compute.
+//   A(m,k) = a_kc ? A[m*lda + k] : A[k*lda + m]
+//   B(n,k) = b_kc ? B[n*ldb + k] : B[k*ldb + n]
+// With splits > 1 the reduction is cut into `splits` contiguous K ranges;
+// each writes a partial [M,N] (ld = N) at `partials` + s*M*N, and a second
+// kernel sums them in split order into C.  The optional addend adds
+//   add[m*add_ld + n] (+ add[m*add_ld + add_off + n] when add_count == 2)
+// to the result (used for the highway gradient of dX).
+struct GemmDesc {
+  const float* A;
+  const float* B;
+  float* C;
+  int M, N, K;
+  long long lda, ldb, ldc;
+  bool a_kc, b_kc;
+  bool bf16;
+  int splits;
+  float* partials;
+  const float* add;
+  long long add_ld, add_off;
+  int add_count;
+};
+
+// Number of K splits the launcher will use for this product (>= 1) and the
+// partial-buffer bytes it then needs.
+int gemm_splits(const GemmDesc& g);
+size_t gemm_partial_bytes(int M, int N, int splits);
+hipError_t gemm_launch(const GemmDesc& g, hipStream_t stream);
+
+// ----------------------------------------------------------------- scans
+struct ScanShape {
+  int L, B, d_in, d, ndir, k, direction;
+};
+
+struct ScanFwdArgs {
+  const float* U;
+  const float* X;
+  const float* v_f;
+  const float* v_r;
+  const float* b_f;
+  const float* b_r;
+  const float* c0;
+  const uint8_t* mask;
+  float* H;
+  float* C;
+  float* c_last;
+};
+
+struct ScanBwdArgs {
+  const float* U;
+  const float* X;
+  const float* C;
+  const float* dH;
+  const float* dc_last;
+  const float* v_f;
+  const float* v_r;
+  const float* b_f;
+  const float* b_r;
+  const float* c0;
+  const uint8_t* mask;
+  float* dU;
+  float* dxh;
+  float* partial;  // [B, 4, ndir*d] per-sequence sums of the v/b gradients
+  float* dc0;
+  float* dv_f;
+  float* dv_r;
+  float* db_f;
+  float* db_r;
+};
+
+hipError_t scan_forward_launch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t stream);
+// Enqueues the reverse scan and the fixed-order reduction of `partial`.
+hipError_t scan_backward_launch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t stream);
+size_t scan_backward_partial_bytes(const ScanShape& s);
+
+// ----------------------------------------------------------------- timing
+// Measurement hook: while a caller has armed it (sru_timing_begin), every
+// kernel launch is bracketed by two hipEventRecord calls on its stream and
+// labelled.  Disarmed (the default) it costs one thread-local load.
+void timing_before(const char* label, hipStream_t stream);
+void timing_after(hipStream_t stream);
+
+}  // namespace sru

@@ -1,0 +1,303 @@
+"""Thin Python binding of libsru.so (argument marshalling only).
+
+Every step of the layer runs in the HIP library; this module checks tensor
+devices/dtypes/shapes, allocates outputs with torch (device memory and
+streams are torch's job here) and passes raw pointers through ctypes.  There
+is no fallback: if the library cannot be loaded, every call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libsru.so")
+
+SRU_OK = 0
+DIR_FWD, DIR_REV, DIR_BI = 0, 1, 2
+GEMM_FP32, GEMM_BF16 = 0, 1
+OP_NT, OP_NN, OP_TN = 0, 1, 2
+
+_lock = threading.Lock()
+_lib = None
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int
+_S = ctypes.c_size_t
+
+# name -> (restype, argtypes); mirrors include/sru.h
+_SIGNATURES = {
+    "sru_status_string": (ctypes.c_char_p, [_I]),
+    "sru_last_hip_error": (_I, []),
+    "sru_version": (_I, []),
+    "sru_forward_workspace_bytes": (_S, [_I] * 6),
+    "sru_backward_workspace_bytes": (_S, [_I] * 6),
+    "sru_forward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I] + [_P] * 4 + [_P, _S, _P]),
+    "sru_backward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I] + [_P] * 4 + [_P] * 7 + [_P, _S, _P]),
+    "sru_gemm_workspace_bytes": (_S, [_I] * 5),
+    "sru_gemm": (_I, [_I] * 5 + [_P, _I, _P, _I, _P, _I] + [_P, _S, _P]),
+    "sru_scan_forward": (_I, [_P] * 7 + [_I] * 5 + [_P] + [_P] * 3 + [_P]),
+    "sru_scan_backward_workspace_bytes": (_S, [_I] * 5),
+    "sru_scan_backward": (_I, [_P] * 10 + [_I] * 5 + [_P] + [_P] * 7 + [_P, _S, _P]),
+    "sru_timing_begin": (_I, [_P, _I]),
+    "sru_timing_end": (_I, []),
+    "sru_timing_label": (ctypes.c_char_p, [_I]),
+}
+
+
+class SruError(RuntimeError):
+    pass
+
+
+def lib():
+    """Load libsru.so (building it first only if it has never been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                from . import build as _build
+                _build.build()
+            h = ctypes.CDLL(LIB_PATH)
+            for name, (res, args) in _SIGNATURES.items():
+                fn = getattr(h, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = h
+    return _lib
+
+
+def exported_symbols():
+    return list(_SIGNATURES)
+
+
+def _check(status: int, what: str):
+    if status != SRU_OK:
+        msg = lib().sru_status_string(status).decode()
+        if status == 5:
+            msg += f" (hipError {lib().sru_last_hip_error()})"
+        raise SruError(f"{what}: {msg}")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _req(t, name, shape, dtype=torch.float32, optional=False):
+    if t is None:
+        if optional:
+            return
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def dims(X, W):
+    L, B, d_in = X.shape
+    ndir, k, d, _ = W.shape
+    return L, B, d_in, d, ndir, k
+
+
+def _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask):
+    L, B, d_in, d, ndir, k = dims(X, W)
+    want_nd = 2 if direction == DIR_BI else 1
+    if ndir != want_nd or k != (3 if d_in == d else 4):
+        raise ValueError(f"W shape {tuple(W.shape)} does not fit d_in={d_in}, direction={direction}")
+    _req(X, "X", (L, B, d_in))
+    _req(W, "W", (ndir, k, d, d_in))
+    for n, t in (("v_f", v_f), ("v_r", v_r), ("b_f", b_f), ("b_r", b_r)):
+        _req(t, n, (ndir, d))
+    _req(c0, "c0", (B, ndir * d), optional=True)
+    _req(mask, "mask", (L, B), dtype=torch.uint8, optional=True)
+    return L, B, d_in, d, ndir, k
+
+
+def forward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype):
+    return lib().sru_forward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype)
+
+
+def backward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype):
+    return lib().sru_backward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype)
+
+
+def workspace(nbytes, device):
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
+            gemm_dtype=GEMM_FP32, store_c=True, out=None, ws=None):
+    """One layer forward; returns dict(U, H, C, c_last) (C None without store_c)."""
+    L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask)
+    dev = X.device
+    if out is None:
+        out = dict(U=torch.empty((L, B, ndir, k, d), device=dev),
+                   H=torch.empty((L, B, ndir * d), device=dev),
+                   C=torch.empty((L, B, ndir * d), device=dev) if store_c else None,
+                   c_last=torch.empty((B, ndir * d), device=dev))
+    need = forward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype)
+    if need and ws is None:
+        ws = workspace(need, dev)
+    st = lib().sru_forward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
+                           L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
+                           _ptr(out["U"]), _ptr(out["H"]), _ptr(out.get("C")),
+                           _ptr(out.get("c_last")), _ptr(ws), need if ws is not None else 0,
+                           _stream())
+    _check(st, "sru_forward")
+    return out
+
+
+def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, direction=DIR_FWD,
+             mask=None, gemm_dtype=GEMM_FP32, want_dc0=True, out=None, ws=None):
+    """One layer backward; returns dict(dX, dW, dv_f, dv_r, db_f, db_r, dc0)."""
+    L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask)
+    _req(U, "U", (L, B, ndir, k, d))
+    _req(C, "C", (L, B, ndir * d))
+    _req(dH, "dH", (L, B, ndir * d))
+    _req(dc_last, "dc_last", (B, ndir * d), optional=True)
+    dev = X.device
+    if out is None:
+        out = dict(dX=torch.empty_like(X), dW=torch.empty_like(W),
+                   dv_f=torch.empty((ndir, d), device=dev), dv_r=torch.empty((ndir, d), device=dev),
+                   db_f=torch.empty((ndir, d), device=dev), db_r=torch.empty((ndir, d), device=dev),
+                   dc0=torch.empty((B, ndir * d), device=dev) if want_dc0 else None)
+    need = backward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype)
+    if ws is None:
+        ws = workspace(need, dev)
+    st = lib().sru_backward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
+                            L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
+                            _ptr(U), _ptr(C), _ptr(dH), _ptr(dc_last),
+                            _ptr(out["dX"]), _ptr(out["dW"]), _ptr(out["dv_f"]), _ptr(out["dv_r"]),
+                            _ptr(out["db_f"]), _ptr(out["db_r"]), _ptr(out.get("dc0")),
+                            _ptr(ws), ws.numel(), _stream())
+    _check(st, "sru_backward")
+    return out
+
+
+def gemm(op, A, B, M, N, K, gemm_dtype=GEMM_FP32, C=None, ws=None):
+    """C[M,N] for op NT (A[M,K] B[N,K]^T), NN (A[M,K] B[K,N]) or TN (A[K,M]^T B[K,N])."""
+    a_shape = (K, M) if op == OP_TN else (M, K)
+    b_shape = (N, K) if op == OP_NT else (K, N)
+    _req(A, "A", a_shape)
+    _req(B, "B", b_shape)
+    if C is None:
+        C = torch.empty((M, N), device=A.device)
+    need = lib().sru_gemm_workspace_bytes(op, M, N, K, gemm_dtype)
+    if need and ws is None:
+        ws = workspace(need, A.device)
+    st = lib().sru_gemm(op, gemm_dtype, M, N, K, _ptr(A), a_shape[1], _ptr(B), b_shape[1],
+                        _ptr(C), N, _ptr(ws), need if need else 0, _stream())
+    _check(st, "sru_gemm")
+    return C
+
+
+def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
+                 store_c=True, out=None):
+    L, B, ndir, k, d = U.shape
+    d_in = X.shape[2] if X is not None else (d if k == 3 else -1)
+    if k == 4 and X is None:
+        raise ValueError("pass X (or its shape via d_in) for k = 4")
+    _req(U, "U", (L, B, ndir, k, d))
+    dev = U.device
+    if out is None:
+        out = dict(H=torch.empty((L, B, ndir * d), device=dev),
+                   C=torch.empty((L, B, ndir * d), device=dev) if store_c else None,
+                   c_last=torch.empty((B, ndir * d), device=dev))
+    st = lib().sru_scan_forward(_ptr(U), _ptr(X), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r),
+                                _ptr(c0), L, B, d_in, d, direction, _ptr(mask),
+                                _ptr(out["H"]), _ptr(out.get("C")), _ptr(out.get("c_last")),
+                                _stream())
+    _check(st, "sru_scan_forward")
+    return out
+
+
+def scan_backward(U, X, C, dH, v_f, v_r, b_f, b_r, c0=None, dc_last=None, direction=DIR_FWD,
+                  mask=None, d_in=None, out=None, ws=None):
+    L, B, ndir, k, d = U.shape
+    if d_in is None:
+        d_in = X.shape[2] if X is not None else d
+    dev = U.device
+    if out is None:
+        out = dict(dU=torch.empty_like(U),
+                   dxh=torch.empty((L, B, ndir, d), device=dev) if k == 3 else None,
+                   dv_f=torch.empty((ndir, d), device=dev), dv_r=torch.empty((ndir, d), device=dev),
+                   db_f=torch.empty((ndir, d), device=dev), db_r=torch.empty((ndir, d), device=dev),
+                   dc0=torch.empty((B, ndir * d), device=dev))
+    need = lib().sru_scan_backward_workspace_bytes(L, B, d_in, d, direction)
+    if ws is None:
+        ws = workspace(need, dev)
+    st = lib().sru_scan_backward(_ptr(U), _ptr(X), _ptr(C), _ptr(dH), _ptr(dc_last),
+                                 _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
+                                 L, B, d_in, d, direction, _ptr(mask),
+                                 _ptr(out["dU"]), _ptr(out.get("dxh")), _ptr(out["dv_f"]),
+                                 _ptr(out["dv_r"]), _ptr(out["db_f"]), _ptr(out["db_r"]),
+                                 _ptr(out.get("dc0")), _ptr(ws), ws.numel(), _stream())
+    _check(st, "sru_scan_backward")
+    return out
+
+
+class Stack:
+    """Stacked SRU layers (layer l+1 reads layer l's H) with preallocated
+    buffers, for the multi-layer forward + backward step.
+
+    `layers` holds per-layer dicts of GPU tensors W, v_f, v_r, b_f, b_r.
+    """
+
+    def __init__(self, layers, L, B, d_in, d, direction, gemm_dtype, device, backward=True):
+        self.layers = layers
+        self.L, self.B, self.d, self.direction, self.gemm_dtype = L, B, d, direction, gemm_dtype
+        ndir = 2 if direction == DIR_BI else 1
+        self.ndir = ndir
+        self.fw = []
+        self.bw = []
+        ws_bytes = 0
+        for li, p in enumerate(layers):
+            din = d_in if li == 0 else ndir * d
+            k = p["W"].shape[1]
+            self.fw.append(dict(U=torch.empty((L, B, ndir, k, d), device=device),
+                                H=torch.empty((L, B, ndir * d), device=device),
+                                C=torch.empty((L, B, ndir * d), device=device),
+                                c_last=torch.empty((B, ndir * d), device=device)))
+            if backward:
+                self.bw.append(dict(dX=torch.empty((L, B, din), device=device),
+                                    dW=torch.empty_like(p["W"]),
+                                    dv_f=torch.empty((ndir, d), device=device),
+                                    dv_r=torch.empty((ndir, d), device=device),
+                                    db_f=torch.empty((ndir, d), device=device),
+                                    db_r=torch.empty((ndir, d), device=device),
+                                    dc0=None))
+                ws_bytes = max(ws_bytes, backward_workspace_bytes(L, B, din, d, direction,
+                                                                  gemm_dtype))
+            ws_bytes = max(ws_bytes, forward_workspace_bytes(L, B, din, d, direction, gemm_dtype))
+        self.ws = workspace(ws_bytes, device)
+
+    def forward(self, X, mask=None):
+        x = X
+        for p, o in zip(self.layers, self.fw):
+            forward(x, p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], None, self.direction, mask,
+                    self.gemm_dtype, out=o, ws=self.ws)
+            x = o["H"]
+        return x
+
+    def backward(self, X, dH, mask=None):
+        g = dH
+        for li in range(len(self.layers) - 1, -1, -1):
+            p, o, b = self.layers[li], self.fw[li], self.bw[li]
+            x = X if li == 0 else self.fw[li - 1]["H"]
+            backward(x, p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], o["U"], o["C"], g,
+                     None, None, self.direction, mask, self.gemm_dtype, want_dc0=False,
+                     out=b, ws=self.ws)
+            g = b["dX"]
+        return g

@@ -1,0 +1,145 @@
+"""C-ABI contract checks that need no GPU: the library loads, exports every
+symbol include/sru.h declares, and rejects invalid arguments before anything
+is enqueued (no compute call is made here)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1709_02755_amd import sru
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sru.h")
+
+OK, E_NULL, E_SHAPE, E_FLAG, E_WS, E_HIP, E_ALIGN = range(7)
+FAKE = ctypes.c_void_p(0x10000)        # never dereferenced: validation fails first
+FAKE_MIS = ctypes.c_void_p(0x10002)    # not 4-byte aligned
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"SRU_API\s+[\w\s\*]+?\b(sru_\w+)\s*\(", text)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    lib = sru.lib()
+    names = declared_symbols()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(sru.exported_symbols()) == names
+
+
+def test_version_and_status_strings():
+    lib = sru.lib()
+    assert lib.sru_version() >> 16 == 1
+    for code in range(7):
+        s = lib.sru_status_string(code).decode()
+        assert s.startswith("SRU_")
+    assert lib.sru_status_string(99).decode() == "unknown sru_status"
+
+
+def _fwd(lib, **kw):
+    a = dict(X=FAKE, W=FAKE, v_f=FAKE, v_r=FAKE, b_f=FAKE, b_r=FAKE, c0=None, L=4, B=2, d_in=8,
+             d=8, direction=0, mask=None, gemm=0, U=FAKE, H=FAKE, C=FAKE, c_last=None, ws=None,
+             ws_bytes=0)
+    a.update(kw)
+    return lib.sru_forward(a["X"], a["W"], a["v_f"], a["v_r"], a["b_f"], a["b_r"], a["c0"],
+                           a["L"], a["B"], a["d_in"], a["d"], a["direction"], a["mask"],
+                           a["gemm"], a["U"], a["H"], a["C"], a["c_last"], a["ws"], a["ws_bytes"],
+                           None)
+
+
+def _bwd(lib, **kw):
+    a = dict(X=FAKE, W=FAKE, v_f=FAKE, v_r=FAKE, b_f=FAKE, b_r=FAKE, c0=None, L=4, B=2, d_in=8,
+             d=8, direction=0, mask=None, gemm=0, U=FAKE, C=FAKE, dH=FAKE, dc_last=None,
+             dX=FAKE, dW=FAKE, dv_f=FAKE, dv_r=FAKE, db_f=FAKE, db_r=FAKE, dc0=None, ws=None,
+             ws_bytes=0)
+    a.update(kw)
+    return lib.sru_backward(a["X"], a["W"], a["v_f"], a["v_r"], a["b_f"], a["b_r"], a["c0"],
+                            a["L"], a["B"], a["d_in"], a["d"], a["direction"], a["mask"],
+                            a["gemm"], a["U"], a["C"], a["dH"], a["dc_last"], a["dX"], a["dW"],
+                            a["dv_f"], a["dv_r"], a["db_f"], a["db_r"], a["dc0"], a["ws"],
+                            a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("field", ["X", "W", "v_f", "v_r", "b_f", "b_r", "U", "H"])
+def test_forward_rejects_null_required_pointer(field):
+    assert _fwd(sru.lib(), **{field: None}) == E_NULL
+
+
+@pytest.mark.parametrize("kw", [dict(L=0), dict(B=0), dict(d=0), dict(d_in=-1),
+                                dict(L=1 << 20, B=1 << 12), dict(d=1 << 30, d_in=1 << 30)])
+def test_forward_rejects_bad_shape(kw):
+    assert _fwd(sru.lib(), **kw) == E_SHAPE
+
+
+@pytest.mark.parametrize("kw", [dict(direction=3), dict(direction=-1), dict(gemm=2)])
+def test_forward_rejects_bad_flag(kw):
+    assert _fwd(sru.lib(), **kw) == E_FLAG
+
+
+def test_forward_rejects_misaligned_pointer():
+    assert _fwd(sru.lib(), H=FAKE_MIS) == E_ALIGN
+
+
+@pytest.mark.parametrize("field", ["X", "W", "U", "C", "dH", "dX", "dW", "dv_f", "db_r"])
+def test_backward_rejects_null_required_pointer(field):
+    assert _bwd(sru.lib(), **{field: None}) == E_NULL
+
+
+def test_backward_requires_workspace():
+    lib = sru.lib()
+    need = lib.sru_backward_workspace_bytes(4, 2, 8, 8, 0, 0)
+    assert need > 0
+    assert _bwd(lib) == E_WS
+    assert _bwd(lib, ws=FAKE, ws_bytes=need - 1) == E_WS
+    # a large enough but misaligned workspace
+    assert _bwd(lib, ws=ctypes.c_void_p(0x10040), ws_bytes=need) == E_ALIGN
+
+
+def test_workspace_queries():
+    lib = sru.lib()
+    assert lib.sru_forward_workspace_bytes(4, 2, 8, 8, 0, 0) == 0
+    assert lib.sru_forward_workspace_bytes(0, 2, 8, 8, 0, 0) == 0
+    assert lib.sru_backward_workspace_bytes(4, 2, 8, 8, 7, 0) == 0
+    # dU (M*N floats) plus dxh plus partials, each 256-aligned
+    L, B, d = 16, 4, 32
+    need = lib.sru_backward_workspace_bytes(L, B, d, d, 2, 0)
+    assert need >= 4 * (L * B * 2 * 3 * d + L * B * 2 * d + 4 * B * 2 * d)
+    assert need % 256 == 0
+    # bf16 and fp32 sizes are both valid; k = 4 has no dxh buffer
+    assert lib.sru_backward_workspace_bytes(L, B, 2 * d, d, 2, 1) > 0
+
+
+def test_gemm_argument_checks():
+    lib = sru.lib()
+    g = lib.sru_gemm
+    assert g(3, 0, 4, 4, 4, FAKE, 4, FAKE, 4, FAKE, 4, None, 0, None) == E_FLAG
+    assert g(0, 5, 4, 4, 4, FAKE, 4, FAKE, 4, FAKE, 4, None, 0, None) == E_FLAG
+    assert g(0, 0, 0, 4, 4, FAKE, 4, FAKE, 4, FAKE, 4, None, 0, None) == E_SHAPE
+    assert g(0, 0, 4, 4, 8, FAKE, 4, FAKE, 8, FAKE, 4, None, 0, None) == E_SHAPE   # lda < K
+    assert g(2, 0, 4, 4, 8, FAKE, 3, FAKE, 4, FAKE, 4, None, 0, None) == E_SHAPE   # TN: lda < M
+    assert g(0, 0, 4, 4, 4, None, 4, FAKE, 4, FAKE, 4, None, 0, None) == E_NULL
+    assert g(0, 0, 4, 4, 4, FAKE_MIS, 4, FAKE, 4, FAKE, 4, None, 0, None) == E_ALIGN
+    # a long TN reduction is split and then needs workspace
+    need = lib.sru_gemm_workspace_bytes(2, 512, 512, 1 << 16, 0)
+    assert need > 0
+    assert g(2, 0, 512, 512, 1 << 16, FAKE, 512, FAKE, 512, FAKE, 512, None, 0, None) == E_WS
+
+
+def test_scan_argument_checks():
+    lib = sru.lib()
+    f = lib.sru_scan_forward
+    assert f(FAKE, None, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 0, None, FAKE, None, None,
+             None) == E_NULL                               # k = 3 needs X
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 9, None, FAKE, None, None,
+             None) == E_FLAG
+    b = lib.sru_scan_backward
+    args = [FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 16, 8, 0, None,
+            FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, None]
+    assert b(*args) == E_SHAPE                             # k = 4 takes no dxh
+    args[17] = None
+    assert b(*args) == E_WS

@@ -1,0 +1,131 @@
+"""GPU parity of the individual kernels through the C ABI's component entry
+points: the MFMA products against numpy's matmul of the same (bf16-rounded)
+operands, and the two scans against the oracle fed the same U / C."""
+
+import numpy as np
+import pytest
+import torch
+
+from helpers import TOL_FP32, check, dev, host
+from oracle import sru_oracle as O
+from paper_1709_02755_amd import sru
+from paper_1709_02755_amd.workloads import random_layer_case
+
+pytestmark = pytest.mark.gpu
+
+
+def _bf16(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16).double().numpy()
+
+
+GEMM_SHAPES = [(1, 1, 1), (7, 5, 3), (63, 65, 130), (130, 63, 65), (256, 256, 32),
+               (257, 513, 96), (384, 128, 128), (1000, 300, 260), (2048, 768, 256)]
+
+
+@pytest.mark.parametrize("op", [sru.OP_NT, sru.OP_NN, sru.OP_TN])
+@pytest.mark.parametrize("dtype", [sru.GEMM_FP32, sru.GEMM_BF16])
+@pytest.mark.parametrize("shape", GEMM_SHAPES)
+def test_gemm_matches_matmul(op, dtype, shape):
+    M, N, K = shape
+    print(f"gemm op={op} dtype={dtype} M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M * 7 + N * 3 + K)
+    a_shape = (K, M) if op == sru.OP_TN else (M, K)
+    b_shape = (N, K) if op == sru.OP_NT else (K, N)
+    A = rng.standard_normal(a_shape).astype(np.float32)
+    B = rng.standard_normal(b_shape).astype(np.float32)
+    Ar, Br = (_bf16(A), _bf16(B)) if dtype == sru.GEMM_BF16 else (A.astype(np.float64), B.astype(np.float64))
+    Am = Ar.T if op == sru.OP_TN else Ar
+    Bm = Br.T if op == sru.OP_NT else Br
+    ref = Am @ Bm
+    C = sru.gemm(op, dev(A), dev(B), M, N, K, dtype)
+    torch.cuda.synchronize()
+    # products of bf16 values are exact in fp32: only accumulation order differs
+    check("C", C, ref, TOL_FP32)
+
+
+@pytest.mark.parametrize("dtype", [sru.GEMM_FP32, sru.GEMM_BF16])
+def test_gemm_long_reduction_split(dtype):
+    """dW-shaped product with K = tokens (split over K, fixed-order sum)."""
+    M, N, K = 384, 256, 12800
+    print(f"gemm TN long K dtype={dtype}", flush=True)
+    rng = np.random.default_rng(5)
+    A = rng.standard_normal((K, M)).astype(np.float32)
+    B = rng.standard_normal((K, N)).astype(np.float32)
+    Ar, Br = (_bf16(A), _bf16(B)) if dtype == sru.GEMM_BF16 else (A.astype(np.float64), B.astype(np.float64))
+    assert sru.lib().sru_gemm_workspace_bytes(sru.OP_TN, M, N, K, dtype) > 0
+    C = sru.gemm(sru.OP_TN, dev(A), dev(B), M, N, K, dtype)
+    torch.cuda.synchronize()
+    check("C", C, Ar.T @ Br, TOL_FP32)
+
+
+def _case(seed, L, B, d_in, d, direction, **kw):
+    return random_layer_case(np.random.default_rng(seed), L, B, d_in, d, direction, **kw)
+
+
+SCAN_CASES = [
+    # (L, B, d_in, d, direction, masked)
+    (1, 1, 1, 1, O.DIR_FWD, False),
+    (5, 3, 7, 7, O.DIR_REV, False),
+    (17, 2, 65, 65, O.DIR_FWD, True),
+    (9, 3, 130, 63, O.DIR_BI, True),
+    (33, 4, 128, 128, O.DIR_BI, False),
+    (40, 5, 64, 64, O.DIR_FWD, True),
+    (23, 2, 96, 48, O.DIR_REV, True),
+]
+
+
+@pytest.mark.parametrize("case", SCAN_CASES)
+def test_scan_forward_on_oracle_projection(case):
+    L, B, d_in, d, direction, masked = case
+    print(f"scan_fwd L={L} B={B} d_in={d_in} d={d} dir={direction} mask={masked}", flush=True)
+    c = _case(L * 31 + d, L, B, d_in, d, direction, masked=masked, c0=True, bias_scale=0.5)
+    ref = O.forward(c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"], c["c0"], direction,
+                    c["mask"])
+    U = ref["U"].astype(np.float32)
+    out = sru.scan_forward(dev(U), dev(c["X"]), dev(c["v_f"]), dev(c["v_r"]), dev(c["b_f"]),
+                           dev(c["b_r"]), dev(c["c0"]), direction, dev(c["mask"]))
+    torch.cuda.synchronize()
+    for k in ("H", "C", "c_last"):
+        check(k, out[k], ref[k], TOL_FP32)
+
+
+@pytest.mark.parametrize("case", SCAN_CASES)
+def test_scan_backward_on_oracle_states(case):
+    L, B, d_in, d, direction, masked = case
+    print(f"scan_bwd L={L} B={B} d_in={d_in} d={d} dir={direction} mask={masked}", flush=True)
+    c = _case(L * 17 + d, L, B, d_in, d, direction, masked=masked, c0=True, dc_last=True,
+              bias_scale=0.5)
+    args = (c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"])
+    fw = O.forward(*args, c["c0"], direction, c["mask"])
+    bw = O.backward(*args, c["dH"], c["c0"], direction, c["mask"], O.GEMM_FP32, c["dc_last"])
+    # the scan sees exactly the fp32 U and C the forward would hand it
+    out = sru.scan_backward(dev(fw["U"].astype(np.float32)), dev(c["X"]),
+                            dev(fw["C"].astype(np.float32)), dev(c["dH"]), dev(c["v_f"]),
+                            dev(c["v_r"]), dev(c["b_f"]), dev(c["b_r"]), dev(c["c0"]),
+                            dev(c["dc_last"]), direction, dev(c["mask"]), d_in=d_in)
+    torch.cuda.synchronize()
+    check("dU", out["dU"], bw["dU"], TOL_FP32)
+    if d_in == d:
+        check("dxh", out["dxh"], bw["dxh"], TOL_FP32)
+    for k in ("dv_f", "dv_r", "db_f", "db_r", "dc0"):
+        check(k, out[k], bw[k], TOL_FP32)
+
+
+def test_scan_saturation_exact_and_finite():
+    """b_f = +100 keeps c = c0 exactly; b_f = -100 gives c = u0 exactly;
+    b_r = +100 gives h = c exactly; no NaN anywhere (sigma saturates)."""
+    L, B, d = 12, 3, 70
+    c = _case(1, L, B, d, d, O.DIR_FWD, c0=True)
+    U = np.random.default_rng(2).standard_normal((L, B, 1, 3, d)).astype(np.float32) * 3
+    big = np.full((1, d), 100.0, np.float32)
+    zero = np.zeros((1, d), np.float32)
+    o = sru.scan_forward(dev(U), dev(c["X"]), dev(c["v_f"]), dev(c["v_r"]), dev(big), dev(zero),
+                         dev(c["c0"]), O.DIR_FWD)
+    C = host(o["C"])
+    assert np.array_equal(C, np.broadcast_to(c["c0"].astype(np.float64), C.shape))
+    o = sru.scan_forward(dev(U), dev(c["X"]), dev(c["v_f"]), dev(c["v_r"]), dev(-big), dev(big),
+                         dev(c["c0"]), O.DIR_FWD)
+    C, H = host(o["C"]), host(o["H"])
+    assert np.array_equal(C, U[:, :, 0, 0].astype(np.float64))
+    assert np.array_equal(H, C)
+    assert np.all(np.isfinite(H))
