@@ -66,8 +66,8 @@ int hip_status(hipError_t e) {
   return SRU_E_HIP;
 }
 
-sru::GemmDesc gemm_desc(int op, bool bf16, int M, int N, int K, const float* A, long long lda,
-                        const float* B, long long ldb, float* C, long long ldc) {
+sru::GemmDesc gemm_desc(int op, bool bf16, int M, int N, int K, const void* A, long long lda,
+                        const void* B, long long ldb, float* C, long long ldc) {
   sru::GemmDesc g{};
   g.A = A;
   g.B = B;
@@ -85,23 +85,33 @@ sru::GemmDesc gemm_desc(int op, bool bf16, int M, int N, int K, const float* A, 
   return g;
 }
 
-// Backward workspace layout: [dU | dxh (k = 3) | v/b partials | dW split partials]
+// Forward workspace: bf16 mode keeps a bf16 copy of W [N, d_in].
+size_t fwd_workspace(const Dims& s, int gemm_dtype) {
+  return gemm_dtype == SRU_GEMM_BF16 ? align_up(2 * (size_t)s.N * (size_t)s.d_in) : 0;
+}
+
+// Backward workspace layout:
+//   [dU (fp32, or bf16 in bf16 mode) | dxh (k = 3) | v/b partials |
+//    W^T in bf16 (bf16 mode) | dW split partials]
 struct BwdLayout {
-  size_t dU, dxh, partial, splitk, total;
+  size_t dU, dxh, partial, wt, splitk, total;
   int splits;
 };
 
 BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
+  const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
   BwdLayout w{};
   size_t off = 0;
   w.dU = off;
-  off += align_up(sizeof(float) * (size_t)s.M * (size_t)s.N);
+  off += align_up((bf16 ? 2 : 4) * (size_t)s.M * (size_t)s.N);
   w.dxh = off;
   if (s.k == 3) off += align_up(sizeof(float) * (size_t)s.M * (size_t)s.nfeat);
   w.partial = off;
   off += align_up(sizeof(float) * 4 * (size_t)s.B * (size_t)s.nfeat);
-  sru::GemmDesc dw = gemm_desc(SRU_OP_TN, gemm_dtype == SRU_GEMM_BF16, (int)s.N, s.d_in, (int)s.M,
-                               nullptr, s.N, nullptr, s.d_in, nullptr, s.d_in);
+  w.wt = off;
+  if (bf16) off += align_up(2 * (size_t)s.N * (size_t)s.d_in);
+  sru::GemmDesc dw = gemm_desc(SRU_OP_TN, bf16, (int)s.N, s.d_in, (int)s.M, nullptr, s.N,
+                               nullptr, s.d_in, nullptr, s.d_in);
   w.splits = sru::gemm_splits(dw);
   w.splitk = off;
   off += align_up(sru::gemm_partial_bytes((int)s.N, s.d_in, w.splits));
@@ -172,7 +182,7 @@ int sru_version(void) { return (1 << 16) | 0; }
 size_t sru_forward_workspace_bytes(int L, int B, int d_in, int d, int direction, int gemm_dtype) {
   Dims s;
   if (make_dims(L, B, d_in, d, direction, s) != SRU_OK || !valid_dtype(gemm_dtype)) return 0;
-  return 0;  // the projection writes U directly; the scan needs no scratch
+  return fwd_workspace(s, gemm_dtype);
 }
 
 size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int direction,
@@ -187,8 +197,6 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
                 int d, int direction, const uint8_t* pad_mask, int gemm_dtype, float* U,
                 float* H, float* C, float* c_last, void* workspace, size_t workspace_bytes,
                 hipStream_t stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   Dims s;
   int st = make_dims(L, B, d_in, d, direction, s);
   if (st != SRU_OK) return st;
@@ -197,9 +205,24 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
   const void* ptrs[] = {X, W, v_f, v_r, b_f, b_r, c0, U, H, C, c_last};
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
+  const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
+  const size_t need = fwd_workspace(s, gemm_dtype);
+  if (need > 0) {
+    if (!workspace || workspace_bytes < need) return SRU_E_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
+  }
 
-  sru::GemmDesc g = gemm_desc(SRU_OP_NT, gemm_dtype == SRU_GEMM_BF16, (int)s.M, (int)s.N, d_in, X,
-                              d_in, W, d_in, U, s.N);
+  // U = X Wcat^T (Sec. 2.1).  bf16 mode: W rounded once into the workspace,
+  // X rounded as it is staged.
+  const void* Wop = W;
+  if (bf16) {
+    uint16_t* wb = static_cast<uint16_t*>(workspace);
+    if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wb, false, stream))) return e;
+    Wop = wb;
+  }
+  sru::GemmDesc g = gemm_desc(SRU_OP_NT, bf16, (int)s.M, (int)s.N, d_in, X, d_in, Wop, d_in, U,
+                              s.N);
+  g.b_bf16 = bf16;
   if (int e = hip_status(sru::gemm_launch(g, stream))) return e;
 
   sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last};
@@ -227,21 +250,31 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   if (!workspace || workspace_bytes < lay.total) return SRU_E_WORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
 
+  const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
   unsigned char* ws = static_cast<unsigned char*>(workspace);
-  float* dU = reinterpret_cast<float*>(ws + lay.dU);
+  void* dU = ws + lay.dU;
   float* dxh = s.k == 3 ? reinterpret_cast<float*>(ws + lay.dxh) : nullptr;
   float* partial = reinterpret_cast<float*>(ws + lay.partial);
+  uint16_t* wt = reinterpret_cast<uint16_t*>(ws + lay.wt);
   float* splitk = reinterpret_cast<float*>(ws + lay.splitk);
 
-  // 1. reverse gradient scan and the v/b sums
-  sru::ScanBwdArgs a{U,   X,       C,   dH,    dc_last, v_f,  v_r,  b_f,  b_r, c0,
-                     pad_mask, dU, dxh, partial, dc0,  dv_f, dv_r, db_f, db_r};
+  // 1. reverse gradient scan and the v/b sums; dU is written in the operand
+  //    type of the products that read it
+  sru::ScanBwdArgs a{U,   X,    C,   dH,      dc_last, v_f,  v_r,  b_f,  b_r,  c0,
+                     pad_mask, dU, bf16, dxh, partial, dc0, dv_f, dv_r, db_f, db_r};
   if (int e = hip_status(sru::scan_backward_launch(scan_shape(s, direction), a, stream))) return e;
 
-  const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
-  // 2. dX = dU W (+ the highway gradient of every direction when k = 3)
-  sru::GemmDesc gx = gemm_desc(SRU_OP_NN, bf16, (int)s.M, d_in, (int)s.N, dU, s.N, W, d_in, dX,
-                               d_in);
+  // 2. dX = dU Wcat (+ the highway gradient of every direction when k = 3).
+  //    bf16 mode: Wcat^T rounded once into the workspace, so the product is
+  //    an NT one with both operands K-contiguous bf16.
+  sru::GemmDesc gx;
+  if (bf16) {
+    if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wt, true, stream))) return e;
+    gx = gemm_desc(SRU_OP_NT, true, (int)s.M, d_in, (int)s.N, dU, s.N, wt, s.N, dX, d_in);
+    gx.a_bf16 = gx.b_bf16 = true;
+  } else {
+    gx = gemm_desc(SRU_OP_NN, false, (int)s.M, d_in, (int)s.N, dU, s.N, W, d_in, dX, d_in);
+  }
   if (s.k == 3) {
     gx.add = dxh;
     gx.add_ld = s.nfeat;
@@ -253,6 +286,7 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   // 3. dW = dU^T X (reduction over all tokens, split over K)
   sru::GemmDesc gw = gemm_desc(SRU_OP_TN, bf16, (int)s.N, d_in, (int)s.M, dU, s.N, X, d_in, dW,
                                d_in);
+  gw.a_bf16 = bf16;
   gw.partials = splitk;
   return hip_status(sru::gemm_launch(gw, stream));
 }
@@ -329,11 +363,10 @@ int sru_scan_backward(const float* U, const float* X, const float* C, const floa
   const sru::ScanShape sh = scan_shape(s, direction);
   const size_t need = align_up(sru::scan_backward_partial_bytes(sh));
   if (!workspace || workspace_bytes < need) return SRU_E_WORKSPACE;
-  sru::ScanBwdArgs a{U,        X,  C,   dH,
-                     dc_last,  v_f, v_r, b_f,
-                     b_r,      c0, pad_mask, dU,
-                     dxh,      static_cast<float*>(workspace), dc0, dv_f,
-                     dv_r,     db_f, db_r};
+  sru::ScanBwdArgs a{U,   X,   C,     dH,  dc_last,
+                     v_f, v_r, b_f,   b_r, c0,
+                     pad_mask, dU, false, dxh, static_cast<float*>(workspace),
+                     dc0, dv_f, dv_r,  db_f, db_r};
   return hip_status(sru::scan_backward_launch(sh, a, stream));
 }
 

@@ -4,17 +4,23 @@
 // tokens at once) and the two products of the backward pass (dX = dU W and
 // dW = dU^T X) are one kernel template:
 //     C[M,N] = sum_k A(m,k) B(n,k)
-// with each operand either K-contiguous ("kc": row-major [rows, K]) or
-// row-contiguous ([K, rows]).  Operands are fp32 in memory; the loader
-// converts them to the compute type while staging a tile into LDS:
-//   * bf16 mode: round-to-nearest-even bf16 (v_cvt_pk_bf16_f32) and
-//     v_mfma_f32_32x32x16_bf16, fp32 accumulation;
+// with each operand either K-contiguous ("KC": row-major [rows, K]) or
+// row-contiguous ("RC": [K, rows]), and stored as fp32 or bf16.  The loader
+// stages a tile into LDS in the compute type:
+//   * bf16 mode: bf16 operands are copied, fp32 ones rounded to bf16 (RNE,
+//     v_cvt_pk_bf16_f32); v_mfma_f32_32x32x16_bf16 with fp32 accumulation;
 //   * fp32 mode: v_mfma_f32_32x32x2_f32.
-// LDS always holds a tile K-contiguous per row ([rows][BK + pad]), so the
-// MFMA fragment of a lane is one 16-byte LDS read.  A row-contiguous source
-// is transposed in registers on its way into LDS (8 k-rows x 4 rows per
-// thread; the bf16 pack of (k, k+1) pairs does the transposition).
+// LDS always holds a tile K-contiguous per row ([rows][BK + 16 bytes]), so a
+// lane's MFMA fragment is one 16-byte LDS read.  An RC operand is transposed
+// in registers on its way into LDS: a thread owns a block of k-rows x rows,
+// and packs the k-run of each row (the fp32 -> bf16 pack of a (k, k+1) pair
+// does the transposition; bf16 pairs are joined with v_perm_b32).
 //
+// Loads never branch and are never masked after the fact: a chunk past the
+// end of K is loaded from an out-of-range buffer offset (the hardware returns
+// zeros), and a row past the end of the operand is clamped to its last row
+// (that row only feeds outputs the epilogue discards), so the compiler issues
+// every global load of a K step back to back and waits once.
 // Pipelining: two LDS buffers; the global loads of tile k+1 are in flight
 // while the MFMAs consume tile k; one barrier per K step.
 // Work mapping: one workgroup per output tile (and K split).  Workgroups are
@@ -30,9 +36,11 @@ namespace sru {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, bool BF16_>
 struct Cfg {
@@ -53,38 +61,97 @@ struct Cfg {
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile is a grid of 32x32 MFMA tiles");
 };
 
-// bf16 tiles 256x256x32, 4 waves of 128x128; fp32 tiles 128x128x32, 4 waves of 64x64.
-using CfgBF16 = Cfg<256, 256, 32, 2, 2, true>;
+// bf16: tiles 256x256x64, 4 waves of 128x128.  fp32: 128x128x32, 4 waves of 64x64.
+using CfgBF16 = Cfg<256, 256, 64, 2, 2, true>;
 using CfgF32 = Cfg<128, 128, 32, 2, 2, false>;
 
-__device__ __forceinline__ floatx4 load4(const float* p, long long idx, int valid) {
-  // valid = number of in-bounds elements starting at idx (<= 0: none)
-  floatx4 v;
-  v[0] = valid > 0 ? p[idx] : 0.f;
-  v[1] = valid > 1 ? p[idx + 1] : 0.f;
-  v[2] = valid > 2 ? p[idx + 2] : 0.f;
-  v[3] = valid > 3 ? p[idx + 3] : 0.f;
-  return v;
+// Source element types: fp32, or bf16 carried as raw 16-bit patterns.
+template <class S> struct Src;
+template <> struct Src<float> { static constexpr int E = 4; };     // elements per 16 bytes
+template <> struct Src<uint16_t> { static constexpr int E = 8; };
+
+__device__ __forceinline__ unsigned pack_bf16(float lo, float hi) {
+  bf16x2 v;
+  v[0] = (__bf16)lo;  // RNE (v_cvt_pk_bf16_f32)
+  v[1] = (__bf16)hi;
+  return __builtin_bit_cast(unsigned, v);
+}
+
+// Vector loads go through a buffer resource: the hardware returns zeros for
+// any offset at or beyond its byte size, so an out-of-range chunk is loaded
+// from the sentinel offset kOOB instead of being masked afterwards (no select
+// on the loaded data, so nothing has to wait for it).  Operands must then be
+// smaller than kOOB bytes; the launcher checks this.
+constexpr unsigned kOOB = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, unsigned bytes) {
+  // dword 3 = 0x00020000: 32-bit data format, the raw-buffer setting of gfx9 parts
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
+// Element-wise variant for unaligned or ragged operands: element e is valid
+// when e < valid.
+template <class S>
+__device__ __forceinline__ u32x4 load16_elems(const S* src, long long idx, int valid) {
+  constexpr int E = Src<S>::E;
+  S tmp[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const bool ok = e < valid;
+    const S x = src[ok ? idx + e : 0];
+    tmp[e] = ok ? x : S(0);
+  }
+  return __builtin_bit_cast(u32x4, tmp);
+}
+
+// Element e of a 16-byte chunk as fp32.  The element is copied to a scalar
+// first: a bit cast applied directly to a vector-element lvalue reads element
+// 0 with this compiler.
+__device__ __forceinline__ float f32_of(const u32x4& v, int e) {
+  const unsigned x = v[e];
+  return __builtin_bit_cast(float, x);
 }
 
 // ---- loader for a K-contiguous operand: element (r, k) at src[r*ld + k]
-template <class C, int R, bool VEC>
+template <class C, int R, class S, bool VEC>
 struct LoaderKC {
-  static constexpr int CPR = C::BK / 4;                 // float4 chunks per row
+  static constexpr int E = Src<S>::E;
+  static constexpr int CPR = C::BK / E;  // 16-byte chunks per row
   static constexpr int PER = R * CPR / C::THREADS;
   static_assert(R * CPR % C::THREADS == 0, "tile must split evenly over the threads");
-  floatx4 v[PER];
+  static_assert(C::BF16 || std::is_same<S, float>::value, "fp32 compute takes fp32 operands");
+  u32x4 v[PER];
+  unsigned base[PER];  // VEC: byte offset of the chunk at k = 0 (rows clamped)
 
-  __device__ __forceinline__ void load(const float* src, long long ld, int r0, int rows, int k0,
-                                       int K, int tid) {
+  __device__ __forceinline__ void init(long long ld, int r0, int rows, int tid) {
+    if constexpr (VEC) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int c = tid + i * C::THREADS;
+        const int r = min(r0 + c / CPR, rows - 1);
+        const int k = (c % CPR) * E;
+        base[i] = (unsigned)(((long long)r * ld + k) * sizeof(S));
+      }
+    }
+  }
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, const S* src, long long ld,
+                                       int r0, int rows, int k0, int K, int tid) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int c = tid + i * C::THREADS;
-      const int r = r0 + c / CPR;
-      const int k = k0 + (c % CPR) * 4;
-      const long long idx = (long long)r * ld + k;
-      if (VEC && r < rows && k + 3 < K) v[i] = *reinterpret_cast<const floatx4*>(src + idx);
-      else v[i] = load4(src, idx, r < rows ? K - k : 0);
+      const int k = k0 + (c % CPR) * E;
+      if constexpr (VEC) {
+        const unsigned off = k < K ? base[i] + (unsigned)(k0 * sizeof(S)) : kOOB;
+        v[i] = buf_load16(rs, off);
+      } else {
+        const int r = r0 + c / CPR;
+        v[i] = load16_elems(src, (long long)r * ld + k, r < rows ? K - k : 0);
+      }
     }
   }
   __device__ __forceinline__ void store(unsigned char* lds, int tid) const {
@@ -92,45 +159,66 @@ struct LoaderKC {
     for (int i = 0; i < PER; ++i) {
       const int c = tid + i * C::THREADS;
       const int r = c / CPR;
-      const int k = (c % CPR) * 4;
+      const int k = (c % CPR) * E;
       unsigned char* dst = lds + (r * C::LDK + k) * C::ESZ;
-      if constexpr (C::BF16) {
-        bf16x4 w;
-        w[0] = (__bf16)v[i][0];
-        w[1] = (__bf16)v[i][1];
-        w[2] = (__bf16)v[i][2];
-        w[3] = (__bf16)v[i][3];
-        *reinterpret_cast<bf16x4*>(dst) = w;
+      if constexpr (C::BF16 && std::is_same<S, float>::value) {
+        u32x2 w;
+        w[0] = pack_bf16(f32_of(v[i], 0), f32_of(v[i], 1));
+        w[1] = pack_bf16(f32_of(v[i], 2), f32_of(v[i], 3));
+        *reinterpret_cast<u32x2*>(dst) = w;
       } else {
-        *reinterpret_cast<floatx4*>(dst) = v[i];
+        *reinterpret_cast<u32x4*>(dst) = v[i];
       }
     }
   }
 };
 
 // ---- loader for a row-contiguous operand: element (r, k) at src[k*ld + r].
-// Each thread owns KB k-rows x 4 rows and writes 4 K-contiguous LDS rows.
-template <class C, int R, bool VEC>
+// A thread owns KB k-rows x E rows (one 16-byte chunk per k-row) and writes
+// E LDS rows of KB elements (16 bytes each).  Consecutive threads take
+// consecutive k-blocks of the same rows, so their LDS writes fall in
+// distinct banks.
+template <class C, int R, class S, bool VEC>
 struct LoaderRC {
-  static constexpr int KB = C::BF16 ? 8 : 4;            // k per micro-block (16 LDS bytes)
-  static constexpr int NMB = (R / 4) * (C::BK / KB);
+  static constexpr int E = Src<S>::E;              // rows per chunk
+  static constexpr int KB = C::BF16 ? 8 : 4;       // k per LDS write (16 bytes)
+  static constexpr int NKB = C::BK / KB;
+  static constexpr int NMB = (R / E) * NKB;
   static constexpr int PER = NMB / C::THREADS;
   static_assert(NMB % C::THREADS == 0, "tile must split evenly over the threads");
-  floatx4 v[PER][KB];
+  static_assert(C::BF16 || std::is_same<S, float>::value, "fp32 compute takes fp32 operands");
+  u32x4 v[PER][KB];
+  unsigned base[PER];  // VEC: byte offset of k-row kb*KB at k0 = 0 (rows clamped)
 
-  __device__ __forceinline__ void load(const float* src, long long ld, int r0, int rows, int k0,
-                                       int K, int tid) {
+  __device__ __forceinline__ void init(long long ld, int r0, int rows, int tid) {
+    if constexpr (VEC) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int c = tid + i * C::THREADS;
+        const int kb = c % NKB;
+        // rows is a multiple of E here, so a clamped chunk stays whole
+        const int r = min(r0 + (c / NKB) * E, rows - E);
+        base[i] = (unsigned)(((long long)kb * KB * ld + r) * sizeof(S));
+      }
+    }
+  }
+  __device__ __forceinline__ void load(__amdgpu_buffer_rsrc_t rs, const S* src, long long ld,
+                                       int r0, int rows, int k0, int K, int tid) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int c = tid + i * C::THREADS;
-      const int r = r0 + (c % (R / 4)) * 4;
-      const int kb = k0 + (c / (R / 4)) * KB;
+      const int kb = c % NKB;
 #pragma unroll
       for (int kk = 0; kk < KB; ++kk) {
-        const int k = kb + kk;
-        const long long idx = (long long)k * ld + r;
-        if (VEC && k < K && r + 3 < rows) v[i][kk] = *reinterpret_cast<const floatx4*>(src + idx);
-        else v[i][kk] = load4(src, idx, k < K ? rows - r : 0);
+        const int k = k0 + kb * KB + kk;
+        if constexpr (VEC) {
+          const unsigned off =
+              k < K ? base[i] + (unsigned)(((long long)k0 + kk) * ld * sizeof(S)) : kOOB;
+          v[i][kk] = buf_load16(rs, off);
+        } else {
+          const int r = r0 + (c / NKB) * E;
+          v[i][kk] = load16_elems(src, (long long)k * ld + r, k < K ? rows - r : 0);
+        }
       }
     }
   }
@@ -138,45 +226,53 @@ struct LoaderRC {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int c = tid + i * C::THREADS;
-      const int r = (c % (R / 4)) * 4;
-      const int kb = (c / (R / 4)) * KB;
+      const int kb = c % NKB;
+      const int r = (c / NKB) * E;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        unsigned char* dst = lds + ((r + e) * C::LDK + kb) * C::ESZ;
-        if constexpr (C::BF16) {
-          bf16x8 w;
-#pragma unroll
-          for (int kk = 0; kk < 8; ++kk) w[kk] = (__bf16)v[i][kk][e];
-          *reinterpret_cast<bf16x8*>(dst) = w;
-        } else {
-          floatx4 w;
+      for (int e = 0; e < E; ++e) {
+        unsigned char* dst = lds + ((r + e) * C::LDK + kb * KB) * C::ESZ;
+        u32x4 w;
+        if constexpr (!C::BF16) {
 #pragma unroll
           for (int kk = 0; kk < 4; ++kk) w[kk] = v[i][kk][e];
-          *reinterpret_cast<floatx4*>(dst) = w;
+        } else if constexpr (std::is_same<S, float>::value) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            w[j] = pack_bf16(f32_of(v[i][2 * j], e), f32_of(v[i][2 * j + 1], e));
+        } else {
+          // element e of chunk kk is half (e % 2) of dword e / 2; pair chunks
+          // (2j, 2j+1) into dword j: low half from k = 2j, high from 2j+1.
+          const unsigned sel = (e & 1) ? 0x07060302u : 0x05040100u;
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            w[j] = __builtin_amdgcn_perm(v[i][2 * j + 1][e >> 1], v[i][2 * j][e >> 1], sel);
         }
+        *reinterpret_cast<u32x4*>(dst) = w;
       }
     }
   }
 };
 
-template <class C, int R, bool KC, bool VEC>
-using Loader = typename std::conditional<KC, LoaderKC<C, R, VEC>, LoaderRC<C, R, VEC>>::type;
+template <class C, int R, bool KC, class S, bool VEC>
+using Loader =
+    typename std::conditional<KC, LoaderKC<C, R, S, VEC>, LoaderRC<C, R, S, VEC>>::type;
 
 struct KernelArgs {
-  const float* A;
-  const float* B;
-  float* out;          // C, or the split partials
+  const void* A;
+  const void* B;
+  unsigned a_bytes, b_bytes;  // operand extents for the buffer resources (VEC)
+  float* out;               // C, or the split partials
   long long lda, ldb, ldo;
-  long long split_stride;  // elements between split outputs (0 when splits == 1)
+  long long split_stride;   // elements between split outputs (0 when splits == 1)
   int M, N, K;
-  int k_per_split;     // multiple of BK
+  int k_per_split;          // multiple of BK
   int tiles_m, tiles_n, splits;
   const float* add;
   long long add_ld, add_off;
   int add_count;
 };
 
-template <class C, bool A_KC, bool B_KC, bool VEC>
+template <class C, bool A_KC, bool B_KC, class SA, class SB, bool VEC>
 __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
 
@@ -200,9 +296,15 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
   const int wave = tid >> 6;
   const int wm0 = (wave / C::WAVES_N) * C::WM;
   const int wn0 = (wave % C::WAVES_N) * C::WN;
+  const SA* A = static_cast<const SA*>(g.A);
+  const SB* B = static_cast<const SB*>(g.B);
 
-  Loader<C, C::BM, A_KC, VEC> la;
-  Loader<C, C::BN, B_KC, VEC> lb;
+  Loader<C, C::BM, A_KC, SA, VEC> la;
+  Loader<C, C::BN, B_KC, SB, VEC> lb;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, g.a_bytes);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(B, g.b_bytes);
+  la.init(g.lda, m0, g.M, tid);
+  lb.init(g.ldb, n0, g.N, tid);
 
   floatx16 acc[C::FM][C::FN];
 #pragma unroll
@@ -212,8 +314,8 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  la.load(g.A, g.lda, m0, g.M, kbeg, kend, tid);
-  lb.load(g.B, g.ldb, n0, g.N, kbeg, kend, tid);
+  la.load(ra, A, g.lda, m0, g.M, kbeg, kend, tid);
+  lb.load(rb, B, g.ldb, n0, g.N, kbeg, kend, tid);
   la.store(smem, tid);
   lb.store(smem + C::A_BYTES, tid);
   __syncthreads();
@@ -222,8 +324,8 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
   for (int k0 = kbeg; k0 < kend; k0 += C::BK) {
     const bool next = k0 + C::BK < kend;
     if (next) {
-      la.load(g.A, g.lda, m0, g.M, k0 + C::BK, kend, tid);
-      lb.load(g.B, g.ldb, n0, g.N, k0 + C::BK, kend, tid);
+      la.load(ra, A, g.lda, m0, g.M, k0 + C::BK, kend, tid);
+      lb.load(rb, B, g.ldb, n0, g.N, k0 + C::BK, kend, tid);
     }
     const unsigned char* As = smem + cur * C::STAGE_BYTES;
     const unsigned char* Bs = As + C::A_BYTES;
@@ -269,6 +371,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
   // Epilogue.  32x32 accumulator layout: element e of lane l is row
   // 8*(e/4) + 4*(l/32) + e%4, column l%32 of the MFMA tile.
   float* out = g.out + (long long)split * g.split_stride;
+  const bool full = m0 + C::BM <= g.M && n0 + C::BN <= g.N;
 #pragma unroll
   for (int i = 0; i < C::FM; ++i)
 #pragma unroll
@@ -277,7 +380,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int m = m0 + wm0 + i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-        if (m < g.M && n < g.N) {
+        if (full || (m < g.M && n < g.N)) {
           float val = acc[i][j][e];
           if (g.add_count > 0) {
             const float* ar = g.add + (long long)m * g.add_ld + n;
@@ -312,6 +415,40 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
+// fp32 -> bf16 conversions (RNE).  Plain copy: 4 elements per thread.
+__global__ __launch_bounds__(256) void to_bf16_kernel(const float* __restrict__ src,
+                                                      long long n, uint16_t* __restrict__ dst) {
+  const long long i = ((long long)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i + 3 < n) {
+    const floatx4 v = *reinterpret_cast<const floatx4*>(src + i);
+    u32x2 w;
+    w[0] = pack_bf16(v[0], v[1]);
+    w[1] = pack_bf16(v[2], v[3]);
+    *reinterpret_cast<u32x2*>(dst + i) = w;
+  } else {
+    for (long long j = i; j < n; ++j)
+      dst[j] = __builtin_bit_cast(uint16_t, (__bf16)src[j]);
+  }
+}
+
+// Transposed: dst[c*rows + r] = bf16(src[r*cols + c]) through a 64x64 LDS tile.
+__global__ __launch_bounds__(256) void to_bf16_t_kernel(const float* __restrict__ src, int rows,
+                                                        int cols, uint16_t* __restrict__ dst) {
+  __shared__ float tile[64][65];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    tile[i][tx] = (r < rows && c < cols) ? src[(long long)r * cols + c] : 0.f;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < cols && r < rows)
+      dst[(long long)c * rows + r] = __builtin_bit_cast(uint16_t, (__bf16)tile[tx][i]);
+  }
+}
+
 template <class C>
 int splits_for(const GemmDesc& g) {
   if (g.a_kc) return 1;  // only the K = tokens product (TN) is split
@@ -324,7 +461,18 @@ int splits_for(const GemmDesc& g) {
   return max(1, min(s, 64));
 }
 
-template <class C, bool A_KC, bool B_KC>
+// Vector (buffer) loads need 16-byte aligned chunks that are either wholly
+// inside or wholly outside the operand, i.e. the contiguous extent (K for KC,
+// the row count for RC) and the leading dimension are multiples of a chunk,
+// and an operand smaller than the out-of-range sentinel.
+template <class S>
+bool vec_ok(const void* p, long long ld, int contiguous_extent, long long bytes) {
+  constexpr int E = Src<S>::E;
+  return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % E == 0 &&
+         contiguous_extent % E == 0 && bytes > 0 && bytes < (long long)kOOB;
+}
+
+template <class C, bool A_KC, bool B_KC, class SA, class SB>
 hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
   const int splits = splits_for<C>(g);
   const int kt = (g.K + C::BK - 1) / C::BK;
@@ -359,13 +507,24 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
     a.add_off = g.add_off;
   }
   const int nwg = a.tiles_m * a.tiles_n * a.splits;
+  // operand extents in bytes: rows x ld (KC) or K x ld (RC), last row exact
+  const long long a_bytes =
+      (long long)sizeof(SA) * (A_KC ? (long long)(g.M - 1) * g.lda + g.K
+                                    : (long long)(g.K - 1) * g.lda + g.M);
+  const long long b_bytes =
+      (long long)sizeof(SB) * (B_KC ? (long long)(g.N - 1) * g.ldb + g.K
+                                    : (long long)(g.K - 1) * g.ldb + g.N);
+  const bool vec = vec_ok<SA>(g.A, g.lda, A_KC ? g.K : g.M, a_bytes) &&
+                   vec_ok<SB>(g.B, g.ldb, B_KC ? g.K : g.N, b_bytes);
+  a.a_bytes = vec ? (unsigned)a_bytes : 0u;
+  a.b_bytes = vec ? (unsigned)b_bytes : 0u;
   timing_before(!g.b_kc ? (g.a_kc ? "gemm_nn" : "gemm_tn") : "gemm_nt", st);
-  const bool vec = ((reinterpret_cast<uintptr_t>(g.A) | reinterpret_cast<uintptr_t>(g.B)) & 15) == 0 &&
-                   g.lda % 4 == 0 && g.ldb % 4 == 0;
   if (vec)
-    hipLaunchKernelGGL((gemm_kernel<C, A_KC, B_KC, true>), dim3(nwg), dim3(C::THREADS), 0, st, a);
+    hipLaunchKernelGGL((gemm_kernel<C, A_KC, B_KC, SA, SB, true>), dim3(nwg), dim3(C::THREADS),
+                       0, st, a);
   else
-    hipLaunchKernelGGL((gemm_kernel<C, A_KC, B_KC, false>), dim3(nwg), dim3(C::THREADS), 0, st, a);
+    hipLaunchKernelGGL((gemm_kernel<C, A_KC, B_KC, SA, SB, false>), dim3(nwg), dim3(C::THREADS),
+                       0, st, a);
   timing_after(st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
@@ -378,11 +537,30 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Operand-type combinations that are instantiated: fp32 x fp32 for every
+// layout in both compute modes, plus the bf16-operand products of the layer:
+// U = X W^T (fp32 X, bf16 W), dX = dU W (bf16 dU, bf16 W^T, as NT) and
+// dW = dU^T X (bf16 dU, fp32 X).
+template <class C, bool A_KC, bool B_KC>
+hipError_t launch_types(const GemmDesc& g, hipStream_t st) {
+  if (!g.a_bf16 && !g.b_bf16) return launch_cfg<C, A_KC, B_KC, float, float>(g, st);
+  if constexpr (C::BF16) {
+    if constexpr (A_KC && B_KC) {
+      if (!g.a_bf16 && g.b_bf16) return launch_cfg<C, true, true, float, uint16_t>(g, st);
+      if (g.a_bf16 && g.b_bf16) return launch_cfg<C, true, true, uint16_t, uint16_t>(g, st);
+    }
+    if constexpr (!A_KC && !B_KC) {
+      if (g.a_bf16 && !g.b_bf16) return launch_cfg<C, false, false, uint16_t, float>(g, st);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
 template <class C>
 hipError_t launch_layout(const GemmDesc& g, hipStream_t st) {
-  if (g.a_kc && g.b_kc) return launch_cfg<C, true, true>(g, st);
-  if (g.a_kc && !g.b_kc) return launch_cfg<C, true, false>(g, st);
-  if (!g.a_kc && !g.b_kc) return launch_cfg<C, false, false>(g, st);
+  if (g.a_kc && g.b_kc) return launch_types<C, true, true>(g, st);
+  if (g.a_kc && !g.b_kc) return launch_types<C, true, false>(g, st);
+  if (!g.a_kc && !g.b_kc) return launch_types<C, false, false>(g, st);
   return hipErrorInvalidValue;  // (row-contiguous A with K-contiguous B is not used)
 }
 
@@ -401,7 +579,24 @@ size_t gemm_partial_bytes(int M, int N, int splits) {
 }
 
 hipError_t gemm_launch(const GemmDesc& g, hipStream_t st) {
+  if ((g.a_bf16 || g.b_bf16) && !g.bf16) return hipErrorInvalidValue;
   return g.bf16 ? launch_layout<CfgBF16>(g, st) : launch_layout<CfgF32>(g, st);
+}
+
+hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, bool transpose,
+                          hipStream_t st) {
+  timing_before(transpose ? "to_bf16_t" : "to_bf16", st);
+  if (transpose) {
+    dim3 grid((cols + 63) / 64, (rows + 63) / 64);
+    hipLaunchKernelGGL(to_bf16_t_kernel, grid, dim3(256), 0, st, src, rows, cols, dst);
+  } else {
+    const long long n = (long long)rows * cols;
+    const long long threads = (n + 3) / 4;
+    hipLaunchKernelGGL(to_bf16_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
+                       src, n, dst);
+  }
+  timing_after(st);
+  return hipGetLastError();
 }
 
 }  // namespace sru

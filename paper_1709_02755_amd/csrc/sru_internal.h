@@ -9,21 +9,25 @@
 namespace sru {
 
 // ----------------------------------------------------------------- GEMM
-// C[M,N] = sum_k A(m,k) B(n,k), fp32 in memory, MFMA compute.
+// C[M,N] = sum_k A(m,k) B(n,k), fp32 result, MFMA compute.
 //   A(m,k) = a_kc ? A[m*lda + k] : A[k*lda + m]
 //   B(n,k) = b_kc ? B[n*ldb + k] : B[k*ldb + n]
+// Each operand is fp32 or bf16 (raw uint16 bits) in memory (a_bf16, b_bf16);
+// bf16 operands require bf16 compute (bf16 == true).  fp32 operands are
+// rounded to bf16 (RNE) when staged, in bf16 compute mode.
 // With splits > 1 the reduction is cut into `splits` contiguous K ranges;
 // each writes a partial [M,N] (ld = N) at `partials` + s*M*N, and a second
 // kernel sums them in split order into C.  The optional addend adds
 //   add[m*add_ld + n] (+ add[m*add_ld + add_off + n] when add_count == 2)
 // to the result (used for the highway gradient of dX).
 struct GemmDesc {
-  const float* A;
-  const float* B;
+  const void* A;
+  const void* B;
   float* C;
   int M, N, K;
   long long lda, ldb, ldc;
   bool a_kc, b_kc;
+  bool a_bf16, b_bf16;
   bool bf16;
   int splits;
   float* partials;
@@ -31,6 +35,11 @@ struct GemmDesc {
   long long add_ld, add_off;
   int add_count;
 };
+
+// fp32 -> bf16 (RNE) copy of a [rows, cols] matrix; transposed ([cols, rows])
+// when `transpose`.
+hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, bool transpose,
+                          hipStream_t stream);
 
 // Number of K splits the launcher will use for this product (>= 1) and the
 // partial-buffer bytes it then needs.
@@ -69,7 +78,8 @@ struct ScanBwdArgs {
   const float* b_r;
   const float* c0;
   const uint8_t* mask;
-  float* dU;
+  void* dU;        // fp32, or bf16 bits when du_bf16
+  bool du_bf16;
   float* dxh;
   float* partial;  // [B, 4, ndir*d] per-sequence sums of the v/b gradients
   float* dc0;

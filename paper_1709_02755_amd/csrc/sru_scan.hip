@@ -13,6 +13,8 @@
 // wavefront keeps PF steps of loads in flight).  The main loop covers whole
 // rings only, so it contains no data-dependent branch; the last L % PF steps
 // run in a guarded tail.
+#include <type_traits>
+
 #include "sru_internal.h"
 
 namespace sru {
@@ -126,7 +128,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
 //   dx_hat = dh (1 - r)                    -> dxh (k = 3) / dU block 3 (k = 4)
 //   v/b sums += (df c_p, dr c_p, df, dr);  g <- gc f + df v_f + dr v_r
 // A padded step writes zeros and leaves g unchanged.
-template <int KB, bool MASK, int PF>
+// DUB: store dU as bf16 (RNE), the operand type of bf16 matrix products.
+template <int KB, bool MASK, bool DUB, int PF>
 __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, ScanBwdArgs a) {
   Lane ln;
   if (!decode_lane(s, ln)) return;
@@ -138,7 +141,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
   const long long h_step = (long long)s.B * nfeat;
   const long long u_off = ((long long)ln.b * s.ndir + ln.dir) * KB * s.d + ln.j;
   const float* up = a.U + u_off;
-  float* dup = a.dU + u_off;
+  using DuT = typename std::conditional<DUB, uint16_t, float>::type;
+  DuT* dup = static_cast<DuT*>(a.dU) + u_off;
   const float* xp = KB == 3 ? a.X + (long long)ln.b * s.d_in + ln.j : nullptr;
   const uint8_t* mp = MASK ? a.mask + ln.b : nullptr;
   const float* cpp = a.C + ln.gid;
@@ -202,11 +206,15 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
     sum_dr += dr;
     const float gn = fmaf(dr, vr, fmaf(df, vf, gc * f));
     g = pad ? g : gn;
-    float* du = dup + t * u_step;
-    __builtin_nontemporal_store(du0, du);
-    __builtin_nontemporal_store(df, du + d);
-    __builtin_nontemporal_store(dr, du + 2 * d);
-    if constexpr (KB == 4) __builtin_nontemporal_store(dx, du + 3 * d);
+    DuT* du = dup + t * u_step;
+    auto put = [](float v, DuT* p) {
+      if constexpr (DUB) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)v), p);
+      else __builtin_nontemporal_store(v, p);
+    };
+    put(du0, du);
+    put(df, du + d);
+    put(dr, du + 2 * d);
+    if constexpr (KB == 4) put(dx, du + 3 * d);
     else __builtin_nontemporal_store(dx, dxp + t * h_step);
     c_t = cprev;
   };
@@ -284,8 +292,12 @@ hipError_t bwd_dispatch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t st
   const int lanes = s.B * s.ndir * s.d;
   const int grid = (lanes + kScanThreads - 1) / kScanThreads;
   timing_before("scan_bwd", st);
-  hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, kBwdPF>), dim3(grid), dim3(kScanThreads), 0, st,
-                     s, a);
+  if (a.du_bf16)
+    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, true, kBwdPF>), dim3(grid), dim3(kScanThreads),
+                       0, st, s, a);
+  else
+    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, false, kBwdPF>), dim3(grid), dim3(kScanThreads),
+                       0, st, s, a);
   timing_after(st);
   return hipGetLastError();
 }
