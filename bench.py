@@ -80,26 +80,32 @@ class HipEvents:
 
 
 # ------------------------------------------------------------------ work model
-def kernel_work(w, splits):
+def kernel_work(w, splits, bf16):
     """Algorithmic bytes / flops per launch of each kernel at workload w
     (first layer shape; all layers of a unidirectional d_in = d stack match).
-    Bytes count each element read or written once (4 B fp32)."""
+    Bytes count each element read or written once: fp32 4 B, bf16 2 B."""
     M = w.L * w.B
     nfeat = w.ndir * w.d
     k = 3
     N = w.ndir * k * w.d
     K = w.d_in
     elems = M * nfeat
+    du_b = 2.0 if bf16 else 4.0
     return {
-        "gemm_nt": dict(flops=2.0 * M * N * K),
-        "gemm_nn": dict(flops=2.0 * M * K * N),
-        "gemm_tn": dict(flops=2.0 * N * K * M),
+        "gemm_u": dict(flops=2.0 * M * N * K),     # U = X W^T
+        "gemm_dx": dict(flops=2.0 * M * K * N),    # dX = dU W
+        "gemm_dw": dict(flops=2.0 * N * K * M),    # dW = dU^T X
         # read U (3 blocks) and x, write h and c: 24 B per (t, b, j)
         "scan_fwd": dict(bytes=elems * 4.0 * (k + 1 + 2)),
-        # read U (3 blocks), x, c, dh; write dU (3 blocks), dx_hat: 40 B
-        "scan_bwd": dict(bytes=elems * 4.0 * (k + 3 + k + 1)),
+        # read U (3 blocks), x, c, dh (24 B); write dU (3 blocks, bf16 when
+        # the products are bf16) and dx_hat (4 B): 34 B (bf16) / 40 B (fp32)
+        "scan_bwd": dict(bytes=elems * (4.0 * (k + 3) + du_b * k + 4.0)),
         "reduce_vb": dict(bytes=4.0 * (4 * w.B * nfeat + 4 * nfeat)),
         "splitk_reduce": dict(bytes=4.0 * (splits + 1) * N * K),
+        # fp32 -> bf16 copies of the product operands: W, X, and W^T for dX
+        "bf16_w": dict(bytes=(4.0 + 2.0) * N * K),
+        "bf16_x": dict(bytes=(4.0 + 2.0) * M * K),
+        "bf16_wt": dict(bytes=(4.0 + 2.0) * N * K),
     }
 
 
@@ -157,7 +163,7 @@ def main():
     ap.add_argument("--workload", type=int, default=3, help="index into the workload table")
     ap.add_argument("--profile-steps", type=int, default=5,
                     help="steps run with per-kernel event brackets")
-    ap.add_argument("--cpu-seqs", type=int, default=2,
+    ap.add_argument("--cpu-seqs", type=int, default=8,
                     help="sequences in the CPU-oracle sample (0 = skip)")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -200,7 +206,7 @@ def main():
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {tokens_per_s:.4g} tokens/s")
 
     # --- per-kernel durations: the library brackets each launch with events
-    per_step = w.layers * (2 + 5)
+    per_step = w.layers * 16  # upper bound on kernels per layer and step
     ev = HipEvents(2 * per_step * args.profile_steps + 2)
     lib = sru.lib()
     lib.sru_timing_begin(ev.events, ev.n)
@@ -223,7 +229,7 @@ def main():
         ws_k = lib.sru_gemm_workspace_bytes(sru.OP_TN, w.ndir * 3 * w.d, w.d_in, w.tokens,
                                             w.gemm_dtype)
         splits = max(1, ws_k // (4 * w.ndir * 3 * w.d * w.d_in))
-    work = kernel_work(w, splits)
+    work = kernel_work(w, splits, w.gemm_dtype == sru.GEMM_BF16)
     gemm_peak = MFMA_PEAK_TFLOPS["bf16" if w.gemm_dtype == sru.GEMM_BF16 else "fp32"]
     kernels = {}
     for lab, (tot, cnt) in agg.items():

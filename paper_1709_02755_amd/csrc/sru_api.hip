@@ -85,16 +85,18 @@ sru::GemmDesc gemm_desc(int op, bool bf16, int M, int N, int K, const void* A, l
   return g;
 }
 
-// Forward workspace: bf16 mode keeps a bf16 copy of W [N, d_in].
+// Forward workspace: bf16 mode keeps bf16 copies of W [N, d_in] and
+// X [M, d_in] (the operands of the projection).
 size_t fwd_workspace(const Dims& s, int gemm_dtype) {
-  return gemm_dtype == SRU_GEMM_BF16 ? align_up(2 * (size_t)s.N * (size_t)s.d_in) : 0;
+  if (gemm_dtype != SRU_GEMM_BF16) return 0;
+  return align_up(2 * (size_t)s.N * (size_t)s.d_in) + align_up(2 * (size_t)s.M * (size_t)s.d_in);
 }
 
 // Backward workspace layout:
 //   [dU (fp32, or bf16 in bf16 mode) | dxh (k = 3) | v/b partials |
-//    W^T in bf16 (bf16 mode) | dW split partials]
+//    W^T and X in bf16 (bf16 mode) | dW split partials]
 struct BwdLayout {
-  size_t dU, dxh, partial, wt, splitk, total;
+  size_t dU, dxh, partial, wt, xb, splitk, total;
   int splits;
 };
 
@@ -110,6 +112,8 @@ BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
   off += align_up(sizeof(float) * 4 * (size_t)s.B * (size_t)s.nfeat);
   w.wt = off;
   if (bf16) off += align_up(2 * (size_t)s.N * (size_t)s.d_in);
+  w.xb = off;
+  if (bf16) off += align_up(2 * (size_t)s.M * (size_t)s.d_in);
   sru::GemmDesc dw = gemm_desc(SRU_OP_TN, bf16, (int)s.N, s.d_in, (int)s.M, nullptr, s.N,
                                nullptr, s.d_in, nullptr, s.d_in);
   w.splits = sru::gemm_splits(dw);
@@ -212,17 +216,23 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
     if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
   }
 
-  // U = X Wcat^T (Sec. 2.1).  bf16 mode: W rounded once into the workspace,
-  // X rounded as it is staged.
+  // U = X Wcat^T (Sec. 2.1).  bf16 mode: W and X rounded once into the
+  // workspace, so both operands of the product are K-contiguous bf16.
   const void* Wop = W;
+  const void* Xop = X;
   if (bf16) {
     uint16_t* wb = static_cast<uint16_t*>(workspace);
-    if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wb, false, stream))) return e;
+    uint16_t* xb = reinterpret_cast<uint16_t*>(static_cast<unsigned char*>(workspace) +
+                                               align_up(2 * (size_t)s.N * (size_t)d_in));
+    if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wb, false, stream, "bf16_w"))) return e;
+    if (int e = hip_status(sru::to_bf16_launch(X, (int)s.M, d_in, xb, false, stream, "bf16_x"))) return e;
     Wop = wb;
+    Xop = xb;
   }
-  sru::GemmDesc g = gemm_desc(SRU_OP_NT, bf16, (int)s.M, (int)s.N, d_in, X, d_in, Wop, d_in, U,
+  sru::GemmDesc g = gemm_desc(SRU_OP_NT, bf16, (int)s.M, (int)s.N, d_in, Xop, d_in, Wop, d_in, U,
                               s.N);
-  g.b_bf16 = bf16;
+  g.a_bf16 = g.b_bf16 = bf16;
+  g.label = "gemm_u";
   if (int e = hip_status(sru::gemm_launch(g, stream))) return e;
 
   sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last};
@@ -269,12 +279,13 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   //    an NT one with both operands K-contiguous bf16.
   sru::GemmDesc gx;
   if (bf16) {
-    if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wt, true, stream))) return e;
+    if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wt, true, stream, "bf16_wt"))) return e;
     gx = gemm_desc(SRU_OP_NT, true, (int)s.M, d_in, (int)s.N, dU, s.N, wt, s.N, dX, d_in);
     gx.a_bf16 = gx.b_bf16 = true;
   } else {
     gx = gemm_desc(SRU_OP_NN, false, (int)s.M, d_in, (int)s.N, dU, s.N, W, d_in, dX, d_in);
   }
+  gx.label = "gemm_dx";
   if (s.k == 3) {
     gx.add = dxh;
     gx.add_ld = s.nfeat;
@@ -283,10 +294,20 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   }
   if (int e = hip_status(sru::gemm_launch(gx, stream))) return e;
 
-  // 3. dW = dU^T X (reduction over all tokens, split over K)
-  sru::GemmDesc gw = gemm_desc(SRU_OP_TN, bf16, (int)s.N, d_in, (int)s.M, dU, s.N, X, d_in, dW,
+  // 3. dW = dU^T X (reduction over all tokens, split over K).  bf16 mode: X
+  //    rounded once into the workspace; both operands are then row-contiguous
+  //    bf16.
+  const void* Xop = X;
+  if (bf16) {
+    uint16_t* xb = reinterpret_cast<uint16_t*>(ws + lay.xb);
+    if (int e = hip_status(sru::to_bf16_launch(X, (int)s.M, d_in, xb, false, stream, "bf16_x")))
+      return e;
+    Xop = xb;
+  }
+  sru::GemmDesc gw = gemm_desc(SRU_OP_TN, bf16, (int)s.N, d_in, (int)s.M, dU, s.N, Xop, d_in, dW,
                                d_in);
-  gw.a_bf16 = bf16;
+  gw.a_bf16 = gw.b_bf16 = bf16;
+  gw.label = "gemm_dw";
   gw.partials = splitk;
   return hip_status(sru::gemm_launch(gw, stream));
 }

@@ -272,22 +272,71 @@ struct KernelArgs {
   int add_count;
 };
 
-template <class C, bool A_KC, bool B_KC, class SA, class SB, bool VEC>
-__global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
+// Epilogue shared by the kernels.  32x32 accumulator layout: element e of
+// lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32 of the MFMA tile.
+// ADD = number of addend tensors (0..2, see KernelArgs).  For each MFMA
+// tile the addend loads are issued together (rows and columns clamped into
+// range, so no branch separates them) before the stores.
+template <class C, int ADD>
+__device__ __forceinline__ void write_tile_add(const KernelArgs& g,
+                                               const floatx16 (&acc)[C::FM][C::FN], int m0,
+                                               int n0, int wm0, int wn0, int lane, int split) {
+  float* out = g.out + (long long)split * g.split_stride;
+  const bool full = m0 + C::BM <= g.M && n0 + C::BN <= g.N;
+#pragma unroll
+  for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+      const int n = n0 + wn0 + j * 32 + (lane & 31);
+      const int mb = m0 + wm0 + i * 32 + (lane >> 5) * 4;
+      float v[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) v[e] = acc[i][j][e];
+      if constexpr (ADD > 0) {
+        const int nc = min(n, g.N - 1);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int mc = min(mb + (e >> 2) * 8 + (e & 3), g.M - 1);
+          const float* ar = g.add + (long long)mc * g.add_ld + nc;
+          v[e] += ar[0];
+          if constexpr (ADD > 1) v[e] += ar[g.add_off];
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int m = mb + (e >> 2) * 8 + (e & 3);
+        if (full || (m < g.M && n < g.N)) out[(long long)m * g.ldo + n] = v[e];
+      }
+    }
+}
 
-  // XCD-aware remap of the linear workgroup id (round-robin dispatch).
+// XCD-aware remap of the linear workgroup id: workgroups are dispatched
+// round-robin over the 8 XCDs; each XCD gets a contiguous run of tiles.
+struct TileIdx {
+  int split, tm, tn;
+};
+__device__ __forceinline__ TileIdx tile_of(const KernelArgs& g) {
   const int nwg = gridDim.x;
   const int w = blockIdx.x;
   const int q = nwg / 8, rmd = nwg % 8, x = w % 8;
   const int u = x * q + (x < rmd ? x : rmd) + w / 8;
   const int nt = g.tiles_m * g.tiles_n;
-  const int split = u / nt;
-  const int t = u - split * nt;
-  const int tm = t / g.tiles_n;
-  const int tn = t - tm * g.tiles_n;
-  const int m0 = tm * C::BM;
-  const int n0 = tn * C::BN;
+  TileIdx r;
+  r.split = u / nt;
+  const int t = u - r.split * nt;
+  r.tm = t / g.tiles_n;
+  r.tn = t - r.tm * g.tiles_n;
+  return r;
+}
+
+template <class C, bool A_KC, bool B_KC, class SA, class SB, bool VEC, int ADD>
+__global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
+
+  const TileIdx ti = tile_of(g);
+  const int split = ti.split;
+  const int m0 = ti.tm * C::BM;
+  const int n0 = ti.tn * C::BN;
   const int kbeg = split * g.k_per_split;
   const int kend = min(g.K, kbeg + g.k_per_split);
 
@@ -368,29 +417,224 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
     cur ^= 1;
   }
 
-  // Epilogue.  32x32 accumulator layout: element e of lane l is row
-  // 8*(e/4) + 4*(l/32) + e%4, column l%32 of the MFMA tile.
-  float* out = g.out + (long long)split * g.split_stride;
-  const bool full = m0 + C::BM <= g.M && n0 + C::BN <= g.N;
+  write_tile_add<C, ADD>(g, acc, m0, n0, wm0, wn0, lane, split);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 x bf16 products with global -> LDS loads that bypass registers.
+// Buffer loads with the LDS flag write each lane's 16 bytes straight into
+// LDS at (wave-uniform base + 16 * lane); a ring of STAGES tiles lets the
+// loads run STAGES-1 K steps ahead of the MFMAs at no register cost.  Both
+// operands have the same layout, selected by RC:
+//
+// K-contiguous (RC = false; U = X W^T and dX = dU W as dU (W^T)^T):
+//   row r of a tile is 64 bytes (BK = 32 k) at r*64, its four 16-byte
+//   k-chunks permuted as slot = chunk ^ swz(r), swz(r) = ((r>>1) ^ (r>>3)) & 3,
+//   which keeps the rows one ds_read_b128 phase touches (8 rows over 32
+//   banks or 16 over 64) on distinct banks.  A wave load fills 16 rows:
+//   lane l takes row l/4, slot l%4.  A fragment is one ds_read_b128.
+// Row-contiguous (RC = true; dW = dU^T X, both operands [K, rows]):
+//   the tile is kept as loaded, k-row s at s*512 (256 rows of bf16), its
+//   32 16-byte row-chunks permuted as slot = chunk ^ 2*(s & 3).  A wave load
+//   fills 2 k-rows: lane l takes k-row l/32, slot l%32.  A fragment (8
+//   consecutive k of one row) is two ds_read_b64_tr_b16: within each group
+//   of 16 lanes, input lane 4s+q names k-row s, rows 4q..4q+3 of the group's
+//   16 rows, and output lane i receives that k-run of row i.  The four
+//   k-rows x 32 bytes one group reads land on 8 distinct 16-byte slots.
+using CfgDirect = Cfg<256, 256, 32, 2, 2, true>;
+constexpr int kDirectStages = 4;
+
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+template <int STAGES, int ADD, bool RC>
+__global__ __launch_bounds__(256) void gemm_direct_kernel(KernelArgs g) {
+  using C = CfgDirect;
+  constexpr int OPB = C::BM * C::BK * 2;       // bytes per operand per stage (16 KiB)
+  constexpr int STB = 2 * OPB;                 // bytes per stage
+  constexpr int BPW = OPB / 1024 / 4;          // 1 KiB load blocks per operand per wave
+  static_assert(C::BM == C::BN && C::BM == 256, "square 256 tile");
+  static_assert(C::BK / C::KSLAB == 2, "two fragment slabs per stage");
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * STB];
+  typedef __attribute__((address_space(3))) void lds_t;
+  typedef __attribute__((address_space(3))) v4i16 lds_v4;
+
+  const TileIdx ti = tile_of(g);
+  const int m0 = ti.tm * C::BM;
+  const int n0 = ti.tn * C::BN;
+  const int kbeg = ti.split * g.k_per_split;
+  const int kend = min(g.K, kbeg + g.k_per_split);
+  const int nk = (kend - kbeg + C::BK - 1) / C::BK;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm0 = (wave / C::WAVES_N) * C::WM;
+  const int wn0 = (wave % C::WAVES_N) * C::WN;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(g.A, g.a_bytes);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(g.B, g.b_bytes);
+
+  // Per-lane source offset of each load block at k = 0 and the k (relative
+  // to the stage) its data belongs to.  KC: rows past the end are clamped to
+  // the last row (they only feed discarded outputs).  RC: chunks of rows
+  // past the end get the out-of-range bit (rows % 8 == 0, chunks are whole).
+  unsigned offa[BPW], offb[BPW], rowoob[BPW];
+  int kk[BPW];
+#pragma unroll
+  for (int j = 0; j < BPW; ++j) {
+    rowoob[j] = 0;
+    const int blk = wave * BPW + j;
+    if constexpr (!RC) {
+      const int r = blk * 16 + (lane >> 2);
+      const int chunk = (lane & 3) ^ swz(r);
+      kk[j] = chunk * 8;
+      const int ra_ = min(m0 + r, g.M - 1);
+      const int rb_ = min(n0 + r, g.N - 1);
+      offa[j] = (unsigned)(((long long)ra_ * g.lda + chunk * 8) * 2);
+      offb[j] = (unsigned)(((long long)rb_ * g.ldb + chunk * 8) * 2);
+    } else {
+      const int srow = blk * 2 + (lane >> 5);
+      const int chunk = (lane & 31) ^ (2 * (srow & 3));
+      kk[j] = srow;
+      const int ra_ = m0 + chunk * 8;
+      const int rb_ = n0 + chunk * 8;
+      offa[j] = (unsigned)(((long long)srow * g.lda + min(ra_, g.M - 8)) * 2);
+      offb[j] = (unsigned)(((long long)srow * g.ldb + min(rb_, g.N - 8)) * 2);
+      rowoob[j] = ((unsigned)(ra_ >= g.M) << 31) | ((unsigned)(rb_ >= g.N) << 30);
+    }
+  }
+  auto issue = [&](int kt) {
+    const int k0 = kbeg + kt * C::BK;
+    unsigned char* st = smem + (kt % STAGES) * STB;
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+      // past the end of K: set the top bit, an out-of-range offset, and the
+      // hardware writes zeros
+      const unsigned oob = (unsigned)(k0 + kk[j] >= kend) << 31;
+      const unsigned da = RC ? (unsigned)((long long)k0 * g.lda * 2) : (unsigned)(k0 * 2);
+      const unsigned db = RC ? (unsigned)((long long)k0 * g.ldb * 2) : (unsigned)(k0 * 2);
+      const int blk = wave * BPW + j;
+      // rowoob: bit 31 marks A's chunk, bit 30 B's (shifted up to bit 31)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_t*)(st + blk * 1024), 16,
+                                               (offa[j] + da) | oob | (rowoob[j] & kOOB), 0, 0,
+                                               0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_t*)(st + OPB + blk * 1024), 16,
+                                               (offb[j] + db) | oob | (rowoob[j] << 1), 0, 0, 0);
+    }
+  };
+
+  floatx16 acc[C::FM][C::FN];
 #pragma unroll
   for (int i = 0; i < C::FM; ++i)
 #pragma unroll
-    for (int j = 0; j < C::FN; ++j) {
-      const int n = n0 + wn0 + j * 32 + (lane & 31);
+    for (int j = 0; j < C::FN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int m = m0 + wm0 + i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-        if (full || (m < g.M && n < g.N)) {
-          float val = acc[i][j][e];
-          if (g.add_count > 0) {
-            const float* ar = g.add + (long long)m * g.add_ld + n;
-            val += ar[0];
-            if (g.add_count > 1) val += ar[g.add_off];
-          }
-          out[(long long)m * g.ldo + n] = val;
-        }
-      }
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s);
+
+  // One 16-byte MFMA fragment: k-chunk c (8 k) of tile row `row`.
+  auto frag = [&](const unsigned char* base, int row, int c) -> floatx4 {
+    if constexpr (!RC) {
+      return *reinterpret_cast<const floatx4*>(base + row * 64 + ((c ^ swz(row)) << 4));
+    } else {
+      // this lane's role in its 16-lane group: k-row s, rows 4q..4q+3
+      const int gl = lane & 15;
+      const int r = (row & ~15) + 4 * (gl & 3);
+      const int kr = c * 8 + (gl >> 2);
+      auto addr = [&](int k) {
+        return base + k * 512 + (((r >> 3) ^ (2 * (k & 3))) << 4) + (r & 7) * 2;
+      };
+      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(addr(kr)));
+      const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(addr(kr + 4)));
+      floatx4 f;
+      f[0] = __builtin_bit_cast(float, __builtin_shufflevector(lo, lo, 0, 1));
+      f[1] = __builtin_bit_cast(float, __builtin_shufflevector(lo, lo, 2, 3));
+      f[2] = __builtin_bit_cast(float, __builtin_shufflevector(hi, hi, 0, 1));
+      f[3] = __builtin_bit_cast(float, __builtin_shufflevector(hi, hi, 2, 3));
+      return f;
     }
+  };
+  // Wait until this wave's part of stage kt has landed: the loads of later
+  // stages (8 instructions per stage per wave) may stay in flight.
+  // s_waitcnt immediate: vmcnt in bits [3:0] and [15:14], expcnt 7 and
+  // lgkmcnt 15 (no wait on those).
+  auto wait_stage = [&](int kt) {
+    const int later = min(STAGES - 2, nk - 1 - kt);
+    if (later >= 2) __builtin_amdgcn_s_waitcnt((16 >> 4) << 14 | (16 & 15) | 0x0F70);
+    else if (later == 1) __builtin_amdgcn_s_waitcnt(8 | 0x0F70);
+    else __builtin_amdgcn_s_waitcnt(0x0F70);
+  };
+  // Workgroup barrier without the release fence of __syncthreads (which
+  // would wait for every outstanding vector memory operation, i.e. drain the
+  // prefetched stages): this wave's LDS reads are waited for explicitly, the
+  // stage's loads by wait_stage, and the memory clobbers keep the compiler
+  // from moving LDS accesses across it.
+  auto barrier = [] {
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0) only (vmcnt 63, expcnt 7)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  struct Frags {
+    floatx4 a[C::FM], b[C::FN];
+  };
+  auto load_frags = [&](Frags& f, int kt, int sl) {
+    const unsigned char* As = smem + (kt % STAGES) * STB;
+    const unsigned char* Bs = As + OPB;
+    const int c = 2 * sl + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) f.a[i] = frag(As, wm0 + i * 32 + (lane & 31), c);
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) f.b[j] = frag(Bs, wn0 + j * 32 + (lane & 31), c);
+  };
+  auto mfmas = [&](const Frags& f) {
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8, f.a[i]), __builtin_bit_cast(bf16x8, f.b[j]), acc[i][j], 0,
+            0, 0);
+  };
+
+  // Software pipeline over the two fragment slabs of a stage (f0: k-chunks
+  // 0-1, f1: k-chunks 2-3): a slab's fragments are read from LDS before the
+  // MFMAs of the previous slab are issued.  The barrier that publishes stage
+  // kt+1 sits before the MFMAs of slab 1 of stage kt; it also ends every
+  // wave's reads of stage kt, which frees that slot for the loads issued at
+  // the top of the next iteration.
+  Frags f0, f1;
+  if (nk > 0) {
+    wait_stage(0);
+    barrier();
+    load_frags(f0, 0, 0);
+  }
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);  // slot of stage kt-1, free
+    load_frags(f1, kt, 1);
+    mfmas(f0);
+    if (kt + 1 < nk) {
+      wait_stage(kt + 1);
+      barrier();
+      load_frags(f0, kt + 1, 0);
+    } else {
+      // last stage: only f1's reads are outstanding; waiting here too keeps
+      // the join of the two paths from waiting on the newer f0 reads
+      __builtin_amdgcn_s_waitcnt(0xC07F);
+    }
+    mfmas(f1);
+  }
+  write_tile_add<C, ADD>(g, acc, m0, n0, wm0, wn0, lane, ti.split);
+}
+
+template <int ADD, bool RC>
+void launch_direct(const KernelArgs& a, int nwg, hipStream_t st) {
+  hipLaunchKernelGGL((gemm_direct_kernel<kDirectStages, ADD, RC>), dim3(nwg), dim3(256), 0, st,
+                     a);
 }
 
 // Sum of split partials in split order, plus the optional addend.
@@ -472,6 +716,19 @@ bool vec_ok(const void* p, long long ld, int contiguous_extent, long long bytes)
          contiguous_extent % E == 0 && bytes > 0 && bytes < (long long)kOOB;
 }
 
+template <class C, bool A_KC, bool B_KC, class SA, class SB, bool VEC>
+void launch_staged(const KernelArgs& a, int nwg, hipStream_t st) {
+  if (a.add_count == 2)
+    hipLaunchKernelGGL((gemm_kernel<C, A_KC, B_KC, SA, SB, VEC, 2>), dim3(nwg), dim3(C::THREADS), 0,
+                       st, a);
+  else if (a.add_count == 1)
+    hipLaunchKernelGGL((gemm_kernel<C, A_KC, B_KC, SA, SB, VEC, 1>), dim3(nwg), dim3(C::THREADS), 0,
+                       st, a);
+  else
+    hipLaunchKernelGGL((gemm_kernel<C, A_KC, B_KC, SA, SB, VEC, 0>), dim3(nwg), dim3(C::THREADS), 0,
+                       st, a);
+}
+
 template <class C, bool A_KC, bool B_KC, class SA, class SB>
 hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
   const int splits = splits_for<C>(g);
@@ -518,13 +775,22 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
                    vec_ok<SB>(g.B, g.ldb, B_KC ? g.K : g.N, b_bytes);
   a.a_bytes = vec ? (unsigned)a_bytes : 0u;
   a.b_bytes = vec ? (unsigned)b_bytes : 0u;
-  timing_before(!g.b_kc ? (g.a_kc ? "gemm_nn" : "gemm_tn") : "gemm_nt", st);
-  if (vec)
-    hipLaunchKernelGGL((gemm_kernel<C, A_KC, B_KC, SA, SB, true>), dim3(nwg), dim3(C::THREADS),
-                       0, st, a);
+  timing_before(g.label ? g.label : !g.b_kc ? (g.a_kc ? "gemm_nn" : "gemm_tn") : "gemm_nt", st);
+  // bf16 operands of one layout, chunk-aligned: the direct-to-LDS kernel
+  constexpr bool kBothBf16 =
+      std::is_same<SA, uint16_t>::value && std::is_same<SB, uint16_t>::value;
+  constexpr bool kDirectOk = C::BF16 && kBothBf16 && A_KC == B_KC && C::BM == CfgDirect::BM &&
+                             C::BN == CfgDirect::BN && C::BK % CfgDirect::BK == 0;
+  if (kDirectOk && vec) {
+    constexpr bool RC = !A_KC;
+    if (a.add_count == 2) launch_direct<2, RC>(a, nwg, st);
+    else if (a.add_count == 1) launch_direct<1, RC>(a, nwg, st);
+    else launch_direct<0, RC>(a, nwg, st);
+  }
+  else if (vec)
+    launch_staged<C, A_KC, B_KC, SA, SB, true>(a, nwg, st);
   else
-    hipLaunchKernelGGL((gemm_kernel<C, A_KC, B_KC, SA, SB, false>), dim3(nwg), dim3(C::THREADS),
-                       0, st, a);
+    launch_staged<C, A_KC, B_KC, SA, SB, false>(a, nwg, st);
   timing_after(st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
@@ -551,6 +817,7 @@ hipError_t launch_types(const GemmDesc& g, hipStream_t st) {
     }
     if constexpr (!A_KC && !B_KC) {
       if (g.a_bf16 && !g.b_bf16) return launch_cfg<C, false, false, uint16_t, float>(g, st);
+      if (g.a_bf16 && g.b_bf16) return launch_cfg<C, false, false, uint16_t, uint16_t>(g, st);
     }
   }
   return hipErrorInvalidValue;
@@ -584,8 +851,8 @@ hipError_t gemm_launch(const GemmDesc& g, hipStream_t st) {
 }
 
 hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, bool transpose,
-                          hipStream_t st) {
-  timing_before(transpose ? "to_bf16_t" : "to_bf16", st);
+                          hipStream_t st, const char* label) {
+  timing_before(label, st);
   if (transpose) {
     dim3 grid((cols + 63) / 64, (rows + 63) / 64);
     hipLaunchKernelGGL(to_bf16_t_kernel, grid, dim3(256), 0, st, src, rows, cols, dst);

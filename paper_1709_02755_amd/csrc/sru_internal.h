@@ -34,12 +34,13 @@ struct GemmDesc {
   const float* add;
   long long add_ld, add_off;
   int add_count;
+  const char* label;  // name for the measurement hook (nullptr: by layout)
 };
 
 // fp32 -> bf16 (RNE) copy of a [rows, cols] matrix; transposed ([cols, rows])
 // when `transpose`.
 hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, bool transpose,
-                          hipStream_t stream);
+                          hipStream_t stream, const char* label);
 
 // Number of K splits the launcher will use for this product (>= 1) and the
 // partial-buffer bytes it then needs.
