@@ -154,6 +154,84 @@ def cpu_baseline(w, inp, nseq):
                       f"({tokens} tokens), fp64 NumPy, per-step projections"}
 
 
+# ------------------------------------------------------------------ counters
+COPY_BYTES = 1 << 30  # calibration copy: 1 GiB read + 1 GiB written
+
+
+def copy_calibration(reps):
+    """A plain elementwise copy of known size (torch's own kernel), run under
+    rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE to scale those counters."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    log(f"copy calibration: {reps} x {COPY_BYTES} bytes")
+
+
+def _pmc_rows(path):
+    import csv
+    rows = []
+    for f in glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            rows.extend(csv.DictReader(fh))
+    if not rows:
+        raise SystemExit(f"no *counter_collection.csv under {path}")
+    return rows
+
+
+def _per_kernel(rows, counter):
+    """Average counter value per dispatch, by kernel-name key."""
+    acc = {}
+    for r in rows:
+        if r.get("Counter_Name") != counter:
+            continue
+        name = r.get("Kernel_Name", "")
+        a = acc.setdefault(name, [0.0, 0])
+        a[0] += float(r["Counter_Value"])
+        a[1] += 1
+    return {k: v[0] / v[1] for k, v in acc.items()}
+
+
+# kernel-name substrings -> labels of the per-launch table
+KERNEL_KEYS = [("scan_fwd_kernel", "scan_fwd"), ("scan_bwd_kernel", "scan_bwd"),
+               ("reduce_vb_kernel", "reduce_vb"), ("splitk_reduce_kernel", "splitk_reduce"),
+               # the three products of the bf16 path (template args: stages, addend, layout)
+               ("gemm_direct_kernel<4, 0, false>", "gemm_u"),
+               ("gemm_direct_kernel<4, 1, false>", "gemm_dx"),
+               ("gemm_direct_kernel<4, 0, true>", "gemm_dw")]
+
+
+def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out):
+    """Turn four rocprofv3 --pmc runs (FETCH_SIZE and WRITE_SIZE of the bench
+    and of the calibration copy) into per-launch HBM bytes for the scans."""
+    def one(d, counter, key):
+        vals = _per_kernel(_pmc_rows(d), counter)
+        hits = {k: v for k, v in vals.items() if key in k}
+        if not hits:
+            raise SystemExit(f"{key} not in {d}")
+        return max(hits.values())
+
+    # FETCH_SIZE / WRITE_SIZE are KiB per dispatch
+    scale_f = COPY_BYTES / (1024.0 * one(copy_fetch_dir, "FETCH_SIZE", "elementwise"))
+    scale_w = COPY_BYTES / (1024.0 * one(copy_write_dir, "WRITE_SIZE", "elementwise"))
+    kernels = {}
+    for key, label in KERNEL_KEYS:
+        try:
+            f = one(fetch_dir, "FETCH_SIZE", key) * 1024.0 * scale_f
+            w = one(write_dir, "WRITE_SIZE", key) * 1024.0 * scale_w
+        except SystemExit:
+            continue
+        kernels[label] = {"fetch_bytes_per_launch": f, "write_bytes_per_launch": w,
+                          "hbm_bytes_per_launch": f + w}
+    res = {"source_hash": source_hash(), "copy_scale_fetch": scale_f,
+           "copy_scale_write": scale_w, "kernels": kernels}
+    with open(out, "w") as fh:
+        json.dump(res, fh, indent=1)
+    print(json.dumps(res, indent=1))
+
+
 # ------------------------------------------------------------------ main
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
@@ -163,9 +241,20 @@ def main():
     ap.add_argument("--workload", type=int, default=3, help="index into the workload table")
     ap.add_argument("--profile-steps", type=int, default=5,
                     help="steps run with per-kernel event brackets")
-    ap.add_argument("--cpu-seqs", type=int, default=8,
+    ap.add_argument("--cpu-seqs", type=int, default=32,
                     help="sequences in the CPU-oracle sample (0 = skip)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="REPS",
+                    help="only run a 1 GiB copy REPS times (counter calibration)")
+    ap.add_argument("--summarize-pmc", nargs=5,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR", "OUT"),
+                    help="build the per-launch HBM traffic table from rocprofv3 --pmc runs")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc)
+        return
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(--gpus must be 1)", file=sys.stderr)
