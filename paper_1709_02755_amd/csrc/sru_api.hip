@@ -92,6 +92,16 @@ size_t fwd_workspace(const Dims& s, int gemm_dtype) {
   return align_up(2 * (size_t)s.N * (size_t)s.d_in) + align_up(2 * (size_t)s.M * (size_t)s.d_in);
 }
 
+// The dW product of sru_backward (the workspace is sized from this same
+// descriptor, so the split count it is sized for is the one launched).
+sru::GemmDesc dw_desc(const Dims& s, bool bf16, const void* dU, const void* X, float* dW) {
+  sru::GemmDesc g = gemm_desc(SRU_OP_TN, bf16, (int)s.N, s.d_in, (int)s.M, dU, s.N, X, s.d_in,
+                              dW, s.d_in);
+  g.a_bf16 = g.b_bf16 = bf16;
+  g.label = "gemm_dw";
+  return g;
+}
+
 // Backward workspace layout:
 //   [dU (fp32, or bf16 in bf16 mode) | dxh (k = 3) | v/b partials |
 //    W^T and X in bf16 (bf16 mode) | dW split partials]
@@ -114,9 +124,7 @@ BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
   if (bf16) off += align_up(2 * (size_t)s.N * (size_t)s.d_in);
   w.xb = off;
   if (bf16) off += align_up(2 * (size_t)s.M * (size_t)s.d_in);
-  sru::GemmDesc dw = gemm_desc(SRU_OP_TN, bf16, (int)s.N, s.d_in, (int)s.M, nullptr, s.N,
-                               nullptr, s.d_in, nullptr, s.d_in);
-  w.splits = sru::gemm_splits(dw);
+  w.splits = sru::gemm_splits(dw_desc(s, bf16, nullptr, nullptr, nullptr));
   w.splitk = off;
   off += align_up(sru::gemm_partial_bytes((int)s.N, s.d_in, w.splits));
   w.total = off;
@@ -267,6 +275,12 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   float* partial = reinterpret_cast<float*>(ws + lay.partial);
   uint16_t* wt = reinterpret_cast<uint16_t*>(ws + lay.wt);
   float* splitk = reinterpret_cast<float*>(ws + lay.splitk);
+  uint16_t* xb = reinterpret_cast<uint16_t*>(ws + lay.xb);
+  sru::GemmDesc gw = dw_desc(s, bf16, dU, bf16 ? static_cast<const void*>(xb) : X, dW);
+  gw.partials = splitk;
+  // the split partials were sized for lay.splits; refuse (before enqueueing
+  // anything) rather than overrun if the launch plan ever differed
+  if (sru::gemm_splits(gw) > lay.splits) return SRU_E_WORKSPACE;
 
   // 1. reverse gradient scan and the v/b sums; dU is written in the operand
   //    type of the products that read it
@@ -297,18 +311,10 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   // 3. dW = dU^T X (reduction over all tokens, split over K).  bf16 mode: X
   //    rounded once into the workspace; both operands are then row-contiguous
   //    bf16.
-  const void* Xop = X;
   if (bf16) {
-    uint16_t* xb = reinterpret_cast<uint16_t*>(ws + lay.xb);
     if (int e = hip_status(sru::to_bf16_launch(X, (int)s.M, d_in, xb, false, stream, "bf16_x")))
       return e;
-    Xop = xb;
   }
-  sru::GemmDesc gw = gemm_desc(SRU_OP_TN, bf16, (int)s.N, d_in, (int)s.M, dU, s.N, Xop, d_in, dW,
-                               d_in);
-  gw.a_bf16 = gw.b_bf16 = bf16;
-  gw.label = "gemm_dw";
-  gw.partials = splitk;
   return hip_status(sru::gemm_launch(gw, stream));
 }
 

@@ -434,31 +434,116 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
 //   banks or 16 over 64) on distinct banks.  A wave load fills 16 rows:
 //   lane l takes row l/4, slot l%4.  A fragment is one ds_read_b128.
 // Row-contiguous (RC = true; dW = dU^T X, both operands [K, rows]):
-//   the tile is kept as loaded, k-row s at s*512 (256 rows of bf16), its
-//   32 16-byte row-chunks permuted as slot = chunk ^ 2*(s & 3).  A wave load
-//   fills 2 k-rows: lane l takes k-row l/32, slot l%32.  A fragment (8
-//   consecutive k of one row) is two ds_read_b64_tr_b16: within each group
-//   of 16 lanes, input lane 4s+q names k-row s, rows 4q..4q+3 of the group's
-//   16 rows, and output lane i receives that k-run of row i.  The four
-//   k-rows x 32 bytes one group reads land on 8 distinct 16-byte slots.
-using CfgDirect = Cfg<256, 256, 32, 2, 2, true>;
-constexpr int kDirectStages = 4;
+//   the tile is kept as loaded, k-row s at s*2R bytes (R rows of bf16), its
+//   R/8 16-byte row-chunks permuted as slot = chunk ^ 2*(s & 3).  A wave
+//   load fills 512/R k-rows.  A fragment (8 consecutive k of one row) is two
+//   ds_read_b64_tr_b16: within each group of 16 lanes, input lane 4s+q names
+//   k-row s, rows 4q..4q+3 of the group's 16 rows, and output lane i
+//   receives that k-run of row i.  The four k-rows x 32 bytes one group
+//   reads land on 8 distinct 16-byte slots.
+//
+// Tiles are BM x BN x 32 with 4 waves of (BM/2) x (BN/2).  A 256 x 128 tile
+// with 3 stages needs 72 KiB of LDS and 128 accumulator registers per lane,
+// so two workgroups share a CU and one's epilogue (the fp32 output write)
+// overlaps the other's MFMAs.
+template <int BM_, int BN_, int STAGES_>
+struct DCfg {
+  static constexpr int BM = BM_, BN = BN_, BK = 32, STAGES = STAGES_;
+  static constexpr int WAVES_M = 2, WAVES_N = 2;
+  static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+  static constexpr int FM = WM / 32, FN = WN / 32;
+  static constexpr int KSLAB = 16;
+  static constexpr int A_OPB = BM * BK * 2, B_OPB = BN * BK * 2;  // bytes per stage
+  static constexpr int STB = A_OPB + B_OPB;
+  static constexpr int A_BPW = A_OPB / 1024 / 4, B_BPW = B_OPB / 1024 / 4;  // blocks per wave
+  static constexpr int IPS = A_BPW + B_BPW;  // load instructions per stage per wave
+  static constexpr int LDS = STAGES * STB;
+  static constexpr int OCC = LDS <= 80 * 1024 ? 2 : 1;  // workgroups per CU
+  static_assert(BM % 128 == 0 && BN % 128 == 0 && BM <= 256 && BN <= 256, "tile");
+};
+using DirectBig = DCfg<256, 256, 4>;    // 1 workgroup per CU
+using DirectTall = DCfg<256, 128, 3>;   // 2 workgroups per CU
 
 __device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_t;
+typedef __attribute__((address_space(3))) v4i16 lds_v4;
 
-template <int STAGES, int ADD, bool RC>
-__global__ __launch_bounds__(256) void gemm_direct_kernel(KernelArgs g) {
-  using C = CfgDirect;
-  constexpr int OPB = C::BM * C::BK * 2;       // bytes per operand per stage (16 KiB)
-  constexpr int STB = 2 * OPB;                 // bytes per stage
-  constexpr int BPW = OPB / 1024 / 4;          // 1 KiB load blocks per operand per wave
-  static_assert(C::BM == C::BN && C::BM == 256, "square 256 tile");
+// s_waitcnt immediate waiting for vmcnt <= n only (expcnt 7, lgkmcnt 15)
+constexpr int vm_wait(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
+
+// One operand's part of the direct loads: R tile rows, this wave's BPW
+// 1 KiB blocks.  off: byte offset at k0 = 0; kk: k (within a stage) of
+// the lane's data; oob: out-of-range bit for rows past the end (RC).
+template <int R, bool RC, int BPW>
+struct DirectOperand {
+  unsigned off[BPW], oob[BPW];
+  int kk[BPW];
+
+  __device__ __forceinline__ void init(int wave, int lane, int r0, int rows, long long ld) {
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+      const int blk = wave * BPW + j;
+      if constexpr (!RC) {
+        const int r = blk * 16 + (lane >> 2);
+        const int chunk = (lane & 3) ^ swz(r);
+        kk[j] = chunk * 8;
+        off[j] = (unsigned)(((long long)min(r0 + r, rows - 1) * ld + chunk * 8) * 2);
+        oob[j] = 0;  // rows past the end are clamped: they feed discarded outputs
+      } else {
+        constexpr int CPK = R / 8;  // 16-byte chunks per k-row
+        const int srow = blk * (512 / R) + lane / CPK;
+        const int chunk = (lane % CPK) ^ (2 * (srow & 3));
+        const int r = r0 + chunk * 8;
+        kk[j] = srow;
+        off[j] = (unsigned)(((long long)srow * ld + min(r, rows - 8)) * 2);
+        oob[j] = (unsigned)(r >= rows) << 31;  // rows % 8 == 0: chunks are whole
+      }
+    }
+  }
+  __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, unsigned char* lds, int wave,
+                                        int k0, int kend, long long ld) const {
+    const unsigned dk = RC ? (unsigned)((long long)k0 * ld * 2) : (unsigned)(k0 * 2);
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+      // past the end of K: an out-of-range offset, for which the hardware
+      // writes zeros
+      const unsigned kob = (unsigned)(k0 + kk[j] >= kend) << 31;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_t*)(lds + (wave * BPW + j) * 1024), 16,
+                                               (off[j] + dk) | kob | oob[j], 0, 0, 0);
+    }
+  }
+  // 16-byte MFMA fragment: k-chunk c (8 k) of tile row `row`
+  __device__ __forceinline__ static floatx4 frag(const unsigned char* base, int row, int c,
+                                                 int lane) {
+    if constexpr (!RC) {
+      return *reinterpret_cast<const floatx4*>(base + row * 64 + ((c ^ swz(row)) << 4));
+    } else {
+      // this lane's role in its 16-lane group: k-row s, rows 4q..4q+3
+      const int gl = lane & 15;
+      const int r = (row & ~15) + 4 * (gl & 3);
+      const int kr = c * 8 + (gl >> 2);
+      auto addr = [&](int k) {
+        return base + k * (2 * R) + (((r >> 3) ^ (2 * (k & 3))) << 4) + (r & 7) * 2;
+      };
+      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(addr(kr)));
+      const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(addr(kr + 4)));
+      floatx4 f;
+      f[0] = __builtin_bit_cast(float, __builtin_shufflevector(lo, lo, 0, 1));
+      f[1] = __builtin_bit_cast(float, __builtin_shufflevector(lo, lo, 2, 3));
+      f[2] = __builtin_bit_cast(float, __builtin_shufflevector(hi, hi, 0, 1));
+      f[3] = __builtin_bit_cast(float, __builtin_shufflevector(hi, hi, 2, 3));
+      return f;
+    }
+  }
+};
+
+template <class C, int ADD, bool RC>
+__global__ __launch_bounds__(256, C::OCC) void gemm_direct_kernel(KernelArgs g) {
+  constexpr int STAGES = C::STAGES;
   static_assert(C::BK / C::KSLAB == 2, "two fragment slabs per stage");
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * STB];
-  typedef __attribute__((address_space(3))) void lds_t;
-  typedef __attribute__((address_space(3))) v4i16 lds_v4;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
 
   const TileIdx ti = tile_of(g);
   const int m0 = ti.tm * C::BM;
@@ -475,53 +560,17 @@ __global__ __launch_bounds__(256) void gemm_direct_kernel(KernelArgs g) {
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(g.A, g.a_bytes);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(g.B, g.b_bytes);
 
-  // Per-lane source offset of each load block at k = 0 and the k (relative
-  // to the stage) its data belongs to.  KC: rows past the end are clamped to
-  // the last row (they only feed discarded outputs).  RC: chunks of rows
-  // past the end get the out-of-range bit (rows % 8 == 0, chunks are whole).
-  unsigned offa[BPW], offb[BPW], rowoob[BPW];
-  int kk[BPW];
-#pragma unroll
-  for (int j = 0; j < BPW; ++j) {
-    rowoob[j] = 0;
-    const int blk = wave * BPW + j;
-    if constexpr (!RC) {
-      const int r = blk * 16 + (lane >> 2);
-      const int chunk = (lane & 3) ^ swz(r);
-      kk[j] = chunk * 8;
-      const int ra_ = min(m0 + r, g.M - 1);
-      const int rb_ = min(n0 + r, g.N - 1);
-      offa[j] = (unsigned)(((long long)ra_ * g.lda + chunk * 8) * 2);
-      offb[j] = (unsigned)(((long long)rb_ * g.ldb + chunk * 8) * 2);
-    } else {
-      const int srow = blk * 2 + (lane >> 5);
-      const int chunk = (lane & 31) ^ (2 * (srow & 3));
-      kk[j] = srow;
-      const int ra_ = m0 + chunk * 8;
-      const int rb_ = n0 + chunk * 8;
-      offa[j] = (unsigned)(((long long)srow * g.lda + min(ra_, g.M - 8)) * 2);
-      offb[j] = (unsigned)(((long long)srow * g.ldb + min(rb_, g.N - 8)) * 2);
-      rowoob[j] = ((unsigned)(ra_ >= g.M) << 31) | ((unsigned)(rb_ >= g.N) << 30);
-    }
-  }
+  using OpA = DirectOperand<C::BM, RC, C::A_BPW>;
+  using OpB = DirectOperand<C::BN, RC, C::B_BPW>;
+  OpA la;
+  OpB lb;
+  la.init(wave, lane, m0, g.M, g.lda);
+  lb.init(wave, lane, n0, g.N, g.ldb);
   auto issue = [&](int kt) {
+    unsigned char* st = smem + (kt % STAGES) * C::STB;
     const int k0 = kbeg + kt * C::BK;
-    unsigned char* st = smem + (kt % STAGES) * STB;
-#pragma unroll
-    for (int j = 0; j < BPW; ++j) {
-      // past the end of K: set the top bit, an out-of-range offset, and the
-      // hardware writes zeros
-      const unsigned oob = (unsigned)(k0 + kk[j] >= kend) << 31;
-      const unsigned da = RC ? (unsigned)((long long)k0 * g.lda * 2) : (unsigned)(k0 * 2);
-      const unsigned db = RC ? (unsigned)((long long)k0 * g.ldb * 2) : (unsigned)(k0 * 2);
-      const int blk = wave * BPW + j;
-      // rowoob: bit 31 marks A's chunk, bit 30 B's (shifted up to bit 31)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_t*)(st + blk * 1024), 16,
-                                               (offa[j] + da) | oob | (rowoob[j] & kOOB), 0, 0,
-                                               0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_t*)(st + OPB + blk * 1024), 16,
-                                               (offb[j] + db) | oob | (rowoob[j] << 1), 0, 0, 0);
-    }
+    la.issue(ra, st, wave, k0, kend, g.lda);
+    lb.issue(rb, st + C::A_OPB, wave, k0, kend, g.ldb);
   };
 
   floatx16 acc[C::FM][C::FN];
@@ -536,37 +585,18 @@ __global__ __launch_bounds__(256) void gemm_direct_kernel(KernelArgs g) {
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nk) issue(s);
 
-  // One 16-byte MFMA fragment: k-chunk c (8 k) of tile row `row`.
-  auto frag = [&](const unsigned char* base, int row, int c) -> floatx4 {
-    if constexpr (!RC) {
-      return *reinterpret_cast<const floatx4*>(base + row * 64 + ((c ^ swz(row)) << 4));
-    } else {
-      // this lane's role in its 16-lane group: k-row s, rows 4q..4q+3
-      const int gl = lane & 15;
-      const int r = (row & ~15) + 4 * (gl & 3);
-      const int kr = c * 8 + (gl >> 2);
-      auto addr = [&](int k) {
-        return base + k * 512 + (((r >> 3) ^ (2 * (k & 3))) << 4) + (r & 7) * 2;
-      };
-      const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(addr(kr)));
-      const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(addr(kr + 4)));
-      floatx4 f;
-      f[0] = __builtin_bit_cast(float, __builtin_shufflevector(lo, lo, 0, 1));
-      f[1] = __builtin_bit_cast(float, __builtin_shufflevector(lo, lo, 2, 3));
-      f[2] = __builtin_bit_cast(float, __builtin_shufflevector(hi, hi, 0, 1));
-      f[3] = __builtin_bit_cast(float, __builtin_shufflevector(hi, hi, 2, 3));
-      return f;
-    }
-  };
   // Wait until this wave's part of stage kt has landed: the loads of later
-  // stages (8 instructions per stage per wave) may stay in flight.
-  // s_waitcnt immediate: vmcnt in bits [3:0] and [15:14], expcnt 7 and
-  // lgkmcnt 15 (no wait on those).
+  // stages (IPS instructions per stage per wave) may stay in flight.
   auto wait_stage = [&](int kt) {
     const int later = min(STAGES - 2, nk - 1 - kt);
-    if (later >= 2) __builtin_amdgcn_s_waitcnt((16 >> 4) << 14 | (16 & 15) | 0x0F70);
-    else if (later == 1) __builtin_amdgcn_s_waitcnt(8 | 0x0F70);
-    else __builtin_amdgcn_s_waitcnt(0x0F70);
+    if constexpr (STAGES >= 4) {
+      if (later >= 2) {
+        __builtin_amdgcn_s_waitcnt(vm_wait(2 * C::IPS));
+        return;
+      }
+    }
+    if (later >= 1) __builtin_amdgcn_s_waitcnt(vm_wait(C::IPS));
+    else __builtin_amdgcn_s_waitcnt(vm_wait(0));
   };
   // Workgroup barrier without the release fence of __syncthreads (which
   // would wait for every outstanding vector memory operation, i.e. drain the
@@ -583,13 +613,13 @@ __global__ __launch_bounds__(256) void gemm_direct_kernel(KernelArgs g) {
     floatx4 a[C::FM], b[C::FN];
   };
   auto load_frags = [&](Frags& f, int kt, int sl) {
-    const unsigned char* As = smem + (kt % STAGES) * STB;
-    const unsigned char* Bs = As + OPB;
+    const unsigned char* As = smem + (kt % STAGES) * C::STB;
+    const unsigned char* Bs = As + C::A_OPB;
     const int c = 2 * sl + (lane >> 5);
 #pragma unroll
-    for (int i = 0; i < C::FM; ++i) f.a[i] = frag(As, wm0 + i * 32 + (lane & 31), c);
+    for (int i = 0; i < C::FM; ++i) f.a[i] = OpA::frag(As, wm0 + i * 32 + (lane & 31), c, lane);
 #pragma unroll
-    for (int j = 0; j < C::FN; ++j) f.b[j] = frag(Bs, wn0 + j * 32 + (lane & 31), c);
+    for (int j = 0; j < C::FN; ++j) f.b[j] = OpB::frag(Bs, wn0 + j * 32 + (lane & 31), c, lane);
   };
   auto mfmas = [&](const Frags& f) {
 #pragma unroll
@@ -631,10 +661,9 @@ __global__ __launch_bounds__(256) void gemm_direct_kernel(KernelArgs g) {
   write_tile_add<C, ADD>(g, acc, m0, n0, wm0, wn0, lane, ti.split);
 }
 
-template <int ADD, bool RC>
+template <class C, int ADD, bool RC>
 void launch_direct(const KernelArgs& a, int nwg, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_direct_kernel<kDirectStages, ADD, RC>), dim3(nwg), dim3(256), 0, st,
-                     a);
+  hipLaunchKernelGGL((gemm_direct_kernel<C, ADD, RC>), dim3(nwg), dim3(256), 0, st, a);
 }
 
 // Sum of split partials in split order, plus the optional addend.
@@ -776,18 +805,7 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
   a.a_bytes = vec ? (unsigned)a_bytes : 0u;
   a.b_bytes = vec ? (unsigned)b_bytes : 0u;
   timing_before(g.label ? g.label : !g.b_kc ? (g.a_kc ? "gemm_nn" : "gemm_tn") : "gemm_nt", st);
-  // bf16 operands of one layout, chunk-aligned: the direct-to-LDS kernel
-  constexpr bool kBothBf16 =
-      std::is_same<SA, uint16_t>::value && std::is_same<SB, uint16_t>::value;
-  constexpr bool kDirectOk = C::BF16 && kBothBf16 && A_KC == B_KC && C::BM == CfgDirect::BM &&
-                             C::BN == CfgDirect::BN && C::BK % CfgDirect::BK == 0;
-  if (kDirectOk && vec) {
-    constexpr bool RC = !A_KC;
-    if (a.add_count == 2) launch_direct<2, RC>(a, nwg, st);
-    else if (a.add_count == 1) launch_direct<1, RC>(a, nwg, st);
-    else launch_direct<0, RC>(a, nwg, st);
-  }
-  else if (vec)
+  if (vec)
     launch_staged<C, A_KC, B_KC, SA, SB, true>(a, nwg, st);
   else
     launch_staged<C, A_KC, B_KC, SA, SB, false>(a, nwg, st);
@@ -799,6 +817,98 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
   timing_before("splitk_reduce", st);
   hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, st, g.partials, a.splits,
                      g.M, g.N, g.C, g.ldc, g.add, g.add_ld, g.add_off, g.add_count);
+  timing_after(st);
+  return hipGetLastError();
+}
+
+// ---- the direct path: plan (shared by workspace sizing and launch) ----
+long long operand_bytes(bool kc, int rows, int K, long long ld, int esz) {
+  return (long long)esz * (kc ? (long long)(rows - 1) * ld + K : (long long)(K - 1) * ld + rows);
+}
+
+// bf16 x bf16 operands of one layout whose 16-byte chunks are whole (the
+// contiguous extent and leading dimension are multiples of 8 elements) and
+// that are smaller than the out-of-range sentinel.
+bool direct_ok(const GemmDesc& g) {
+  if (!g.bf16 || !g.a_bf16 || !g.b_bf16 || g.a_kc != g.b_kc) return false;
+  const long long ab = operand_bytes(g.a_kc, g.M, g.K, g.lda, 2);
+  const long long bb = operand_bytes(g.b_kc, g.N, g.K, g.ldb, 2);
+  return vec_ok<uint16_t>(g.A, g.lda, g.a_kc ? g.K : g.M, ab) &&
+         vec_ok<uint16_t>(g.B, g.ldb, g.b_kc ? g.K : g.N, bb);
+}
+
+// Split count for the direct path: the K = tokens product (row-contiguous
+// operands) is cut so that about two workgroups per CU are busy.
+int direct_splits(const GemmDesc& g) {
+  using C = DirectTall;
+  if (g.a_kc) return 1;
+  const int tiles = ((g.M + C::BM - 1) / C::BM) * ((g.N + C::BN - 1) / C::BN);
+  const int kt = (g.K + C::BK - 1) / C::BK;
+  int s = max(1, (2 * 256) / tiles);
+  s = min(s, max(1, kt / 8));  // at least 8 K steps per split
+  const int kps = ((kt + s - 1) / s) * C::BK;
+  return (g.K + kps - 1) / kps;
+}
+
+// Explicit instantiations: the host pass did not emit the launch stubs of
+// every specialisation referenced through launch_direct_add.
+template __global__ void gemm_direct_kernel<DirectTall, 0, false>(KernelArgs);
+template __global__ void gemm_direct_kernel<DirectTall, 1, false>(KernelArgs);
+template __global__ void gemm_direct_kernel<DirectTall, 2, false>(KernelArgs);
+template __global__ void gemm_direct_kernel<DirectTall, 0, true>(KernelArgs);
+template __global__ void gemm_direct_kernel<DirectTall, 1, true>(KernelArgs);
+template __global__ void gemm_direct_kernel<DirectTall, 2, true>(KernelArgs);
+
+template <int ADD>
+void launch_direct_add(const KernelArgs& a, int nwg, bool rc, hipStream_t st) {
+  if (rc) launch_direct<DirectTall, ADD, true>(a, nwg, st);
+  else launch_direct<DirectTall, ADD, false>(a, nwg, st);
+}
+
+hipError_t launch_direct_gemm(const GemmDesc& g, hipStream_t st) {
+  using C = DirectTall;
+  const int splits = direct_splits(g);
+  const int kt = (g.K + C::BK - 1) / C::BK;
+  const int kps = ((kt + splits - 1) / splits) * C::BK;
+  KernelArgs a{};
+  a.A = g.A;
+  a.B = g.B;
+  a.lda = g.lda;
+  a.ldb = g.ldb;
+  a.M = g.M;
+  a.N = g.N;
+  a.K = g.K;
+  a.a_bytes = (unsigned)operand_bytes(g.a_kc, g.M, g.K, g.lda, 2);
+  a.b_bytes = (unsigned)operand_bytes(g.b_kc, g.N, g.K, g.ldb, 2);
+  a.k_per_split = kps;
+  a.tiles_m = (g.M + C::BM - 1) / C::BM;
+  a.tiles_n = (g.N + C::BN - 1) / C::BN;
+  a.splits = splits;
+  if (splits > 1) {
+    a.out = g.partials;
+    a.ldo = g.N;
+    a.split_stride = (long long)g.M * g.N;
+  } else {
+    a.out = g.C;
+    a.ldo = g.ldc;
+    a.add = g.add;
+    a.add_count = g.add_count;
+    a.add_ld = g.add_ld;
+    a.add_off = g.add_off;
+  }
+  const int nwg = a.tiles_m * a.tiles_n * splits;
+  timing_before(g.label ? g.label : !g.b_kc ? (g.a_kc ? "gemm_nn" : "gemm_tn") : "gemm_nt", st);
+  if (a.add_count == 2) launch_direct_add<2>(a, nwg, !g.a_kc, st);
+  else if (a.add_count == 1) launch_direct_add<1>(a, nwg, !g.a_kc, st);
+  else launch_direct_add<0>(a, nwg, !g.a_kc, st);
+  timing_after(st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  const long long total = (long long)g.M * g.N;
+  const int grid = (int)std::min<long long>((total + 255) / 256, 8192);
+  timing_before("splitk_reduce", st);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, st, g.partials, splits, g.M,
+                     g.N, g.C, g.ldc, g.add, g.add_ld, g.add_off, g.add_count);
   timing_after(st);
   return hipGetLastError();
 }
@@ -834,6 +944,7 @@ hipError_t launch_layout(const GemmDesc& g, hipStream_t st) {
 }  // namespace
 
 int gemm_splits(const GemmDesc& g) {
+  if (direct_ok(g)) return direct_splits(g);
   const int s = g.bf16 ? splits_for<CfgBF16>(g) : splits_for<CfgF32>(g);
   const int bk = g.bf16 ? CfgBF16::BK : CfgF32::BK;
   const int kt = (g.K + bk - 1) / bk;
@@ -847,6 +958,7 @@ size_t gemm_partial_bytes(int M, int N, int splits) {
 
 hipError_t gemm_launch(const GemmDesc& g, hipStream_t st) {
   if ((g.a_bf16 || g.b_bf16) && !g.bf16) return hipErrorInvalidValue;
+  if (direct_ok(g)) return launch_direct_gemm(g, st);
   return g.bf16 ? launch_layout<CfgBF16>(g, st) : launch_layout<CfgF32>(g, st);
 }
 
