@@ -32,6 +32,14 @@
 
 #include "sru_internal.h"
 
+// Direct-path tile configurations (K-contiguous and row-contiguous operands)
+#ifndef SRU_DIRECT_KC
+#define SRU_DIRECT_KC DirectLine
+#endif
+#ifndef SRU_DIRECT_RC
+#define SRU_DIRECT_RC DirectLine
+#endif
+
 namespace sru {
 namespace {
 
@@ -270,6 +278,7 @@ struct KernelArgs {
   const float* add;
   long long add_ld, add_off;
   int add_count;
+  int vec_out;  // output (and addend) rows allow 16-byte accesses: see write_tile_rows
 };
 
 // Epilogue shared by the kernels.  32x32 accumulator layout: element e of
@@ -306,6 +315,73 @@ __device__ __forceinline__ void write_tile_add(const KernelArgs& g,
       for (int e = 0; e < 16; ++e) {
         const int m = mb + (e >> 2) * 8 + (e & 3);
         if (full || (m < g.M && n < g.N)) out[(long long)m * g.ldo + n] = v[e];
+      }
+    }
+}
+
+// Epilogue of the direct kernel, whose MFMAs take the B-operand fragment
+// first and so accumulate the transposed tile: element e of lane l is row
+// l%32, column 8*(e/4) + 4*(l/32) + e%4 of the 32x32 output tile.  Each
+// group of four elements is four consecutive columns of one row, written
+// (and its addend read) as one 16-byte access when the tile lies wholly
+// inside the output and vec_out holds (16-byte aligned rows).
+template <class C, int ADD>
+__device__ __forceinline__ void write_tile_rows(const KernelArgs& g,
+                                                const floatx16 (&acc)[C::FM][C::FN], int m0,
+                                                int n0, int wm0, int wn0, int lane, int split) {
+  float* out = g.out + (long long)split * g.split_stride;
+  const int cl = 4 * (lane >> 5);
+  if (g.vec_out && m0 + C::BM <= g.M && n0 + C::BN <= g.N) {
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+      const int m = m0 + wm0 + i * 32 + (lane & 31);
+      float* orow = out + (long long)m * g.ldo + n0 + wn0 + cl;
+      const float* arow = ADD > 0 ? g.add + (long long)m * g.add_ld + n0 + wn0 + cl : nullptr;
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j) {
+        floatx4 v[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[q][e] = acc[i][j][4 * q + e];
+        if constexpr (ADD > 0) {
+          floatx4 a0[4], a1[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            a0[q] = *reinterpret_cast<const floatx4*>(arow + j * 32 + 8 * q);
+            if constexpr (ADD > 1)
+              a1[q] = *reinterpret_cast<const floatx4*>(arow + g.add_off + j * 32 + 8 * q);
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            v[q] += a0[q];
+            if constexpr (ADD > 1) v[q] += a1[q];
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) *reinterpret_cast<floatx4*>(orow + j * 32 + 8 * q) = v[q];
+      }
+    }
+    return;
+  }
+  // edge tiles (or unaligned rows): element by element, inside the bounds
+#pragma unroll
+  for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j) {
+      const int m = m0 + wm0 + i * 32 + (lane & 31);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int n = n0 + wn0 + j * 32 + 8 * (e >> 2) + cl + (e & 3);
+        if (m < g.M && n < g.N) {
+          float v = acc[i][j][e];
+          if constexpr (ADD > 0) {
+            const float* ar = g.add + (long long)m * g.add_ld + n;
+            v += ar[0];
+            if constexpr (ADD > 1) v += ar[g.add_off];
+          }
+          out[(long long)m * g.ldo + n] = v;
+        }
       }
     }
 }
@@ -428,11 +504,12 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
 // operands have the same layout, selected by RC:
 //
 // K-contiguous (RC = false; U = X W^T and dX = dU W as dU (W^T)^T):
-//   row r of a tile is 64 bytes (BK = 32 k) at r*64, its four 16-byte
-//   k-chunks permuted as slot = chunk ^ swz(r), swz(r) = ((r>>1) ^ (r>>3)) & 3,
-//   which keeps the rows one ds_read_b128 phase touches (8 rows over 32
-//   banks or 16 over 64) on distinct banks.  A wave load fills 16 rows:
-//   lane l takes row l/4, slot l%4.  A fragment is one ds_read_b128.
+//   row r of a tile holds BK k (2*BK bytes) at r*2*BK, its 16-byte k-chunks
+//   permuted as slot = chunk ^ swz(r), which keeps the 16 rows of one
+//   ds_read_b128 phase on distinct banks.  BK = 64 makes each row one whole
+//   128-byte line of the operand: a wave load (8 rows, lane l: row l/8,
+//   slot l%8) then touches 8 lines instead of 16 half lines, which is what
+//   bounds the load rate.  A fragment is one ds_read_b128.
 // Row-contiguous (RC = true; dW = dU^T X, both operands [K, rows]):
 //   the tile is kept as loaded, k-row s at s*2R bytes (R rows of bf16), its
 //   R/8 16-byte row-chunks permuted as slot = chunk ^ 2*(s & 3).  A wave
@@ -442,29 +519,35 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
 //   receives that k-run of row i.  The four k-rows x 32 bytes one group
 //   reads land on 8 distinct 16-byte slots.
 //
-// Tiles are BM x BN x 32 with 4 waves of (BM/2) x (BN/2).  A 256 x 128 tile
-// with 3 stages needs 72 KiB of LDS and 128 accumulator registers per lane,
-// so two workgroups share a CU and one's epilogue (the fp32 output write)
-// overlaps the other's MFMAs.
-template <int BM_, int BN_, int STAGES_>
+// Each wave owns a 128 x 64 block of the tile (4 x 2 MFMA tiles of 32 x 32,
+// 128 accumulator registers per lane); two waves share each SIMD, so one's
+// LDS reads and barrier waits hide behind the other's MFMAs.  A 256 x 256
+// tile (8 waves) loads a third fewer bytes per flop than 256 x 128 (4
+// waves, two workgroups per CU); the loads, not the MFMAs, bound the
+// smaller tile.
+template <int BM_, int BN_, int BK_, int WAVES_M_, int WAVES_N_, int STAGES_>
 struct DCfg {
-  static constexpr int BM = BM_, BN = BN_, BK = 32, STAGES = STAGES_;
-  static constexpr int WAVES_M = 2, WAVES_N = 2;
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, STAGES = STAGES_;
+  static constexpr int WAVES_M = WAVES_M_, WAVES_N = WAVES_N_, WAVES = WAVES_M * WAVES_N;
+  static constexpr int THREADS = 64 * WAVES;
   static constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   static constexpr int FM = WM / 32, FN = WN / 32;
-  static constexpr int KSLAB = 16;
+  static constexpr int KSLAB = 16, SLABS = BK / KSLAB;
   static constexpr int A_OPB = BM * BK * 2, B_OPB = BN * BK * 2;  // bytes per stage
   static constexpr int STB = A_OPB + B_OPB;
-  static constexpr int A_BPW = A_OPB / 1024 / 4, B_BPW = B_OPB / 1024 / 4;  // blocks per wave
+  static constexpr int A_BPW = A_OPB / 1024 / WAVES, B_BPW = B_OPB / 1024 / WAVES;
   static constexpr int IPS = A_BPW + B_BPW;  // load instructions per stage per wave
   static constexpr int LDS = STAGES * STB;
   static constexpr int OCC = LDS <= 80 * 1024 ? 2 : 1;  // workgroups per CU
-  static_assert(BM % 128 == 0 && BN % 128 == 0 && BM <= 256 && BN <= 256, "tile");
+  static_assert(BK == 32 || BK == 64, "k per stage");
+  static_assert(WM == 128 && WN == 64, "wave block");
+  static_assert(A_BPW * 1024 * WAVES == A_OPB && B_BPW * 1024 * WAVES == B_OPB,
+                "whole 1 KiB load blocks per wave");
+  static_assert(LDS <= 160 * 1024 && IPS * (STAGES - 1) < 64, "LDS and vmcnt");
 };
-using DirectBig = DCfg<256, 256, 4>;    // 1 workgroup per CU
-using DirectTall = DCfg<256, 128, 3>;   // 2 workgroups per CU
-
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+using DirectTall = DCfg<256, 128, 32, 2, 2, 3>;  // 4 waves, 2 workgroups per CU
+using DirectWide = DCfg<256, 256, 32, 2, 4, 4>;  // 8 waves, 1 workgroup per CU
+using DirectLine = DCfg<256, 256, 64, 2, 4, 2>;  // 8 waves, whole-line loads
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_t;
@@ -476,18 +559,24 @@ constexpr int vm_wait(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
 // One operand's part of the direct loads: R tile rows, this wave's BPW
 // 1 KiB blocks.  off: byte offset at k0 = 0; kk: k (within a stage) of
 // the lane's data; oob: out-of-range bit for rows past the end (RC).
-template <int R, bool RC, int BPW>
+template <int R, bool RC, int BPW, int BK>
 struct DirectOperand {
+  static constexpr int LPR = BK / 8;    // KC: 16-byte chunks (lanes) per row
+  static constexpr int RPB = 64 / LPR;  // KC: rows per 1 KiB block
   unsigned off[BPW], oob[BPW];
   int kk[BPW];
 
+  __device__ __forceinline__ static int swz(int r) {
+    if constexpr (BK == 32) return ((r >> 1) ^ (r >> 3)) & 3;
+    else return (r >> 1) & 7;
+  }
   __device__ __forceinline__ void init(int wave, int lane, int r0, int rows, long long ld) {
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
       const int blk = wave * BPW + j;
       if constexpr (!RC) {
-        const int r = blk * 16 + (lane >> 2);
-        const int chunk = (lane & 3) ^ swz(r);
+        const int r = blk * RPB + lane / LPR;
+        const int chunk = (lane % LPR) ^ swz(r);
         kk[j] = chunk * 8;
         off[j] = (unsigned)(((long long)min(r0 + r, rows - 1) * ld + chunk * 8) * 2);
         oob[j] = 0;  // rows past the end are clamped: they feed discarded outputs
@@ -518,7 +607,7 @@ struct DirectOperand {
   __device__ __forceinline__ static floatx4 frag(const unsigned char* base, int row, int c,
                                                  int lane) {
     if constexpr (!RC) {
-      return *reinterpret_cast<const floatx4*>(base + row * 64 + ((c ^ swz(row)) << 4));
+      return *reinterpret_cast<const floatx4*>(base + row * (2 * BK) + ((c ^ swz(row)) << 4));
     } else {
       // this lane's role in its 16-lane group: k-row s, rows 4q..4q+3
       const int gl = lane & 15;
@@ -540,9 +629,8 @@ struct DirectOperand {
 };
 
 template <class C, int ADD, bool RC>
-__global__ __launch_bounds__(256, C::OCC) void gemm_direct_kernel(KernelArgs g) {
+__global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelArgs g) {
   constexpr int STAGES = C::STAGES;
-  static_assert(C::BK / C::KSLAB == 2, "two fragment slabs per stage");
   __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
 
   const TileIdx ti = tile_of(g);
@@ -560,8 +648,8 @@ __global__ __launch_bounds__(256, C::OCC) void gemm_direct_kernel(KernelArgs g) 
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(g.A, g.a_bytes);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(g.B, g.b_bytes);
 
-  using OpA = DirectOperand<C::BM, RC, C::A_BPW>;
-  using OpB = DirectOperand<C::BN, RC, C::B_BPW>;
+  using OpA = DirectOperand<C::BM, RC, C::A_BPW, C::BK>;
+  using OpB = DirectOperand<C::BN, RC, C::B_BPW, C::BK>;
   OpA la;
   OpB lb;
   la.init(wave, lane, m0, g.M, g.lda);
@@ -595,8 +683,13 @@ __global__ __launch_bounds__(256, C::OCC) void gemm_direct_kernel(KernelArgs g) 
         return;
       }
     }
-    if (later >= 1) __builtin_amdgcn_s_waitcnt(vm_wait(C::IPS));
-    else __builtin_amdgcn_s_waitcnt(vm_wait(0));
+    if constexpr (STAGES >= 3) {
+      if (later >= 1) {
+        __builtin_amdgcn_s_waitcnt(vm_wait(C::IPS));
+        return;
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));
   };
   // Workgroup barrier without the release fence of __syncthreads (which
   // would wait for every outstanding vector memory operation, i.e. drain the
@@ -627,43 +720,48 @@ __global__ __launch_bounds__(256, C::OCC) void gemm_direct_kernel(KernelArgs g) 
 #pragma unroll
       for (int j = 0; j < C::FN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8, f.a[i]), __builtin_bit_cast(bf16x8, f.b[j]), acc[i][j], 0,
-            0, 0);
+            __builtin_bit_cast(bf16x8, f.b[j]), __builtin_bit_cast(bf16x8, f.a[i]), acc[i][j], 0,
+            0, 0);  // B first: the transposed tile, see write_tile_rows
   };
 
-  // Software pipeline over the two fragment slabs of a stage (f0: k-chunks
-  // 0-1, f1: k-chunks 2-3): a slab's fragments are read from LDS before the
-  // MFMAs of the previous slab are issued.  The barrier that publishes stage
-  // kt+1 sits before the MFMAs of slab 1 of stage kt; it also ends every
-  // wave's reads of stage kt, which frees that slot for the loads issued at
-  // the top of the next iteration.
-  Frags f0, f1;
+  // Software pipeline over the SLABS fragment slabs (16 k each) of a stage:
+  // a slab's fragments are read from LDS before the MFMAs of the previous
+  // slab are issued (f[0] and f[1] alternate; SLABS is even, so slab 0 of
+  // every stage is f[0]).  The barrier that publishes stage kt+1 sits before
+  // the MFMAs of the last slab of stage kt; it also ends every wave's reads
+  // of stage kt, which frees that slot for the loads issued at the top of
+  // the next iteration.  The last stage is peeled off so that no branch
+  // separates the reads of the next f[0] from the MFMAs of the last slab: at
+  // a join the compiler would count those newer reads into the wait.
+  Frags f[2];
   if (nk > 0) {
     wait_stage(0);
     barrier();
-    load_frags(f0, 0, 0);
-  }
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);  // slot of stage kt-1, free
-    load_frags(f1, kt, 1);
-    mfmas(f0);
-    if (kt + 1 < nk) {
+    load_frags(f[0], 0, 0);
+    for (int kt = 0; kt + 1 < nk; ++kt) {
+      if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);  // slot of stage kt-1, free
+#pragma unroll
+      for (int sl = 0; sl + 1 < C::SLABS; ++sl) {
+        load_frags(f[(sl + 1) & 1], kt, sl + 1);
+        mfmas(f[sl & 1]);
+      }
       wait_stage(kt + 1);
       barrier();
-      load_frags(f0, kt + 1, 0);
-    } else {
-      // last stage: only f1's reads are outstanding; waiting here too keeps
-      // the join of the two paths from waiting on the newer f0 reads
-      __builtin_amdgcn_s_waitcnt(0xC07F);
+      load_frags(f[0], kt + 1, 0);
+      mfmas(f[1]);
     }
-    mfmas(f1);
+#pragma unroll
+    for (int sl = 0; sl < C::SLABS; ++sl) {
+      if (sl + 1 < C::SLABS) load_frags(f[(sl + 1) & 1], nk - 1, sl + 1);
+      mfmas(f[sl & 1]);
+    }
   }
-  write_tile_add<C, ADD>(g, acc, m0, n0, wm0, wn0, lane, ti.split);
+  write_tile_rows<C, ADD>(g, acc, m0, n0, wm0, wn0, lane, ti.split);
 }
 
 template <class C, int ADD, bool RC>
 void launch_direct(const KernelArgs& a, int nwg, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_direct_kernel<C, ADD, RC>), dim3(nwg), dim3(256), 0, st, a);
+  hipLaunchKernelGGL((gemm_direct_kernel<C, ADD, RC>), dim3(nwg), dim3(C::THREADS), 0, st, a);
 }
 
 // Sum of split partials in split order, plus the optional addend.
@@ -838,36 +936,38 @@ bool direct_ok(const GemmDesc& g) {
 }
 
 // Split count for the direct path: the K = tokens product (row-contiguous
-// operands) is cut so that about two workgroups per CU are busy.
-int direct_splits(const GemmDesc& g) {
-  using C = DirectTall;
+// operands) is cut so that every CU gets its workgroups (at least 8 K steps
+// per split).
+template <class C>
+int direct_splits_cfg(const GemmDesc& g) {
   if (g.a_kc) return 1;
   const int tiles = ((g.M + C::BM - 1) / C::BM) * ((g.N + C::BN - 1) / C::BN);
   const int kt = (g.K + C::BK - 1) / C::BK;
-  int s = max(1, (2 * 256) / tiles);
-  s = min(s, max(1, kt / 8));  // at least 8 K steps per split
+  int s = max(1, (C::OCC * 256) / tiles);
+  s = min(s, max(1, kt / 8));
   const int kps = ((kt + s - 1) / s) * C::BK;
   return (g.K + kps - 1) / kps;
 }
 
-// Explicit instantiations: the host pass did not emit the launch stubs of
-// every specialisation referenced through launch_direct_add.
-template __global__ void gemm_direct_kernel<DirectTall, 0, false>(KernelArgs);
-template __global__ void gemm_direct_kernel<DirectTall, 1, false>(KernelArgs);
-template __global__ void gemm_direct_kernel<DirectTall, 2, false>(KernelArgs);
-template __global__ void gemm_direct_kernel<DirectTall, 0, true>(KernelArgs);
-template __global__ void gemm_direct_kernel<DirectTall, 1, true>(KernelArgs);
-template __global__ void gemm_direct_kernel<DirectTall, 2, true>(KernelArgs);
+using CfgKC = SRU_DIRECT_KC;
+using CfgRC = SRU_DIRECT_RC;
 
-template <int ADD>
-void launch_direct_add(const KernelArgs& a, int nwg, bool rc, hipStream_t st) {
-  if (rc) launch_direct<DirectTall, ADD, true>(a, nwg, st);
-  else launch_direct<DirectTall, ADD, false>(a, nwg, st);
+int direct_splits(const GemmDesc& g) {
+  return g.a_kc ? direct_splits_cfg<CfgKC>(g) : direct_splits_cfg<CfgRC>(g);
 }
 
-hipError_t launch_direct_gemm(const GemmDesc& g, hipStream_t st) {
-  using C = DirectTall;
-  const int splits = direct_splits(g);
+// Explicit instantiations: the host pass did not emit the launch stubs of
+// every specialisation referenced through launch_direct_cfg.
+template __global__ void gemm_direct_kernel<CfgKC, 0, false>(KernelArgs);
+template __global__ void gemm_direct_kernel<CfgKC, 1, false>(KernelArgs);
+template __global__ void gemm_direct_kernel<CfgKC, 2, false>(KernelArgs);
+template __global__ void gemm_direct_kernel<CfgRC, 0, true>(KernelArgs);
+template __global__ void gemm_direct_kernel<CfgRC, 1, true>(KernelArgs);
+template __global__ void gemm_direct_kernel<CfgRC, 2, true>(KernelArgs);
+
+template <class C, bool RC>
+hipError_t launch_direct_cfg(const GemmDesc& g, hipStream_t st) {
+  const int splits = direct_splits_cfg<C>(g);
   const int kt = (g.K + C::BK - 1) / C::BK;
   const int kps = ((kt + splits - 1) / splits) * C::BK;
   KernelArgs a{};
@@ -896,19 +996,22 @@ hipError_t launch_direct_gemm(const GemmDesc& g, hipStream_t st) {
     a.add_ld = g.add_ld;
     a.add_off = g.add_off;
   }
+  auto al16 = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  a.vec_out = a.ldo % 4 == 0 && a.split_stride % 4 == 0 && al16(a.out) &&
+              (a.add_count == 0 || (a.add_ld % 4 == 0 && a.add_off % 4 == 0 && al16(a.add)));
   const int nwg = a.tiles_m * a.tiles_n * splits;
   timing_before(g.label ? g.label : !g.b_kc ? (g.a_kc ? "gemm_nn" : "gemm_tn") : "gemm_nt", st);
-  if (a.add_count == 2) launch_direct_add<2>(a, nwg, !g.a_kc, st);
-  else if (a.add_count == 1) launch_direct_add<1>(a, nwg, !g.a_kc, st);
-  else launch_direct_add<0>(a, nwg, !g.a_kc, st);
+  if (a.add_count == 2) launch_direct<C, 2, RC>(a, nwg, st);
+  else if (a.add_count == 1) launch_direct<C, 1, RC>(a, nwg, st);
+  else launch_direct<C, 0, RC>(a, nwg, st);
   timing_after(st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   const long long total = (long long)g.M * g.N;
   const int grid = (int)std::min<long long>((total + 255) / 256, 8192);
   timing_before("splitk_reduce", st);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, st, g.partials, splits, g.M,
-                     g.N, g.C, g.ldc, g.add, g.add_ld, g.add_off, g.add_count);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, st, g.partials, a.splits,
+                     g.M, g.N, g.C, g.ldc, g.add, g.add_ld, g.add_off, g.add_count);
   timing_after(st);
   return hipGetLastError();
 }
@@ -958,7 +1061,8 @@ size_t gemm_partial_bytes(int M, int N, int splits) {
 
 hipError_t gemm_launch(const GemmDesc& g, hipStream_t st) {
   if ((g.a_bf16 || g.b_bf16) && !g.bf16) return hipErrorInvalidValue;
-  if (direct_ok(g)) return launch_direct_gemm(g, st);
+  if (direct_ok(g))
+    return g.a_kc ? launch_direct_cfg<CfgKC, false>(g, st) : launch_direct_cfg<CfgRC, true>(g, st);
   return g.bf16 ? launch_layout<CfgBF16>(g, st) : launch_layout<CfgF32>(g, st);
 }
 
