@@ -105,12 +105,22 @@ SRU_API size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int d
  *        (NULL = do not store: inference);
  *        c_last [B, ndir*d] -- state after each sequence's last valid step
  *        (NULL = do not store).
+ *   bf16 companions (gemm_dtype = SRU_GEMM_BF16 only, else they must be
+ *   NULL; each may be NULL; 16-byte aligned device buffers of uint16 bf16
+ *   bit patterns, rounded to nearest even):
+ *        X_bf16 [M, d_in] in -- X rounded to bf16, e.g. the H_bf16 of the
+ *        layer below; it must equal that rounding of X (it replaces X as the
+ *        projection operand).  NULL: X is rounded into the workspace.
+ *        W_bf16 [N, d_in] out -- Wcat rounded to bf16, for sru_backward.
+ *        H_bf16 [L, B, ndir*d] out -- H rounded to bf16 (the next layer's
+ *        X_bf16).
  */
 SRU_API int sru_forward(const float* X, const float* W,
                 const float* v_f, const float* v_r, const float* b_f, const float* b_r,
                 const float* c0, int L, int B, int d_in, int d, int direction,
                 const uint8_t* pad_mask, int gemm_dtype,
                 float* U, float* H, float* C, float* c_last,
+                const uint16_t* X_bf16, uint16_t* W_bf16, uint16_t* H_bf16,
                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
@@ -121,6 +131,9 @@ SRU_API int sru_forward(const float* X, const float* W,
  *        [B, ndir*d] (w.r.t. c_last; NULL = zeros).
  *   out: dX [L, B, d_in], dW [ndir, k, d, d_in], dv_f, dv_r, db_f, db_r
  *        [ndir, d], dc0 [B, ndir*d] (NULL = do not compute).
+ *   bf16 companions (SRU_GEMM_BF16 only, else NULL; each may be NULL; as
+ *   in sru_forward): X_bf16 = X rounded to bf16; W_bf16 = Wcat rounded to
+ *   bf16 (the W_bf16 sru_forward wrote).  NULL: rounded into the workspace.
  */
 SRU_API int sru_backward(const float* X, const float* W,
                  const float* v_f, const float* v_r, const float* b_f, const float* b_r,
@@ -128,7 +141,8 @@ SRU_API int sru_backward(const float* X, const float* W,
                  const uint8_t* pad_mask, int gemm_dtype,
                  const float* U, const float* C, const float* dH, const float* dc_last,
                  float* dX, float* dW, float* dv_f, float* dv_r, float* db_f, float* db_r,
-                 float* dc0, void* workspace, size_t workspace_bytes, hipStream_t stream);
+                 float* dc0, const uint16_t* X_bf16, const uint16_t* W_bf16,
+                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Component entry points: the individual steps of the two calls above, with
@@ -151,12 +165,13 @@ SRU_API int sru_gemm(int op, int gemm_dtype, int M, int N, int K,
              void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* The fused forward scan (Algorithm 1 with the Eq. 3 reading) on a given U.
- * X is read only when k = 3 (d_in == d).  C and c_last may be NULL. */
+ * X is read only when k = 3 (d_in == d).  C, c_last and H_bf16 (bf16 copy
+ * of H, 2-byte aligned) may be NULL. */
 SRU_API int sru_scan_forward(const float* U, const float* X,
                      const float* v_f, const float* v_r, const float* b_f, const float* b_r,
                      const float* c0, int L, int B, int d_in, int d, int direction,
                      const uint8_t* pad_mask, float* H, float* C, float* c_last,
-                     hipStream_t stream);
+                     uint16_t* H_bf16, hipStream_t stream);
 
 /* The reverse-time gradient scan on a given U, C, dH.
  *   out: dU [L, B, ndir, k, d] (gradient w.r.t. the projections; when k = 4

@@ -3,6 +3,7 @@
 // frees or synchronises.
 #include <limits.h>
 
+#include <initializer_list>
 #include <vector>
 
 #include "../../include/sru.h"
@@ -30,6 +31,17 @@ bool valid_direction(int d) { return d == SRU_DIR_FWD || d == SRU_DIR_REV || d =
 bool valid_dtype(int t) { return t == SRU_GEMM_FP32 || t == SRU_GEMM_BF16; }
 
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3) == 0; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// The optional bf16 companions: only with bf16 GEMMs, 16-byte aligned.
+int check_bf16_side(int gemm_dtype, std::initializer_list<const void*> ptrs) {
+  for (const void* p : ptrs) {
+    if (!p) continue;
+    if (gemm_dtype != SRU_GEMM_BF16) return SRU_E_FLAG;
+    if (!aligned16(p)) return SRU_E_ALIGN;
+  }
+  return SRU_OK;
+}
 
 struct Dims {
   int L, B, d_in, d, ndir, k;
@@ -104,7 +116,7 @@ sru::GemmDesc dw_desc(const Dims& s, bool bf16, const void* dU, const void* X, f
 
 // Backward workspace layout:
 //   [dU (fp32, or bf16 in bf16 mode) | dxh (k = 3) | v/b partials |
-//    W^T and X in bf16 (bf16 mode) | dW split partials]
+//    Wcat (or Wcat^T) and X in bf16 (bf16 mode) | dW split partials]
 struct BwdLayout {
   size_t dU, dxh, partial, wt, xb, splitk, total;
   int splits;
@@ -207,8 +219,8 @@ size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int direction
 int sru_forward(const float* X, const float* W, const float* v_f, const float* v_r,
                 const float* b_f, const float* b_r, const float* c0, int L, int B, int d_in,
                 int d, int direction, const uint8_t* pad_mask, int gemm_dtype, float* U,
-                float* H, float* C, float* c_last, void* workspace, size_t workspace_bytes,
-                hipStream_t stream) {
+                float* H, float* C, float* c_last, const uint16_t* X_bf16, uint16_t* W_bf16,
+                uint16_t* H_bf16, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   Dims s;
   int st = make_dims(L, B, d_in, d, direction, s);
   if (st != SRU_OK) return st;
@@ -217,6 +229,7 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
   const void* ptrs[] = {X, W, v_f, v_r, b_f, b_r, c0, U, H, C, c_last};
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
+  if (int e = check_bf16_side(gemm_dtype, {X_bf16, W_bf16, H_bf16})) return e;
   const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
   const size_t need = fwd_workspace(s, gemm_dtype);
   if (need > 0) {
@@ -224,18 +237,23 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
     if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
   }
 
-  // U = X Wcat^T (Sec. 2.1).  bf16 mode: W and X rounded once into the
-  // workspace, so both operands of the product are K-contiguous bf16.
+  // U = X Wcat^T (Sec. 2.1).  bf16 mode: W and X rounded once (into
+  // W_bf16 / the workspace, unless the caller holds X_bf16), so both
+  // operands of the product are K-contiguous bf16.
   const void* Wop = W;
   const void* Xop = X;
   if (bf16) {
-    uint16_t* wb = static_cast<uint16_t*>(workspace);
-    uint16_t* xb = reinterpret_cast<uint16_t*>(static_cast<unsigned char*>(workspace) +
-                                               align_up(2 * (size_t)s.N * (size_t)d_in));
+    uint16_t* wb = W_bf16 ? W_bf16 : static_cast<uint16_t*>(workspace);
     if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wb, false, stream, "bf16_w"))) return e;
-    if (int e = hip_status(sru::to_bf16_launch(X, (int)s.M, d_in, xb, false, stream, "bf16_x"))) return e;
     Wop = wb;
-    Xop = xb;
+    if (X_bf16) {
+      Xop = X_bf16;
+    } else {
+      uint16_t* xb = reinterpret_cast<uint16_t*>(static_cast<unsigned char*>(workspace) +
+                                                 align_up(2 * (size_t)s.N * (size_t)d_in));
+      if (int e = hip_status(sru::to_bf16_launch(X, (int)s.M, d_in, xb, false, stream, "bf16_x"))) return e;
+      Xop = xb;
+    }
   }
   sru::GemmDesc g = gemm_desc(SRU_OP_NT, bf16, (int)s.M, (int)s.N, d_in, Xop, d_in, Wop, d_in, U,
                               s.N);
@@ -243,7 +261,7 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
   g.label = "gemm_u";
   if (int e = hip_status(sru::gemm_launch(g, stream))) return e;
 
-  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last};
+  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16};
   return hip_status(sru::scan_forward_launch(scan_shape(s, direction), a, stream));
 }
 
@@ -252,7 +270,8 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
                  int d, int direction, const uint8_t* pad_mask, int gemm_dtype, const float* U,
                  const float* C, const float* dH, const float* dc_last, float* dX, float* dW,
                  float* dv_f, float* dv_r, float* db_f, float* db_r, float* dc0,
-                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                 const uint16_t* X_bf16, const uint16_t* W_bf16, void* workspace,
+                 size_t workspace_bytes, hipStream_t stream) {
   Dims s;
   int st = make_dims(L, B, d_in, d, direction, s);
   if (st != SRU_OK) return st;
@@ -264,6 +283,7 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
                         db_f, db_r, dc0};
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
+  if (int e = check_bf16_side(gemm_dtype, {X_bf16, W_bf16})) return e;
   const BwdLayout lay = bwd_layout(s, gemm_dtype);
   if (!workspace || workspace_bytes < lay.total) return SRU_E_WORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
@@ -276,7 +296,8 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   uint16_t* wt = reinterpret_cast<uint16_t*>(ws + lay.wt);
   float* splitk = reinterpret_cast<float*>(ws + lay.splitk);
   uint16_t* xb = reinterpret_cast<uint16_t*>(ws + lay.xb);
-  sru::GemmDesc gw = dw_desc(s, bf16, dU, bf16 ? static_cast<const void*>(xb) : X, dW);
+  const void* Xop = !bf16 ? static_cast<const void*>(X) : X_bf16 ? X_bf16 : xb;
+  sru::GemmDesc gw = dw_desc(s, bf16, dU, Xop, dW);
   gw.partials = splitk;
   // the split partials were sized for lay.splits; refuse (before enqueueing
   // anything) rather than overrun if the launch plan ever differed
@@ -289,13 +310,25 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   if (int e = hip_status(sru::scan_backward_launch(scan_shape(s, direction), a, stream))) return e;
 
   // 2. dX = dU Wcat (+ the highway gradient of every direction when k = 3).
-  //    bf16 mode: Wcat^T rounded once into the workspace, so the product is
-  //    an NT one with both operands K-contiguous bf16.
+  //    bf16 mode: Wcat in bf16 (W_bf16, or rounded into the workspace) read
+  //    row-contiguous by the direct kernel; where that path does not apply,
+  //    Wcat^T is rounded into the workspace and the product is an NT one.
   sru::GemmDesc gx;
   if (bf16) {
-    if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wt, true, stream, "bf16_wt"))) return e;
-    gx = gemm_desc(SRU_OP_NT, true, (int)s.M, d_in, (int)s.N, dU, s.N, wt, s.N, dX, d_in);
+    gx = gemm_desc(SRU_OP_NN, true, (int)s.M, d_in, (int)s.N, dU, s.N, W_bf16 ? W_bf16 : wt,
+                   d_in, dX, d_in);
     gx.a_bf16 = gx.b_bf16 = true;
+    if (sru::gemm_is_direct(gx)) {
+      if (!W_bf16) {
+        if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wt, false, stream, "bf16_w")))
+          return e;
+      }
+    } else {
+      if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wt, true, stream, "bf16_wt")))
+        return e;
+      gx = gemm_desc(SRU_OP_NT, true, (int)s.M, d_in, (int)s.N, dU, s.N, wt, s.N, dX, d_in);
+      gx.a_bf16 = gx.b_bf16 = true;
+    }
   } else {
     gx = gemm_desc(SRU_OP_NN, false, (int)s.M, d_in, (int)s.N, dU, s.N, W, d_in, dX, d_in);
   }
@@ -309,9 +342,9 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   if (int e = hip_status(sru::gemm_launch(gx, stream))) return e;
 
   // 3. dW = dU^T X (reduction over all tokens, split over K).  bf16 mode: X
-  //    rounded once into the workspace; both operands are then row-contiguous
-  //    bf16.
-  if (bf16) {
+  //    in bf16 (X_bf16, or rounded into the workspace); both operands are
+  //    then row-contiguous bf16.
+  if (bf16 && !X_bf16) {
     if (int e = hip_status(sru::to_bf16_launch(X, (int)s.M, d_in, xb, false, stream, "bf16_x")))
       return e;
   }
@@ -351,7 +384,7 @@ int sru_gemm(int op, int gemm_dtype, int M, int N, int K, const float* A, int ld
 int sru_scan_forward(const float* U, const float* X, const float* v_f, const float* v_r,
                      const float* b_f, const float* b_r, const float* c0, int L, int B, int d_in,
                      int d, int direction, const uint8_t* pad_mask, float* H, float* C,
-                     float* c_last, hipStream_t stream) {
+                     float* c_last, uint16_t* H_bf16, hipStream_t stream) {
   Dims s;
   int st = make_dims(L, B, d_in, d, direction, s);
   if (st != SRU_OK) return st;
@@ -360,7 +393,8 @@ int sru_scan_forward(const float* U, const float* X, const float* v_f, const flo
   const void* ptrs[] = {U, X, v_f, v_r, b_f, b_r, c0, H, C, c_last};
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
-  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last};
+  if ((reinterpret_cast<uintptr_t>(H_bf16) & 1) != 0) return SRU_E_ALIGN;
+  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16};
   return hip_status(sru::scan_forward_launch(scan_shape(s, direction), a, stream));
 }
 

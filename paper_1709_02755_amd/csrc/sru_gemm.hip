@@ -32,13 +32,6 @@
 
 #include "sru_internal.h"
 
-// Direct-path tile configurations (K-contiguous and row-contiguous operands)
-#ifndef SRU_DIRECT_KC
-#define SRU_DIRECT_KC DirectLine
-#endif
-#ifndef SRU_DIRECT_RC
-#define SRU_DIRECT_RC DirectLine
-#endif
 
 namespace sru {
 namespace {
@@ -628,7 +621,7 @@ struct DirectOperand {
   }
 };
 
-template <class C, int ADD, bool RC>
+template <class C, int ADD, bool A_RC, bool B_RC>
 __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelArgs g) {
   constexpr int STAGES = C::STAGES;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
@@ -648,8 +641,8 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(g.A, g.a_bytes);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(g.B, g.b_bytes);
 
-  using OpA = DirectOperand<C::BM, RC, C::A_BPW, C::BK>;
-  using OpB = DirectOperand<C::BN, RC, C::B_BPW, C::BK>;
+  using OpA = DirectOperand<C::BM, A_RC, C::A_BPW, C::BK>;
+  using OpB = DirectOperand<C::BN, B_RC, C::B_BPW, C::BK>;
   OpA la;
   OpB lb;
   la.init(wave, lane, m0, g.M, g.lda);
@@ -759,9 +752,10 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
   write_tile_rows<C, ADD>(g, acc, m0, n0, wm0, wn0, lane, ti.split);
 }
 
-template <class C, int ADD, bool RC>
+template <class C, int ADD, bool A_RC, bool B_RC>
 void launch_direct(const KernelArgs& a, int nwg, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_direct_kernel<C, ADD, RC>), dim3(nwg), dim3(C::THREADS), 0, st, a);
+  hipLaunchKernelGGL((gemm_direct_kernel<C, ADD, A_RC, B_RC>), dim3(nwg), dim3(C::THREADS), 0, st,
+                     a);
 }
 
 // Sum of split partials in split order, plus the optional addend.
@@ -924,11 +918,12 @@ long long operand_bytes(bool kc, int rows, int K, long long ld, int esz) {
   return (long long)esz * (kc ? (long long)(rows - 1) * ld + K : (long long)(K - 1) * ld + rows);
 }
 
-// bf16 x bf16 operands of one layout whose 16-byte chunks are whole (the
-// contiguous extent and leading dimension are multiples of 8 elements) and
-// that are smaller than the out-of-range sentinel.
+// bf16 x bf16 operands whose 16-byte chunks are whole (the contiguous
+// extent and leading dimension are multiples of 8 elements) and that are
+// smaller than the out-of-range sentinel.  Layouts: both K-contiguous, both
+// row-contiguous, or A K-contiguous with B row-contiguous (dX = dU W).
 bool direct_ok(const GemmDesc& g) {
-  if (!g.bf16 || !g.a_bf16 || !g.b_bf16 || g.a_kc != g.b_kc) return false;
+  if (!g.bf16 || !g.a_bf16 || !g.b_bf16 || (!g.a_kc && g.b_kc)) return false;
   const long long ab = operand_bytes(g.a_kc, g.M, g.K, g.lda, 2);
   const long long bb = operand_bytes(g.b_kc, g.N, g.K, g.ldb, 2);
   return vec_ok<uint16_t>(g.A, g.lda, g.a_kc ? g.K : g.M, ab) &&
@@ -949,23 +944,26 @@ int direct_splits_cfg(const GemmDesc& g) {
   return (g.K + kps - 1) / kps;
 }
 
-using CfgKC = SRU_DIRECT_KC;
-using CfgRC = SRU_DIRECT_RC;
+using CfgDirect = DirectLine;
 
-int direct_splits(const GemmDesc& g) {
-  return g.a_kc ? direct_splits_cfg<CfgKC>(g) : direct_splits_cfg<CfgRC>(g);
-}
+int direct_splits(const GemmDesc& g) { return direct_splits_cfg<CfgDirect>(g); }
 
 // Explicit instantiations: the host pass did not emit the launch stubs of
 // every specialisation referenced through launch_direct_cfg.
-template __global__ void gemm_direct_kernel<CfgKC, 0, false>(KernelArgs);
-template __global__ void gemm_direct_kernel<CfgKC, 1, false>(KernelArgs);
-template __global__ void gemm_direct_kernel<CfgKC, 2, false>(KernelArgs);
-template __global__ void gemm_direct_kernel<CfgRC, 0, true>(KernelArgs);
-template __global__ void gemm_direct_kernel<CfgRC, 1, true>(KernelArgs);
-template __global__ void gemm_direct_kernel<CfgRC, 2, true>(KernelArgs);
+#define SRU_DIRECT_INST(ADD, ARC, BRC) \
+  template __global__ void gemm_direct_kernel<CfgDirect, ADD, ARC, BRC>(KernelArgs);
+SRU_DIRECT_INST(0, false, false)
+SRU_DIRECT_INST(1, false, false)
+SRU_DIRECT_INST(2, false, false)
+SRU_DIRECT_INST(0, true, true)
+SRU_DIRECT_INST(1, true, true)
+SRU_DIRECT_INST(2, true, true)
+SRU_DIRECT_INST(0, false, true)
+SRU_DIRECT_INST(1, false, true)
+SRU_DIRECT_INST(2, false, true)
+#undef SRU_DIRECT_INST
 
-template <class C, bool RC>
+template <class C, bool A_RC, bool B_RC>
 hipError_t launch_direct_cfg(const GemmDesc& g, hipStream_t st) {
   const int splits = direct_splits_cfg<C>(g);
   const int kt = (g.K + C::BK - 1) / C::BK;
@@ -1001,9 +999,9 @@ hipError_t launch_direct_cfg(const GemmDesc& g, hipStream_t st) {
               (a.add_count == 0 || (a.add_ld % 4 == 0 && a.add_off % 4 == 0 && al16(a.add)));
   const int nwg = a.tiles_m * a.tiles_n * splits;
   timing_before(g.label ? g.label : !g.b_kc ? (g.a_kc ? "gemm_nn" : "gemm_tn") : "gemm_nt", st);
-  if (a.add_count == 2) launch_direct<C, 2, RC>(a, nwg, st);
-  else if (a.add_count == 1) launch_direct<C, 1, RC>(a, nwg, st);
-  else launch_direct<C, 0, RC>(a, nwg, st);
+  if (a.add_count == 2) launch_direct<C, 2, A_RC, B_RC>(a, nwg, st);
+  else if (a.add_count == 1) launch_direct<C, 1, A_RC, B_RC>(a, nwg, st);
+  else launch_direct<C, 0, A_RC, B_RC>(a, nwg, st);
   timing_after(st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
@@ -1046,6 +1044,8 @@ hipError_t launch_layout(const GemmDesc& g, hipStream_t st) {
 
 }  // namespace
 
+bool gemm_is_direct(const GemmDesc& g) { return direct_ok(g); }
+
 int gemm_splits(const GemmDesc& g) {
   if (direct_ok(g)) return direct_splits(g);
   const int s = g.bf16 ? splits_for<CfgBF16>(g) : splits_for<CfgF32>(g);
@@ -1061,8 +1061,11 @@ size_t gemm_partial_bytes(int M, int N, int splits) {
 
 hipError_t gemm_launch(const GemmDesc& g, hipStream_t st) {
   if ((g.a_bf16 || g.b_bf16) && !g.bf16) return hipErrorInvalidValue;
-  if (direct_ok(g))
-    return g.a_kc ? launch_direct_cfg<CfgKC, false>(g, st) : launch_direct_cfg<CfgRC, true>(g, st);
+  if (direct_ok(g)) {
+    if (!g.a_kc) return launch_direct_cfg<CfgDirect, true, true>(g, st);
+    if (!g.b_kc) return launch_direct_cfg<CfgDirect, false, true>(g, st);
+    return launch_direct_cfg<CfgDirect, false, false>(g, st);
+  }
   return g.bf16 ? launch_layout<CfgBF16>(g, st) : launch_layout<CfgF32>(g, st);
 }
 

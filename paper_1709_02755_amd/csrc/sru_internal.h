@@ -45,6 +45,8 @@ hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, b
 // Number of K splits the launcher will use for this product (>= 1) and the
 // partial-buffer bytes it then needs.
 int gemm_splits(const GemmDesc& g);
+// whether gemm_launch runs g on the direct (global -> LDS) bf16 kernel
+bool gemm_is_direct(const GemmDesc& g);
 size_t gemm_partial_bytes(int M, int N, int splits);
 hipError_t gemm_launch(const GemmDesc& g, hipStream_t stream);
 
@@ -65,6 +67,7 @@ struct ScanFwdArgs {
   float* H;
   float* C;
   float* c_last;
+  uint16_t* Hb;  // optional bf16 (RNE) copy of H
 };
 
 struct ScanBwdArgs {

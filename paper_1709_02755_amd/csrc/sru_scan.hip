@@ -46,7 +46,7 @@ __device__ __forceinline__ bool decode_lane(const ScanShape& s, Lane& ln) {
 }
 
 // ------------------------------------------------------------ forward scan
-template <int KB, bool MASK, bool STORE_C, int PF>
+template <int KB, bool MASK, bool STORE_C, bool STORE_HB, int PF>
 __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, ScanFwdArgs a) {
   Lane ln;
   if (!decode_lane(s, ln)) return;
@@ -60,6 +60,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
   const uint8_t* mp = MASK ? a.mask + ln.b : nullptr;
   float* hp = a.H + ln.gid;
   float* cp = STORE_C ? a.C + ln.gid : nullptr;
+  uint16_t* hbp = STORE_HB ? a.Hb + ln.gid : nullptr;
   const int d = s.d;
 
   const float vf = a.v_f[ln.fidx], vr = a.v_r[ln.fidx];
@@ -96,6 +97,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
     }
     __builtin_nontemporal_store(h, hp + t * h_step);
     if constexpr (STORE_C) __builtin_nontemporal_store(c, cp + t * h_step);
+    if constexpr (STORE_HB)
+      __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), hbp + t * h_step);
   };
 
 #pragma unroll
@@ -271,20 +274,24 @@ __global__ __launch_bounds__(256) void reduce_vb_kernel(const float* __restrict_
 constexpr int kFwdPF = 8;
 constexpr int kBwdPF = 6;
 
-template <int KB, bool MASK, bool STORE_C>
+template <int KB, bool MASK, bool STORE_C, bool STORE_HB>
 hipError_t fwd_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st) {
   const int lanes = s.B * s.ndir * s.d;
   const int grid = (lanes + kScanThreads - 1) / kScanThreads;
   timing_before("scan_fwd", st);
-  hipLaunchKernelGGL((scan_fwd_kernel<KB, MASK, STORE_C, kFwdPF>), dim3(grid), dim3(kScanThreads),
-                     0, st, s, a);
+  hipLaunchKernelGGL((scan_fwd_kernel<KB, MASK, STORE_C, STORE_HB, kFwdPF>), dim3(grid),
+                     dim3(kScanThreads), 0, st, s, a);
   timing_after(st);
   return hipGetLastError();
 }
 
 template <int KB, bool MASK>
 hipError_t fwd_dispatch_c(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st) {
-  return a.C ? fwd_dispatch<KB, MASK, true>(s, a, st) : fwd_dispatch<KB, MASK, false>(s, a, st);
+  if (a.Hb)
+    return a.C ? fwd_dispatch<KB, MASK, true, true>(s, a, st)
+               : fwd_dispatch<KB, MASK, false, true>(s, a, st);
+  return a.C ? fwd_dispatch<KB, MASK, true, false>(s, a, st)
+             : fwd_dispatch<KB, MASK, false, false>(s, a, st);
 }
 
 template <int KB, bool MASK>

@@ -36,11 +36,12 @@ _SIGNATURES = {
     "sru_version": (_I, []),
     "sru_forward_workspace_bytes": (_S, [_I] * 6),
     "sru_backward_workspace_bytes": (_S, [_I] * 6),
-    "sru_forward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I] + [_P] * 4 + [_P, _S, _P]),
-    "sru_backward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I] + [_P] * 4 + [_P] * 7 + [_P, _S, _P]),
+    "sru_forward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I] + [_P] * 4 + [_P] * 3 + [_P, _S, _P]),
+    "sru_backward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I] + [_P] * 4 + [_P] * 7 + [_P] * 2
+                     + [_P, _S, _P]),
     "sru_gemm_workspace_bytes": (_S, [_I] * 5),
     "sru_gemm": (_I, [_I] * 5 + [_P, _I, _P, _I, _P, _I] + [_P, _S, _P]),
-    "sru_scan_forward": (_I, [_P] * 7 + [_I] * 5 + [_P] + [_P] * 3 + [_P]),
+    "sru_scan_forward": (_I, [_P] * 7 + [_I] * 5 + [_P] + [_P] * 3 + [_P] + [_P]),
     "sru_scan_backward_workspace_bytes": (_S, [_I] * 5),
     "sru_scan_backward": (_I, [_P] * 10 + [_I] * 5 + [_P] + [_P] * 7 + [_P, _S, _P]),
     "sru_timing_begin": (_I, [_P, _I]),
@@ -138,9 +139,14 @@ def workspace(nbytes, device):
 
 
 def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
-            gemm_dtype=GEMM_FP32, store_c=True, out=None, ws=None):
-    """One layer forward; returns dict(U, H, C, c_last) (C None without store_c)."""
+            gemm_dtype=GEMM_FP32, store_c=True, out=None, ws=None, X_bf16=None):
+    """One layer forward; returns dict(U, H, C, c_last) (C None without store_c).
+
+    bf16 GEMMs only: X_bf16 (torch.bfloat16, X rounded) replaces the
+    rounding of X; entries W_bf16 / H_bf16 of `out` (bfloat16 tensors), if
+    present, receive Wcat and H rounded to bf16."""
     L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask)
+    _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True)
     dev = X.device
     if out is None:
         out = dict(U=torch.empty((L, B, ndir, k, d), device=dev),
@@ -153,16 +159,23 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
     st = lib().sru_forward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                            L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
                            _ptr(out["U"]), _ptr(out["H"]), _ptr(out.get("C")),
-                           _ptr(out.get("c_last")), _ptr(ws), need if ws is not None else 0,
+                           _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("W_bf16")),
+                           _ptr(out.get("H_bf16")), _ptr(ws), need if ws is not None else 0,
                            _stream())
     _check(st, "sru_forward")
     return out
 
 
 def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, direction=DIR_FWD,
-             mask=None, gemm_dtype=GEMM_FP32, want_dc0=True, out=None, ws=None):
-    """One layer backward; returns dict(dX, dW, dv_f, dv_r, db_f, db_r, dc0)."""
+             mask=None, gemm_dtype=GEMM_FP32, want_dc0=True, out=None, ws=None, X_bf16=None,
+             W_bf16=None):
+    """One layer backward; returns dict(dX, dW, dv_f, dv_r, db_f, db_r, dc0).
+
+    bf16 GEMMs only: X_bf16 / W_bf16 (bfloat16 roundings of X and Wcat, as
+    forward() writes them) replace the library's own rounding."""
     L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask)
+    _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True)
+    _req(W_bf16, "W_bf16", tuple(W.shape), dtype=torch.bfloat16, optional=True)
     _req(U, "U", (L, B, ndir, k, d))
     _req(C, "C", (L, B, ndir * d))
     _req(dH, "dH", (L, B, ndir * d))
@@ -181,7 +194,7 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
                             _ptr(U), _ptr(C), _ptr(dH), _ptr(dc_last),
                             _ptr(out["dX"]), _ptr(out["dW"]), _ptr(out["dv_f"]), _ptr(out["dv_r"]),
                             _ptr(out["db_f"]), _ptr(out["db_r"]), _ptr(out.get("dc0")),
-                            _ptr(ws), ws.numel(), _stream())
+                            _ptr(X_bf16), _ptr(W_bf16), _ptr(ws), ws.numel(), _stream())
     _check(st, "sru_backward")
     return out
 
@@ -218,7 +231,7 @@ def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None
     st = lib().sru_scan_forward(_ptr(U), _ptr(X), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r),
                                 _ptr(c0), L, B, d_in, d, direction, _ptr(mask),
                                 _ptr(out["H"]), _ptr(out.get("C")), _ptr(out.get("c_last")),
-                                _stream())
+                                _ptr(out.get("H_bf16")), _stream())
     _check(st, "sru_scan_forward")
     return out
 
@@ -253,6 +266,9 @@ class Stack:
     buffers, for the multi-layer forward + backward step.
 
     `layers` holds per-layer dicts of GPU tensors W, v_f, v_r, b_f, b_r.
+    With bf16 GEMMs each layer's forward also writes bf16 copies of Wcat and
+    H: the next layer's projection and every backward product read those
+    instead of rounding X and W again.
     """
 
     def __init__(self, layers, L, B, d_in, d, direction, gemm_dtype, device, backward=True):
@@ -270,6 +286,11 @@ class Stack:
                                 H=torch.empty((L, B, ndir * d), device=device),
                                 C=torch.empty((L, B, ndir * d), device=device),
                                 c_last=torch.empty((B, ndir * d), device=device)))
+            if gemm_dtype == GEMM_BF16:
+                self.fw[-1]["W_bf16"] = torch.empty(tuple(p["W"].shape), dtype=torch.bfloat16,
+                                                    device=device)
+                self.fw[-1]["H_bf16"] = torch.empty((L, B, ndir * d), dtype=torch.bfloat16,
+                                                    device=device)
             if backward:
                 self.bw.append(dict(dX=torch.empty((L, B, din), device=device),
                                     dW=torch.empty_like(p["W"]),
@@ -284,11 +305,11 @@ class Stack:
         self.ws = workspace(ws_bytes, device)
 
     def forward(self, X, mask=None):
-        x = X
+        x, xb = X, None
         for p, o in zip(self.layers, self.fw):
             forward(x, p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], None, self.direction, mask,
-                    self.gemm_dtype, out=o, ws=self.ws)
-            x = o["H"]
+                    self.gemm_dtype, out=o, ws=self.ws, X_bf16=xb)
+            x, xb = o["H"], o.get("H_bf16")
         return x
 
     def backward(self, X, dH, mask=None):
@@ -296,8 +317,9 @@ class Stack:
         for li in range(len(self.layers) - 1, -1, -1):
             p, o, b = self.layers[li], self.fw[li], self.bw[li]
             x = X if li == 0 else self.fw[li - 1]["H"]
+            xb = None if li == 0 else self.fw[li - 1].get("H_bf16")
             backward(x, p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], o["U"], o["C"], g,
                      None, None, self.direction, mask, self.gemm_dtype, want_dc0=False,
-                     out=b, ws=self.ws)
+                     out=b, ws=self.ws, X_bf16=xb, W_bf16=o.get("W_bf16"))
             g = b["dX"]
         return g

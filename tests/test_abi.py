@@ -43,26 +43,26 @@ def test_version_and_status_strings():
 
 def _fwd(lib, **kw):
     a = dict(X=FAKE, W=FAKE, v_f=FAKE, v_r=FAKE, b_f=FAKE, b_r=FAKE, c0=None, L=4, B=2, d_in=8,
-             d=8, direction=0, mask=None, gemm=0, U=FAKE, H=FAKE, C=FAKE, c_last=None, ws=None,
-             ws_bytes=0)
+             d=8, direction=0, mask=None, gemm=0, U=FAKE, H=FAKE, C=FAKE, c_last=None, Xb=None,
+             Wb=None, Hb=None, ws=None, ws_bytes=0)
     a.update(kw)
     return lib.sru_forward(a["X"], a["W"], a["v_f"], a["v_r"], a["b_f"], a["b_r"], a["c0"],
                            a["L"], a["B"], a["d_in"], a["d"], a["direction"], a["mask"],
-                           a["gemm"], a["U"], a["H"], a["C"], a["c_last"], a["ws"], a["ws_bytes"],
-                           None)
+                           a["gemm"], a["U"], a["H"], a["C"], a["c_last"], a["Xb"], a["Wb"],
+                           a["Hb"], a["ws"], a["ws_bytes"], None)
 
 
 def _bwd(lib, **kw):
     a = dict(X=FAKE, W=FAKE, v_f=FAKE, v_r=FAKE, b_f=FAKE, b_r=FAKE, c0=None, L=4, B=2, d_in=8,
              d=8, direction=0, mask=None, gemm=0, U=FAKE, C=FAKE, dH=FAKE, dc_last=None,
-             dX=FAKE, dW=FAKE, dv_f=FAKE, dv_r=FAKE, db_f=FAKE, db_r=FAKE, dc0=None, ws=None,
-             ws_bytes=0)
+             dX=FAKE, dW=FAKE, dv_f=FAKE, dv_r=FAKE, db_f=FAKE, db_r=FAKE, dc0=None, Xb=None,
+             Wb=None, ws=None, ws_bytes=0)
     a.update(kw)
     return lib.sru_backward(a["X"], a["W"], a["v_f"], a["v_r"], a["b_f"], a["b_r"], a["c0"],
                             a["L"], a["B"], a["d_in"], a["d"], a["direction"], a["mask"],
                             a["gemm"], a["U"], a["C"], a["dH"], a["dc_last"], a["dX"], a["dW"],
-                            a["dv_f"], a["dv_r"], a["db_f"], a["db_r"], a["dc0"], a["ws"],
-                            a["ws_bytes"], None)
+                            a["dv_f"], a["dv_r"], a["db_f"], a["db_r"], a["dc0"], a["Xb"],
+                            a["Wb"], a["ws"], a["ws_bytes"], None)
 
 
 @pytest.mark.parametrize("field", ["X", "W", "v_f", "v_r", "b_f", "b_r", "U", "H"])
@@ -83,6 +83,24 @@ def test_forward_rejects_bad_flag(kw):
 
 def test_forward_rejects_misaligned_pointer():
     assert _fwd(sru.lib(), H=FAKE_MIS) == E_ALIGN
+
+
+@pytest.mark.parametrize("field", ["Xb", "Wb", "Hb"])
+def test_forward_bf16_companions_checked(field):
+    lib = sru.lib()
+    # only with bf16 GEMMs
+    assert _fwd(lib, **{field: FAKE}) == E_FLAG
+    # 16-byte aligned (checked before the workspace)
+    assert _fwd(lib, gemm=1, **{field: ctypes.c_void_p(0x10008)}) == E_ALIGN
+    assert _fwd(lib, gemm=1, **{field: FAKE}) == E_WS
+
+
+@pytest.mark.parametrize("field", ["Xb", "Wb"])
+def test_backward_bf16_companions_checked(field):
+    lib = sru.lib()
+    assert _bwd(lib, **{field: FAKE}) == E_FLAG
+    assert _bwd(lib, gemm=1, **{field: ctypes.c_void_p(0x10008)}) == E_ALIGN
+    assert _bwd(lib, gemm=1, **{field: FAKE}) == E_WS
 
 
 @pytest.mark.parametrize("field", ["X", "W", "U", "C", "dH", "dX", "dW", "dv_f", "db_r"])
@@ -134,9 +152,11 @@ def test_scan_argument_checks():
     lib = sru.lib()
     f = lib.sru_scan_forward
     assert f(FAKE, None, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 0, None, FAKE, None, None,
-             None) == E_NULL                               # k = 3 needs X
+             None, None) == E_NULL                         # k = 3 needs X
     assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 9, None, FAKE, None, None,
-             None) == E_FLAG
+             None, None) == E_FLAG
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 0, None, FAKE, None, None,
+             ctypes.c_void_p(0x10001), None) == E_ALIGN    # bf16 H: 2-byte aligned
     b = lib.sru_scan_backward
     args = [FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 16, 8, 0, None,
             FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, None]
