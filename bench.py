@@ -95,18 +95,38 @@ def kernel_work(w, splits, bf16):
         "gemm_u": dict(flops=2.0 * M * N * K),     # U = X W^T
         "gemm_dx": dict(flops=2.0 * M * K * N),    # dX = dU W
         "gemm_dw": dict(flops=2.0 * N * K * M),    # dW = dU^T X
-        # read U (3 blocks) and x, write h and c: 24 B per (t, b, j)
-        "scan_fwd": dict(bytes=elems * 4.0 * (k + 1 + 2)),
+        # read U (3 blocks) and x, write h and c: 24 B per (t, b, j); with
+        # bf16 products also the bf16 copy of h (the next layer's operand)
+        "scan_fwd": dict(bytes=elems * (4.0 * (k + 1 + 2) + (2.0 if bf16 else 0.0))),
         # read U (3 blocks), x, c, dh (24 B); write dU (3 blocks, bf16 when
         # the products are bf16) and dx_hat (4 B): 34 B (bf16) / 40 B (fp32)
         "scan_bwd": dict(bytes=elems * (4.0 * (k + 3) + du_b * k + 4.0)),
         "reduce_vb": dict(bytes=4.0 * (4 * w.B * nfeat + 4 * nfeat)),
         "splitk_reduce": dict(bytes=4.0 * (splits + 1) * N * K),
-        # fp32 -> bf16 copies of the product operands: W, X, and W^T for dX
+        # fp32 -> bf16 copies of the product operands: Wcat, X (first layer),
+        # and Wcat^T where dX cannot read Wcat row-contiguous
         "bf16_w": dict(bytes=(4.0 + 2.0) * N * K),
         "bf16_x": dict(bytes=(4.0 + 2.0) * M * K),
         "bf16_wt": dict(bytes=(4.0 + 2.0) * N * K),
     }
+
+
+def dw_splits(lib, w):
+    """Split count of the dW product as sru_backward plans it.  The backward
+    workspace ends with the split partials (fp32 [splits, N, d_in]); the
+    buffers before them are laid out as the library does (each 256-aligned:
+    dU, dx_hat for k = 3, v/b partials, bf16 Wcat and X in bf16 mode)."""
+    a = lambda x: (x + 255) // 256 * 256
+    bf16 = w.gemm_dtype == 1
+    M, nfeat = w.tokens, w.ndir * w.d
+    k = 3 if w.d_in == w.d else 4
+    N = w.ndir * k * w.d
+    total = lib.sru_backward_workspace_bytes(w.L, w.B, w.d_in, w.d, w.direction, w.gemm_dtype)
+    before = a((2 if bf16 else 4) * M * N) + (a(4 * M * nfeat) if k == 3 else 0)
+    before += a(16 * w.B * nfeat)
+    if bf16:
+        before += a(2 * N * w.d_in) + a(2 * M * w.d_in)
+    return max(1, (total - before) // (4 * N * w.d_in))
 
 
 def source_hash():
@@ -194,13 +214,15 @@ def _per_kernel(rows, counter):
     return {k: v[0] / v[1] for k, v in acc.items()}
 
 
-# kernel-name substrings -> labels of the per-launch table
-KERNEL_KEYS = [("scan_fwd_kernel", "scan_fwd"), ("scan_bwd_kernel", "scan_bwd"),
-               ("reduce_vb_kernel", "reduce_vb"), ("splitk_reduce_kernel", "splitk_reduce"),
-               # the three products of the bf16 path (template args: stages, addend, layout)
-               ("gemm_direct_kernel<4, 0, false>", "gemm_u"),
-               ("gemm_direct_kernel<4, 1, false>", "gemm_dx"),
-               ("gemm_direct_kernel<4, 0, true>", "gemm_dw")]
+# kernel-name substrings (all must occur) -> labels of the per-launch table
+KERNEL_KEYS = [(("scan_fwd_kernel",), "scan_fwd"), (("scan_bwd_kernel",), "scan_bwd"),
+               (("reduce_vb_kernel",), "reduce_vb"), (("splitk_reduce_kernel",), "splitk_reduce"),
+               (("to_bf16_kernel",), "bf16_x"),
+               # the three products of the bf16 path (template args after the
+               # tile configuration: addend count, A row-contiguous, B row-contiguous)
+               (("gemm_direct_kernel", ">, 0, false, false>"), "gemm_u"),
+               (("gemm_direct_kernel", ">, 1, false, true>"), "gemm_dx"),
+               (("gemm_direct_kernel", ">, 0, true, true>"), "gemm_dw")]
 
 
 def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out):
@@ -208,7 +230,8 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out):
     and of the calibration copy) into per-launch HBM bytes for the scans."""
     def one(d, counter, key):
         vals = _per_kernel(_pmc_rows(d), counter)
-        hits = {k: v for k, v in vals.items() if key in k}
+        keys = (key,) if isinstance(key, str) else key
+        hits = {k: v for k, v in vals.items() if all(s in k for s in keys)}
         if not hits:
             raise SystemExit(f"{key} not in {d}")
         return max(hits.values())
@@ -241,7 +264,7 @@ def main():
     ap.add_argument("--workload", type=int, default=3, help="index into the workload table")
     ap.add_argument("--profile-steps", type=int, default=5,
                     help="steps run with per-kernel event brackets")
-    ap.add_argument("--cpu-seqs", type=int, default=32,
+    ap.add_argument("--cpu-seqs", type=int, default=64,
                     help="sequences in the CPU-oracle sample (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="REPS",
                     help="only run a 1 GiB copy REPS times (counter calibration)")
@@ -313,11 +336,7 @@ def main():
         a[0] += ms
         a[1] += 1
     ev.close()
-    splits = 1
-    if w.backward:
-        ws_k = lib.sru_gemm_workspace_bytes(sru.OP_TN, w.ndir * 3 * w.d, w.d_in, w.tokens,
-                                            w.gemm_dtype)
-        splits = max(1, ws_k // (4 * w.ndir * 3 * w.d * w.d_in))
+    splits = dw_splits(lib, w) if w.backward else 1
     work = kernel_work(w, splits, w.gemm_dtype == sru.GEMM_BF16)
     gemm_peak = MFMA_PEAK_TFLOPS["bf16" if w.gemm_dtype == sru.GEMM_BF16 else "fp32"]
     kernels = {}
