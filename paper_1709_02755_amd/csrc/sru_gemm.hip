@@ -725,7 +725,9 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
   // of stage kt, which frees that slot for the loads issued at the top of
   // the next iteration.  The last stage is peeled off so that no branch
   // separates the reads of the next f[0] from the MFMAs of the last slab: at
-  // a join the compiler would count those newer reads into the wait.
+  // a join the compiler would count those newer reads into the wait.  A
+  // scheduling barrier after each slab's reads keeps the compiler from
+  // sinking them next to the MFMAs that consume them.
   Frags f[2];
   if (nk > 0) {
     wait_stage(0);
@@ -736,16 +738,19 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
 #pragma unroll
       for (int sl = 0; sl + 1 < C::SLABS; ++sl) {
         load_frags(f[(sl + 1) & 1], kt, sl + 1);
+        __builtin_amdgcn_sched_barrier(0);  // reads of the next slab stay ahead
         mfmas(f[sl & 1]);
       }
       wait_stage(kt + 1);
       barrier();
       load_frags(f[0], kt + 1, 0);
+      __builtin_amdgcn_sched_barrier(0);  // reads of the next slab stay ahead
       mfmas(f[1]);
     }
 #pragma unroll
     for (int sl = 0; sl < C::SLABS; ++sl) {
       if (sl + 1 < C::SLABS) load_frags(f[(sl + 1) & 1], nk - 1, sl + 1);
+      __builtin_amdgcn_sched_barrier(0);  // reads of the next slab stay ahead
       mfmas(f[sl & 1]);
     }
   }

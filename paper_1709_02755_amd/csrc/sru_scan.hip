@@ -111,6 +111,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
       step(s0 + p, r0[p], r1[p], r2[p], rx[p], rm[p]);
       const int sn = s0 + p + PF < L ? s0 + p + PF : L - 1;
       load(sn, r0[p], r1[p], r2[p], rx[p], rm[p]);
+      // keep each prefetch where it is: sunk loads shorten the distance
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 #pragma unroll
@@ -219,7 +221,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
     put(dr, du + 2 * d);
     if constexpr (KB == 4) put(dx, du + 3 * d);
     else __builtin_nontemporal_store(dx, dxp + t * h_step);
-    c_t = cprev;
+    // c_t takes the value in a register of its own.  Were it to share
+    // cprev's register, the ring's registers would shift by one slot per
+    // step and the loop would copy still-loading values at its back edge.
+    asm volatile("v_mov_b32 %0, %1" : "=v"(c_t) : "v"(cprev));
   };
 
 #pragma unroll
@@ -232,6 +237,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
       step(i0 + p, r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);
       const int in = i0 + p + PF < L ? i0 + p + PF : L - 1;
       load(in, r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);
+      __builtin_amdgcn_sched_barrier(0);  // as in the forward scan
     }
   }
 #pragma unroll
