@@ -785,16 +785,20 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
-// fp32 -> bf16 conversions (RNE).  Plain copy: 4 elements per thread.
+// fp32 -> bf16 conversions (RNE).  Plain copy: 8 elements per thread (two
+// 16-byte loads, one 16-byte store).
 __global__ __launch_bounds__(256) void to_bf16_kernel(const float* __restrict__ src,
                                                       long long n, uint16_t* __restrict__ dst) {
-  const long long i = ((long long)blockIdx.x * 256 + threadIdx.x) * 4;
-  if (i + 3 < n) {
-    const floatx4 v = *reinterpret_cast<const floatx4*>(src + i);
-    u32x2 w;
-    w[0] = pack_bf16(v[0], v[1]);
-    w[1] = pack_bf16(v[2], v[3]);
-    *reinterpret_cast<u32x2*>(dst + i) = w;
+  const long long i = ((long long)blockIdx.x * 256 + threadIdx.x) * 8;
+  if (i + 7 < n) {
+    const floatx4 v0 = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(src + i));
+    const floatx4 v1 = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(src + i + 4));
+    u32x4 w;
+    w[0] = pack_bf16(v0[0], v0[1]);
+    w[1] = pack_bf16(v0[2], v0[3]);
+    w[2] = pack_bf16(v1[0], v1[1]);
+    w[3] = pack_bf16(v1[2], v1[3]);
+    *reinterpret_cast<u32x4*>(dst + i) = w;
   } else {
     for (long long j = i; j < n; ++j)
       dst[j] = __builtin_bit_cast(uint16_t, (__bf16)src[j]);
@@ -1082,7 +1086,7 @@ hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, b
     hipLaunchKernelGGL(to_bf16_t_kernel, grid, dim3(256), 0, st, src, rows, cols, dst);
   } else {
     const long long n = (long long)rows * cols;
-    const long long threads = (n + 3) / 4;
+    const long long threads = (n + 7) / 8;
     hipLaunchKernelGGL(to_bf16_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
                        src, n, dst);
   }

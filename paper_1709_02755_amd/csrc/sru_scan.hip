@@ -252,29 +252,38 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
   if (a.dc0) a.dc0[ln.gid] = g;
 }
 
-// Sum of the per-sequence partials over b, in a fixed order (deterministic):
-// four interleaved running sums, combined pairwise at the end.
-__global__ __launch_bounds__(256) void reduce_vb_kernel(const float* __restrict__ partial, int B,
-                                                        int nfeat, float* dv_f, float* dv_r,
-                                                        float* db_f, float* db_r) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= 4 * nfeat) return;
-  const int q = i / nfeat;
-  const int f = i - q * nfeat;
+// Sum of the per-sequence partials over b, in a fixed order (deterministic).
+// A workgroup covers 64 consecutive outputs; its 8 waves take b = w, w+8,
+// ... in sequence, and the 8 wave sums of an output are added as a fixed
+// tree through LDS.  The loads of a lane are independent, so a launch costs
+// about one memory round trip.
+constexpr int kVbWaves = 8;
+__global__ __launch_bounds__(64 * kVbWaves) void reduce_vb_kernel(const float* __restrict__ partial,
+                                                                  int B, int nfeat, float* dv_f,
+                                                                  float* dv_r, float* db_f,
+                                                                  float* db_r) {
+  __shared__ float red[kVbWaves][64];
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int o = blockIdx.x * 64 + lane;  // output: q * nfeat + f
+  const bool live = o < 4 * nfeat;
   const long long stride = 4LL * nfeat;
-  const float* p = partial + (long long)q * nfeat + f;
-  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-  int b = 0;
-  for (; b + 4 <= B; b += 4) {
-    s0 += p[(b + 0) * stride];
-    s1 += p[(b + 1) * stride];
-    s2 += p[(b + 2) * stride];
-    s3 += p[(b + 3) * stride];
+  float s = 0.f;
+  if (live) {
+    const float* p = partial + o;
+#pragma unroll 8
+    for (int b = w; b < B; b += kVbWaves) s += p[b * stride];
   }
-  for (; b < B; ++b) s0 += p[b * stride];
-  const float total = (s0 + s1) + (s2 + s3);
-  float* out = q == 0 ? dv_f : q == 1 ? dv_r : q == 2 ? db_f : db_r;
-  out[f] = total;
+  red[w][lane] = s;
+  __syncthreads();
+  if (w == 0 && live) {
+    const float t = ((red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane])) +
+                    ((red[4][lane] + red[5][lane]) + (red[6][lane] + red[7][lane]));
+    const int q = o / nfeat;
+    const int f = o - q * nfeat;
+    float* out = q == 0 ? dv_f : q == 1 ? dv_r : q == 2 ? db_f : db_r;
+    out[f] = t;
+  }
 }
 
 constexpr int kFwdPF = 8;
@@ -334,10 +343,10 @@ hipError_t scan_backward_launch(const ScanShape& s, const ScanBwdArgs& a, hipStr
   else e = m ? bwd_dispatch<4, true>(s, a, st) : bwd_dispatch<4, false>(s, a, st);
   if (e != hipSuccess) return e;
   const int nfeat = s.ndir * s.d;
-  const int grid = (4 * nfeat + 255) / 256;
+  const int grid = (4 * nfeat + 63) / 64;
   timing_before("reduce_vb", st);
-  hipLaunchKernelGGL(reduce_vb_kernel, dim3(grid), dim3(256), 0, st, a.partial, s.B, nfeat,
-                     a.dv_f, a.dv_r, a.db_f, a.db_r);
+  hipLaunchKernelGGL(reduce_vb_kernel, dim3(grid), dim3(64 * kVbWaves), 0, st, a.partial, s.B,
+                     nfeat, a.dv_f, a.dv_r, a.db_f, a.db_r);
   timing_after(st);
   return hipGetLastError();
 }

@@ -89,6 +89,51 @@ def test_scan_forward_on_oracle_projection(case):
         check(k, out[k], ref[k], TOL_FP32)
 
 
+# Forward scan without a mask at ragged sizes (L below, at and above the
+# prefetch ring, a partial last wave, k = 3 and 4, every direction), with
+# and without C, writing the bf16 copy of H as well.
+LDS_SCAN_CASES = [
+    # (L, B, d_in, d, direction)
+    (1, 1, 4, 4, O.DIR_FWD),
+    (5, 3, 20, 20, O.DIR_REV),
+    (27, 3, 40, 20, O.DIR_BI),
+    (29, 2, 96, 96, O.DIR_FWD),
+    (61, 5, 64, 64, O.DIR_BI),
+    (100, 4, 96, 64, O.DIR_REV),
+    (130, 3, 128, 128, O.DIR_FWD),
+]
+
+
+@pytest.mark.parametrize("store_c", [True, False])
+@pytest.mark.parametrize("case", LDS_SCAN_CASES)
+def test_scan_forward_outputs_unmasked(case, store_c):
+    L, B, d_in, d, direction = case
+    print(f"scan_fwd outputs L={L} B={B} d_in={d_in} d={d} dir={direction} C={store_c}",
+          flush=True)
+    c = _case(L * 17 + d, L, B, d_in, d, direction, c0=True, bias_scale=0.5)
+    ref = O.forward(c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"], c["c0"], direction,
+                    None)
+    U = ref["U"].astype(np.float32)
+    ndir = 2 if direction == O.DIR_BI else 1
+    out = dict(H=torch.full((L, B, ndir * d), float("nan"), device="cuda"),
+               C=torch.full((L, B, ndir * d), float("nan"), device="cuda") if store_c else None,
+               c_last=torch.full((B, ndir * d), float("nan"), device="cuda"),
+               H_bf16=torch.zeros((L, B, ndir * d), dtype=torch.bfloat16, device="cuda"))
+    out = sru.scan_forward(dev(U), dev(c["X"]), dev(c["v_f"]), dev(c["v_r"]), dev(c["b_f"]),
+                           dev(c["b_r"]), dev(c["c0"]), direction, None, out=out)
+    torch.cuda.synchronize()
+    keys = ("H", "C", "c_last") if store_c else ("H", "c_last")
+    for k in keys:
+        check(k, out[k], ref[k], TOL_FP32)
+    assert torch.equal(out["H_bf16"].view(torch.int16), out["H"].to(torch.bfloat16).view(torch.int16))
+    # the same without the bf16 copy
+    out2 = sru.scan_forward(dev(U), dev(c["X"]), dev(c["v_f"]), dev(c["v_r"]), dev(c["b_f"]),
+                            dev(c["b_r"]), dev(c["c0"]), direction, None, store_c=store_c)
+    torch.cuda.synchronize()
+    for k in keys:
+        assert torch.equal(out2[k], out[k]), k
+
+
 @pytest.mark.parametrize("case", SCAN_CASES)
 def test_scan_backward_on_oracle_states(case):
     L, B, d_in, d, direction, masked = case
