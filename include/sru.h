@@ -3,12 +3,12 @@
  * Simple Recurrent Unit layer (Lei et al., "Simple Recurrent Units for Highly
  * Parallelizable Recurrence", EMNLP 2018).
  *
- * The layer (Sec. 2, Eq. 1-4), per direction, for t in the direction's order:
+ * The layer (Sec. 3, Eq. 1-4), per direction, for t in the direction's order:
  *   f_t = sigma(W_f x_t + v_f * c_{t-1} + b_f)
  *   c_t = f_t * c_{t-1} + (1 - f_t) * (W x_t)
  *   r_t = sigma(W_r x_t + v_r * c_{t-1} + b_r)
  *   h_t = r_t * c_t + (1 - r_t) * x_hat_t
- * computed as in Sec. 2.1: one matrix product U = X [W; W_f; W_r]^T over all
+ * computed as in Sec. 3.1: one matrix product U = X [W; W_f; W_r]^T over all
  * L*B tokens, then one fused element-wise scan, parallel over (batch, hidden
  * unit, direction) and sequential over t (Algorithm 1).  The reset gate reads
  * c_{t-1} as Eq. 3 writes it.
@@ -95,7 +95,7 @@ SRU_API size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int d
                                     int gemm_dtype);
 
 /*
- * Forward pass of one layer (Sec. 2 Eq. 1-4, organised as Sec. 2.1 /
+ * Forward pass of one layer (Sec. 3 Eq. 1-4, organised as Sec. 3.1 /
  * Algorithm 1).
  *   in : X, W, v_f, v_r, b_f, b_r; c0 (NULL = zeros); pad_mask (NULL = none)
  *   out: U [M, N] -- the batched projection, kept by the caller for
@@ -155,7 +155,7 @@ typedef enum {
   SRU_OP_TN = 2  /* C[M,N] = A[K,M]^T * B[K,N]   (dW = dU^T X)   */
 } sru_gemm_op;
 
-/* Matrix product on the MFMA units (the batched projection of Sec. 2.1 and
+/* Matrix product on the MFMA units (the batched projection of Sec. 3.1 and
  * its two backward products).  Row-major operands with leading dimensions
  * lda, ldb, ldc (elements).  gemm_dtype as above.  TN may split the
  * reduction; it then needs sru_gemm_workspace_bytes of workspace. */

@@ -6,7 +6,7 @@ leg of the benchmark use it.  It shares no code with the HIP library and
 imports nothing from the product package.
 
 What it computes (Lei et al., "Simple Recurrent Units for Highly
-Parallelizable Recurrence", Sec. 2, Eq. 1-4):
+Parallelizable Recurrence", Sec. 3, Eq. 1-4):
 
     f_t = sigma(W_f x_t + v_f * c_{t-1} + b_f)          (Eq. 1)
     c_t = f_t * c_{t-1} + (1 - f_t) * (W x_t)            (Eq. 2)
@@ -14,9 +14,9 @@ Parallelizable Recurrence", Sec. 2, Eq. 1-4):
     h_t = r_t * c_t + (1 - r_t) * x_t                    (Eq. 4)
 
 The forward pass is the plain per-step definition (the "naive
-implementation" of Sec. 2.1 that evaluates Eq. 1-4 one step at a time, with
+implementation" of Sec. 3.1 that evaluates Eq. 1-4 one step at a time, with
 the projections x_t W^T computed inside the time loop).  The batched
-reorganisation of Sec. 2.1 (one matrix product for all steps, then the fused
+reorganisation of Sec. 3.1 (one matrix product for all steps, then the fused
 element-wise loop of Algorithm 1) is what the GPU path implements; the oracle
 does NOT assume it, and the test suite checks the two organisations agree.
 
@@ -246,7 +246,7 @@ def forward_alg1_scalar(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
                         pad_mask=None):
     """Tiny-shape cross-check in the shape of Algorithm 1 (fp32 GEMM mode).
 
-    The projections for all steps come first as one batched product (Sec. 2.1),
+    The projections for all steps come first as one batched product (Sec. 3.1),
     then independent scalar recurrences run per (example i, dimension j),
     reading the gate columns at offsets j, j+d, j+2d of the batched tensor.
     The reset gate uses the previous state (Eq. 3 reading).  Pure Python loops:

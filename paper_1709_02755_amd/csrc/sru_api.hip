@@ -237,7 +237,7 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
     if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
   }
 
-  // U = X Wcat^T (Sec. 2.1).  bf16 mode: W and X rounded once (into
+  // U = X Wcat^T (Sec. 3.1).  bf16 mode: W and X rounded once (into
   // W_bf16 / the workspace, unless the caller holds X_bf16), so both
   // operands of the product are K-contiguous bf16.
   const void* Wop = W;

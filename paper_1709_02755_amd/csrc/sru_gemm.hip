@@ -1,6 +1,6 @@
 // Matrix products of the SRU layer on the gfx950 matrix cores (MFMA).
 //
-// The forward projection of Sec. 2.1 (U = X [W; W_f; W_r]^T over all L*B
+// The forward projection of Sec. 3.1 (U = X [W; W_f; W_r]^T over all L*B
 // tokens at once) and the two products of the backward pass (dX = dU W and
 // dW = dU^T X) are one kernel template:
 //     C[M,N] = sum_k A(m,k) B(n,k)

@@ -1,6 +1,6 @@
 // Element-wise scans of the SRU layer on gfx950.
 //
-// Forward: the fused kernel of Sec. 2.1 / Algorithm 1.  One lane per
+// Forward: the fused kernel of Sec. 3.1 / Algorithm 1.  One lane per
 // (batch b, direction, hidden unit j), sequential over t, the state c held in
 // a register.  Eq. 1-4 with the reset gate on c_{t-1} (Eq. 3).
 // Backward: the chain rule of Eq. 1-4 in reverse step order; one lane per

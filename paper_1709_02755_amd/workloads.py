@@ -6,7 +6,7 @@ tests) and the CPU oracle receive the float32 arrays it returns.
 
 The paper trains on public datasets (SST, SQuAD, WMT, Enwik8) that are not
 available here; these synthetic tensors stand in for them, with the shapes
-below and the value distributions of the initialisation paragraph (Sec. 2.2):
+below and the value distributions of the initialisation paragraph (Sec. 3.2):
 weights uniform on [-sqrt(3/d), +sqrt(3/d)], i.e. variance 1/d.
 
 Draw order (fixed, PCG64 = numpy.random.default_rng(seed)), all in float64

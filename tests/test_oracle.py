@@ -38,7 +38,7 @@ def _bw(c, direction, gemm=O.GEMM_FP32, **over):
 
 # ---------------------------------------------------------------- hand example
 def test_hand_worked_example_gates_half():
-    """Sec. 2 Eq. 1-4 at sigma(0) = 1/2: exact dyadic values worked by hand."""
+    """Sec. 3 Eq. 1-4 at sigma(0) = 1/2: exact dyadic values worked by hand."""
     g = json.load(open(os.path.join(HERE, "golden", "hand_example_gates_half.json")))
     s, e = g["setup"], g["expected"]
     X = np.array(s["x"], np.float32).reshape(3, 1, 1)
@@ -247,7 +247,7 @@ def _flip_within_length(A, lengths):
 def test_bidirectional_is_two_independent_directions(k4):
     """Bidirectional output = [forward layer with W_fwd | the forward layer
     with W_rev run on each sequence reversed within its length, reversed
-    back], and likewise every gradient (Sec. 2.1: the two directions are
+    back], and likewise every gradient (Sec. 3.1: the two directions are
     batched, not coupled)."""
     rng = np.random.default_rng(5)
     L, B, d = 8, 4, 3
@@ -325,7 +325,7 @@ def test_masked_equals_truncated_sequences(rng):
 @pytest.mark.parametrize("direction", [F, R, BI])
 @pytest.mark.parametrize("k4", [False, True])
 def test_batched_reorganisation_equals_per_step(direction, k4):
-    """Sec. 2.1: batching the projections over all steps and then running the
+    """Sec. 3.1: batching the projections over all steps and then running the
     scalar element-wise loop (Algorithm 1, reset gate on c_{t-1}) gives the
     same result as Eq. 1-4 step by step."""
     rng = np.random.default_rng(3)
