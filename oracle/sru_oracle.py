@@ -22,8 +22,12 @@ does NOT assume it, and the test suite checks the two organisations agree.
 
 Readings of the paper taken here (each is also listed in the design notes):
   * The reset gate uses c_{t-1}, as Eq. 3 writes it (Algorithm 1 evaluates r
-    after updating c; Eq. 3 is taken as the definition).
+    after updating c; Eq. 3 is taken as the definition).  With
+    reset_new=True it uses c_t instead: Algorithm 1's order.
   * Highway scaling alpha = 1 (Eq. 4 as printed, no scaling correction).
+    Sec. 3.2 multiplies the highway term by a constant alpha (sqrt(3), or
+    sqrt(1 + 2 e^b) for a reset-gate bias b, Appendix A); the alpha
+    argument does that:  h_t = r_t * c_t + (1 - r_t) * x_hat * alpha.
   * "b_v" after Eq. 4 is read as b_r.
   * When d_in != d, Eq. 4 has no x_t of width d; the highway term uses a
     fourth learned block W_h (x_hat = W_h x_t), stored as projection block 3.
@@ -85,6 +89,12 @@ def sigmoid(z):
         return 1.0 / (1.0 + np.exp(-z))
 
 
+def scaling_alpha(b):
+    """Highway scaling constant for a reset-gate bias b (Sec. 3.2, derived in
+    Appendix A): alpha = sqrt(1 + 2 e^b), sqrt(3) at b = 0."""
+    return float(np.sqrt(1.0 + 2.0 * np.exp(b)))
+
+
 def _ndir(direction):
     if direction not in (DIR_FWD, DIR_REV, DIR_BI):
         raise ValueError(f"unknown direction {direction}")
@@ -109,8 +119,11 @@ def _check_shapes(X, W, direction):
 
 
 def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
-            pad_mask=None, gemm_dtype=GEMM_FP32):
+            pad_mask=None, gemm_dtype=GEMM_FP32, alpha=1.0, reset_new=False):
     """Eq. 1-4 evaluated step by step; returns dict(U, H, C, c_last).
+
+    alpha scales the highway term (Sec. 3.2); reset_new makes the reset gate
+    read the updated state c_t (Algorithm 1's order) instead of c_{t-1}.
 
     U holds the per-step projections x_t W^T (one block per gate), assembled
     in the [L, B, ndir, k, d] layout so that it can be compared with the
@@ -138,9 +151,10 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
             u = [xp @ Wp[dirn, q].T for q in range(k)]          # W x_t, W_f x_t, ...
             x_hat = x_t if k == 3 else u[3]
             f = sigmoid(u[1] + v_f[dirn] * c + b_f[dirn])        # Eq. 1
-            r = sigmoid(u[2] + v_r[dirn] * c + b_r[dirn])        # Eq. 3 (old c)
             c_new = f * c + (1.0 - f) * u[0]                      # Eq. 2
-            h = r * c_new + (1.0 - r) * x_hat                     # Eq. 4
+            s = c_new if reset_new else c                         # state r reads
+            r = sigmoid(u[2] + v_r[dirn] * s + b_r[dirn])        # Eq. 3
+            h = r * c_new + (1.0 - r) * x_hat * alpha             # Eq. 4 (Sec. 3.2)
             valid = ~pad[t][:, None]
             c = np.where(valid, c_new, c)
             H[t, :, dirn] = np.where(valid, h, 0.0)
@@ -152,8 +166,9 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
 
 
 def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
-             pad_mask=None, gemm_dtype=GEMM_FP32, dc_last=None, fw=None):
-    """Reverse-step chain rule of Eq. 1-4.
+             pad_mask=None, gemm_dtype=GEMM_FP32, dc_last=None, fw=None, alpha=1.0,
+             reset_new=False):
+    """Reverse-step chain rule of Eq. 1-4 (alpha and reset_new as in forward).
 
     Returns dict(dX, dW, dv_f, dv_r, db_f, db_r, dc0, dU, dxh) where dU is
     the gradient with respect to the projections ([L, B, ndir, k, d]) and dxh
@@ -173,7 +188,7 @@ def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
 
     if fw is None:
         fw = forward(X, W, v_f, v_r, b_f, b_r, c0_.reshape(B, ndir * d), direction,
-                     pad_mask, gemm_dtype)
+                     pad_mask, gemm_dtype, alpha, reset_new)
     U = fw["U"]
     C = fw["C"].reshape(L, B, ndir, d)
     Wp = bf16_round(W) if bf16 else W
@@ -202,12 +217,15 @@ def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
             dh = np.where(valid, dH[t, :, dirn], 0.0)
 
             f = sigmoid(u1 + v_f[dirn] * c_p + b_f[dirn])
-            r = sigmoid(u2 + v_r[dirn] * c_p + b_r[dirn])
+            s = c_t if reset_new else c_p             # the state r reads
+            r = sigmoid(u2 + v_r[dirn] * s + b_r[dirn])
+            dr = dh * (c_t - alpha * x_hat) * r * (1.0 - r)  # through r's pre-activation
             gc = g + dh * r                            # dh/dc_t = r
-            dr = dh * (c_t - x_hat) * r * (1.0 - r)    # through r's pre-activation
+            if reset_new:
+                gc = gc + dr * v_r[dirn]               # r also depends on c_t
             df = gc * (c_p - u0) * f * (1.0 - f)       # through f's pre-activation
             du0 = gc * (1.0 - f)
-            dxhat = dh * (1.0 - r)
+            dxhat = dh * (1.0 - r) * alpha
             df = np.where(valid, df, 0.0)
             dr = np.where(valid, dr, 0.0)
             du0 = np.where(valid, du0, 0.0)
@@ -221,10 +239,12 @@ def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
             else:
                 dU[t, :, dirn, 3] = dxhat
             dv_f[dirn] += (df * c_p).sum(axis=0)
-            dv_r[dirn] += (dr * c_p).sum(axis=0)
+            dv_r[dirn] += (dr * s).sum(axis=0)
             db_f[dirn] += df.sum(axis=0)
             db_r[dirn] += dr.sum(axis=0)
-            g_prev = gc * f + df * v_f[dirn] + dr * v_r[dirn]
+            g_prev = gc * f + df * v_f[dirn]
+            if not reset_new:
+                g_prev = g_prev + dr * v_r[dirn]       # r depends on c_{t-1}
             g = np.where(valid, g_prev, g)             # padded step: identity on c
 
             # Projections: dX gets dU_t W, dW gets dU_t^T x_t (per step).
@@ -243,13 +263,14 @@ def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
 
 
 def forward_alg1_scalar(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
-                        pad_mask=None):
+                        pad_mask=None, alpha=1.0, reset_new=False):
     """Tiny-shape cross-check in the shape of Algorithm 1 (fp32 GEMM mode).
 
     The projections for all steps come first as one batched product (Sec. 3.1),
     then independent scalar recurrences run per (example i, dimension j),
     reading the gate columns at offsets j, j+d, j+2d of the batched tensor.
-    The reset gate uses the previous state (Eq. 3 reading).  Pure Python loops:
+    The reset gate uses the previous state (Eq. 3 reading) unless reset_new,
+    where it follows Algorithm 1's order (r after c).  Pure Python loops:
     only for tiny shapes.
     """
     X = _f64(X)
@@ -274,16 +295,18 @@ def forward_alg1_scalar(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
                         continue
                     u = Ub[l, i, dirn]
                     f = float(sigmoid(u[j + d] + v_f[dirn, j] * c + b_f[dirn, j]))
-                    r = float(sigmoid(u[j + 2 * d] + v_r[dirn, j] * c + b_r[dirn, j]))
+                    c_prev = c
                     c = f * c + (1.0 - f) * u[j]
+                    s = c if reset_new else c_prev
+                    r = float(sigmoid(u[j + 2 * d] + v_r[dirn, j] * s + b_r[dirn, j]))
                     xh = X[l, i, j] if k == 3 else u[j + 3 * d]
-                    H[l, i, dirn, j] = r * c + (1.0 - r) * xh
+                    H[l, i, dirn, j] = r * c + (1.0 - r) * xh * alpha
                     C[l, i, dirn, j] = c
     return dict(H=H.reshape(L, B, ndir * d), C=C.reshape(L, B, ndir * d))
 
 
 def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
-                           need_backward=True):
+                           need_backward=True, alpha=1.0, reset_new=False):
     """Stacked layers: layer l+1 takes layer l's H as its X.
 
     `layers` is a list of dicts with W, v_f, v_r, b_f, b_r (c0 = 0).
@@ -294,7 +317,7 @@ def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
     fws = []
     for p in layers:
         fw = forward(xs[-1], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], None,
-                     direction, pad_mask, gemm_dtype)
+                     direction, pad_mask, gemm_dtype, alpha, reset_new)
         fws.append(fw)
         xs.append(fw["H"])
     grads = []
@@ -303,7 +326,8 @@ def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
         for li in range(len(layers) - 1, -1, -1):
             p = layers[li]
             bw = backward(xs[li], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], g,
-                          None, direction, pad_mask, gemm_dtype, fw=fws[li])
+                          None, direction, pad_mask, gemm_dtype, fw=fws[li], alpha=alpha,
+                          reset_new=reset_new)
             grads.append(bw)
             g = bw["dX"]
         grads.reverse()

@@ -456,3 +456,146 @@ def test_single_step_closed_form(rng):
     c1 = f * c0 + (1 - f) * (x @ W[0, 0].T)
     np.testing.assert_allclose(fw["C"][0], c1, rtol=1e-13, atol=1e-14)
     np.testing.assert_allclose(fw["H"][0], r * c1 + (1 - r) * x, rtol=1e-13, atol=1e-14)
+
+
+# ------------------------------------------------- gate and highway variants
+# Sec. 3.2's scaling correction (alpha on the highway term) and Algorithm 1's
+# order of the reset gate (r_t from the updated state c_t).
+
+VARIANTS = [(np.sqrt(3.0), False), (0.7, True), (1.0, True), (np.sqrt(3.0), True)]
+
+
+@pytest.mark.parametrize("alpha,reset_new", VARIANTS)
+@pytest.mark.parametrize("direction,k4", [(F, False), (BI, True), (R, False)])
+def test_variant_gradients_match_finite_differences(alpha, reset_new, direction, k4):
+    """The backward of both variants against central differences of the
+    forward in fp64: every input, a padded sequence, c0 and dc_last."""
+    rng = np.random.default_rng(31 + direction + 5 * k4 + int(10 * alpha) + 7 * reset_new)
+    L, B, d = 4, 3, 3
+    d_in = 2 * d if k4 else d
+    c = _case(rng, L, B, d_in, d, direction, c0=True, dc_last=True, bias_scale=0.5,
+              masked=True, v_scale=1.5)
+    base = {k: (None if v is None else np.asarray(v, np.float64)) for k, v in c.items()
+            if k in ("X", "W", "v_f", "v_r", "b_f", "b_r", "c0")}
+    dH, dcl, mask = c["dH"].astype(np.float64), c["dc_last"].astype(np.float64), c["mask"]
+
+    def loss(p):
+        fw = O.forward(p["X"], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], p["c0"],
+                       direction, mask, alpha=alpha, reset_new=reset_new)
+        return _loss(fw, dH, dcl)
+
+    bw = O.backward(base["X"], base["W"], base["v_f"], base["v_r"], base["b_f"], base["b_r"],
+                    dH, base["c0"], direction, mask, O.GEMM_FP32, dcl, alpha=alpha,
+                    reset_new=reset_new)
+    names = dict(X="dX", W="dW", v_f="dv_f", v_r="dv_r", b_f="db_f", b_r="db_r", c0="dc0")
+    h = 1e-6
+    for pname, gname in names.items():
+        p0 = base[pname]
+        num = np.zeros(p0.size)
+        for i in range(p0.size):
+            pp = dict(base)
+            a = p0.copy().ravel(); a[i] += h; pp[pname] = a.reshape(p0.shape)
+            lp = loss(pp)
+            a = p0.copy().ravel(); a[i] -= h; pp[pname] = a.reshape(p0.shape)
+            lm = loss(pp)
+            num[i] = (lp - lm) / (2 * h)
+        ana = np.asarray(bw[gname]).ravel()
+        scale = max(np.max(np.abs(num)), 1e-3)
+        assert np.max(np.abs(ana - num)) / scale < 1e-6, (pname, ana, num)
+
+
+def test_reset_gate_new_state_closed_form(rng):
+    """Algorithm 1's order with b_f = -100: c_t = W x_t, so
+    r_t = sigma(W_r x_t + v_r * W x_t + b_r) and
+    h_t = r_t W x_t + (1 - r_t) alpha x_t (sigma from scipy)."""
+    L, B, d = 6, 3, 4
+    alpha = 1.3
+    c = _case(rng, L, B, d, d, F, c0=True, v_scale=2.0, bias_scale=1.0)
+    c["b_f"] = np.full((1, d), -100.0, np.float32)
+    fw = O.forward(c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"], c["c0"], F,
+                   alpha=alpha, reset_new=True)
+    X = c["X"].astype(np.float64)
+    W = c["W"].astype(np.float64)
+    u0 = np.matmul(X, W[0, 0].T)
+    r = scipy.special.expit(np.matmul(X, W[0, 2].T) + c["v_r"][0] * u0 + c["b_r"][0])
+    np.testing.assert_allclose(fw["H"], r * u0 + (1 - r) * alpha * X, rtol=1e-12, atol=1e-13)
+
+
+def test_reset_orders_agree_without_v_r(rng):
+    """v_r = 0 removes the reset gate's state input: both orders coincide
+    exactly in the forward pass and in every gradient but dv_r (whose
+    derivative is the state the gate reads: c_{t-1} or c_t)."""
+    c = _case(rng, 9, 3, 6, 5, BI, c0=True, dc_last=True, masked=True, bias_scale=0.5)
+    c["v_r"] = np.zeros_like(c["v_r"])
+    args = (c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"])
+    a = O.forward(*args, c["c0"], BI, c["mask"], alpha=1.7)
+    b = O.forward(*args, c["c0"], BI, c["mask"], alpha=1.7, reset_new=True)
+    for k in ("H", "C", "c_last"):
+        assert np.array_equal(a[k], b[k]), k
+    ga = O.backward(*args, c["dH"], c["c0"], BI, c["mask"], O.GEMM_FP32, c["dc_last"], alpha=1.7)
+    gb = O.backward(*args, c["dH"], c["c0"], BI, c["mask"], O.GEMM_FP32, c["dc_last"],
+                    alpha=1.7, reset_new=True)
+    for k in ("dX", "dW", "dv_f", "db_f", "db_r", "dc0"):
+        np.testing.assert_allclose(ga[k], gb[k], rtol=1e-13, atol=1e-15)
+    assert not np.allclose(ga["dv_r"], gb["dv_r"])
+
+
+@pytest.mark.parametrize("k4", [False, True])
+def test_highway_scale_extremes(rng, k4):
+    """b_r = -100 closes the reset gate: h_t = alpha x_hat (x_t, or W_h x_t
+    via numpy.matmul for k = 4).  b_r = +100 opens it: h_t = c_t, whatever
+    alpha is."""
+    d = 4
+    d_in = 6 if k4 else d
+    c = _case(rng, 5, 3, d_in, d, F, c0=True, bias_scale=0.5)
+    alpha = 1.9
+    c["b_r"] = np.full((1, d), -100.0, np.float32)
+    fw = O.forward(c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"], c["c0"], F,
+                   alpha=alpha)
+    X = c["X"].astype(np.float64)
+    xhat = np.matmul(X, c["W"][0, 3].astype(np.float64).T) if k4 else X
+    np.testing.assert_allclose(fw["H"], alpha * xhat, rtol=1e-12, atol=1e-12)
+    c["b_r"] = np.full((1, d), 100.0, np.float32)
+    fw = O.forward(c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"], c["c0"], F,
+                   alpha=alpha)
+    np.testing.assert_allclose(fw["H"], fw["C"], rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("b", [0.0, -1.0])
+def test_scaling_correction_variance_appendix(b):
+    """Appendix A: at initialisation Var[h]/Var[x] is about
+    (e^{2b} Var[c]/Var[x] + alpha^2) / (e^b + 1)^2, with Var[c]/Var[x] -> 1/3
+    for independent steps and -> 1 for identical steps; alpha =
+    sqrt(1 + 2 e^b) makes the identical-step ratio 1.  Loose statistical
+    bounds (5 %)."""
+    assert O.scaling_alpha(0.0) == pytest.approx(np.sqrt(3.0), rel=1e-15)
+    rng = np.random.default_rng(2)
+    L, B, d = 160, 48, 192
+    bound = np.sqrt(3.0 / d)
+    W = rng.uniform(-bound, bound, (1, 3, d, d)).astype(np.float32)
+    z = np.zeros((1, d), np.float32)
+    br = np.full((1, d), b, np.float32)
+    alpha = O.scaling_alpha(b)
+    Xi = (0.01 * rng.standard_normal((L, B, d))).astype(np.float32)
+    Xc = np.broadcast_to((0.01 * rng.standard_normal((1, B, d))).astype(np.float32), (L, B, d)).copy()
+    burn = 40
+    hi = O.forward(Xi, W, z, z, z, br, None, F, alpha=alpha)["H"]
+    hc = O.forward(Xc, W, z, z, z, br, None, F, alpha=alpha)["H"]
+    ri = np.var(hi[burn:]) / np.var(Xi[burn:])
+    rc = np.var(hc[burn:]) / np.var(Xc[burn:])
+    eb = np.exp(b)
+    want_i = (eb * eb / 3.0 + alpha ** 2) / (eb + 1.0) ** 2
+    assert abs(ri - want_i) < 0.05 * want_i, (ri, want_i)
+    assert abs(rc - 1.0) < 0.05, rc
+
+
+@pytest.mark.parametrize("alpha,reset_new", VARIANTS)
+def test_alg1_scalar_loop_matches_variants(rng, alpha, reset_new):
+    """The per-(i, j) scalar loop in Algorithm 1's shape agrees with the
+    vectorised per-step forward for both variants."""
+    c = _case(rng, 6, 2, 5, 3, BI, c0=True, masked=True, bias_scale=0.5, v_scale=1.5)
+    args = (c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"], c["c0"], BI, c["mask"])
+    a = O.forward(*args, alpha=alpha, reset_new=reset_new)
+    b = O.forward_alg1_scalar(*args, alpha=alpha, reset_new=reset_new)
+    for k in ("H", "C"):
+        np.testing.assert_allclose(a[k], b[k], rtol=1e-12, atol=1e-13)
