@@ -266,6 +266,10 @@ def main():
                     help="steps run with per-kernel event brackets")
     ap.add_argument("--cpu-seqs", type=int, default=64,
                     help="sequences in the CPU-oracle sample (0 = skip)")
+    ap.add_argument("--highway-scale", type=float, default=1.0,
+                    help="alpha on the highway term (Sec. 3.2 scaling correction; 1 = none)")
+    ap.add_argument("--reset-new", action="store_true",
+                    help="reset gate reads c_t (Algorithm 1's order) instead of c_{t-1}")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="REPS",
                     help="only run a 1 GiB copy REPS times (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=5,
@@ -297,7 +301,8 @@ def main():
     layers = [{k: to(v) for k, v in p.items()} for p in inp["layers"]]
     X, dH, mask = to(inp["X"]), to(inp["dH"]), to(inp["mask"])
     st = sru.Stack(layers, w.L, w.B, w.d_in, w.d, w.direction, w.gemm_dtype, dev,
-                   backward=w.backward)
+                   backward=w.backward, highway_scale=args.highway_scale,
+                   reset_new=args.reset_new)
 
     def step():
         st.forward(X, mask)
@@ -392,6 +397,8 @@ def main():
                    "passes": "fwd+bwd" if w.backward else "fwd",
                    "gemm": "bf16 operands, fp32 accumulate" if w.gemm_dtype else "fp32",
                    "scan": "fp32", "tokens_per_step": w.tokens, "global_batch": w.B,
+                   "highway_scale": args.highway_scale,
+                   "reset_gate": "c_t (Algorithm 1)" if args.reset_new else "c_{t-1} (Eq. 3)",
                    "seq_len": w.L, "parallelism": "single GPU"},
         "roofline": roofline,
         "scan_hbm": scan_hbm,

@@ -77,6 +77,22 @@ typedef enum {
 typedef enum { SRU_DIR_FWD = 0, SRU_DIR_REV = 1, SRU_DIR_BI = 2 } sru_direction;
 typedef enum { SRU_GEMM_FP32 = 0, SRU_GEMM_BF16 = 1 } sru_gemm_dtype;
 
+/* Gate variants.  Every layer and scan call takes a `const sru_options*`;
+ * NULL means Eq. 1-4 as printed: highway_scale = 1 and the reset gate on
+ * c_{t-1} (Eq. 3).  The same options must be passed to the forward and the
+ * backward call of a layer.  Host memory, read during the call only.
+ *   highway_scale: alpha in h_t = r_t c_t + (1 - r_t) alpha x_hat, the
+ *     scaling correction of Sec. 3.2 (sqrt(3), or sqrt(1 + 2 e^b) for a
+ *     reset-gate bias b, Appendix A).  Must be finite.
+ *   reset_state: SRU_RESET_PREV, r_t = sigma(W_r x_t + v_r c_{t-1} + b_r)
+ *     (Eq. 3); SRU_RESET_NEW, r_t reads c_t: the order of Algorithm 1.
+ *     Anything else is SRU_E_FLAG. */
+typedef enum { SRU_RESET_PREV = 0, SRU_RESET_NEW = 1 } sru_reset_state;
+typedef struct {
+  float highway_scale;
+  int reset_state;
+} sru_options;
+
 /* Human-readable name of a status code (static string, never NULL). */
 SRU_API const char* sru_status_string(int status);
 
@@ -118,7 +134,7 @@ SRU_API size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int d
 SRU_API int sru_forward(const float* X, const float* W,
                 const float* v_f, const float* v_r, const float* b_f, const float* b_r,
                 const float* c0, int L, int B, int d_in, int d, int direction,
-                const uint8_t* pad_mask, int gemm_dtype,
+                const uint8_t* pad_mask, int gemm_dtype, const sru_options* options,
                 float* U, float* H, float* C, float* c_last,
                 const uint16_t* X_bf16, uint16_t* W_bf16, uint16_t* H_bf16,
                 void* workspace, size_t workspace_bytes, hipStream_t stream);
@@ -138,7 +154,7 @@ SRU_API int sru_forward(const float* X, const float* W,
 SRU_API int sru_backward(const float* X, const float* W,
                  const float* v_f, const float* v_r, const float* b_f, const float* b_r,
                  const float* c0, int L, int B, int d_in, int d, int direction,
-                 const uint8_t* pad_mask, int gemm_dtype,
+                 const uint8_t* pad_mask, int gemm_dtype, const sru_options* options,
                  const float* U, const float* C, const float* dH, const float* dc_last,
                  float* dX, float* dW, float* dv_f, float* dv_r, float* db_f, float* db_r,
                  float* dc0, const uint16_t* X_bf16, const uint16_t* W_bf16,
@@ -170,8 +186,8 @@ SRU_API int sru_gemm(int op, int gemm_dtype, int M, int N, int K,
 SRU_API int sru_scan_forward(const float* U, const float* X,
                      const float* v_f, const float* v_r, const float* b_f, const float* b_r,
                      const float* c0, int L, int B, int d_in, int d, int direction,
-                     const uint8_t* pad_mask, float* H, float* C, float* c_last,
-                     uint16_t* H_bf16, hipStream_t stream);
+                     const uint8_t* pad_mask, const sru_options* options, float* H, float* C,
+                     float* c_last, uint16_t* H_bf16, hipStream_t stream);
 
 /* The reverse-time gradient scan on a given U, C, dH.
  *   out: dU [L, B, ndir, k, d] (gradient w.r.t. the projections; when k = 4
@@ -184,7 +200,7 @@ SRU_API int sru_scan_backward(const float* U, const float* X, const float* C, co
                       const float* dc_last,
                       const float* v_f, const float* v_r, const float* b_f, const float* b_r,
                       const float* c0, int L, int B, int d_in, int d, int direction,
-                      const uint8_t* pad_mask,
+                      const uint8_t* pad_mask, const sru_options* options,
                       float* dU, float* dxh, float* dv_f, float* dv_r, float* db_f,
                       float* db_r, float* dc0,
                       void* workspace, size_t workspace_bytes, hipStream_t stream);

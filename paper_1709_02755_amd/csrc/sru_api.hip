@@ -3,6 +3,8 @@
 // frees or synchronises.
 #include <limits.h>
 
+#include <cmath>
+
 #include <initializer_list>
 #include <vector>
 
@@ -68,8 +70,23 @@ int make_dims(int L, int B, int d_in, int d, int direction, Dims& s) {
   return SRU_OK;
 }
 
-sru::ScanShape scan_shape(const Dims& s, int direction) {
-  return sru::ScanShape{s.L, s.B, s.d_in, s.d, s.ndir, s.k, direction};
+// The gate variants of an entry point (NULL = Eq. 1-4 as printed).
+struct Opts {
+  float alpha = 1.0f;
+  int reset_new = 0;
+};
+
+int read_options(const sru_options* o, Opts& op) {
+  if (!o) return SRU_OK;
+  if (!std::isfinite(o->highway_scale)) return SRU_E_FLAG;
+  if (o->reset_state != SRU_RESET_PREV && o->reset_state != SRU_RESET_NEW) return SRU_E_FLAG;
+  op.alpha = o->highway_scale;
+  op.reset_new = o->reset_state == SRU_RESET_NEW;
+  return SRU_OK;
+}
+
+sru::ScanShape scan_shape(const Dims& s, int direction, const Opts& op = Opts()) {
+  return sru::ScanShape{s.L, s.B, s.d_in, s.d, s.ndir, s.k, direction, op.alpha, op.reset_new};
 }
 
 int hip_status(hipError_t e) {
@@ -218,13 +235,16 @@ size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int direction
 
 int sru_forward(const float* X, const float* W, const float* v_f, const float* v_r,
                 const float* b_f, const float* b_r, const float* c0, int L, int B, int d_in,
-                int d, int direction, const uint8_t* pad_mask, int gemm_dtype, float* U,
+                int d, int direction, const uint8_t* pad_mask, int gemm_dtype,
+                const sru_options* options, float* U,
                 float* H, float* C, float* c_last, const uint16_t* X_bf16, uint16_t* W_bf16,
                 uint16_t* H_bf16, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   Dims s;
   int st = make_dims(L, B, d_in, d, direction, s);
   if (st != SRU_OK) return st;
   if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
+  Opts op;
+  if (int e = read_options(options, op)) return e;
   if (!X || !W || !v_f || !v_r || !b_f || !b_r || !U || !H) return SRU_E_NULLPTR;
   const void* ptrs[] = {X, W, v_f, v_r, b_f, b_r, c0, U, H, C, c_last};
   for (const void* p : ptrs)
@@ -262,12 +282,13 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
   if (int e = hip_status(sru::gemm_launch(g, stream))) return e;
 
   sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16};
-  return hip_status(sru::scan_forward_launch(scan_shape(s, direction), a, stream));
+  return hip_status(sru::scan_forward_launch(scan_shape(s, direction, op), a, stream));
 }
 
 int sru_backward(const float* X, const float* W, const float* v_f, const float* v_r,
                  const float* b_f, const float* b_r, const float* c0, int L, int B, int d_in,
-                 int d, int direction, const uint8_t* pad_mask, int gemm_dtype, const float* U,
+                 int d, int direction, const uint8_t* pad_mask, int gemm_dtype,
+                 const sru_options* options, const float* U,
                  const float* C, const float* dH, const float* dc_last, float* dX, float* dW,
                  float* dv_f, float* dv_r, float* db_f, float* db_r, float* dc0,
                  const uint16_t* X_bf16, const uint16_t* W_bf16, void* workspace,
@@ -276,6 +297,8 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   int st = make_dims(L, B, d_in, d, direction, s);
   if (st != SRU_OK) return st;
   if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
+  Opts op;
+  if (int e = read_options(options, op)) return e;
   if (!X || !W || !v_f || !v_r || !b_f || !b_r || !U || !C || !dH || !dX || !dW || !dv_f ||
       !dv_r || !db_f || !db_r)
     return SRU_E_NULLPTR;
@@ -307,7 +330,8 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   //    type of the products that read it
   sru::ScanBwdArgs a{U,   X,    C,   dH,      dc_last, v_f,  v_r,  b_f,  b_r,  c0,
                      pad_mask, dU, bf16, dxh, partial, dc0, dv_f, dv_r, db_f, db_r};
-  if (int e = hip_status(sru::scan_backward_launch(scan_shape(s, direction), a, stream))) return e;
+  if (int e = hip_status(sru::scan_backward_launch(scan_shape(s, direction, op), a, stream)))
+    return e;
 
   // 2. dX = dU Wcat (+ the highway gradient of every direction when k = 3).
   //    bf16 mode: Wcat in bf16 (W_bf16, or rounded into the workspace) read
@@ -383,11 +407,13 @@ int sru_gemm(int op, int gemm_dtype, int M, int N, int K, const float* A, int ld
 
 int sru_scan_forward(const float* U, const float* X, const float* v_f, const float* v_r,
                      const float* b_f, const float* b_r, const float* c0, int L, int B, int d_in,
-                     int d, int direction, const uint8_t* pad_mask, float* H, float* C,
-                     float* c_last, uint16_t* H_bf16, hipStream_t stream) {
+                     int d, int direction, const uint8_t* pad_mask, const sru_options* options,
+                     float* H, float* C, float* c_last, uint16_t* H_bf16, hipStream_t stream) {
   Dims s;
   int st = make_dims(L, B, d_in, d, direction, s);
   if (st != SRU_OK) return st;
+  Opts op;
+  if (int e = read_options(options, op)) return e;
   if (!U || !v_f || !v_r || !b_f || !b_r || !H) return SRU_E_NULLPTR;
   if (s.k == 3 && !X) return SRU_E_NULLPTR;
   const void* ptrs[] = {U, X, v_f, v_r, b_f, b_r, c0, H, C, c_last};
@@ -395,7 +421,7 @@ int sru_scan_forward(const float* U, const float* X, const float* v_f, const flo
     if (p && !aligned4(p)) return SRU_E_ALIGN;
   if ((reinterpret_cast<uintptr_t>(H_bf16) & 1) != 0) return SRU_E_ALIGN;
   sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16};
-  return hip_status(sru::scan_forward_launch(scan_shape(s, direction), a, stream));
+  return hip_status(sru::scan_forward_launch(scan_shape(s, direction, op), a, stream));
 }
 
 size_t sru_scan_backward_workspace_bytes(int L, int B, int d_in, int d, int direction) {
@@ -407,12 +433,15 @@ size_t sru_scan_backward_workspace_bytes(int L, int B, int d_in, int d, int dire
 int sru_scan_backward(const float* U, const float* X, const float* C, const float* dH,
                       const float* dc_last, const float* v_f, const float* v_r, const float* b_f,
                       const float* b_r, const float* c0, int L, int B, int d_in, int d,
-                      int direction, const uint8_t* pad_mask, float* dU, float* dxh,
-                      float* dv_f, float* dv_r, float* db_f, float* db_r, float* dc0,
-                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                      int direction, const uint8_t* pad_mask, const sru_options* options,
+                      float* dU, float* dxh, float* dv_f, float* dv_r, float* db_f,
+                      float* db_r, float* dc0, void* workspace, size_t workspace_bytes,
+                      hipStream_t stream) {
   Dims s;
   int st = make_dims(L, B, d_in, d, direction, s);
   if (st != SRU_OK) return st;
+  Opts op;
+  if (int e = read_options(options, op)) return e;
   if (!U || !C || !dH || !v_f || !v_r || !b_f || !b_r || !dU || !dv_f || !dv_r || !db_f || !db_r)
     return SRU_E_NULLPTR;
   if (s.k == 3 && (!X || !dxh)) return SRU_E_NULLPTR;
@@ -421,7 +450,7 @@ int sru_scan_backward(const float* U, const float* X, const float* C, const floa
                         db_f, db_r, dc0};
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
-  const sru::ScanShape sh = scan_shape(s, direction);
+  const sru::ScanShape sh = scan_shape(s, direction, op);
   const size_t need = align_up(sru::scan_backward_partial_bytes(sh));
   if (!workspace || workspace_bytes < need) return SRU_E_WORKSPACE;
   sru::ScanBwdArgs a{U,   X,   C,     dH,  dc_last,

@@ -53,6 +53,8 @@ hipError_t gemm_launch(const GemmDesc& g, hipStream_t stream);
 // ----------------------------------------------------------------- scans
 struct ScanShape {
   int L, B, d_in, d, ndir, k, direction;
+  float alpha;    // highway scale (Sec. 3.2); 1 = Eq. 4 as printed
+  int reset_new;  // reset gate reads c_t (Algorithm 1) instead of c_{t-1} (Eq. 3)
 };
 
 struct ScanFwdArgs {

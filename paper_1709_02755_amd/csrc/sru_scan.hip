@@ -2,7 +2,8 @@
 //
 // Forward: the fused kernel of Sec. 3.1 / Algorithm 1.  One lane per
 // (batch b, direction, hidden unit j), sequential over t, the state c held in
-// a register.  Eq. 1-4 with the reset gate on c_{t-1} (Eq. 3).
+// a register.  Eq. 1-4 with the reset gate on c_{t-1} (Eq. 3), or on c_t
+// (Algorithm 1's order, RN), and the highway term scaled by alpha (Sec. 3.2).
 // Backward: the chain rule of Eq. 1-4 in reverse step order; one lane per
 // (b, direction, j) again, the carried gradient dloss/dc in a register.
 //
@@ -46,7 +47,7 @@ __device__ __forceinline__ bool decode_lane(const ScanShape& s, Lane& ln) {
 }
 
 // ------------------------------------------------------------ forward scan
-template <int KB, bool MASK, bool STORE_C, bool STORE_HB, int PF>
+template <int KB, bool MASK, bool STORE_C, bool STORE_HB, bool RN, int PF>
 __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, ScanFwdArgs a) {
   Lane ln;
   if (!decode_lane(s, ln)) return;
@@ -65,6 +66,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
 
   const float vf = a.v_f[ln.fidx], vr = a.v_r[ln.fidx];
   const float bf = a.b_f[ln.fidx], br = a.b_r[ln.fidx];
+  const float alpha = s.alpha;
   float c = a.c0 ? a.c0[ln.gid] : 0.0f;
 
   float r0[PF], r1[PF], r2[PF], rx[PF];
@@ -85,9 +87,9 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
   auto step = [&](int st, float u0, float u1, float u2, float xh, uint8_t m) {
     const long long t = tindex(st);
     const float f = sigmoid_fast(fmaf(vf, c, u1 + bf));   // Eq. 1
-    const float r = sigmoid_fast(fmaf(vr, c, u2 + br));   // Eq. 3, previous c
     const float cn = fmaf(f, c, (1.0f - f) * u0);         // Eq. 2
-    float h = fmaf(r, cn, (1.0f - r) * xh);               // Eq. 4
+    const float r = sigmoid_fast(fmaf(vr, RN ? cn : c, u2 + br));  // Eq. 3
+    float h = fmaf(r, cn, (1.0f - r) * (alpha * xh));     // Eq. 4 (Sec. 3.2)
     if constexpr (MASK) {
       const bool pad = m != 0;
       c = pad ? c : cn;
@@ -134,7 +136,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
 //   v/b sums += (df c_p, dr c_p, df, dr);  g <- gc f + df v_f + dr v_r
 // A padded step writes zeros and leaves g unchanged.
 // DUB: store dU as bf16 (RNE), the operand type of bf16 matrix products.
-template <int KB, bool MASK, bool DUB, int PF>
+template <int KB, bool MASK, bool DUB, bool RN, int PF>
 __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, ScanBwdArgs a) {
   Lane ln;
   if (!decode_lane(s, ln)) return;
@@ -156,6 +158,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
 
   const float vf = a.v_f[ln.fidx], vr = a.v_r[ln.fidx];
   const float bf = a.b_f[ln.fidx], br = a.b_r[ln.fidx];
+  const float alpha = s.alpha;
   const float c0v = a.c0 ? a.c0[ln.gid] : 0.0f;
   float g = a.dc_last ? a.dc_last[ln.gid] : 0.0f;
   float sum_df_c = 0.f, sum_dr_c = 0.f, sum_df = 0.f, sum_dr = 0.f;
@@ -187,18 +190,21 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
     const int pos = L - 1 - i;
     const long long t = tpos(pos);
     const float c_p = pos > 0 ? cprev : c0v;
+    const float c_r = RN ? c_t : c_p;  // the state the reset gate reads
     const float f = sigmoid_fast(fmaf(vf, c_p, u1 + bf));
-    const float r = sigmoid_fast(fmaf(vr, c_p, u2 + br));
+    const float r = sigmoid_fast(fmaf(vr, c_r, u2 + br));
     bool pad = false;
     if constexpr (MASK) pad = m != 0;
     const float dhv = pad ? 0.0f : dh;
-    const float gc = fmaf(dhv, r, g);
     const float rr = r * (1.0f - r);
     const float ff = f * (1.0f - f);
-    float dr = dhv * (c_t - xh) * rr;
+    float dr = dhv * (c_t - alpha * xh) * rr;
+    // total gradient into c_t: from later steps, through h, and (RN)
+    // through the reset gate
+    const float gc = RN ? fmaf(dr, vr, fmaf(dhv, r, g)) : fmaf(dhv, r, g);
     float df = gc * (c_p - u0) * ff;
     float du0 = gc * (1.0f - f);
-    float dx = dhv * (1.0f - r);
+    float dx = dhv * (1.0f - r) * alpha;
     if constexpr (MASK) {
       dr = pad ? 0.0f : dr;
       df = pad ? 0.0f : df;
@@ -206,10 +212,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
       dx = pad ? 0.0f : dx;
     }
     sum_df_c = fmaf(df, c_p, sum_df_c);
-    sum_dr_c = fmaf(dr, c_p, sum_dr_c);
+    sum_dr_c = fmaf(dr, c_r, sum_dr_c);
     sum_df += df;
     sum_dr += dr;
-    const float gn = fmaf(dr, vr, fmaf(df, vf, gc * f));
+    const float gn = RN ? fmaf(df, vf, gc * f) : fmaf(dr, vr, fmaf(df, vf, gc * f));
     g = pad ? g : gn;
     DuT* du = dup + t * u_step;
     auto put = [](float v, DuT* p) {
@@ -294,8 +300,12 @@ hipError_t fwd_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st
   const int lanes = s.B * s.ndir * s.d;
   const int grid = (lanes + kScanThreads - 1) / kScanThreads;
   timing_before("scan_fwd", st);
-  hipLaunchKernelGGL((scan_fwd_kernel<KB, MASK, STORE_C, STORE_HB, kFwdPF>), dim3(grid),
-                     dim3(kScanThreads), 0, st, s, a);
+  if (s.reset_new)
+    hipLaunchKernelGGL((scan_fwd_kernel<KB, MASK, STORE_C, STORE_HB, true, kFwdPF>), dim3(grid),
+                       dim3(kScanThreads), 0, st, s, a);
+  else
+    hipLaunchKernelGGL((scan_fwd_kernel<KB, MASK, STORE_C, STORE_HB, false, kFwdPF>), dim3(grid),
+                       dim3(kScanThreads), 0, st, s, a);
   timing_after(st);
   return hipGetLastError();
 }
@@ -314,12 +324,18 @@ hipError_t bwd_dispatch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t st
   const int lanes = s.B * s.ndir * s.d;
   const int grid = (lanes + kScanThreads - 1) / kScanThreads;
   timing_before("scan_bwd", st);
-  if (a.du_bf16)
-    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, true, kBwdPF>), dim3(grid), dim3(kScanThreads),
-                       0, st, s, a);
+  if (a.du_bf16 && s.reset_new)
+    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, true, true, kBwdPF>), dim3(grid),
+                       dim3(kScanThreads), 0, st, s, a);
+  else if (a.du_bf16)
+    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, true, false, kBwdPF>), dim3(grid),
+                       dim3(kScanThreads), 0, st, s, a);
+  else if (s.reset_new)
+    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, false, true, kBwdPF>), dim3(grid),
+                       dim3(kScanThreads), 0, st, s, a);
   else
-    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, false, kBwdPF>), dim3(grid), dim3(kScanThreads),
-                       0, st, s, a);
+    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, false, false, kBwdPF>), dim3(grid),
+                       dim3(kScanThreads), 0, st, s, a);
   timing_after(st);
   return hipGetLastError();
 }

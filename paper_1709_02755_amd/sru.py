@@ -36,14 +36,15 @@ _SIGNATURES = {
     "sru_version": (_I, []),
     "sru_forward_workspace_bytes": (_S, [_I] * 6),
     "sru_backward_workspace_bytes": (_S, [_I] * 6),
-    "sru_forward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I] + [_P] * 4 + [_P] * 3 + [_P, _S, _P]),
-    "sru_backward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I] + [_P] * 4 + [_P] * 7 + [_P] * 2
+    "sru_forward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I, _P] + [_P] * 4 + [_P] * 3
+                    + [_P, _S, _P]),
+    "sru_backward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I, _P] + [_P] * 4 + [_P] * 7 + [_P] * 2
                      + [_P, _S, _P]),
     "sru_gemm_workspace_bytes": (_S, [_I] * 5),
     "sru_gemm": (_I, [_I] * 5 + [_P, _I, _P, _I, _P, _I] + [_P, _S, _P]),
-    "sru_scan_forward": (_I, [_P] * 7 + [_I] * 5 + [_P] + [_P] * 3 + [_P] + [_P]),
+    "sru_scan_forward": (_I, [_P] * 7 + [_I] * 5 + [_P, _P] + [_P] * 3 + [_P] + [_P]),
     "sru_scan_backward_workspace_bytes": (_S, [_I] * 5),
-    "sru_scan_backward": (_I, [_P] * 10 + [_I] * 5 + [_P] + [_P] * 7 + [_P, _S, _P]),
+    "sru_scan_backward": (_I, [_P] * 10 + [_I] * 5 + [_P, _P] + [_P] * 7 + [_P, _S, _P]),
     "sru_timing_begin": (_I, [_P, _I]),
     "sru_timing_end": (_I, []),
     "sru_timing_label": (ctypes.c_char_p, [_I]),
@@ -52,6 +53,28 @@ _SIGNATURES = {
 
 class SruError(RuntimeError):
     pass
+
+
+RESET_PREV, RESET_NEW = 0, 1
+
+
+class Options(ctypes.Structure):
+    """sru_options: highway_scale (alpha, Sec. 3.2) and reset_state
+    (RESET_PREV: Eq. 3; RESET_NEW: Algorithm 1's order)."""
+    _fields_ = [("highway_scale", ctypes.c_float), ("reset_state", ctypes.c_int)]
+
+
+def _options(highway_scale=1.0, reset_new=False):
+    """NULL for Eq. 1-4 as printed, else a pointer to an sru_options."""
+    if highway_scale == 1.0 and not reset_new:
+        return None
+    return ctypes.byref(Options(float(highway_scale), RESET_NEW if reset_new else RESET_PREV))
+
+
+def highway_scale_for_bias(b):
+    """alpha = sqrt(1 + 2 e^b) for a reset-gate bias b (Sec. 3.2, Appendix A)."""
+    import math
+    return math.sqrt(1.0 + 2.0 * math.exp(b))
 
 
 def lib():
@@ -139,7 +162,8 @@ def workspace(nbytes, device):
 
 
 def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
-            gemm_dtype=GEMM_FP32, store_c=True, out=None, ws=None, X_bf16=None):
+            gemm_dtype=GEMM_FP32, store_c=True, out=None, ws=None, X_bf16=None,
+            highway_scale=1.0, reset_new=False):
     """One layer forward; returns dict(U, H, C, c_last) (C None without store_c).
 
     bf16 GEMMs only: X_bf16 (torch.bfloat16, X rounded) replaces the
@@ -158,6 +182,7 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
         ws = workspace(need, dev)
     st = lib().sru_forward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                            L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
+                           _options(highway_scale, reset_new),
                            _ptr(out["U"]), _ptr(out["H"]), _ptr(out.get("C")),
                            _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("W_bf16")),
                            _ptr(out.get("H_bf16")), _ptr(ws), need if ws is not None else 0,
@@ -168,7 +193,7 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
 
 def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, direction=DIR_FWD,
              mask=None, gemm_dtype=GEMM_FP32, want_dc0=True, out=None, ws=None, X_bf16=None,
-             W_bf16=None):
+             W_bf16=None, highway_scale=1.0, reset_new=False):
     """One layer backward; returns dict(dX, dW, dv_f, dv_r, db_f, db_r, dc0).
 
     bf16 GEMMs only: X_bf16 / W_bf16 (bfloat16 roundings of X and Wcat, as
@@ -191,6 +216,7 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
         ws = workspace(need, dev)
     st = lib().sru_backward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                             L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
+                            _options(highway_scale, reset_new),
                             _ptr(U), _ptr(C), _ptr(dH), _ptr(dc_last),
                             _ptr(out["dX"]), _ptr(out["dW"]), _ptr(out["dv_f"]), _ptr(out["dv_r"]),
                             _ptr(out["db_f"]), _ptr(out["db_r"]), _ptr(out.get("dc0")),
@@ -217,7 +243,7 @@ def gemm(op, A, B, M, N, K, gemm_dtype=GEMM_FP32, C=None, ws=None):
 
 
 def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
-                 store_c=True, out=None):
+                 store_c=True, out=None, highway_scale=1.0, reset_new=False):
     L, B, ndir, k, d = U.shape
     d_in = X.shape[2] if X is not None else (d if k == 3 else -1)
     if k == 4 and X is None:
@@ -230,6 +256,7 @@ def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None
                    c_last=torch.empty((B, ndir * d), device=dev))
     st = lib().sru_scan_forward(_ptr(U), _ptr(X), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r),
                                 _ptr(c0), L, B, d_in, d, direction, _ptr(mask),
+                                _options(highway_scale, reset_new),
                                 _ptr(out["H"]), _ptr(out.get("C")), _ptr(out.get("c_last")),
                                 _ptr(out.get("H_bf16")), _stream())
     _check(st, "sru_scan_forward")
@@ -237,7 +264,7 @@ def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None
 
 
 def scan_backward(U, X, C, dH, v_f, v_r, b_f, b_r, c0=None, dc_last=None, direction=DIR_FWD,
-                  mask=None, d_in=None, out=None, ws=None):
+                  mask=None, d_in=None, out=None, ws=None, highway_scale=1.0, reset_new=False):
     L, B, ndir, k, d = U.shape
     if d_in is None:
         d_in = X.shape[2] if X is not None else d
@@ -254,6 +281,7 @@ def scan_backward(U, X, C, dH, v_f, v_r, b_f, b_r, c0=None, dc_last=None, direct
     st = lib().sru_scan_backward(_ptr(U), _ptr(X), _ptr(C), _ptr(dH), _ptr(dc_last),
                                  _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                                  L, B, d_in, d, direction, _ptr(mask),
+                                 _options(highway_scale, reset_new),
                                  _ptr(out["dU"]), _ptr(out.get("dxh")), _ptr(out["dv_f"]),
                                  _ptr(out["dv_r"]), _ptr(out["db_f"]), _ptr(out["db_r"]),
                                  _ptr(out.get("dc0")), _ptr(ws), ws.numel(), _stream())
@@ -271,8 +299,10 @@ class Stack:
     instead of rounding X and W again.
     """
 
-    def __init__(self, layers, L, B, d_in, d, direction, gemm_dtype, device, backward=True):
+    def __init__(self, layers, L, B, d_in, d, direction, gemm_dtype, device, backward=True,
+                 highway_scale=1.0, reset_new=False):
         self.layers = layers
+        self.variant = dict(highway_scale=highway_scale, reset_new=reset_new)
         self.L, self.B, self.d, self.direction, self.gemm_dtype = L, B, d, direction, gemm_dtype
         ndir = 2 if direction == DIR_BI else 1
         self.ndir = ndir
@@ -308,7 +338,7 @@ class Stack:
         x, xb = X, None
         for p, o in zip(self.layers, self.fw):
             forward(x, p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], None, self.direction, mask,
-                    self.gemm_dtype, out=o, ws=self.ws, X_bf16=xb)
+                    self.gemm_dtype, out=o, ws=self.ws, X_bf16=xb, **self.variant)
             x, xb = o["H"], o.get("H_bf16")
         return x
 
@@ -320,6 +350,6 @@ class Stack:
             xb = None if li == 0 else self.fw[li - 1].get("H_bf16")
             backward(x, p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], o["U"], o["C"], g,
                      None, None, self.direction, mask, self.gemm_dtype, want_dc0=False,
-                     out=b, ws=self.ws, X_bf16=xb, W_bf16=o.get("W_bf16"))
+                     out=b, ws=self.ws, X_bf16=xb, W_bf16=o.get("W_bf16"), **self.variant)
             g = b["dX"]
         return g

@@ -43,24 +43,25 @@ def test_version_and_status_strings():
 
 def _fwd(lib, **kw):
     a = dict(X=FAKE, W=FAKE, v_f=FAKE, v_r=FAKE, b_f=FAKE, b_r=FAKE, c0=None, L=4, B=2, d_in=8,
-             d=8, direction=0, mask=None, gemm=0, U=FAKE, H=FAKE, C=FAKE, c_last=None, Xb=None,
-             Wb=None, Hb=None, ws=None, ws_bytes=0)
+             d=8, direction=0, mask=None, gemm=0, opts=None, U=FAKE, H=FAKE, C=FAKE,
+             c_last=None, Xb=None, Wb=None, Hb=None, ws=None, ws_bytes=0)
     a.update(kw)
     return lib.sru_forward(a["X"], a["W"], a["v_f"], a["v_r"], a["b_f"], a["b_r"], a["c0"],
                            a["L"], a["B"], a["d_in"], a["d"], a["direction"], a["mask"],
-                           a["gemm"], a["U"], a["H"], a["C"], a["c_last"], a["Xb"], a["Wb"],
+                           a["gemm"], a["opts"], a["U"], a["H"], a["C"], a["c_last"], a["Xb"], a["Wb"],
                            a["Hb"], a["ws"], a["ws_bytes"], None)
 
 
 def _bwd(lib, **kw):
     a = dict(X=FAKE, W=FAKE, v_f=FAKE, v_r=FAKE, b_f=FAKE, b_r=FAKE, c0=None, L=4, B=2, d_in=8,
-             d=8, direction=0, mask=None, gemm=0, U=FAKE, C=FAKE, dH=FAKE, dc_last=None,
+             d=8, direction=0, mask=None, gemm=0, opts=None, U=FAKE, C=FAKE, dH=FAKE,
+             dc_last=None,
              dX=FAKE, dW=FAKE, dv_f=FAKE, dv_r=FAKE, db_f=FAKE, db_r=FAKE, dc0=None, Xb=None,
              Wb=None, ws=None, ws_bytes=0)
     a.update(kw)
     return lib.sru_backward(a["X"], a["W"], a["v_f"], a["v_r"], a["b_f"], a["b_r"], a["c0"],
                             a["L"], a["B"], a["d_in"], a["d"], a["direction"], a["mask"],
-                            a["gemm"], a["U"], a["C"], a["dH"], a["dc_last"], a["dX"], a["dW"],
+                            a["gemm"], a["opts"], a["U"], a["C"], a["dH"], a["dc_last"], a["dX"], a["dW"],
                             a["dv_f"], a["dv_r"], a["db_f"], a["db_r"], a["dc0"], a["Xb"],
                             a["Wb"], a["ws"], a["ws_bytes"], None)
 
@@ -151,15 +152,33 @@ def test_gemm_argument_checks():
 def test_scan_argument_checks():
     lib = sru.lib()
     f = lib.sru_scan_forward
-    assert f(FAKE, None, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 0, None, FAKE, None, None,
-             None, None) == E_NULL                         # k = 3 needs X
-    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 9, None, FAKE, None, None,
-             None, None) == E_FLAG
-    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 0, None, FAKE, None, None,
-             ctypes.c_void_p(0x10001), None) == E_ALIGN    # bf16 H: 2-byte aligned
+    assert f(FAKE, None, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 0, None, None, FAKE, None,
+             None, None, None) == E_NULL                   # k = 3 needs X
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 9, None, None, FAKE, None,
+             None, None, None) == E_FLAG
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 0, None, None, FAKE, None,
+             None, ctypes.c_void_p(0x10001), None) == E_ALIGN  # bf16 H: 2-byte aligned
     b = lib.sru_scan_backward
     args = [FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 16, 8, 0, None,
-            FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, None]
+            None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, None]
     assert b(*args) == E_SHAPE                             # k = 4 takes no dxh
-    args[17] = None
+    args[18] = None
     assert b(*args) == E_WS
+
+
+@pytest.mark.parametrize("alpha,reset", [(float("nan"), 0), (float("inf"), 0), (1.0, 2),
+                                         (1.0, -1)])
+def test_invalid_options_rejected(alpha, reset):
+    lib = sru.lib()
+    bad = ctypes.byref(sru.Options(alpha, reset))
+    assert _fwd(lib, opts=bad) == E_FLAG
+    assert _bwd(lib, opts=bad) == E_FLAG
+
+
+def test_valid_options_pass_validation():
+    # a valid options struct is read and the call proceeds to the next check
+    lib = sru.lib()
+    ok = ctypes.byref(sru.Options(3.0 ** 0.5, sru.RESET_NEW))
+    assert _fwd(lib, opts=ok, H=FAKE_MIS) == E_ALIGN
+    assert _bwd(lib, opts=ok) == E_WS
+    assert abs(sru.highway_scale_for_bias(0.0) - 3.0 ** 0.5) < 1e-15
