@@ -82,25 +82,30 @@ class HipEvents:
 # ------------------------------------------------------------------ work model
 def kernel_work(w, splits, bf16):
     """Algorithmic bytes / flops per launch of each kernel at workload w
-    (first layer shape; all layers of a unidirectional d_in = d stack match).
+    (first layer shape; all layers of the stacks benchmarked match, except
+    that the top layer writes no bf16 copy of H: averaged over layers).
     Bytes count each element read or written once: fp32 4 B, bf16 2 B."""
     M = w.L * w.B
     nfeat = w.ndir * w.d
-    k = 3
+    k = 3 if w.d_in == w.d else 4
     N = w.ndir * k * w.d
     K = w.d_in
     elems = M * nfeat
     du_b = 2.0 if bf16 else 4.0
+    hb = 2.0 * (w.layers - 1) / w.layers if bf16 else 0.0  # bf16 copy of H
     return {
         "gemm_u": dict(flops=2.0 * M * N * K),     # U = X W^T
         "gemm_dx": dict(flops=2.0 * M * K * N),    # dX = dU W
         "gemm_dw": dict(flops=2.0 * N * K * M),    # dW = dU^T X
-        # read U (3 blocks) and x, write h and c: 24 B per (t, b, j); with
-        # bf16 products also the bf16 copy of h (the next layer's operand)
-        "scan_fwd": dict(bytes=elems * (4.0 * (k + 1 + 2) + (2.0 if bf16 else 0.0))),
-        # read U (3 blocks), x, c, dh (24 B); write dU (3 blocks, bf16 when
-        # the products are bf16) and dx_hat (4 B): 34 B (bf16) / 40 B (fp32)
-        "scan_bwd": dict(bytes=elems * (4.0 * (k + 3) + du_b * k + 4.0)),
+        # read U's three blocks and x_hat (x, or U block 3), write h and c
+        # (24 B per (t, b, j); 20 B without c); with bf16 products below the
+        # top layer also the bf16 copy of h (the next layer's operand)
+        "scan_fwd": dict(bytes=elems * (16.0 + 4.0 + (4.0 if w.store_c or w.backward else 0.0)
+                                        + hb)),
+        # read U's blocks, x_hat, c, dh (24 B); write dU (k blocks, bf16 when
+        # the products are bf16) and, for k = 3, dx_hat (4 B): 34 B (bf16) /
+        # 40 B (fp32) at k = 3
+        "scan_bwd": dict(bytes=elems * (24.0 + du_b * k + (4.0 if k == 3 else 0.0))),
         "reduce_vb": dict(bytes=4.0 * (4 * w.B * nfeat + 4 * nfeat)),
         "splitk_reduce": dict(bytes=4.0 * (splits + 1) * N * K),
         # fp32 -> bf16 copies of the product operands: Wcat, X (first layer),
@@ -152,7 +157,8 @@ def pmc_traffic(label):
 # ------------------------------------------------------------------ CPU oracle
 def cpu_baseline(w, inp, nseq):
     """The fp64 oracle (test infrastructure, never the product path) on the
-    first `nseq` sequences of the same inputs: full stack forward + backward."""
+    first `nseq` sequences of the same inputs: the full stack, forward and
+    (when the workload has one) backward."""
     from oracle import sru_oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -164,13 +170,15 @@ def cpu_baseline(w, inp, nseq):
     X = inp["X"][:, sl]
     mask = None if inp["mask"] is None else inp["mask"][:, sl]
     t0 = time.perf_counter()
-    O.stack_forward_backward(X, inp["layers"], w.direction, mask, w.gemm_dtype,
-                             inp["dH"][:, sl], need_backward=True)
+    dH = None if inp["dH"] is None else inp["dH"][:, sl]
+    O.stack_forward_backward(X, inp["layers"], w.direction, mask, w.gemm_dtype, dH,
+                             need_backward=w.backward)
     secs = time.perf_counter() - t0
     tokens = w.L * nseq
+    passes = "fwd+bwd" if w.backward else "fwd"
     return {"value": tokens / secs, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "seconds": secs,
-            "sample": f"{w.layers}-layer fwd+bwd stack on {nseq} of {w.B} sequences "
+            "sample": f"{w.layers}-layer {passes} stack on {nseq} of {w.B} sequences "
                       f"({tokens} tokens), fp64 NumPy, per-step projections"}
 
 
@@ -302,11 +310,12 @@ def main():
     X, dH, mask = to(inp["X"]), to(inp["dH"]), to(inp["mask"])
     st = sru.Stack(layers, w.L, w.B, w.d_in, w.d, w.direction, w.gemm_dtype, dev,
                    backward=w.backward, highway_scale=args.highway_scale,
-                   reset_new=args.reset_new)
+                   reset_new=args.reset_new, store_c=w.store_c)
 
     def step():
         st.forward(X, mask)
-        st.backward(X, dH, mask)
+        if w.backward:
+            st.backward(X, dH, mask)
 
     for _ in range(args.warmup):
         step()
@@ -379,7 +388,9 @@ def main():
             f"({cpu['cores']} threads)")
 
     out = {
-        "metric": "SRU fwd+bwd tokens/s at L256 B64 d1024; scan-kernel HBM GB/s % of peak",
+        "metric": ("SRU fwd+bwd tokens/s at L256 B64 d1024; scan-kernel HBM GB/s % of peak"
+                   if args.workload == 3 else
+                   f"SRU {'fwd+bwd' if w.backward else 'fwd'} tokens/s at {w.name}"),
         "value": tokens_per_s,
         "unit": "tokens/s",
         "n_gpus": 1,

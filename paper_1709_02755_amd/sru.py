@@ -295,12 +295,13 @@ class Stack:
 
     `layers` holds per-layer dicts of GPU tensors W, v_f, v_r, b_f, b_r.
     With bf16 GEMMs each layer's forward also writes bf16 copies of Wcat and
-    H: the next layer's projection and every backward product read those
-    instead of rounding X and W again.
+    (below the top layer) H: the next layer's projection and every backward
+    product read those instead of rounding X and W again.  Without a
+    backward pass, store_c=False skips the states C (inference).
     """
 
     def __init__(self, layers, L, B, d_in, d, direction, gemm_dtype, device, backward=True,
-                 highway_scale=1.0, reset_new=False):
+                 highway_scale=1.0, reset_new=False, store_c=True):
         self.layers = layers
         self.variant = dict(highway_scale=highway_scale, reset_new=reset_new)
         self.L, self.B, self.d, self.direction, self.gemm_dtype = L, B, d, direction, gemm_dtype
@@ -312,15 +313,17 @@ class Stack:
         for li, p in enumerate(layers):
             din = d_in if li == 0 else ndir * d
             k = p["W"].shape[1]
+            keep_c = store_c or backward  # the backward reads C
             self.fw.append(dict(U=torch.empty((L, B, ndir, k, d), device=device),
                                 H=torch.empty((L, B, ndir * d), device=device),
-                                C=torch.empty((L, B, ndir * d), device=device),
+                                C=torch.empty((L, B, ndir * d), device=device) if keep_c else None,
                                 c_last=torch.empty((B, ndir * d), device=device)))
             if gemm_dtype == GEMM_BF16:
                 self.fw[-1]["W_bf16"] = torch.empty(tuple(p["W"].shape), dtype=torch.bfloat16,
                                                     device=device)
-                self.fw[-1]["H_bf16"] = torch.empty((L, B, ndir * d), dtype=torch.bfloat16,
-                                                    device=device)
+                if li + 1 < len(layers):  # the next layer's operand; none after the last
+                    self.fw[-1]["H_bf16"] = torch.empty((L, B, ndir * d), dtype=torch.bfloat16,
+                                                        device=device)
             if backward:
                 self.bw.append(dict(dX=torch.empty((L, B, din), device=device),
                                     dW=torch.empty_like(p["W"]),

@@ -45,6 +45,7 @@ class Workload:
     len_lo: int | None      # None: all sequences full length
     bf_uniform: bool        # b_f ~ U(-1, 1) (else 0)
     seed: int
+    store_c: bool = True    # keep every state C (False: inference, no backward)
 
     @property
     def ndir(self) -> int:
@@ -61,7 +62,9 @@ class Workload:
 
 
 # The five workloads of the build target (sizes and distributions as stated
-# there); seeds are the workload index.
+# there), then the inference shape of the SRU that replaces a Transformer's
+# feed-forward layer (Sec. 4.3: d_model = 512 in, d_sru = 2048, batches of
+# about 5120 tokens; forward only, no C); seeds are the workload index.
 WORKLOADS = [
     Workload("sru1_L32_B4_d128_fp32_fwd", 1, DIR_FWD, 32, 4, 128, 128,
              GEMM_FP32, False, None, False, 0),
@@ -73,6 +76,8 @@ WORKLOADS = [
              GEMM_BF16, True, None, True, 3),
     Workload("sru4_L128_B128_d2048_bf16_masked", 4, DIR_FWD, 128, 128, 2048, 2048,
              GEMM_BF16, True, 64, True, 4),
+    Workload("ffn_L64_B80_din512_d2048_bf16_infer", 1, DIR_FWD, 64, 80, 512, 2048,
+             GEMM_BF16, False, None, True, 5, store_c=False),
 ]
 
 
@@ -84,7 +89,7 @@ def scaled(w: Workload, *, L=None, B=None, d=None, layers=None, name=None) -> Wo
     len_lo = None if w.len_lo is None else max(1, (w.len_lo * L) // w.L)
     return Workload(name or f"{w.name}@L{L}_B{B or w.B}_d{d}", layers or w.layers,
                     w.direction, L, B or w.B, d_in, d, w.gemm_dtype, w.backward,
-                    len_lo, w.bf_uniform, w.seed)
+                    len_lo, w.bf_uniform, w.seed, w.store_c)
 
 
 def lengths_to_mask(lengths: np.ndarray, L: int) -> np.ndarray:

@@ -117,3 +117,44 @@ def test_chunked_state_carry_on_gpu():
     torch.cuda.synchronize()
     assert torch.equal(torch.cat([a["H"], b["H"]]), full["H"])
     assert torch.equal(b["c_last"], full["c_last"])
+
+
+@pytest.mark.parametrize("direction,gemm", [(O.DIR_FWD, O.GEMM_FP32), (O.DIR_FWD, O.GEMM_BF16),
+                                            (O.DIR_REV, O.GEMM_BF16)])
+def test_chunked_backward_carry_on_gpu(direction, gemm):
+    """Truncation-free back-propagation in chunks: forward over the chunks
+    with c_last -> c0, backward over them in reverse processing order with
+    dc0 -> dc_last.  H, dX and dc0 equal the one-call layer bit for bit (the
+    same operations per step and per output row); parameter gradients are
+    the chunks' sum, equal to the one-call ones within the tolerance (a
+    different summation order)."""
+    L, B, d, h = 40, 6, 128, 24
+    print(f"chunked backward dir={direction} gemm={gemm}", flush=True)
+    c = random_layer_case(np.random.default_rng(21 + direction), L, B, d, d, direction,
+                          c0=True, dc_last=True, bias_scale=0.5)
+    X, W = dev(c["X"]), dev(c["W"])
+    p = [dev(c[k]) for k in ("v_f", "v_r", "b_f", "b_r")]
+    c0, dcl, dH = dev(c["c0"]), dev(c["dc_last"]), dev(c["dH"])
+    kw = dict(direction=direction, gemm_dtype=gemm)
+    full = sru.forward(X, W, *p, c0=c0, **kw)
+    fb = sru.backward(X, W, *p, full["U"], full["C"], dH, c0=c0, dc_last=dcl, **kw)
+    first, second = (slice(0, h), slice(h, L)) if direction == O.DIR_FWD else (slice(h, L),
+                                                                               slice(0, h))
+    part = lambda t, s: t[s].contiguous()
+    fa = sru.forward(part(X, first), W, *p, c0=c0, **kw)
+    fs = sru.forward(part(X, second), W, *p, c0=fa["c_last"], **kw)
+    gs = sru.backward(part(X, second), W, *p, fs["U"], fs["C"], part(dH, second), c0=fa["c_last"],
+                      dc_last=dcl, **kw)
+    ga = sru.backward(part(X, first), W, *p, fa["U"], fa["C"], part(dH, first), c0=c0,
+                      dc_last=gs["dc0"], **kw)
+    torch.cuda.synchronize()
+    H = torch.empty_like(full["H"])
+    H[first], H[second] = fa["H"], fs["H"]
+    dX = torch.empty_like(fb["dX"])
+    dX[first], dX[second] = ga["dX"], gs["dX"]
+    assert torch.equal(H, full["H"])
+    assert torch.equal(dX, fb["dX"])
+    assert torch.equal(ga["dc0"], fb["dc0"])
+    tol = TOL_FP32 if gemm == O.GEMM_FP32 else 1e-5
+    for k in ("dW", "dv_f", "dv_r", "db_f", "db_r"):
+        check(k, ga[k] + gs[k], host(fb[k]), tol)

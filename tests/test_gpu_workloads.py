@@ -117,3 +117,25 @@ def test_workload_full_size_stack_on_batch_slice(wi):
     inp = make_inputs(w)
     st = run_stack(w, inp)
     compare_stack(w, inp, st, bsel=[0, w.B - 1])
+
+
+def test_inference_workload_full_size():
+    """The Transformer-FFN inference shape (d_in 512 -> d 2048, k = 4,
+    forward only, no C) at its full size in the benchmark's launch
+    configuration; the oracle on a slice of the batch (sequences never
+    interact)."""
+    w = WORKLOADS[5]
+    print(f"workload {w.name}", flush=True)
+    assert not w.backward and not w.store_c and w.d_in != w.d
+    inp = make_inputs(w)
+    layers = [layer_to_dev(p) for p in inp["layers"]]
+    st = sru.Stack(layers, w.L, w.B, w.d_in, w.d, w.direction, w.gemm_dtype, "cuda",
+                   backward=False, store_c=False)
+    H = st.forward(dev(inp["X"]), None)
+    torch.cuda.synchronize()
+    assert st.fw[0]["C"] is None and "H_bf16" not in st.fw[0]
+    bsel = slice(0, 8)
+    ref = O.stack_forward_backward(inp["X"][:, bsel], inp["layers"], w.direction, None,
+                                   w.gemm_dtype, None, need_backward=False)
+    check("H", host(H)[:, bsel], ref["Hs"][0], _tol(w))
+    check("c_last", host(st.fw[0]["c_last"])[bsel], ref["Cs"][0][-1], _tol(w))

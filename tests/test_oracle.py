@@ -380,6 +380,33 @@ def test_chunked_state_carry(rng):
     np.testing.assert_allclose(np.concatenate([a64["H"], b64["H"]]), full["H"], rtol=0, atol=0)
 
 
+@pytest.mark.parametrize("direction", [F, R])
+def test_chunked_backward_carry(rng, direction):
+    """Back-propagation through time in chunks: the later chunk's backward
+    (with the full dc_last) hands its dc0 to the earlier chunk's backward as
+    dc_last.  Per-step gradients and dc0 equal the one-call backward exactly;
+    the parameter gradients are the sum over the chunks.  For the reverse
+    direction the later chunk (in its processing order) is the earlier time
+    range."""
+    L, h = 10, 4
+    c = _case(rng, L, 3, 5, 4, direction, c0=True, dc_last=True, bias_scale=0.5, masked=True)
+    args = (c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"])
+    full = O.backward(c["X"], *args, c["dH"], c["c0"], direction, c["mask"], O.GEMM_FP32,
+                      c["dc_last"])
+    first, second = (slice(0, h), slice(h, L)) if direction == F else (slice(h, L), slice(0, h))
+    fa = O.forward(c["X"][first], *args, c["c0"], direction, c["mask"][first])
+    gb = O.backward(c["X"][second], *args, c["dH"][second], fa["c_last"], direction,
+                    c["mask"][second], O.GEMM_FP32, c["dc_last"])
+    ga = O.backward(c["X"][first], *args, c["dH"][first], c["c0"], direction, c["mask"][first],
+                    O.GEMM_FP32, gb["dc0"])
+    dX = np.zeros_like(full["dX"])
+    dX[first], dX[second] = ga["dX"], gb["dX"]
+    np.testing.assert_allclose(dX, full["dX"], rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(ga["dc0"], full["dc0"], rtol=1e-12, atol=1e-13)
+    for k in ("dW", "dv_f", "dv_r", "db_f", "db_r"):
+        np.testing.assert_allclose(ga[k] + gb[k], full[k], rtol=1e-12, atol=1e-13)
+
+
 # ---------------------------------------------------------------- pin 11
 def test_permutation_equivariance(rng):
     """Permuting the batch permutes every output; permuting hidden units
