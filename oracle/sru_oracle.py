@@ -333,3 +333,99 @@ def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
         grads.reverse()
     return dict(Hs=[fw["H"] for fw in fws], Cs=[fw["C"] for fw in fws],
                 Us=[fw["U"] for fw in fws], grads=grads, xs=xs)
+
+
+# ------------------------------------------------------ low-rank projection
+# The projection (bottleneck) trick of Sec. 4.4: the stacked weights are a
+# product of two smaller matrices, so the batched product runs as two.  The
+# text writes the product as P^T Q with Q of shape [d_in, d'] and P of shape
+# [3 d_out, d']; those shapes only compose as P Q^T, which is the reading
+# taken here:  Wcat [ndir*k*d, d_in] = P Q^T,  U = (X Q) P^T.
+# In bf16 mode the operands of each of the two products are rounded:
+# X and Q for T = X Q; T and P for U = T P^T (and likewise backward).
+
+def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
+                    pad_mask=None, gemm_dtype=GEMM_FP32, alpha=1.0, reset_new=False):
+    """Layer with Wcat = P Q^T.  Q [d_in, dp], P [ndir, k, d, dp].
+    Returns dict(T, U, H, C, c_last) with T = X Q [L, B, dp]."""
+    X = _f64(X)
+    Q = _f64(Q)
+    P = _f64(P)
+    L, B, d_in = X.shape
+    ndir, k, d, dp = P.shape
+    bf16 = gemm_dtype == GEMM_BF16
+    rnd = bf16_round if bf16 else (lambda a: a)
+    T = rnd(X) @ rnd(Q)                                   # [L, B, dp]
+    U = (rnd(T) @ rnd(P).reshape(ndir * k * d, dp).T).reshape(L, B, ndir, k, d)
+    # the scan of Eq. 1-4 on this U: the dense oracle with W chosen so that
+    # its per-step projections are exactly U is not available, so the step
+    # loop is run here on U directly
+    out = _scan_on_u(X, U, v_f, v_r, b_f, b_r, c0, direction, pad_mask, alpha, reset_new)
+    out["T"] = T
+    out["U"] = U
+    return out
+
+
+def _scan_on_u(X, U, v_f, v_r, b_f, b_r, c0, direction, pad_mask, alpha, reset_new):
+    """Eq. 1-4 per step given the projections U [L, B, ndir, k, d]."""
+    L, B, ndir, k, d = U.shape
+    v_f, v_r, b_f, b_r = (_f64(a).reshape(ndir, d) for a in (v_f, v_r, b_f, b_r))
+    c0 = np.zeros((B, ndir, d)) if c0 is None else _f64(c0).reshape(B, ndir, d)
+    pad = np.zeros((L, B), bool) if pad_mask is None else (np.asarray(pad_mask) != 0)
+    H = np.zeros((L, B, ndir, d))
+    C = np.zeros((L, B, ndir, d))
+    c_last = np.zeros((B, ndir, d))
+    for dirn in range(ndir):
+        steps = range(L - 1, -1, -1) if _is_reverse(direction, dirn) else range(L)
+        c = c0[:, dirn].copy()
+        for t in steps:
+            u = U[t, :, dirn]
+            x_hat = X[t] if k == 3 else u[:, 3]
+            f = sigmoid(u[:, 1] + v_f[dirn] * c + b_f[dirn])
+            c_new = f * c + (1.0 - f) * u[:, 0]
+            s = c_new if reset_new else c
+            r = sigmoid(u[:, 2] + v_r[dirn] * s + b_r[dirn])
+            h = r * c_new + (1.0 - r) * x_hat * alpha
+            valid = ~pad[t][:, None]
+            c = np.where(valid, c_new, c)
+            H[t, :, dirn] = np.where(valid, h, 0.0)
+            C[t, :, dirn] = c
+        c_last[:, dirn] = c
+    return dict(H=H.reshape(L, B, ndir * d), C=C.reshape(L, B, ndir * d),
+                c_last=c_last.reshape(B, ndir * d))
+
+
+def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
+                     pad_mask=None, gemm_dtype=GEMM_FP32, dc_last=None, fw=None, alpha=1.0,
+                     reset_new=False):
+    """Gradients of the low-rank layer: dict(dX, dQ, dP, dv_f, dv_r, db_f,
+    db_r, dc0, dU, dT).  The scan part is the dense backward's (the recurrence
+    only sees U); then dT = dU P, dX = dT Q^T (+ the highway gradient when
+    k = 3), dP = dU^T T, dQ = X^T dT, each product on rounded operands in
+    bf16 mode."""
+    X = _f64(X)
+    Q = _f64(Q)
+    P = _f64(P)
+    L, B, d_in = X.shape
+    ndir, k, d, dp = P.shape
+    bf16 = gemm_dtype == GEMM_BF16
+    rnd = bf16_round if bf16 else (lambda a: a)
+    if fw is None:
+        fw = forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0, direction, pad_mask, gemm_dtype,
+                             alpha, reset_new)
+    # The recurrence gradients: run the dense backward with a weight whose
+    # products are never used (W = 0) on the forward states of this layer.
+    Wz = np.zeros((ndir, k, d, d_in))
+    bw = backward(X, Wz, v_f, v_r, b_f, b_r, dH, c0, direction, pad_mask, GEMM_FP32, dc_last,
+                  fw=dict(U=fw["U"], C=fw["C"]), alpha=alpha, reset_new=reset_new)
+    dU = bw["dU"].reshape(L, B, ndir * k * d)
+    Pm = P.reshape(ndir * k * d, dp)
+    dT = rnd(dU) @ rnd(Pm)                                  # [L, B, dp]
+    dX = rnd(dT) @ rnd(Q).T
+    if k == 3:
+        dX = dX + bw["dxh"].sum(axis=2)
+    dUm = rnd(dU).reshape(L * B, -1)
+    dP = (dUm.T @ rnd(fw["T"]).reshape(L * B, dp)).reshape(ndir, k, d, dp)
+    dQ = rnd(X).reshape(L * B, d_in).T @ rnd(dT).reshape(L * B, dp)
+    return dict(dX=dX, dQ=dQ, dP=dP, dv_f=bw["dv_f"], dv_r=bw["dv_r"], db_f=bw["db_f"],
+                db_r=bw["db_r"], dc0=bw["dc0"], dU=bw["dU"], dT=dT, dxh=bw["dxh"])

@@ -626,3 +626,86 @@ def test_alg1_scalar_loop_matches_variants(rng, alpha, reset_new):
     b = O.forward_alg1_scalar(*args, alpha=alpha, reset_new=reset_new)
     for k in ("H", "C"):
         np.testing.assert_allclose(a[k], b[k], rtol=1e-12, atol=1e-13)
+
+
+# ------------------------------------------------------ low-rank projection
+def _lowrank_case(rng, L, B, d_in, d, dp, direction, masked=True):
+    c = _case(rng, L, B, d_in, d, direction, c0=True, dc_last=True, bias_scale=0.5,
+              masked=masked)
+    ndir, k = c["W"].shape[:2]
+    c["Q"] = (rng.standard_normal((d_in, dp)) / np.sqrt(d_in)).astype(np.float32)
+    c["P"] = (rng.standard_normal((ndir, k, d, dp)) / np.sqrt(dp)).astype(np.float32)
+    return c
+
+
+@pytest.mark.parametrize("direction,k4", [(F, False), (BI, True), (R, True)])
+def test_lowrank_equals_dense_with_product_weight(rng, direction, k4):
+    """Sec. 4.4: the factorised layer is the dense layer with Wcat = P Q^T
+    (forward states exactly, up to the association of the matrix products)."""
+    d = 5
+    c = _lowrank_case(rng, 7, 3, 8 if k4 else d, d, 3, direction)
+    ndir, k = c["W"].shape[:2]
+    P64, Q64 = c["P"].astype(np.float64), c["Q"].astype(np.float64)
+    W = (P64.reshape(-1, Q64.shape[1]) @ Q64.T).reshape(ndir, k, d, -1)
+    args = (c["v_f"], c["v_r"], c["b_f"], c["b_r"], c["c0"], direction, c["mask"])
+    lr = O.forward_lowrank(c["X"], c["Q"], c["P"], *args, alpha=1.3, reset_new=True)
+    dn = O.forward(c["X"], W, *args, alpha=1.3, reset_new=True)
+    for key in ("U", "H", "C", "c_last"):
+        np.testing.assert_allclose(lr[key], dn[key], rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("direction,k4", [(F, False), (BI, True)])
+def test_lowrank_gradients_chain_rule_of_dense(rng, direction, k4):
+    """With W = P Q^T the dense gradient dW (pinned by finite differences
+    above) gives dP = dW Q and dQ = dW^T P, summed over the stacked blocks;
+    dX and the recurrence gradients equal the dense ones."""
+    d = 4
+    c = _lowrank_case(rng, 6, 3, 7 if k4 else d, d, 3, direction)
+    ndir, k = c["W"].shape[:2]
+    P64, Q64 = c["P"].astype(np.float64), c["Q"].astype(np.float64)
+    Pm = P64.reshape(-1, Q64.shape[1])
+    W = (Pm @ Q64.T).reshape(ndir, k, d, -1)
+    args = (c["v_f"], c["v_r"], c["b_f"], c["b_r"])
+    lr = O.backward_lowrank(c["X"], c["Q"], c["P"], *args, c["dH"], c["c0"], direction,
+                            c["mask"], O.GEMM_FP32, c["dc_last"])
+    dn = O.backward(c["X"], W, *args, c["dH"], c["c0"], direction, c["mask"], O.GEMM_FP32,
+                    c["dc_last"])
+    dWm = dn["dW"].reshape(-1, Q64.shape[0])
+    np.testing.assert_allclose(lr["dP"].reshape(-1, Q64.shape[1]), dWm @ Q64, rtol=1e-10,
+                               atol=1e-12)
+    np.testing.assert_allclose(lr["dQ"], dWm.T @ Pm, rtol=1e-10, atol=1e-12)
+    for key in ("dX", "dv_f", "dv_r", "db_f", "db_r", "dc0"):
+        np.testing.assert_allclose(lr[key], dn[key], rtol=1e-10, atol=1e-12)
+
+
+def test_lowrank_gradients_match_finite_differences(rng):
+    """The factorised layer's backward against central differences in fp64
+    for X, Q, P, v, b and c0 (k = 4, bidirectional, a padded sequence)."""
+    c = _lowrank_case(rng, 4, 2, 5, 3, 2, BI)
+    base = {k: np.asarray(c[k], np.float64) for k in
+            ("X", "Q", "P", "v_f", "v_r", "b_f", "b_r", "c0")}
+    dH, dcl, mask = c["dH"].astype(np.float64), c["dc_last"].astype(np.float64), c["mask"]
+
+    def loss(p):
+        fw = O.forward_lowrank(p["X"], p["Q"], p["P"], p["v_f"], p["v_r"], p["b_f"], p["b_r"],
+                               p["c0"], BI, mask)
+        return _loss(fw, dH, dcl)
+
+    bw = O.backward_lowrank(base["X"], base["Q"], base["P"], base["v_f"], base["v_r"],
+                            base["b_f"], base["b_r"], dH, base["c0"], BI, mask, O.GEMM_FP32, dcl)
+    names = dict(X="dX", Q="dQ", P="dP", v_f="dv_f", v_r="dv_r", b_f="db_f", b_r="db_r",
+                 c0="dc0")
+    h = 1e-6
+    for pname, gname in names.items():
+        p0 = base[pname]
+        num = np.zeros(p0.size)
+        for i in range(p0.size):
+            pp = dict(base)
+            a = p0.copy().ravel(); a[i] += h; pp[pname] = a.reshape(p0.shape)
+            lp = loss(pp)
+            a = p0.copy().ravel(); a[i] -= h; pp[pname] = a.reshape(p0.shape)
+            lm = loss(pp)
+            num[i] = (lp - lm) / (2 * h)
+        ana = np.asarray(bw[gname]).ravel()
+        scale = max(np.max(np.abs(num)), 1e-3)
+        assert np.max(np.abs(ana - num)) / scale < 1e-6, (pname, ana, num)
