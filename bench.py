@@ -92,7 +92,25 @@ def kernel_work(w, splits, bf16):
     K = w.d_in
     elems = M * nfeat
     du_b = 2.0 if bf16 else 4.0
-    hb = 2.0 * (w.layers - 1) / w.layers if bf16 else 0.0  # bf16 copy of H
+    hb = 2.0 * (w.layers - 1) / w.layers if bf16 and w.dp is None else 0.0  # bf16 copy of H
+    if w.dp is not None:  # low-rank layers: Wcat = P Q^T, rank dp
+        dp = w.dp
+        low = {
+            "gemm_t": dict(flops=2.0 * M * dp * K),    # T = X Q
+            "gemm_u": dict(flops=2.0 * M * N * dp),    # U = T P^T
+            "gemm_dt": dict(flops=2.0 * M * dp * N),   # dT = dU P
+            "gemm_dx": dict(flops=2.0 * M * K * dp),   # dX = dT Q^T
+            "gemm_dp": dict(flops=2.0 * N * dp * M),   # dP = dU^T T
+            "gemm_dq": dict(flops=2.0 * K * dp * M),   # dQ = X^T dT
+            "bf16_x": dict(bytes=(4.0 + 2.0) * M * K),
+            "bf16_q": dict(bytes=(4.0 + 2.0) * K * dp),
+            "bf16_p": dict(bytes=(4.0 + 2.0) * N * dp),
+            "bf16_t": dict(bytes=(4.0 + 2.0) * M * dp),
+            "bf16_dt": dict(bytes=(4.0 + 2.0) * M * dp),
+            "splitk_reduce": dict(),  # two reductions of different sizes: time only
+        }
+    else:
+        low = {}
     return {
         "gemm_u": dict(flops=2.0 * M * N * K),     # U = X W^T
         "gemm_dx": dict(flops=2.0 * M * K * N),    # dX = dU W
@@ -113,6 +131,7 @@ def kernel_work(w, splits, bf16):
         "bf16_w": dict(bytes=(4.0 + 2.0) * N * K),
         "bf16_x": dict(bytes=(4.0 + 2.0) * M * K),
         "bf16_wt": dict(bytes=(4.0 + 2.0) * N * K),
+        **low,
     }
 
 
@@ -350,7 +369,7 @@ def main():
         a[0] += ms
         a[1] += 1
     ev.close()
-    splits = dw_splits(lib, w) if w.backward else 1
+    splits = dw_splits(lib, w) if w.backward and w.dp is None else 1
     work = kernel_work(w, splits, w.gemm_dtype == sru.GEMM_BF16)
     gemm_peak = MFMA_PEAK_TFLOPS["bf16" if w.gemm_dtype == sru.GEMM_BF16 else "fp32"]
     kernels = {}

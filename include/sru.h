@@ -160,6 +160,40 @@ SRU_API int sru_backward(const float* X, const float* W,
                  float* dc0, const uint16_t* X_bf16, const uint16_t* W_bf16,
                  void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Low-rank projection: the bottleneck trick of Sec. 4.4, the stacked weights
+ * re-parameterised as a product of two smaller matrices:
+ *     Wcat [ndir*k*d, d_in] = P Q^T,  Q [d_in, dp],  P [ndir, k, d, dp].
+ * (The text prints P^T Q, which does not compose with the shapes it states;
+ * P Q^T is the reading taken.)  The layer is otherwise the one of
+ * sru_forward / sru_backward, with the same conventions and options.
+ *   forward : T = X Q [L, B, dp] -- an output, kept by the caller for the
+ *             backward -- then U = T P^T and the scan.
+ *   backward: the reverse scan, then dT = dU P, dX = dT Q^T (+ the highway
+ *             gradient when k = 3), dP = dU^T T and dQ = X^T dT.
+ * bf16 mode rounds the operands of each product (X and Q, T and P, dU and
+ * P, dT and Q, dU and T, X and dT), and needs d_in, dp and ndir*k*d to be
+ * multiples of 8 (else SRU_E_SHAPE).  Workspace as queried.
+ */
+SRU_API size_t sru_forward_lowrank_workspace_bytes(int L, int B, int d_in, int d, int dp,
+                                                   int direction, int gemm_dtype);
+SRU_API size_t sru_backward_lowrank_workspace_bytes(int L, int B, int d_in, int d, int dp,
+                                                    int direction, int gemm_dtype);
+SRU_API int sru_forward_lowrank(const float* X, const float* Q, const float* P,
+                        const float* v_f, const float* v_r, const float* b_f, const float* b_r,
+                        const float* c0, int L, int B, int d_in, int d, int dp, int direction,
+                        const uint8_t* pad_mask, int gemm_dtype, const sru_options* options,
+                        float* T, float* U, float* H, float* C, float* c_last,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+SRU_API int sru_backward_lowrank(const float* X, const float* Q, const float* P,
+                         const float* v_f, const float* v_r, const float* b_f, const float* b_r,
+                         const float* c0, int L, int B, int d_in, int d, int dp, int direction,
+                         const uint8_t* pad_mask, int gemm_dtype, const sru_options* options,
+                         const float* T, const float* U, const float* C, const float* dH,
+                         const float* dc_last, float* dX, float* dQ, float* dP,
+                         float* dv_f, float* dv_r, float* db_f, float* db_r, float* dc0,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Component entry points: the individual steps of the two calls above, with
  * the same conventions, for testing and per-kernel measurement.

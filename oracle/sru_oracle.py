@@ -316,8 +316,12 @@ def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
     xs = [np.asarray(X, np.float64)]
     fws = []
     for p in layers:
-        fw = forward(xs[-1], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], None,
-                     direction, pad_mask, gemm_dtype, alpha, reset_new)
+        if "Q" in p:  # low-rank layer (Sec. 4.4)
+            fw = forward_lowrank(xs[-1], p["Q"], p["P"], p["v_f"], p["v_r"], p["b_f"], p["b_r"],
+                                 None, direction, pad_mask, gemm_dtype, alpha, reset_new)
+        else:
+            fw = forward(xs[-1], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], None,
+                         direction, pad_mask, gemm_dtype, alpha, reset_new)
         fws.append(fw)
         xs.append(fw["H"])
     grads = []
@@ -325,9 +329,14 @@ def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
         g = np.asarray(dH_top, np.float64)
         for li in range(len(layers) - 1, -1, -1):
             p = layers[li]
-            bw = backward(xs[li], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], g,
-                          None, direction, pad_mask, gemm_dtype, fw=fws[li], alpha=alpha,
-                          reset_new=reset_new)
+            if "Q" in p:
+                bw = backward_lowrank(xs[li], p["Q"], p["P"], p["v_f"], p["v_r"], p["b_f"],
+                                      p["b_r"], g, None, direction, pad_mask, gemm_dtype,
+                                      fw=fws[li], alpha=alpha, reset_new=reset_new)
+            else:
+                bw = backward(xs[li], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], g,
+                              None, direction, pad_mask, gemm_dtype, fw=fws[li], alpha=alpha,
+                              reset_new=reset_new)
             grads.append(bw)
             g = bw["dX"]
         grads.reverse()

@@ -5,6 +5,7 @@
 
 #include <cmath>
 
+#include <algorithm>
 #include <initializer_list>
 #include <vector>
 
@@ -156,6 +157,77 @@ BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
   w.splits = sru::gemm_splits(dw_desc(s, bf16, nullptr, nullptr, nullptr));
   w.splitk = off;
   off += align_up(sru::gemm_partial_bytes((int)s.N, s.d_in, w.splits));
+  w.total = off;
+  return w;
+}
+
+// ---------------------------------------------------------------- low rank
+// Wcat = P Q^T (Sec. 4.4).  Products, with M = L*B, N = ndir*k*d, dp = d':
+//   forward : T = X Q (NN, K = d_in), U = T P^T (NT, K = dp)
+//   backward: dT = dU P (NN, K = N), dX = dT Q^T (NT, K = dp; + highway),
+//             dP = dU^T T (TN, K = M), dQ = X^T dT (TN, K = M)
+// In bf16 mode every operand is rounded into the workspace, so each product
+// runs on the direct kernel; that needs whole 16-byte chunks.
+bool lowrank_dims_ok(const Dims& s, int dp, int gemm_dtype) {
+  if (gemm_dtype != SRU_GEMM_BF16) return true;
+  return s.d_in % 8 == 0 && dp % 8 == 0 && s.N % 8 == 0;
+}
+
+struct LrFwdLayout {
+  size_t xb, qb, tb, pb, total;
+};
+LrFwdLayout lr_fwd_layout(const Dims& s, int dp, int gemm_dtype) {
+  LrFwdLayout w{};
+  if (gemm_dtype != SRU_GEMM_BF16) return w;
+  size_t off = 0;
+  w.xb = off; off += align_up(2 * (size_t)s.M * s.d_in);
+  w.qb = off; off += align_up(2 * (size_t)s.d_in * dp);
+  w.tb = off; off += align_up(2 * (size_t)s.M * dp);
+  w.pb = off; off += align_up(2 * (size_t)s.N * dp);
+  w.total = off;
+  return w;
+}
+
+// The two reductions over tokens (dP, dQ), described for sizing and launch.
+sru::GemmDesc lr_dp_desc(const Dims& s, int dp, bool bf16, const void* dU, const void* T,
+                         float* dP) {
+  sru::GemmDesc g = gemm_desc(SRU_OP_TN, bf16, (int)s.N, dp, (int)s.M, dU, s.N, T, dp, dP, dp);
+  g.a_bf16 = g.b_bf16 = bf16;
+  g.label = "gemm_dp";
+  return g;
+}
+sru::GemmDesc lr_dq_desc(const Dims& s, int dp, bool bf16, const void* X, const void* dT,
+                         float* dQ) {
+  sru::GemmDesc g = gemm_desc(SRU_OP_TN, bf16, s.d_in, dp, (int)s.M, X, s.d_in, dT, dp, dQ, dp);
+  g.a_bf16 = g.b_bf16 = bf16;
+  g.label = "gemm_dq";
+  return g;
+}
+
+struct LrBwdLayout {
+  size_t dU, dxh, partial, dT, pb, qb, tb, xb, dtb, splitk, total;
+  int splits_p, splits_q;
+};
+LrBwdLayout lr_bwd_layout(const Dims& s, int dp, int gemm_dtype) {
+  const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
+  LrBwdLayout w{};
+  size_t off = 0;
+  w.dU = off; off += align_up((bf16 ? 2 : 4) * (size_t)s.M * s.N);
+  w.dxh = off; if (s.k == 3) off += align_up(4 * (size_t)s.M * s.nfeat);
+  w.partial = off; off += align_up(16 * (size_t)s.B * s.nfeat);
+  w.dT = off; off += align_up(4 * (size_t)s.M * dp);
+  if (bf16) {
+    w.pb = off; off += align_up(2 * (size_t)s.N * dp);
+    w.qb = off; off += align_up(2 * (size_t)s.d_in * dp);
+    w.tb = off; off += align_up(2 * (size_t)s.M * dp);
+    w.xb = off; off += align_up(2 * (size_t)s.M * s.d_in);
+    w.dtb = off; off += align_up(2 * (size_t)s.M * dp);
+  }
+  w.splits_p = sru::gemm_splits(lr_dp_desc(s, dp, bf16, nullptr, nullptr, nullptr));
+  w.splits_q = sru::gemm_splits(lr_dq_desc(s, dp, bf16, nullptr, nullptr, nullptr));
+  w.splitk = off;
+  off += align_up(std::max(sru::gemm_partial_bytes((int)s.N, dp, w.splits_p),
+                           sru::gemm_partial_bytes(s.d_in, dp, w.splits_q)));
   w.total = off;
   return w;
 }
@@ -458,6 +530,167 @@ int sru_scan_backward(const float* U, const float* X, const float* C, const floa
                      pad_mask, dU, false, dxh, static_cast<float*>(workspace),
                      dc0, dv_f, dv_r,  db_f, db_r};
   return hip_status(sru::scan_backward_launch(sh, a, stream));
+}
+
+size_t sru_forward_lowrank_workspace_bytes(int L, int B, int d_in, int d, int dp,
+                                           int direction, int gemm_dtype) {
+  Dims s;
+  if (make_dims(L, B, d_in, d, direction, s) != SRU_OK || !valid_dtype(gemm_dtype) || dp <= 0)
+    return 0;
+  return lr_fwd_layout(s, dp, gemm_dtype).total;
+}
+
+size_t sru_backward_lowrank_workspace_bytes(int L, int B, int d_in, int d, int dp,
+                                            int direction, int gemm_dtype) {
+  Dims s;
+  if (make_dims(L, B, d_in, d, direction, s) != SRU_OK || !valid_dtype(gemm_dtype) || dp <= 0)
+    return 0;
+  return lr_bwd_layout(s, dp, gemm_dtype).total;
+}
+
+int sru_forward_lowrank(const float* X, const float* Q, const float* P, const float* v_f,
+                        const float* v_r, const float* b_f, const float* b_r, const float* c0,
+                        int L, int B, int d_in, int d, int dp, int direction,
+                        const uint8_t* pad_mask, int gemm_dtype, const sru_options* options,
+                        float* T, float* U, float* H, float* C, float* c_last, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  Dims s;
+  int st = make_dims(L, B, d_in, d, direction, s);
+  if (st != SRU_OK) return st;
+  if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
+  Opts op;
+  if (int e = read_options(options, op)) return e;
+  if (dp <= 0 || s.M * dp > kMaxElems || s.N * dp > kMaxElems) return SRU_E_SHAPE;
+  if (!lowrank_dims_ok(s, dp, gemm_dtype)) return SRU_E_SHAPE;
+  if (!X || !Q || !P || !v_f || !v_r || !b_f || !b_r || !T || !U || !H) return SRU_E_NULLPTR;
+  const void* ptrs[] = {X, Q, P, v_f, v_r, b_f, b_r, c0, T, U, H, C, c_last};
+  for (const void* p : ptrs)
+    if (p && !aligned4(p)) return SRU_E_ALIGN;
+  const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
+  const LrFwdLayout lay = lr_fwd_layout(s, dp, gemm_dtype);
+  if (lay.total > 0) {
+    if (!workspace || workspace_bytes < lay.total) return SRU_E_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
+  }
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  auto bf = [&](size_t off) { return reinterpret_cast<uint16_t*>(ws + off); };
+  auto round = [&](const float* src, int rows, int cols, uint16_t* dst, const char* label) {
+    return hip_status(sru::to_bf16_launch(src, rows, cols, dst, false, stream, label));
+  };
+
+  // T = X Q
+  if (bf16) {
+    if (int e = round(X, (int)s.M, d_in, bf(lay.xb), "bf16_x")) return e;
+    if (int e = round(Q, d_in, dp, bf(lay.qb), "bf16_q")) return e;
+  }
+  sru::GemmDesc gt = gemm_desc(SRU_OP_NN, bf16, (int)s.M, dp, d_in,
+                               bf16 ? (const void*)bf(lay.xb) : X, d_in,
+                               bf16 ? (const void*)bf(lay.qb) : Q, dp, T, dp);
+  gt.a_bf16 = gt.b_bf16 = bf16;
+  gt.label = "gemm_t";
+  if (int e = hip_status(sru::gemm_launch(gt, stream))) return e;
+  // U = T P^T
+  if (bf16) {
+    if (int e = round(T, (int)s.M, dp, bf(lay.tb), "bf16_t")) return e;
+    if (int e = round(P, (int)s.N, dp, bf(lay.pb), "bf16_p")) return e;
+  }
+  sru::GemmDesc gu = gemm_desc(SRU_OP_NT, bf16, (int)s.M, (int)s.N, dp,
+                               bf16 ? (const void*)bf(lay.tb) : T, dp,
+                               bf16 ? (const void*)bf(lay.pb) : P, dp, U, s.N);
+  gu.a_bf16 = gu.b_bf16 = bf16;
+  gu.label = "gemm_u";
+  if (int e = hip_status(sru::gemm_launch(gu, stream))) return e;
+
+  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, nullptr};
+  return hip_status(sru::scan_forward_launch(scan_shape(s, direction, op), a, stream));
+}
+
+int sru_backward_lowrank(const float* X, const float* Q, const float* P, const float* v_f,
+                         const float* v_r, const float* b_f, const float* b_r, const float* c0,
+                         int L, int B, int d_in, int d, int dp, int direction,
+                         const uint8_t* pad_mask, int gemm_dtype, const sru_options* options,
+                         const float* T, const float* U, const float* C, const float* dH,
+                         const float* dc_last, float* dX, float* dQ, float* dP, float* dv_f,
+                         float* dv_r, float* db_f, float* db_r, float* dc0, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+  Dims s;
+  int st = make_dims(L, B, d_in, d, direction, s);
+  if (st != SRU_OK) return st;
+  if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
+  Opts op;
+  if (int e = read_options(options, op)) return e;
+  if (dp <= 0 || s.M * dp > kMaxElems || s.N * dp > kMaxElems) return SRU_E_SHAPE;
+  if (!lowrank_dims_ok(s, dp, gemm_dtype)) return SRU_E_SHAPE;
+  if (!X || !Q || !P || !v_f || !v_r || !b_f || !b_r || !T || !U || !C || !dH || !dX || !dQ ||
+      !dP || !dv_f || !dv_r || !db_f || !db_r)
+    return SRU_E_NULLPTR;
+  const void* ptrs[] = {X, Q, P, v_f, v_r, b_f, b_r, c0, T, U, C, dH, dc_last, dX, dQ, dP, dv_f,
+                        dv_r, db_f, db_r, dc0};
+  for (const void* p : ptrs)
+    if (p && !aligned4(p)) return SRU_E_ALIGN;
+  const LrBwdLayout lay = lr_bwd_layout(s, dp, gemm_dtype);
+  if (!workspace || workspace_bytes < lay.total) return SRU_E_WORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
+
+  const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  auto bf = [&](size_t off) { return reinterpret_cast<uint16_t*>(ws + off); };
+  void* dU = ws + lay.dU;
+  float* dxh = s.k == 3 ? reinterpret_cast<float*>(ws + lay.dxh) : nullptr;
+  float* partial = reinterpret_cast<float*>(ws + lay.partial);
+  float* dT = reinterpret_cast<float*>(ws + lay.dT);
+  float* splitk = reinterpret_cast<float*>(ws + lay.splitk);
+  sru::GemmDesc gp = lr_dp_desc(s, dp, bf16, dU, bf16 ? (const void*)bf(lay.tb) : T, dP);
+  sru::GemmDesc gq = lr_dq_desc(s, dp, bf16, bf16 ? (const void*)bf(lay.xb) : X,
+                                bf16 ? (const void*)bf(lay.dtb) : dT, dQ);
+  gp.partials = gq.partials = splitk;
+  // the split partials were sized for these plans: refuse before enqueueing
+  if (sru::gemm_splits(gp) > lay.splits_p || sru::gemm_splits(gq) > lay.splits_q)
+    return SRU_E_WORKSPACE;
+  auto round = [&](const float* src, int rows, int cols, uint16_t* dst, const char* label) {
+    return hip_status(sru::to_bf16_launch(src, rows, cols, dst, false, stream, label));
+  };
+
+  // 1. reverse gradient scan (dU in the products' operand type)
+  sru::ScanBwdArgs a{U,   X,    C,   dH,      dc_last, v_f,  v_r,  b_f,  b_r,  c0,
+                     pad_mask, dU, bf16, dxh, partial, dc0, dv_f, dv_r, db_f, db_r};
+  if (int e = hip_status(sru::scan_backward_launch(scan_shape(s, direction, op), a, stream)))
+    return e;
+  // 2. dT = dU P
+  if (bf16) {
+    if (int e = round(P, (int)s.N, dp, bf(lay.pb), "bf16_p")) return e;
+  }
+  sru::GemmDesc gd = gemm_desc(SRU_OP_NN, bf16, (int)s.M, dp, (int)s.N, dU, s.N,
+                               bf16 ? (const void*)bf(lay.pb) : P, dp, dT, dp);
+  gd.a_bf16 = gd.b_bf16 = bf16;
+  gd.label = "gemm_dt";
+  if (int e = hip_status(sru::gemm_launch(gd, stream))) return e;
+  // 3. dX = dT Q^T (+ the highway gradient of every direction when k = 3)
+  if (bf16) {
+    if (int e = round(dT, (int)s.M, dp, bf(lay.dtb), "bf16_dt")) return e;
+    if (int e = round(Q, d_in, dp, bf(lay.qb), "bf16_q")) return e;
+  }
+  sru::GemmDesc gx = gemm_desc(SRU_OP_NT, bf16, (int)s.M, d_in, dp,
+                               bf16 ? (const void*)bf(lay.dtb) : dT, dp,
+                               bf16 ? (const void*)bf(lay.qb) : Q, dp, dX, d_in);
+  gx.a_bf16 = gx.b_bf16 = bf16;
+  gx.label = "gemm_dx";
+  if (s.k == 3) {
+    gx.add = dxh;
+    gx.add_ld = s.nfeat;
+    gx.add_off = d;
+    gx.add_count = s.ndir;
+  }
+  if (int e = hip_status(sru::gemm_launch(gx, stream))) return e;
+  // 4. dP = dU^T T, 5. dQ = X^T dT (reductions over all tokens)
+  if (bf16) {
+    if (int e = round(T, (int)s.M, dp, bf(lay.tb), "bf16_t")) return e;
+  }
+  if (int e = hip_status(sru::gemm_launch(gp, stream))) return e;
+  if (bf16) {
+    if (int e = round(X, (int)s.M, d_in, bf(lay.xb), "bf16_x")) return e;
+  }
+  return hip_status(sru::gemm_launch(gq, stream));
 }
 
 }  // extern "C"

@@ -45,6 +45,11 @@ _SIGNATURES = {
     "sru_scan_forward": (_I, [_P] * 7 + [_I] * 5 + [_P, _P] + [_P] * 3 + [_P] + [_P]),
     "sru_scan_backward_workspace_bytes": (_S, [_I] * 5),
     "sru_scan_backward": (_I, [_P] * 10 + [_I] * 5 + [_P, _P] + [_P] * 7 + [_P, _S, _P]),
+    "sru_forward_lowrank_workspace_bytes": (_S, [_I] * 7),
+    "sru_backward_lowrank_workspace_bytes": (_S, [_I] * 7),
+    "sru_forward_lowrank": (_I, [_P] * 8 + [_I] * 6 + [_P, _I, _P] + [_P] * 5 + [_P, _S, _P]),
+    "sru_backward_lowrank": (_I, [_P] * 8 + [_I] * 6 + [_P, _I, _P] + [_P] * 5 + [_P] * 8
+                             + [_P, _S, _P]),
     "sru_timing_begin": (_I, [_P, _I]),
     "sru_timing_end": (_I, []),
     "sru_timing_label": (ctypes.c_char_p, [_I]),
@@ -225,6 +230,73 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
     return out
 
 
+def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
+                    gemm_dtype=GEMM_FP32, store_c=True, out=None, ws=None, highway_scale=1.0,
+                    reset_new=False):
+    """Layer with Wcat = P Q^T (Sec. 4.4); Q [d_in, dp], P [ndir, k, d, dp].
+    Returns dict(T, U, H, C, c_last); T = X Q is needed by the backward."""
+    L, B, d_in = X.shape
+    ndir, k, d, dp = P.shape
+    _req(X, "X", (L, B, d_in))
+    _req(Q, "Q", (d_in, dp))
+    _req(P, "P", (ndir, k, d, dp))
+    for n, t in (("v_f", v_f), ("v_r", v_r), ("b_f", b_f), ("b_r", b_r)):
+        _req(t, n, (ndir, d))
+    _req(c0, "c0", (B, ndir * d), optional=True)
+    _req(mask, "mask", (L, B), dtype=torch.uint8, optional=True)
+    dev = X.device
+    if out is None:
+        out = dict(T=torch.empty((L, B, dp), device=dev),
+                   U=torch.empty((L, B, ndir, k, d), device=dev),
+                   H=torch.empty((L, B, ndir * d), device=dev),
+                   C=torch.empty((L, B, ndir * d), device=dev) if store_c else None,
+                   c_last=torch.empty((B, ndir * d), device=dev))
+    need = lib().sru_forward_lowrank_workspace_bytes(L, B, d_in, d, dp, direction, gemm_dtype)
+    if need and ws is None:
+        ws = workspace(need, dev)
+    st = lib().sru_forward_lowrank(_ptr(X), _ptr(Q), _ptr(P), _ptr(v_f), _ptr(v_r), _ptr(b_f),
+                                   _ptr(b_r), _ptr(c0), L, B, d_in, d, dp, direction, _ptr(mask),
+                                   gemm_dtype, _options(highway_scale, reset_new), _ptr(out["T"]),
+                                   _ptr(out["U"]), _ptr(out["H"]), _ptr(out.get("C")),
+                                   _ptr(out.get("c_last")), _ptr(ws),
+                                   need if ws is not None else 0, _stream())
+    _check(st, "sru_forward_lowrank")
+    return out
+
+
+def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, T, U, C, dH, c0=None, dc_last=None,
+                     direction=DIR_FWD, mask=None, gemm_dtype=GEMM_FP32, want_dc0=True, out=None,
+                     ws=None, highway_scale=1.0, reset_new=False):
+    """Backward of forward_lowrank; returns dict(dX, dQ, dP, dv_f, dv_r, db_f,
+    db_r, dc0)."""
+    L, B, d_in = X.shape
+    ndir, k, d, dp = P.shape
+    _req(T, "T", (L, B, dp))
+    _req(U, "U", (L, B, ndir, k, d))
+    _req(C, "C", (L, B, ndir * d))
+    _req(dH, "dH", (L, B, ndir * d))
+    _req(dc_last, "dc_last", (B, ndir * d), optional=True)
+    dev = X.device
+    if out is None:
+        out = dict(dX=torch.empty_like(X), dQ=torch.empty_like(Q), dP=torch.empty_like(P),
+                   dv_f=torch.empty((ndir, d), device=dev), dv_r=torch.empty((ndir, d), device=dev),
+                   db_f=torch.empty((ndir, d), device=dev), db_r=torch.empty((ndir, d), device=dev),
+                   dc0=torch.empty((B, ndir * d), device=dev) if want_dc0 else None)
+    need = lib().sru_backward_lowrank_workspace_bytes(L, B, d_in, d, dp, direction, gemm_dtype)
+    if ws is None:
+        ws = workspace(need, dev)
+    st = lib().sru_backward_lowrank(_ptr(X), _ptr(Q), _ptr(P), _ptr(v_f), _ptr(v_r), _ptr(b_f),
+                                    _ptr(b_r), _ptr(c0), L, B, d_in, d, dp, direction,
+                                    _ptr(mask), gemm_dtype, _options(highway_scale, reset_new),
+                                    _ptr(T), _ptr(U), _ptr(C), _ptr(dH), _ptr(dc_last),
+                                    _ptr(out["dX"]), _ptr(out["dQ"]), _ptr(out["dP"]),
+                                    _ptr(out["dv_f"]), _ptr(out["dv_r"]), _ptr(out["db_f"]),
+                                    _ptr(out["db_r"]), _ptr(out.get("dc0")), _ptr(ws),
+                                    ws.numel(), _stream())
+    _check(st, "sru_backward_lowrank")
+    return out
+
+
 def gemm(op, A, B, M, N, K, gemm_dtype=GEMM_FP32, C=None, ws=None):
     """C[M,N] for op NT (A[M,K] B[N,K]^T), NN (A[M,K] B[K,N]) or TN (A[K,M]^T B[K,N])."""
     a_shape = (K, M) if op == OP_TN else (M, K)
@@ -293,11 +365,12 @@ class Stack:
     """Stacked SRU layers (layer l+1 reads layer l's H) with preallocated
     buffers, for the multi-layer forward + backward step.
 
-    `layers` holds per-layer dicts of GPU tensors W, v_f, v_r, b_f, b_r.
-    With bf16 GEMMs each layer's forward also writes bf16 copies of Wcat and
-    (below the top layer) H: the next layer's projection and every backward
-    product read those instead of rounding X and W again.  Without a
-    backward pass, store_c=False skips the states C (inference).
+    `layers` holds per-layer dicts of GPU tensors v_f, v_r, b_f, b_r and
+    either W (dense) or Q, P (the low-rank projection, Wcat = P Q^T).
+    With bf16 GEMMs each dense layer's forward also writes bf16 copies of
+    Wcat and (below the top layer) H: the next layer's projection and every
+    backward product read those instead of rounding X and W again.  Without
+    a backward pass, store_c=False skips the states C (inference).
     """
 
     def __init__(self, layers, L, B, d_in, d, direction, gemm_dtype, device, backward=True,
@@ -312,36 +385,57 @@ class Stack:
         ws_bytes = 0
         for li, p in enumerate(layers):
             din = d_in if li == 0 else ndir * d
-            k = p["W"].shape[1]
+            low = "Q" in p
+            k = (p["P"] if low else p["W"]).shape[1]
             keep_c = store_c or backward  # the backward reads C
-            self.fw.append(dict(U=torch.empty((L, B, ndir, k, d), device=device),
-                                H=torch.empty((L, B, ndir * d), device=device),
-                                C=torch.empty((L, B, ndir * d), device=device) if keep_c else None,
-                                c_last=torch.empty((B, ndir * d), device=device)))
-            if gemm_dtype == GEMM_BF16:
-                self.fw[-1]["W_bf16"] = torch.empty(tuple(p["W"].shape), dtype=torch.bfloat16,
-                                                    device=device)
-                if li + 1 < len(layers):  # the next layer's operand; none after the last
-                    self.fw[-1]["H_bf16"] = torch.empty((L, B, ndir * d), dtype=torch.bfloat16,
-                                                        device=device)
+            o = dict(U=torch.empty((L, B, ndir, k, d), device=device),
+                     H=torch.empty((L, B, ndir * d), device=device),
+                     C=torch.empty((L, B, ndir * d), device=device) if keep_c else None,
+                     c_last=torch.empty((B, ndir * d), device=device))
+            if low:
+                dp = p["Q"].shape[1]
+                o["T"] = torch.empty((L, B, dp), device=device)
+            elif gemm_dtype == GEMM_BF16:
+                o["W_bf16"] = torch.empty(tuple(p["W"].shape), dtype=torch.bfloat16,
+                                          device=device)
+                nxt = layers[li + 1] if li + 1 < len(layers) else None
+                if nxt is not None and "Q" not in nxt:  # the next dense layer's operand
+                    o["H_bf16"] = torch.empty((L, B, ndir * d), dtype=torch.bfloat16,
+                                              device=device)
+            self.fw.append(o)
             if backward:
-                self.bw.append(dict(dX=torch.empty((L, B, din), device=device),
-                                    dW=torch.empty_like(p["W"]),
-                                    dv_f=torch.empty((ndir, d), device=device),
-                                    dv_r=torch.empty((ndir, d), device=device),
-                                    db_f=torch.empty((ndir, d), device=device),
-                                    db_r=torch.empty((ndir, d), device=device),
-                                    dc0=None))
-                ws_bytes = max(ws_bytes, backward_workspace_bytes(L, B, din, d, direction,
-                                                                  gemm_dtype))
-            ws_bytes = max(ws_bytes, forward_workspace_bytes(L, B, din, d, direction, gemm_dtype))
+                g = dict(dX=torch.empty((L, B, din), device=device),
+                         dv_f=torch.empty((ndir, d), device=device),
+                         dv_r=torch.empty((ndir, d), device=device),
+                         db_f=torch.empty((ndir, d), device=device),
+                         db_r=torch.empty((ndir, d), device=device), dc0=None)
+                if low:
+                    g["dQ"] = torch.empty_like(p["Q"])
+                    g["dP"] = torch.empty_like(p["P"])
+                    ws_bytes = max(ws_bytes, lib().sru_backward_lowrank_workspace_bytes(
+                        L, B, din, d, dp, direction, gemm_dtype))
+                else:
+                    g["dW"] = torch.empty_like(p["W"])
+                    ws_bytes = max(ws_bytes, backward_workspace_bytes(L, B, din, d, direction,
+                                                                      gemm_dtype))
+                self.bw.append(g)
+            if low:
+                ws_bytes = max(ws_bytes, lib().sru_forward_lowrank_workspace_bytes(
+                    L, B, din, d, dp, direction, gemm_dtype))
+            else:
+                ws_bytes = max(ws_bytes, forward_workspace_bytes(L, B, din, d, direction,
+                                                                 gemm_dtype))
         self.ws = workspace(ws_bytes, device)
 
     def forward(self, X, mask=None):
         x, xb = X, None
         for p, o in zip(self.layers, self.fw):
-            forward(x, p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], None, self.direction, mask,
-                    self.gemm_dtype, out=o, ws=self.ws, X_bf16=xb, **self.variant)
+            v = (p["v_f"], p["v_r"], p["b_f"], p["b_r"], None, self.direction, mask,
+                 self.gemm_dtype)
+            if "Q" in p:
+                forward_lowrank(x, p["Q"], p["P"], *v, out=o, ws=self.ws, **self.variant)
+            else:
+                forward(x, p["W"], *v, out=o, ws=self.ws, X_bf16=xb, **self.variant)
             x, xb = o["H"], o.get("H_bf16")
         return x
 
@@ -350,9 +444,15 @@ class Stack:
         for li in range(len(self.layers) - 1, -1, -1):
             p, o, b = self.layers[li], self.fw[li], self.bw[li]
             x = X if li == 0 else self.fw[li - 1]["H"]
-            xb = None if li == 0 else self.fw[li - 1].get("H_bf16")
-            backward(x, p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], o["U"], o["C"], g,
-                     None, None, self.direction, mask, self.gemm_dtype, want_dc0=False,
-                     out=b, ws=self.ws, X_bf16=xb, W_bf16=o.get("W_bf16"), **self.variant)
+            v = (p["v_f"], p["v_r"], p["b_f"], p["b_r"])
+            if "Q" in p:
+                backward_lowrank(x, p["Q"], p["P"], *v, o["T"], o["U"], o["C"], g, None, None,
+                                 self.direction, mask, self.gemm_dtype, want_dc0=False, out=b,
+                                 ws=self.ws, **self.variant)
+            else:
+                xb = None if li == 0 else self.fw[li - 1].get("H_bf16")
+                backward(x, p["W"], *v, o["U"], o["C"], g, None, None, self.direction, mask,
+                         self.gemm_dtype, want_dc0=False, out=b, ws=self.ws, X_bf16=xb,
+                         W_bf16=o.get("W_bf16"), **self.variant)
             g = b["dX"]
         return g

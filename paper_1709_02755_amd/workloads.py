@@ -14,7 +14,9 @@ then cast to float32:
   1. lengths, if the workload is masked: integers uniform in [lo, L]
      inclusive, then lengths[0] = L so the full length always occurs;
   2. X ~ N(0, 1) of shape [L, B, d_in] (padded positions included);
-  3. per layer: W ~ U(-sqrt(3/d), sqrt(3/d)) of shape [ndir, k, d, d_in],
+  3. per layer: W ~ U(-sqrt(3/d), sqrt(3/d)) of shape [ndir, k, d, d_in]
+     (low-rank workloads instead: Q ~ U(-sqrt(3/d_in), sqrt(3/d_in)) of shape
+     [d_in, dp], then P ~ U(-sqrt(3/dp), sqrt(3/dp)) of shape [ndir, k, d, dp]),
      v_f, v_r ~ U(-0.5, 0.5), b_f ~ U(-1, 1) or 0, b_r = 0;
   4. dH ~ N(0, 1) on the last layer's H (only when a backward pass runs).
 c0 = 0 everywhere.
@@ -46,6 +48,7 @@ class Workload:
     bf_uniform: bool        # b_f ~ U(-1, 1) (else 0)
     seed: int
     store_c: bool = True    # keep every state C (False: inference, no backward)
+    dp: int | None = None   # projection rank: Wcat = P Q^T (Sec. 4.4), else dense
 
     @property
     def ndir(self) -> int:
@@ -78,6 +81,9 @@ WORKLOADS = [
              GEMM_BF16, True, 64, True, 4),
     Workload("ffn_L64_B80_din512_d2048_bf16_infer", 1, DIR_FWD, 64, 80, 512, 2048,
              GEMM_BF16, False, None, True, 5, store_c=False),
+    # the headline stack with the projection trick at the paper's rank 512
+    Workload("sru6_L256_B64_d1024_dp512_bf16", 6, DIR_FWD, 256, 64, 1024, 1024,
+             GEMM_BF16, True, None, True, 6, dp=512),
 ]
 
 
@@ -87,9 +93,10 @@ def scaled(w: Workload, *, L=None, B=None, d=None, layers=None, name=None) -> Wo
     d = w.d if d is None else d
     d_in = d if w.d_in == w.d else (w.d_in * d) // w.d
     len_lo = None if w.len_lo is None else max(1, (w.len_lo * L) // w.L)
+    dp = None if w.dp is None else max(8, (w.dp * d) // w.d)
     return Workload(name or f"{w.name}@L{L}_B{B or w.B}_d{d}", layers or w.layers,
                     w.direction, L, B or w.B, d_in, d, w.gemm_dtype, w.backward,
-                    len_lo, w.bf_uniform, w.seed, w.store_c)
+                    len_lo, w.bf_uniform, w.seed, w.store_c, dp)
 
 
 def lengths_to_mask(lengths: np.ndarray, L: int) -> np.ndarray:
@@ -98,15 +105,21 @@ def lengths_to_mask(lengths: np.ndarray, L: int) -> np.ndarray:
     return (t >= np.asarray(lengths)[None, :]).astype(np.uint8)
 
 
-def draw_layer(rng, ndir: int, k: int, d: int, d_in: int, bf_uniform: bool) -> dict:
-    bound = math.sqrt(3.0 / d)
-    W = rng.uniform(-bound, bound, size=(ndir, k, d, d_in))
+def draw_layer(rng, ndir: int, k: int, d: int, d_in: int, bf_uniform: bool,
+               dp: int | None = None) -> dict:
+    if dp is None:
+        bound = math.sqrt(3.0 / d)
+        mats = dict(W=rng.uniform(-bound, bound, size=(ndir, k, d, d_in)))
+    else:
+        bq, bp = math.sqrt(3.0 / d_in), math.sqrt(3.0 / dp)
+        Q = rng.uniform(-bq, bq, size=(d_in, dp))
+        mats = dict(Q=Q, P=rng.uniform(-bp, bp, size=(ndir, k, d, dp)))
     v_f = rng.uniform(-0.5, 0.5, size=(ndir, d))
     v_r = rng.uniform(-0.5, 0.5, size=(ndir, d))
     b_f = rng.uniform(-1.0, 1.0, size=(ndir, d)) if bf_uniform else np.zeros((ndir, d))
     b_r = np.zeros((ndir, d))
     return {k_: np.ascontiguousarray(v.astype(np.float32)) for k_, v in
-            dict(W=W, v_f=v_f, v_r=v_r, b_f=b_f, b_r=b_r).items()}
+            dict(mats, v_f=v_f, v_r=v_r, b_f=b_f, b_r=b_r).items()}
 
 
 def make_inputs(w: Workload, seed: int | None = None) -> dict:
@@ -122,7 +135,7 @@ def make_inputs(w: Workload, seed: int | None = None) -> dict:
     layers = []
     for li in range(w.layers):
         d_in, k = w.layer_dims(li)
-        layers.append(draw_layer(rng, w.ndir, k, w.d, d_in, w.bf_uniform))
+        layers.append(draw_layer(rng, w.ndir, k, w.d, d_in, w.bf_uniform, w.dp))
     dH = None
     if w.backward:
         dH = rng.standard_normal((w.L, w.B, w.ndir * w.d)).astype(np.float32)

@@ -9,6 +9,11 @@ from conftest import rel_err
 # bf16-GEMM path, measured as max |g - r| / max(|r|, rms(r)) per tensor.
 TOL_FP32 = 1e-5
 TOL_BF16 = 2e-2
+# The low-rank projection (Wcat = P Q^T) computes each projection as two
+# chained products, so every gradient passes twice as many bf16-rounded
+# operands as on the dense path; independent roundings add in quadrature,
+# which scales the dense bar by sqrt(2) (2.8e-2), rounded up.
+TOL_BF16_LOWRANK = 3e-2
 
 
 def dev(a, dtype=None):

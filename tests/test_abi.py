@@ -182,3 +182,25 @@ def test_valid_options_pass_validation():
     assert _fwd(lib, opts=ok, H=FAKE_MIS) == E_ALIGN
     assert _bwd(lib, opts=ok) == E_WS
     assert abs(sru.highway_scale_for_bias(0.0) - 3.0 ** 0.5) < 1e-15
+
+
+def test_lowrank_argument_checks():
+    lib = sru.lib()
+    f = lib.sru_forward_lowrank
+
+    def fwd(**kw):
+        a = dict(L=4, B=2, d_in=8, d=8, dp=8, direction=0, gemm=0, T=FAKE, ws=None, ws_bytes=0)
+        a.update(kw)
+        return f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, a["L"], a["B"], a["d_in"], a["d"],
+                 a["dp"], a["direction"], None, a["gemm"], None, a["T"], FAKE, FAKE, FAKE, None,
+                 a["ws"], a["ws_bytes"], None)
+    assert fwd(dp=0) == E_SHAPE
+    assert fwd(gemm=1, dp=6) == E_SHAPE        # bf16 products need dp % 8 == 0
+    assert fwd(gemm=1, d_in=12) == E_SHAPE
+    assert fwd(T=None) == E_NULL
+    assert fwd(direction=5) == E_FLAG
+    need = lib.sru_forward_lowrank_workspace_bytes(4, 2, 8, 8, 8, 0, 1)
+    assert need > 0 and lib.sru_forward_lowrank_workspace_bytes(4, 2, 8, 8, 8, 0, 0) == 0
+    assert fwd(gemm=1) == E_WS
+    assert lib.sru_backward_lowrank_workspace_bytes(4, 2, 8, 8, 8, 0, 0) > 0
+    assert lib.sru_backward_lowrank_workspace_bytes(4, 2, 8, 8, 0, 0, 0) == 0
