@@ -39,6 +39,11 @@ Readings of the paper taken here (each is also listed in the design notes):
     [forward | reverse].
   * bf16 GEMM mode rounds the operands of the three matrix products (and only
     those) to bfloat16, round-to-nearest-even; state and gates stay wide.
+  * linear=True is ablation (1) of the ablation analysis (Sec. 4.5): the
+    point-wise terms v_f * c_{t-1} and v_r * c_{t-1} are removed from both
+    gates, so f_t and r_t depend on x_t only and c_t = f_t c_{t-1} +
+    (1 - f_t) W x_t is a linear recurrence in c.  The removed term is taken
+    as zero; v_f and v_r are then not read and have no gradient (None).
 
 The backward pass is not in the paper (training by back-propagation is
 implied by the optimisers of Sec. 4).  It is the chain rule of Eq. 1-4 taken
@@ -105,6 +110,14 @@ def _is_reverse(direction, dirn):
     return direction == DIR_REV or (direction == DIR_BI and dirn == 1)
 
 
+def _gate_weights(v_f, v_r, ndir, d, linear):
+    """v_f, v_r as [ndir, d] fp64, or zeros for the linear variant (the
+    removed point-wise term contributes nothing)."""
+    if linear:
+        return np.zeros((ndir, d)), np.zeros((ndir, d))
+    return _f64(v_f).reshape(ndir, d), _f64(v_r).reshape(ndir, d)
+
+
 def _check_shapes(X, W, direction):
     L, B, d_in = X.shape
     ndir, k, d, d_in_w = W.shape
@@ -119,11 +132,12 @@ def _check_shapes(X, W, direction):
 
 
 def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
-            pad_mask=None, gemm_dtype=GEMM_FP32, alpha=1.0, reset_new=False):
+            pad_mask=None, gemm_dtype=GEMM_FP32, alpha=1.0, reset_new=False, linear=False):
     """Eq. 1-4 evaluated step by step; returns dict(U, H, C, c_last).
 
     alpha scales the highway term (Sec. 3.2); reset_new makes the reset gate
-    read the updated state c_t (Algorithm 1's order) instead of c_{t-1}.
+    read the updated state c_t (Algorithm 1's order) instead of c_{t-1};
+    linear removes the v * c_{t-1} terms of both gates (ablation (1)).
 
     U holds the per-step projections x_t W^T (one block per gate), assembled
     in the [L, B, ndir, k, d] layout so that it can be compared with the
@@ -132,7 +146,8 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
     X = _f64(X)
     W = _f64(W)
     L, B, d_in, ndir, k, d = _check_shapes(X, W, direction)
-    v_f, v_r, b_f, b_r = (_f64(a).reshape(ndir, d) for a in (v_f, v_r, b_f, b_r))
+    v_f, v_r = _gate_weights(v_f, v_r, ndir, d, linear)
+    b_f, b_r = (_f64(a).reshape(ndir, d) for a in (b_f, b_r))
     c0 = np.zeros((B, ndir, d)) if c0 is None else _f64(c0).reshape(B, ndir, d)
     pad = np.zeros((L, B), bool) if pad_mask is None else (np.asarray(pad_mask) != 0)
     bf16 = gemm_dtype == GEMM_BF16
@@ -167,8 +182,9 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
 
 def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
              pad_mask=None, gemm_dtype=GEMM_FP32, dc_last=None, fw=None, alpha=1.0,
-             reset_new=False):
-    """Reverse-step chain rule of Eq. 1-4 (alpha and reset_new as in forward).
+             reset_new=False, linear=False):
+    """Reverse-step chain rule of Eq. 1-4 (alpha, reset_new and linear as in
+    forward; with linear, dv_f and dv_r are None).
 
     Returns dict(dX, dW, dv_f, dv_r, db_f, db_r, dc0, dU, dxh) where dU is
     the gradient with respect to the projections ([L, B, ndir, k, d]) and dxh
@@ -179,7 +195,8 @@ def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
     X = _f64(X)
     W = _f64(W)
     L, B, d_in, ndir, k, d = _check_shapes(X, W, direction)
-    v_f, v_r, b_f, b_r = (_f64(a).reshape(ndir, d) for a in (v_f, v_r, b_f, b_r))
+    v_f, v_r = _gate_weights(v_f, v_r, ndir, d, linear)
+    b_f, b_r = (_f64(a).reshape(ndir, d) for a in (b_f, b_r))
     c0_ = np.zeros((B, ndir, d)) if c0 is None else _f64(c0).reshape(B, ndir, d)
     pad = np.zeros((L, B), bool) if pad_mask is None else (np.asarray(pad_mask) != 0)
     dH = _f64(dH).reshape(L, B, ndir, d)
@@ -188,7 +205,7 @@ def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
 
     if fw is None:
         fw = forward(X, W, v_f, v_r, b_f, b_r, c0_.reshape(B, ndir * d), direction,
-                     pad_mask, gemm_dtype, alpha, reset_new)
+                     pad_mask, gemm_dtype, alpha, reset_new)  # v already zero if linear
     U = fw["U"]
     C = fw["C"].reshape(L, B, ndir, d)
     Wp = bf16_round(W) if bf16 else W
@@ -258,12 +275,14 @@ def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
             if k == 3:
                 dX[t] += dxh[t, :, dirn]
         dc0[:, dirn] = g
+    if linear:
+        dv_f = dv_r = None
     return dict(dX=dX, dW=dW, dv_f=dv_f, dv_r=dv_r, db_f=db_f, db_r=db_r,
                 dc0=dc0.reshape(B, ndir * d), dU=dU, dxh=dxh)
 
 
 def forward_alg1_scalar(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
-                        pad_mask=None, alpha=1.0, reset_new=False):
+                        pad_mask=None, alpha=1.0, reset_new=False, linear=False):
     """Tiny-shape cross-check in the shape of Algorithm 1 (fp32 GEMM mode).
 
     The projections for all steps come first as one batched product (Sec. 3.1),
@@ -276,7 +295,8 @@ def forward_alg1_scalar(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
     X = _f64(X)
     W = _f64(W)
     L, B, d_in, ndir, k, d = _check_shapes(X, W, direction)
-    v_f, v_r, b_f, b_r = (_f64(a).reshape(ndir, d) for a in (v_f, v_r, b_f, b_r))
+    v_f, v_r = _gate_weights(v_f, v_r, ndir, d, linear)
+    b_f, b_r = (_f64(a).reshape(ndir, d) for a in (b_f, b_r))
     c0 = np.zeros((B, ndir, d)) if c0 is None else _f64(c0).reshape(B, ndir, d)
     pad = np.zeros((L, B), bool) if pad_mask is None else (np.asarray(pad_mask) != 0)
     # Batched projection: rows (dir, block, j) of the stacked weight.
@@ -306,7 +326,7 @@ def forward_alg1_scalar(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
 
 
 def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
-                           need_backward=True, alpha=1.0, reset_new=False):
+                           need_backward=True, alpha=1.0, reset_new=False, linear=False):
     """Stacked layers: layer l+1 takes layer l's H as its X.
 
     `layers` is a list of dicts with W, v_f, v_r, b_f, b_r (c0 = 0).
@@ -318,10 +338,10 @@ def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
     for p in layers:
         if "Q" in p:  # low-rank layer (Sec. 4.4)
             fw = forward_lowrank(xs[-1], p["Q"], p["P"], p["v_f"], p["v_r"], p["b_f"], p["b_r"],
-                                 None, direction, pad_mask, gemm_dtype, alpha, reset_new)
+                                 None, direction, pad_mask, gemm_dtype, alpha, reset_new, linear)
         else:
             fw = forward(xs[-1], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], None,
-                         direction, pad_mask, gemm_dtype, alpha, reset_new)
+                         direction, pad_mask, gemm_dtype, alpha, reset_new, linear)
         fws.append(fw)
         xs.append(fw["H"])
     grads = []
@@ -332,11 +352,12 @@ def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
             if "Q" in p:
                 bw = backward_lowrank(xs[li], p["Q"], p["P"], p["v_f"], p["v_r"], p["b_f"],
                                       p["b_r"], g, None, direction, pad_mask, gemm_dtype,
-                                      fw=fws[li], alpha=alpha, reset_new=reset_new)
+                                      fw=fws[li], alpha=alpha, reset_new=reset_new,
+                                      linear=linear)
             else:
                 bw = backward(xs[li], p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"], g,
                               None, direction, pad_mask, gemm_dtype, fw=fws[li], alpha=alpha,
-                              reset_new=reset_new)
+                              reset_new=reset_new, linear=linear)
             grads.append(bw)
             g = bw["dX"]
         grads.reverse()
@@ -354,7 +375,8 @@ def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
 # X and Q for T = X Q; T and P for U = T P^T (and likewise backward).
 
 def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
-                    pad_mask=None, gemm_dtype=GEMM_FP32, alpha=1.0, reset_new=False):
+                    pad_mask=None, gemm_dtype=GEMM_FP32, alpha=1.0, reset_new=False,
+                    linear=False):
     """Layer with Wcat = P Q^T.  Q [d_in, dp], P [ndir, k, d, dp].
     Returns dict(T, U, H, C, c_last) with T = X Q [L, B, dp]."""
     X = _f64(X)
@@ -369,16 +391,18 @@ def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
     # the scan of Eq. 1-4 on this U: the dense oracle with W chosen so that
     # its per-step projections are exactly U is not available, so the step
     # loop is run here on U directly
-    out = _scan_on_u(X, U, v_f, v_r, b_f, b_r, c0, direction, pad_mask, alpha, reset_new)
+    out = _scan_on_u(X, U, v_f, v_r, b_f, b_r, c0, direction, pad_mask, alpha, reset_new,
+                     linear)
     out["T"] = T
     out["U"] = U
     return out
 
 
-def _scan_on_u(X, U, v_f, v_r, b_f, b_r, c0, direction, pad_mask, alpha, reset_new):
+def _scan_on_u(X, U, v_f, v_r, b_f, b_r, c0, direction, pad_mask, alpha, reset_new, linear):
     """Eq. 1-4 per step given the projections U [L, B, ndir, k, d]."""
     L, B, ndir, k, d = U.shape
-    v_f, v_r, b_f, b_r = (_f64(a).reshape(ndir, d) for a in (v_f, v_r, b_f, b_r))
+    v_f, v_r = _gate_weights(v_f, v_r, ndir, d, linear)
+    b_f, b_r = (_f64(a).reshape(ndir, d) for a in (b_f, b_r))
     c0 = np.zeros((B, ndir, d)) if c0 is None else _f64(c0).reshape(B, ndir, d)
     pad = np.zeros((L, B), bool) if pad_mask is None else (np.asarray(pad_mask) != 0)
     H = np.zeros((L, B, ndir, d))
@@ -406,7 +430,7 @@ def _scan_on_u(X, U, v_f, v_r, b_f, b_r, c0, direction, pad_mask, alpha, reset_n
 
 def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
                      pad_mask=None, gemm_dtype=GEMM_FP32, dc_last=None, fw=None, alpha=1.0,
-                     reset_new=False):
+                     reset_new=False, linear=False):
     """Gradients of the low-rank layer: dict(dX, dQ, dP, dv_f, dv_r, db_f,
     db_r, dc0, dU, dT).  The scan part is the dense backward's (the recurrence
     only sees U); then dT = dU P, dX = dT Q^T (+ the highway gradient when
@@ -421,12 +445,13 @@ def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD
     rnd = bf16_round if bf16 else (lambda a: a)
     if fw is None:
         fw = forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0, direction, pad_mask, gemm_dtype,
-                             alpha, reset_new)
+                             alpha, reset_new, linear)
     # The recurrence gradients: run the dense backward with a weight whose
     # products are never used (W = 0) on the forward states of this layer.
     Wz = np.zeros((ndir, k, d, d_in))
     bw = backward(X, Wz, v_f, v_r, b_f, b_r, dH, c0, direction, pad_mask, GEMM_FP32, dc_last,
-                  fw=dict(U=fw["U"], C=fw["C"]), alpha=alpha, reset_new=reset_new)
+                  fw=dict(U=fw["U"], C=fw["C"]), alpha=alpha, reset_new=reset_new,
+                  linear=linear)
     dU = bw["dU"].reshape(L, B, ndir * k * d)
     Pm = P.reshape(ndir * k * d, dp)
     dT = rnd(dU) @ rnd(Pm)                                  # [L, B, dp]

@@ -709,3 +709,159 @@ def test_lowrank_gradients_match_finite_differences(rng):
         ana = np.asarray(bw[gname]).ravel()
         scale = max(np.max(np.abs(num)), 1e-3)
         assert np.max(np.abs(ana - num)) / scale < 1e-6, (pname, ana, num)
+
+
+# ---------------------------------------------------------------- linear variant
+# Ablation (1) of Sec. 4.5: the point-wise v * c_{t-1} terms leave both gates,
+# so f_t and r_t depend on x_t only and Eq. 2 is a linear recurrence in c.
+
+def _linear_gates(c, dirn, k4):
+    """u0, f, r, x_hat per (t, b, j) from an independent matmul + expit."""
+    X = c["X"].astype(np.float64)
+    W = c["W"].astype(np.float64)
+    u = [np.matmul(X, W[dirn, q].T) for q in range(W.shape[1])]
+    f = scipy.special.expit(u[1] + c["b_f"][dirn])
+    r = scipy.special.expit(u[2] + c["b_r"][dirn])
+    return u[0], f, r, (u[3] if k4 else X)
+
+
+@pytest.mark.parametrize("direction,k4", [(F, False), (R, True), (BI, False), (BI, True)])
+def test_linear_variant_closed_form(rng, direction, k4):
+    """c_t unrolls to prod f * c_0 + sum_s prod_{s<m<=t} f_m (1 - f_s) u0_s
+    over the direction's step order, a padded step contributing f = 1 and no
+    input; h_t = r_t c_t + (1 - r_t) alpha x_hat_t, 0 where padded.  v is
+    drawn large to show that it is not read."""
+    L, B, d = 9, 4, 3
+    d_in = 5 if k4 else d
+    c = _case(rng, L, B, d_in, d, direction, c0=True, bias_scale=1.0, masked=True, v_scale=2.0)
+    alpha = 1.4
+    fw = O.forward(c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"], c["c0"], direction,
+                   c["mask"], alpha=alpha, linear=True)
+    ndir = 2 if direction == BI else 1
+    pad = c["mask"] != 0
+    C = fw["C"].reshape(L, B, ndir, d)
+    H = fw["H"].reshape(L, B, ndir, d)
+    c0 = c["c0"].astype(np.float64).reshape(B, ndir, d)
+    for dirn in range(ndir):
+        u0, f, r, xh = _linear_gates(c, dirn, k4)
+        f = np.where(pad[:, :, None], 1.0, f)
+        inp = np.where(pad[:, :, None], 0.0, (1 - f) * u0)
+        order = list(range(L - 1, -1, -1)) if (direction == R or dirn == 1) else list(range(L))
+        for i, t in enumerate(order):
+            acc = np.prod([f[order[m]] for m in range(i + 1)], axis=0) * c0[:, dirn]
+            for s in range(i + 1):
+                tail = np.prod([f[order[m]] for m in range(s + 1, i + 1)], axis=0) \
+                    if s < i else np.ones((B, d))
+                acc = acc + tail * inp[order[s]]
+            np.testing.assert_allclose(C[t, :, dirn], acc, rtol=1e-11, atol=1e-12)
+            h = r[t] * acc + (1 - r[t]) * alpha * xh[t][:, :d] if not k4 else \
+                r[t] * acc + (1 - r[t]) * alpha * xh[t]
+            h = np.where(pad[t][:, None], 0.0, h)
+            np.testing.assert_allclose(H[t, :, dirn], h, rtol=1e-11, atol=1e-12)
+
+
+def test_linear_variant_ignores_v_and_reset_order(rng):
+    """Without the v terms, v is never read (None works) and the reset gate no
+    longer sees any state, so Algorithm 1's order gives the same layer."""
+    c = _case(rng, 6, 3, 4, 4, BI, c0=True, dc_last=True, bias_scale=0.5, masked=True)
+    args = (c["b_f"], c["b_r"])
+    fa = O.forward(c["X"], c["W"], c["v_f"], c["v_r"], *args, c["c0"], BI, c["mask"],
+                   linear=True)
+    fb = O.forward(c["X"], c["W"], None, None, *args, c["c0"], BI, c["mask"], linear=True,
+                   reset_new=True)
+    for key in ("U", "H", "C", "c_last"):
+        assert np.array_equal(fa[key], fb[key]), key
+    ba = O.backward(c["X"], c["W"], c["v_f"], c["v_r"], *args, c["dH"], c["c0"], BI, c["mask"],
+                    O.GEMM_FP32, c["dc_last"], linear=True)
+    bb = O.backward(c["X"], c["W"], None, None, *args, c["dH"], c["c0"], BI, c["mask"],
+                    O.GEMM_FP32, c["dc_last"], linear=True, reset_new=True)
+    for key in ("dX", "dW", "db_f", "db_r", "dc0", "dU", "dxh"):
+        assert np.array_equal(ba[key], bb[key]), key
+    assert ba["dv_f"] is None and ba["dv_r"] is None
+
+
+def test_linear_variant_is_gated_model_at_zero_v(rng):
+    """Removing v * c equals the gated layer at v = 0 (every output and every
+    gradient but dv, which the variant does not have)."""
+    c = _case(rng, 7, 3, 6, 3, R, c0=True, dc_last=True, bias_scale=0.5, masked=True)
+    z = np.zeros_like(c["v_f"])
+    lin = O.backward(c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"], c["dH"], c["c0"],
+                     R, c["mask"], O.GEMM_FP32, c["dc_last"], alpha=0.8, linear=True)
+    gat = O.backward(c["X"], c["W"], z, z, c["b_f"], c["b_r"], c["dH"], c["c0"], R, c["mask"],
+                     O.GEMM_FP32, c["dc_last"], alpha=0.8)
+    for key in ("dX", "dW", "db_f", "db_r", "dc0", "dU", "dxh"):
+        np.testing.assert_array_equal(lin[key], gat[key], err_msg=key)
+
+
+@pytest.mark.parametrize("direction,k4", [(F, False), (BI, True)])
+def test_linear_variant_gradients_match_finite_differences(direction, k4):
+    """Backward of the variant against central differences of its forward in
+    fp64: X, W, b and c0, a padded sequence, dc_last, alpha != 1."""
+    rng = np.random.default_rng(71 + direction + 3 * k4)
+    L, B, d = 5, 3, 3
+    d_in = 2 * d if k4 else d
+    c = _case(rng, L, B, d_in, d, direction, c0=True, dc_last=True, bias_scale=0.5,
+              masked=True)
+    base = {k: np.asarray(c[k], np.float64) for k in ("X", "W", "b_f", "b_r", "c0")}
+    dH, dcl, mask = c["dH"].astype(np.float64), c["dc_last"].astype(np.float64), c["mask"]
+    alpha = 1.3
+
+    def loss(p):
+        fw = O.forward(p["X"], p["W"], None, None, p["b_f"], p["b_r"], p["c0"], direction, mask,
+                       alpha=alpha, linear=True)
+        return _loss(fw, dH, dcl)
+
+    bw = O.backward(base["X"], base["W"], None, None, base["b_f"], base["b_r"], dH, base["c0"],
+                    direction, mask, O.GEMM_FP32, dcl, alpha=alpha, linear=True)
+    h = 1e-6
+    for pname, gname in dict(X="dX", W="dW", b_f="db_f", b_r="db_r", c0="dc0").items():
+        p0 = base[pname]
+        num = np.zeros(p0.size)
+        for i in range(p0.size):
+            pp = dict(base)
+            a = p0.copy().ravel(); a[i] += h; pp[pname] = a.reshape(p0.shape)
+            lp = loss(pp)
+            a = p0.copy().ravel(); a[i] -= h; pp[pname] = a.reshape(p0.shape)
+            lm = loss(pp)
+            num[i] = (lp - lm) / (2 * h)
+        ana = np.asarray(bw[gname]).ravel()
+        scale = max(np.max(np.abs(num)), 1e-3)
+        assert np.max(np.abs(ana - num)) / scale < 1e-6, (pname, ana, num)
+
+
+def test_linear_variant_carried_gradient_closed_form(rng):
+    """The carried gradient of the linear recurrence unrolls: with
+    G_s = sum_{t>=s} prod_{s<m<=t} f_m dh_t r_t + prod_{s<m<L} f_m dc_last,
+    du0_s = G_s (1 - f_s) and dc0 = f_0 G_0 (forward direction, no padding)."""
+    L, B, d = 8, 2, 4
+    c = _case(rng, L, B, d, d, F, c0=True, dc_last=True, bias_scale=1.0)
+    bw = O.backward(c["X"], c["W"], None, None, c["b_f"], c["b_r"], c["dH"], c["c0"], F, None,
+                    O.GEMM_FP32, c["dc_last"], linear=True)
+    u0, f, r, _ = _linear_gates(c, 0, False)
+    dh = c["dH"].astype(np.float64)
+    dcl = c["dc_last"].astype(np.float64)
+    G = np.zeros((L, B, d))
+    for s in range(L):
+        acc = np.prod(f[s + 1:], axis=0) * dcl
+        for t in range(s, L):
+            acc = acc + np.prod(f[s + 1:t + 1], axis=0) * dh[t] * r[t]
+        G[s] = acc
+    np.testing.assert_allclose(bw["dU"][:, :, 0, 0], G * (1 - f), rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(bw["dc0"], f[0] * G[0], rtol=1e-11, atol=1e-12)
+
+
+def test_linear_variant_lowrank_equals_dense_product_weight(rng):
+    """The factorised layer with the variant is the dense variant layer with
+    Wcat = P Q^T (forward and every gradient the two share)."""
+    c = _lowrank_case(rng, 6, 3, 7, 4, 3, BI)
+    ndir, k = c["W"].shape[:2]
+    P64, Q64 = c["P"].astype(np.float64), c["Q"].astype(np.float64)
+    W = (P64.reshape(-1, Q64.shape[1]) @ Q64.T).reshape(ndir, k, 4, -1)
+    args = (None, None, c["b_f"], c["b_r"])
+    lr = O.backward_lowrank(c["X"], c["Q"], c["P"], *args, c["dH"], c["c0"], BI, c["mask"],
+                            O.GEMM_FP32, c["dc_last"], linear=True)
+    dn = O.backward(c["X"], W, *args, c["dH"], c["c0"], BI, c["mask"], O.GEMM_FP32,
+                    c["dc_last"], linear=True)
+    for key in ("dX", "db_f", "db_r", "dc0"):
+        np.testing.assert_allclose(lr[key], dn[key], rtol=1e-10, atol=1e-12)
+    assert lr["dv_f"] is None
