@@ -92,6 +92,7 @@ def kernel_work(w, splits, bf16):
     K = w.d_in
     elems = M * nfeat
     du_b = 2.0 if bf16 else 4.0
+    nq = 2 if w.linear else 4  # v/b sums per feature (no v in the linear variant)
     hb = 2.0 * (w.layers - 1) / w.layers if bf16 and w.dp is None else 0.0  # bf16 copy of H
     if w.dp is not None:  # low-rank layers: Wcat = P Q^T, rank dp
         dp = w.dp
@@ -124,7 +125,7 @@ def kernel_work(w, splits, bf16):
         # the products are bf16) and, for k = 3, dx_hat (4 B): 34 B (bf16) /
         # 40 B (fp32) at k = 3
         "scan_bwd": dict(bytes=elems * (24.0 + du_b * k + (4.0 if k == 3 else 0.0))),
-        "reduce_vb": dict(bytes=4.0 * (4 * w.B * nfeat + 4 * nfeat)),
+        "reduce_vb": dict(bytes=4.0 * (nq * w.B * nfeat + nq * nfeat)),
         "splitk_reduce": dict(bytes=4.0 * (splits + 1) * N * K),
         # fp32 -> bf16 copies of the product operands: Wcat, X (first layer),
         # and Wcat^T where dX cannot read Wcat row-contiguous
@@ -191,7 +192,7 @@ def cpu_baseline(w, inp, nseq):
     t0 = time.perf_counter()
     dH = None if inp["dH"] is None else inp["dH"][:, sl]
     O.stack_forward_backward(X, inp["layers"], w.direction, mask, w.gemm_dtype, dH,
-                             need_backward=w.backward)
+                             need_backward=w.backward, linear=w.linear)
     secs = time.perf_counter() - t0
     tokens = w.L * nseq
     passes = "fwd+bwd" if w.backward else "fwd"
@@ -243,6 +244,7 @@ def _per_kernel(rows, counter):
 
 # kernel-name substrings (all must occur) -> labels of the per-launch table
 KERNEL_KEYS = [(("scan_fwd_kernel",), "scan_fwd"), (("scan_bwd_kernel",), "scan_bwd"),
+               (("scan_fwd_lin_kernel",), "scan_fwd"), (("scan_bwd_lin_kernel",), "scan_bwd"),
                (("reduce_vb_kernel",), "reduce_vb"), (("splitk_reduce_kernel",), "splitk_reduce"),
                (("to_bf16_kernel",), "bf16_x"),
                # the three products of the bf16 path (template args after the
@@ -329,7 +331,7 @@ def main():
     X, dH, mask = to(inp["X"]), to(inp["dH"]), to(inp["mask"])
     st = sru.Stack(layers, w.L, w.B, w.d_in, w.d, w.direction, w.gemm_dtype, dev,
                    backward=w.backward, highway_scale=args.highway_scale,
-                   reset_new=args.reset_new, store_c=w.store_c)
+                   reset_new=args.reset_new, store_c=w.store_c, linear=w.linear)
 
     def step():
         st.forward(X, mask)
@@ -419,7 +421,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16" if w.gemm_dtype == sru.GEMM_BF16 else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "layers": w.layers, "L": w.L, "B": w.B,
                    "d_in": w.d_in, "d": w.d,
@@ -429,6 +431,8 @@ def main():
                    "scan": "fp32", "tokens_per_step": w.tokens, "global_batch": w.B,
                    "highway_scale": args.highway_scale,
                    "reset_gate": "c_t (Algorithm 1)" if args.reset_new else "c_{t-1} (Eq. 3)",
+                   "recurrence": ("linear: v * c removed (ablation (1), Sec. 4.5)" if w.linear
+                                  else "gated (Eq. 1-4)"),
                    "seq_len": w.L, "parallelism": "single GPU"},
         "roofline": roofline,
         "scan_hbm": scan_hbm,

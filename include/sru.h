@@ -78,19 +78,32 @@ typedef enum { SRU_DIR_FWD = 0, SRU_DIR_REV = 1, SRU_DIR_BI = 2 } sru_direction;
 typedef enum { SRU_GEMM_FP32 = 0, SRU_GEMM_BF16 = 1 } sru_gemm_dtype;
 
 /* Gate variants.  Every layer and scan call takes a `const sru_options*`;
- * NULL means Eq. 1-4 as printed: highway_scale = 1 and the reset gate on
- * c_{t-1} (Eq. 3).  The same options must be passed to the forward and the
- * backward call of a layer.  Host memory, read during the call only.
+ * NULL means Eq. 1-4 as printed: highway_scale = 1, the reset gate on
+ * c_{t-1} (Eq. 3) and the gated recurrence.  The same options must be
+ * passed to the forward and the backward call of a layer.  Host memory,
+ * read during the call only.
  *   highway_scale: alpha in h_t = r_t c_t + (1 - r_t) alpha x_hat, the
  *     scaling correction of Sec. 3.2 (sqrt(3), or sqrt(1 + 2 e^b) for a
  *     reset-gate bias b, Appendix A).  Must be finite.
  *   reset_state: SRU_RESET_PREV, r_t = sigma(W_r x_t + v_r c_{t-1} + b_r)
  *     (Eq. 3); SRU_RESET_NEW, r_t reads c_t: the order of Algorithm 1.
- *     Anything else is SRU_E_FLAG. */
+ *     Anything else is SRU_E_FLAG.
+ *   recurrence: SRU_RECURRENCE_GATED, Eq. 1-4; SRU_RECURRENCE_LINEAR,
+ *     ablation (1) of Sec. 4.5: the point-wise v_f * c_{t-1} and
+ *     v_r * c_{t-1} terms are removed from both gates, so
+ *       f_t = sigma(W_f x_t + b_f),  r_t = sigma(W_r x_t + b_r)
+ *     and c_t = f_t c_{t-1} + (1 - f_t) W x_t is linear in c.  v_f and v_r
+ *     are then not read, dv_f and dv_r not written (all may be NULL), and
+ *     reset_state has no effect (r reads no state).  The scans then run in
+ *     parallel over chunks of time as well as over (b, direction, j), which
+ *     keeps the GPU busy when B*ndir*d is small.  Anything else is
+ *     SRU_E_FLAG. */
 typedef enum { SRU_RESET_PREV = 0, SRU_RESET_NEW = 1 } sru_reset_state;
+typedef enum { SRU_RECURRENCE_GATED = 0, SRU_RECURRENCE_LINEAR = 1 } sru_recurrence;
 typedef struct {
   float highway_scale;
   int reset_state;
+  int recurrence;
 } sru_options;
 
 /* Human-readable name of a status code (static string, never NULL). */

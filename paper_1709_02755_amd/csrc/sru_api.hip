@@ -75,20 +75,29 @@ int make_dims(int L, int B, int d_in, int d, int direction, Dims& s) {
 struct Opts {
   float alpha = 1.0f;
   int reset_new = 0;
+  int linear = 0;  // v * c_{t-1} removed: v_f, v_r, dv_f, dv_r unused (may be NULL)
 };
 
 int read_options(const sru_options* o, Opts& op) {
   if (!o) return SRU_OK;
   if (!std::isfinite(o->highway_scale)) return SRU_E_FLAG;
   if (o->reset_state != SRU_RESET_PREV && o->reset_state != SRU_RESET_NEW) return SRU_E_FLAG;
+  if (o->recurrence != SRU_RECURRENCE_GATED && o->recurrence != SRU_RECURRENCE_LINEAR)
+    return SRU_E_FLAG;
   op.alpha = o->highway_scale;
-  op.reset_new = o->reset_state == SRU_RESET_NEW;
+  op.linear = o->recurrence == SRU_RECURRENCE_LINEAR;
+  // without v the reset gate reads no state, so the two orders coincide
+  op.reset_new = !op.linear && o->reset_state == SRU_RESET_NEW;
   return SRU_OK;
 }
 
 sru::ScanShape scan_shape(const Dims& s, int direction, const Opts& op = Opts()) {
-  return sru::ScanShape{s.L, s.B, s.d_in, s.d, s.ndir, s.k, direction, op.alpha, op.reset_new};
+  return sru::ScanShape{s.L, s.B, s.d_in, s.d, s.ndir, s.k, direction, op.alpha, op.reset_new,
+                        op.linear};
 }
+
+// v_f, v_r (and dv_f, dv_r) are required by the gated recurrence only
+bool missing_v(const Opts& op, const void* a, const void* b) { return !op.linear && (!a || !b); }
 
 int hip_status(hipError_t e) {
   if (e == hipSuccess) return SRU_OK;
@@ -317,7 +326,7 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
   if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
   Opts op;
   if (int e = read_options(options, op)) return e;
-  if (!X || !W || !v_f || !v_r || !b_f || !b_r || !U || !H) return SRU_E_NULLPTR;
+  if (!X || !W || missing_v(op, v_f, v_r) || !b_f || !b_r || !U || !H) return SRU_E_NULLPTR;
   const void* ptrs[] = {X, W, v_f, v_r, b_f, b_r, c0, U, H, C, c_last};
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
@@ -371,8 +380,8 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
   Opts op;
   if (int e = read_options(options, op)) return e;
-  if (!X || !W || !v_f || !v_r || !b_f || !b_r || !U || !C || !dH || !dX || !dW || !dv_f ||
-      !dv_r || !db_f || !db_r)
+  if (!X || !W || missing_v(op, v_f, v_r) || !b_f || !b_r || !U || !C || !dH || !dX || !dW ||
+      missing_v(op, dv_f, dv_r) || !db_f || !db_r)
     return SRU_E_NULLPTR;
   const void* ptrs[] = {X, W, v_f, v_r, b_f, b_r, c0, U, C, dH, dc_last, dX, dW, dv_f, dv_r,
                         db_f, db_r, dc0};
@@ -486,7 +495,7 @@ int sru_scan_forward(const float* U, const float* X, const float* v_f, const flo
   if (st != SRU_OK) return st;
   Opts op;
   if (int e = read_options(options, op)) return e;
-  if (!U || !v_f || !v_r || !b_f || !b_r || !H) return SRU_E_NULLPTR;
+  if (!U || missing_v(op, v_f, v_r) || !b_f || !b_r || !H) return SRU_E_NULLPTR;
   if (s.k == 3 && !X) return SRU_E_NULLPTR;
   const void* ptrs[] = {U, X, v_f, v_r, b_f, b_r, c0, H, C, c_last};
   for (const void* p : ptrs)
@@ -514,7 +523,8 @@ int sru_scan_backward(const float* U, const float* X, const float* C, const floa
   if (st != SRU_OK) return st;
   Opts op;
   if (int e = read_options(options, op)) return e;
-  if (!U || !C || !dH || !v_f || !v_r || !b_f || !b_r || !dU || !dv_f || !dv_r || !db_f || !db_r)
+  if (!U || !C || !dH || missing_v(op, v_f, v_r) || !b_f || !b_r || !dU ||
+      missing_v(op, dv_f, dv_r) || !db_f || !db_r)
     return SRU_E_NULLPTR;
   if (s.k == 3 && (!X || !dxh)) return SRU_E_NULLPTR;
   if (s.k == 4 && dxh) return SRU_E_SHAPE;
@@ -562,7 +572,8 @@ int sru_forward_lowrank(const float* X, const float* Q, const float* P, const fl
   if (int e = read_options(options, op)) return e;
   if (dp <= 0 || s.M * dp > kMaxElems || s.N * dp > kMaxElems) return SRU_E_SHAPE;
   if (!lowrank_dims_ok(s, dp, gemm_dtype)) return SRU_E_SHAPE;
-  if (!X || !Q || !P || !v_f || !v_r || !b_f || !b_r || !T || !U || !H) return SRU_E_NULLPTR;
+  if (!X || !Q || !P || missing_v(op, v_f, v_r) || !b_f || !b_r || !T || !U || !H)
+    return SRU_E_NULLPTR;
   const void* ptrs[] = {X, Q, P, v_f, v_r, b_f, b_r, c0, T, U, H, C, c_last};
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
@@ -621,8 +632,8 @@ int sru_backward_lowrank(const float* X, const float* Q, const float* P, const f
   if (int e = read_options(options, op)) return e;
   if (dp <= 0 || s.M * dp > kMaxElems || s.N * dp > kMaxElems) return SRU_E_SHAPE;
   if (!lowrank_dims_ok(s, dp, gemm_dtype)) return SRU_E_SHAPE;
-  if (!X || !Q || !P || !v_f || !v_r || !b_f || !b_r || !T || !U || !C || !dH || !dX || !dQ ||
-      !dP || !dv_f || !dv_r || !db_f || !db_r)
+  if (!X || !Q || !P || missing_v(op, v_f, v_r) || !b_f || !b_r || !T || !U || !C || !dH ||
+      !dX || !dQ || !dP || missing_v(op, dv_f, dv_r) || !db_f || !db_r)
     return SRU_E_NULLPTR;
   const void* ptrs[] = {X, Q, P, v_f, v_r, b_f, b_r, c0, T, U, C, dH, dc_last, dX, dQ, dP, dv_f,
                         dv_r, db_f, db_r, dc0};

@@ -55,6 +55,8 @@ struct ScanShape {
   int L, B, d_in, d, ndir, k, direction;
   float alpha;    // highway scale (Sec. 3.2); 1 = Eq. 4 as printed
   int reset_new;  // reset gate reads c_t (Algorithm 1) instead of c_{t-1} (Eq. 3)
+  int linear;     // v * c_{t-1} removed from both gates (ablation (1), Sec. 4.5);
+                  // v_f, v_r, dv_f, dv_r are then unused
 };
 
 struct ScanFwdArgs {

@@ -258,20 +258,313 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
   if (a.dc0) a.dc0[ln.gid] = g;
 }
 
+// ------------------------------------------------- linear variant, chunked
+// Ablation (1) of Sec. 4.5 removes v * c_{t-1} from both gates: f and r then
+// depend on the projections only, and each step is an affine map of the
+// state, c -> f c + (1 - f) u0.  Affine maps compose, so time can be split
+// into chunks that are scanned in parallel:
+//   1. every chunk folds its steps into one map (A, S) = (prod f, the state
+//      reached from 0),
+//   2. a chunk's incoming state is the previous state pushed through the
+//      maps of the chunks before it,
+//   3. every chunk rescans its steps from that state.
+// A workgroup is 64 lanes (b, direction, j) times NW waves; it walks the
+// direction's step order in blocks of NW * CH steps, wave w taking steps
+// [w CH, (w + 1) CH) of a block.  Step 1 runs on the block's loads held in
+// registers, the maps meet in LDS (step 2), and step 3 rescans the same
+// registers, so every element is read and written once, as in the
+// sequential scan.  The block's final state (after the rescan, held by
+// the wave that owns the block's last step) is the next
+// block's incoming state.  The backward pass does the
+// same on the carried gradient, g -> f (g + dh r), in reverse step order.
+// No wave leaves early: every wave reaches every barrier.
+constexpr int kLinMaxWaves = 16;
+
+// Workgroup barrier for LDS hand-offs: waits for this wave's LDS accesses
+// only (the release fence of __syncthreads would also drain every
+// outstanding global store); the memory clobbers keep the compiler from
+// moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0) (vmcnt 63, expcnt 7)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Lane of a chunked workgroup: as decode_lane, with the lane index taken
+// from threadIdx.x mod 64.  Lanes past the end (live = false) take the last
+// lane's coordinates, so every address they form is in range; they store
+// nothing.
+__device__ __forceinline__ bool decode_lane_lin(const ScanShape& s, Lane& ln) {
+  const int nfeat = s.ndir * s.d;
+  const int total = s.B * nfeat;
+  const int gid = blockIdx.x * 64 + (threadIdx.x & 63);
+  const bool live = gid < total;
+  ln.gid = live ? gid : total - 1;
+  ln.b = ln.gid / nfeat;
+  ln.fidx = ln.gid - ln.b * nfeat;
+  ln.dir = ln.fidx / s.d;
+  ln.j = ln.fidx - ln.dir * s.d;
+  ln.rev = s.direction == 1 || (s.direction == 2 && ln.dir == 1);
+  return live;
+}
+
+template <int KB, bool MASK, bool STORE_C, bool STORE_HB, int CH>
+__global__ __launch_bounds__(64 * kLinMaxWaves) void scan_fwd_lin_kernel(ScanShape s,
+                                                                         ScanFwdArgs a) {
+  __shared__ float2 agg[2][kLinMaxWaves][64];  // (A, S) per block parity, wave, lane
+  __shared__ float carry_lds[2][64];           // block's final state, per parity
+  Lane ln;
+  const bool live = decode_lane_lin(s, ln);
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int NW = blockDim.x >> 6;
+  const int L = s.L;
+  const int d = s.d;
+  const long long nfeat = (long long)s.ndir * s.d;
+  const long long u_step = (long long)s.B * s.ndir * KB * s.d;
+  const long long x_step = (long long)s.B * s.d_in;
+  const long long h_step = (long long)s.B * nfeat;
+  const float* up = a.U + ((long long)ln.b * s.ndir + ln.dir) * KB * s.d + ln.j;
+  const float* xp = KB == 3 ? a.X + (long long)ln.b * s.d_in + ln.j : nullptr;
+  const uint8_t* mp = MASK ? a.mask + ln.b : nullptr;
+  const float bf = a.b_f[ln.fidx], br = a.b_r[ln.fidx];
+  const float alpha = s.alpha;
+  float carry = a.c0 ? a.c0[ln.gid] : 0.0f;
+  auto tindex = [&](int st) { return ln.rev ? L - 1 - st : st; };
+
+  int blk = 0;
+  for (int base = 0; base < L; base += NW * CH, ++blk) {
+    const int p = blk & 1;
+    const int st0 = base + w * CH;
+    float ru0[CH], rf[CH], ru2[CH], rx[CH];
+    bool act[CH];
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int st = st0 + i < L ? st0 + i : L - 1;
+      const long long t = tindex(st);
+      const float* u = up + t * u_step;
+      ru0[i] = __builtin_nontemporal_load(u);
+      rf[i] = __builtin_nontemporal_load(u + d);
+      ru2[i] = __builtin_nontemporal_load(u + 2 * d);
+      if constexpr (KB == 4) rx[i] = __builtin_nontemporal_load(u + 3 * d);
+      else rx[i] = xp[t * x_step];
+      act[i] = st0 + i < L;
+      if constexpr (MASK) act[i] = act[i] && mp[t * s.B] == 0;
+    }
+    // 1. this chunk's map
+    float A = 1.0f, S = 0.0f;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const float f = sigmoid_fast(rf[i] + bf);  // Eq. 1 without v * c
+      rf[i] = f;
+      if (act[i]) {
+        S = fmaf(f, S, (1.0f - f) * ru0[i]);
+        A *= f;
+      }
+    }
+    agg[p][w][lane] = make_float2(A, S);
+    lds_barrier();
+    // 2. incoming state: the previous block's final state through the maps
+    //    of the chunks before this one
+    float c = blk == 0 ? carry : carry_lds[p ^ 1][lane];
+    for (int m = 0; m < w; ++m) {
+      const float2 g = agg[p][m][lane];
+      c = fmaf(g.x, c, g.y);
+    }
+    // 3. rescan
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      if (st0 + i >= L) break;
+      const long long t = tindex(st0 + i);
+      const float f = rf[i];
+      const float cn = fmaf(f, c, (1.0f - f) * ru0[i]);            // Eq. 2
+      const float r = sigmoid_fast(ru2[i] + br);                   // Eq. 3 without v * c
+      float h = fmaf(r, cn, (1.0f - r) * (alpha * rx[i]));         // Eq. 4 (Sec. 3.2)
+      if (act[i]) c = cn;
+      else h = 0.0f;
+      if (live) {
+        __builtin_nontemporal_store(h, a.H + ln.gid + t * h_step);
+        if constexpr (STORE_C) __builtin_nontemporal_store(c, a.C + ln.gid + t * h_step);
+        if constexpr (STORE_HB)
+          __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h),
+                                      a.Hb + ln.gid + t * h_step);
+      }
+    }
+    // the wave holding the block's last step publishes the rescanned state
+    const int w_last = (min(L - base, NW * CH) - 1) / CH;
+    if (w == w_last) {
+      carry_lds[p][lane] = c;
+      if (base + NW * CH >= L && live && a.c_last) a.c_last[ln.gid] = c;
+    }
+  }
+}
+
+// Backward of the variant.  Processing index i visits forward-order
+// position pos = L-1-i.  cval(i) = C at position L-1-i (c0 for i = L), so
+// step i has c_t = cval(i) and c_p = cval(i+1).  Per step:
+//   gc = g + dh r;  du0 = gc (1 - f);  df = gc (c_p - u0) f (1 - f)
+//   dr = dh (c_t - alpha x_hat) r (1 - r);  dx_hat = dh (1 - r) alpha
+//   g <- gc f          (the map g -> f g + f dh r)
+// b_f / b_r sums go to partial[b][2|3][feature] after a fixed-order sum
+// over the workgroup's waves.
+template <int KB, bool MASK, bool DUB, int CH>
+__global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_lin_kernel(ScanShape s,
+                                                                         ScanBwdArgs a) {
+  __shared__ float2 agg[2][kLinMaxWaves][64];
+  __shared__ float carry_lds[2][64];
+  Lane ln;
+  const bool live = decode_lane_lin(s, ln);
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int NW = blockDim.x >> 6;
+  const int L = s.L;
+  const int d = s.d;
+  const long long nfeat = (long long)s.ndir * s.d;
+  const long long u_step = (long long)s.B * s.ndir * KB * s.d;
+  const long long x_step = (long long)s.B * s.d_in;
+  const long long h_step = (long long)s.B * nfeat;
+  const long long u_off = ((long long)ln.b * s.ndir + ln.dir) * KB * s.d + ln.j;
+  const float* up = a.U + u_off;
+  using DuT = typename std::conditional<DUB, uint16_t, float>::type;
+  DuT* dup = static_cast<DuT*>(a.dU) + u_off;
+  const float* xp = KB == 3 ? a.X + (long long)ln.b * s.d_in + ln.j : nullptr;
+  const uint8_t* mp = MASK ? a.mask + ln.b : nullptr;
+  const float* cpp = a.C + ln.gid;
+  const float* dhp = a.dH + ln.gid;
+  const float bf = a.b_f[ln.fidx], br = a.b_r[ln.fidx];
+  const float alpha = s.alpha;
+  const float c0v = a.c0 ? a.c0[ln.gid] : 0.0f;
+  float carry = a.dc_last ? a.dc_last[ln.gid] : 0.0f;
+  float sum_df = 0.f, sum_dr = 0.f;
+  // time index of processing index i (clamped into range)
+  auto tproc = [&](int i) {
+    const int pos = L - 1 - (i < L ? i : L - 1);
+    return (long long)(ln.rev ? L - 1 - pos : pos);
+  };
+
+  int blk = 0;
+  for (int base = 0; base < L; base += NW * CH, ++blk) {
+    const int p = blk & 1;
+    const int i0 = base + w * CH;
+    float ru0[CH], rf[CH], rr[CH], rx[CH], rdh[CH], rc[CH + 1];
+    bool act[CH];
+#pragma unroll
+    for (int m = 0; m < CH; ++m) {
+      const long long t = tproc(i0 + m);
+      const float* u = up + t * u_step;
+      ru0[m] = __builtin_nontemporal_load(u);
+      rf[m] = __builtin_nontemporal_load(u + d);
+      rr[m] = __builtin_nontemporal_load(u + 2 * d);
+      if constexpr (KB == 4) rx[m] = __builtin_nontemporal_load(u + 3 * d);
+      else rx[m] = xp[t * x_step];
+      rdh[m] = __builtin_nontemporal_load(dhp + t * h_step);
+      rc[m] = cpp[t * h_step];
+      act[m] = i0 + m < L;
+      if constexpr (MASK) act[m] = act[m] && mp[t * s.B] == 0;
+    }
+    {
+      const int ie = i0 + CH;  // c_p of the chunk's last step
+      rc[CH] = ie < L ? cpp[tproc(ie) * h_step] : c0v;
+    }
+    // 1. this chunk's map on the carried gradient
+    float A = 1.0f, S = 0.0f;
+#pragma unroll
+    for (int m = 0; m < CH; ++m) {
+      const float f = sigmoid_fast(rf[m] + bf);
+      const float r = sigmoid_fast(rr[m] + br);
+      rf[m] = f;
+      rr[m] = r;
+      if (act[m]) {
+        S = f * fmaf(rdh[m], r, S);
+        A *= f;
+      }
+    }
+    agg[p][w][lane] = make_float2(A, S);
+    lds_barrier();
+    // 2. incoming gradient
+    float g = blk == 0 ? carry : carry_lds[p ^ 1][lane];
+    for (int m = 0; m < w; ++m) {
+      const float2 q = agg[p][m][lane];
+      g = fmaf(q.x, g, q.y);
+    }
+    // 3. rescan
+#pragma unroll
+    for (int m = 0; m < CH; ++m) {
+      if (i0 + m >= L) break;
+      const long long t = tproc(i0 + m);
+      const float f = rf[m], r = rr[m];
+      const float c_t = rc[m];
+      const float c_p = i0 + m + 1 < L ? rc[m + 1] : c0v;
+      const float dh = act[m] ? rdh[m] : 0.0f;
+      const float gc = fmaf(dh, r, g);
+      float du0 = gc * (1.0f - f);
+      float df = gc * (c_p - ru0[m]) * (f * (1.0f - f));
+      float dr = dh * (c_t - alpha * rx[m]) * (r * (1.0f - r));
+      float dx = dh * (1.0f - r) * alpha;
+      if (act[m]) {
+        g = gc * f;
+      } else {
+        du0 = df = dr = dx = 0.0f;
+      }
+      sum_df += df;
+      sum_dr += dr;
+      if (live) {
+        DuT* du = dup + t * u_step;
+        auto put = [](float v, DuT* q) {
+          if constexpr (DUB)
+            __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)v), q);
+          else
+            __builtin_nontemporal_store(v, q);
+        };
+        put(du0, du);
+        put(df, du + d);
+        put(dr, du + 2 * d);
+        if constexpr (KB == 4) put(dx, du + 3 * d);
+        else __builtin_nontemporal_store(dx, a.dxh + ln.gid + t * h_step);
+      }
+    }
+    const int w_last = (min(L - base, NW * CH) - 1) / CH;
+    if (w == w_last) {
+      carry_lds[p][lane] = g;
+      if (base + NW * CH >= L && live && a.dc0) a.dc0[ln.gid] = g;
+    }
+  }
+  // fixed-order sum of the waves' b sums (agg is free: every wave is past
+  // its last read of it once it reaches this barrier)
+  lds_barrier();
+  agg[0][w][lane] = make_float2(sum_df, sum_dr);
+  lds_barrier();
+  if (w == 0 && live) {
+    float sdf = 0.f, sdr = 0.f;
+    for (int m = 0; m < NW; ++m) {
+      const float2 q = agg[0][m][lane];
+      sdf += q.x;
+      sdr += q.y;
+    }
+    float* part = a.partial + (long long)ln.b * 4 * nfeat + ln.fidx;
+    part[2 * nfeat] = sdf;
+    part[3 * nfeat] = sdr;
+  }
+}
+
 // Sum of the per-sequence partials over b, in a fixed order (deterministic).
 // A workgroup covers 64 consecutive outputs; its 8 waves take b = w, w+8,
 // ... in sequence, and the 8 wave sums of an output are added as a fixed
 // tree through LDS.  The loads of a lane are independent, so a launch costs
 // about one memory round trip.
 constexpr int kVbWaves = 8;
+// Outputs q = qlo .. 3 (q: dv_f, dv_r, db_f, db_r); the linear variant has
+// no v and sums from q = 2.
 __global__ __launch_bounds__(64 * kVbWaves) void reduce_vb_kernel(const float* __restrict__ partial,
-                                                                  int B, int nfeat, float* dv_f,
-                                                                  float* dv_r, float* db_f,
-                                                                  float* db_r) {
+                                                                  int B, int nfeat, int qlo,
+                                                                  float* dv_f, float* dv_r,
+                                                                  float* db_f, float* db_r) {
   __shared__ float red[kVbWaves][64];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int o = blockIdx.x * 64 + lane;  // output: q * nfeat + f
+  const int o = qlo * nfeat + blockIdx.x * 64 + lane;  // output: q * nfeat + f
   const bool live = o < 4 * nfeat;
   const long long stride = 4LL * nfeat;
   float s = 0.f;
@@ -294,6 +587,29 @@ __global__ __launch_bounds__(64 * kVbWaves) void reduce_vb_kernel(const float* _
 
 constexpr int kFwdPF = 8;
 constexpr int kBwdPF = 6;
+constexpr int kFwdLinCH = 12;
+constexpr int kBwdLinCH = 8;
+
+// Waves per workgroup of the chunked scans: enough chunks that the launch
+// holds about 4096 waves (4 per SIMD), at most 16 per workgroup and no more
+// chunks than the sequence has steps.
+int lin_waves(const ScanShape& s, int ch) {
+  const int groups = (s.B * s.ndir * s.d + 63) / 64;
+  int nw = 1;
+  while (nw < kLinMaxWaves && groups * nw * 2 <= 4096 && nw * ch < s.L) nw *= 2;
+  return nw;
+}
+
+template <int KB, bool MASK, bool STORE_C, bool STORE_HB>
+hipError_t fwd_lin_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st) {
+  const int grid = (s.B * s.ndir * s.d + 63) / 64;
+  const int nw = lin_waves(s, kFwdLinCH);
+  timing_before("scan_fwd", st);
+  hipLaunchKernelGGL((scan_fwd_lin_kernel<KB, MASK, STORE_C, STORE_HB, kFwdLinCH>), dim3(grid),
+                     dim3(64 * nw), 0, st, s, a);
+  timing_after(st);
+  return hipGetLastError();
+}
 
 template <int KB, bool MASK, bool STORE_C, bool STORE_HB>
 hipError_t fwd_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st) {
@@ -312,6 +628,13 @@ hipError_t fwd_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st
 
 template <int KB, bool MASK>
 hipError_t fwd_dispatch_c(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st) {
+  if (s.linear) {
+    if (a.Hb)
+      return a.C ? fwd_lin_dispatch<KB, MASK, true, true>(s, a, st)
+                 : fwd_lin_dispatch<KB, MASK, false, true>(s, a, st);
+    return a.C ? fwd_lin_dispatch<KB, MASK, true, false>(s, a, st)
+               : fwd_lin_dispatch<KB, MASK, false, false>(s, a, st);
+  }
   if (a.Hb)
     return a.C ? fwd_dispatch<KB, MASK, true, true>(s, a, st)
                : fwd_dispatch<KB, MASK, false, true>(s, a, st);
@@ -324,7 +647,16 @@ hipError_t bwd_dispatch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t st
   const int lanes = s.B * s.ndir * s.d;
   const int grid = (lanes + kScanThreads - 1) / kScanThreads;
   timing_before("scan_bwd", st);
-  if (a.du_bf16 && s.reset_new)
+  if (s.linear) {
+    const int g = (lanes + 63) / 64;
+    const int nw = lin_waves(s, kBwdLinCH);
+    if (a.du_bf16)
+      hipLaunchKernelGGL((scan_bwd_lin_kernel<KB, MASK, true, kBwdLinCH>), dim3(g), dim3(64 * nw),
+                         0, st, s, a);
+    else
+      hipLaunchKernelGGL((scan_bwd_lin_kernel<KB, MASK, false, kBwdLinCH>), dim3(g),
+                         dim3(64 * nw), 0, st, s, a);
+  } else if (a.du_bf16 && s.reset_new)
     hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, true, true, kBwdPF>), dim3(grid),
                        dim3(kScanThreads), 0, st, s, a);
   else if (a.du_bf16)
@@ -359,10 +691,11 @@ hipError_t scan_backward_launch(const ScanShape& s, const ScanBwdArgs& a, hipStr
   else e = m ? bwd_dispatch<4, true>(s, a, st) : bwd_dispatch<4, false>(s, a, st);
   if (e != hipSuccess) return e;
   const int nfeat = s.ndir * s.d;
-  const int grid = (4 * nfeat + 63) / 64;
+  const int qlo = s.linear ? 2 : 0;
+  const int grid = ((4 - qlo) * nfeat + 63) / 64;
   timing_before("reduce_vb", st);
   hipLaunchKernelGGL(reduce_vb_kernel, dim3(grid), dim3(64 * kVbWaves), 0, st, a.partial, s.B,
-                     nfeat, a.dv_f, a.dv_r, a.db_f, a.db_r);
+                     nfeat, qlo, a.dv_f, a.dv_r, a.db_f, a.db_r);
   timing_after(st);
   return hipGetLastError();
 }

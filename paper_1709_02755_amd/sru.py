@@ -61,19 +61,24 @@ class SruError(RuntimeError):
 
 
 RESET_PREV, RESET_NEW = 0, 1
+RECURRENCE_GATED, RECURRENCE_LINEAR = 0, 1
 
 
 class Options(ctypes.Structure):
-    """sru_options: highway_scale (alpha, Sec. 3.2) and reset_state
-    (RESET_PREV: Eq. 3; RESET_NEW: Algorithm 1's order)."""
-    _fields_ = [("highway_scale", ctypes.c_float), ("reset_state", ctypes.c_int)]
+    """sru_options: highway_scale (alpha, Sec. 3.2), reset_state
+    (RESET_PREV: Eq. 3; RESET_NEW: Algorithm 1's order) and recurrence
+    (RECURRENCE_LINEAR: v * c removed from both gates, ablation (1) of
+    Sec. 4.5; v_f, v_r may then be None and have no gradient)."""
+    _fields_ = [("highway_scale", ctypes.c_float), ("reset_state", ctypes.c_int),
+                ("recurrence", ctypes.c_int)]
 
 
-def _options(highway_scale=1.0, reset_new=False):
+def _options(highway_scale=1.0, reset_new=False, linear=False):
     """NULL for Eq. 1-4 as printed, else a pointer to an sru_options."""
-    if highway_scale == 1.0 and not reset_new:
+    if highway_scale == 1.0 and not reset_new and not linear:
         return None
-    return ctypes.byref(Options(float(highway_scale), RESET_NEW if reset_new else RESET_PREV))
+    return ctypes.byref(Options(float(highway_scale), RESET_NEW if reset_new else RESET_PREV,
+                                RECURRENCE_LINEAR if linear else RECURRENCE_GATED))
 
 
 def highway_scale_for_bias(b):
@@ -147,7 +152,9 @@ def _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask):
         raise ValueError(f"W shape {tuple(W.shape)} does not fit d_in={d_in}, direction={direction}")
     _req(X, "X", (L, B, d_in))
     _req(W, "W", (ndir, k, d, d_in))
-    for n, t in (("v_f", v_f), ("v_r", v_r), ("b_f", b_f), ("b_r", b_r)):
+    for n, t in (("v_f", v_f), ("v_r", v_r)):
+        _req(t, n, (ndir, d), optional=True)  # the library reports a missing v
+    for n, t in (("b_f", b_f), ("b_r", b_r)):
         _req(t, n, (ndir, d))
     _req(c0, "c0", (B, ndir * d), optional=True)
     _req(mask, "mask", (L, B), dtype=torch.uint8, optional=True)
@@ -168,7 +175,7 @@ def workspace(nbytes, device):
 
 def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
             gemm_dtype=GEMM_FP32, store_c=True, out=None, ws=None, X_bf16=None,
-            highway_scale=1.0, reset_new=False):
+            highway_scale=1.0, reset_new=False, linear=False):
     """One layer forward; returns dict(U, H, C, c_last) (C None without store_c).
 
     bf16 GEMMs only: X_bf16 (torch.bfloat16, X rounded) replaces the
@@ -187,7 +194,7 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
         ws = workspace(need, dev)
     st = lib().sru_forward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                            L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
-                           _options(highway_scale, reset_new),
+                           _options(highway_scale, reset_new, linear),
                            _ptr(out["U"]), _ptr(out["H"]), _ptr(out.get("C")),
                            _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("W_bf16")),
                            _ptr(out.get("H_bf16")), _ptr(ws), need if ws is not None else 0,
@@ -198,7 +205,7 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
 
 def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, direction=DIR_FWD,
              mask=None, gemm_dtype=GEMM_FP32, want_dc0=True, out=None, ws=None, X_bf16=None,
-             W_bf16=None, highway_scale=1.0, reset_new=False):
+             W_bf16=None, highway_scale=1.0, reset_new=False, linear=False):
     """One layer backward; returns dict(dX, dW, dv_f, dv_r, db_f, db_r, dc0).
 
     bf16 GEMMs only: X_bf16 / W_bf16 (bfloat16 roundings of X and Wcat, as
@@ -213,7 +220,8 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
     dev = X.device
     if out is None:
         out = dict(dX=torch.empty_like(X), dW=torch.empty_like(W),
-                   dv_f=torch.empty((ndir, d), device=dev), dv_r=torch.empty((ndir, d), device=dev),
+                   dv_f=None if linear else torch.empty((ndir, d), device=dev),
+                   dv_r=None if linear else torch.empty((ndir, d), device=dev),
                    db_f=torch.empty((ndir, d), device=dev), db_r=torch.empty((ndir, d), device=dev),
                    dc0=torch.empty((B, ndir * d), device=dev) if want_dc0 else None)
     need = backward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype)
@@ -221,9 +229,9 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
         ws = workspace(need, dev)
     st = lib().sru_backward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                             L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
-                            _options(highway_scale, reset_new),
+                            _options(highway_scale, reset_new, linear),
                             _ptr(U), _ptr(C), _ptr(dH), _ptr(dc_last),
-                            _ptr(out["dX"]), _ptr(out["dW"]), _ptr(out["dv_f"]), _ptr(out["dv_r"]),
+                            _ptr(out["dX"]), _ptr(out["dW"]), _ptr(out.get("dv_f")), _ptr(out.get("dv_r")),
                             _ptr(out["db_f"]), _ptr(out["db_r"]), _ptr(out.get("dc0")),
                             _ptr(X_bf16), _ptr(W_bf16), _ptr(ws), ws.numel(), _stream())
     _check(st, "sru_backward")
@@ -232,7 +240,7 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
 
 def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
                     gemm_dtype=GEMM_FP32, store_c=True, out=None, ws=None, highway_scale=1.0,
-                    reset_new=False):
+                    reset_new=False, linear=False):
     """Layer with Wcat = P Q^T (Sec. 4.4); Q [d_in, dp], P [ndir, k, d, dp].
     Returns dict(T, U, H, C, c_last); T = X Q is needed by the backward."""
     L, B, d_in = X.shape
@@ -240,7 +248,9 @@ def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mas
     _req(X, "X", (L, B, d_in))
     _req(Q, "Q", (d_in, dp))
     _req(P, "P", (ndir, k, d, dp))
-    for n, t in (("v_f", v_f), ("v_r", v_r), ("b_f", b_f), ("b_r", b_r)):
+    for n, t in (("v_f", v_f), ("v_r", v_r)):
+        _req(t, n, (ndir, d), optional=True)
+    for n, t in (("b_f", b_f), ("b_r", b_r)):
         _req(t, n, (ndir, d))
     _req(c0, "c0", (B, ndir * d), optional=True)
     _req(mask, "mask", (L, B), dtype=torch.uint8, optional=True)
@@ -256,7 +266,7 @@ def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mas
         ws = workspace(need, dev)
     st = lib().sru_forward_lowrank(_ptr(X), _ptr(Q), _ptr(P), _ptr(v_f), _ptr(v_r), _ptr(b_f),
                                    _ptr(b_r), _ptr(c0), L, B, d_in, d, dp, direction, _ptr(mask),
-                                   gemm_dtype, _options(highway_scale, reset_new), _ptr(out["T"]),
+                                   gemm_dtype, _options(highway_scale, reset_new, linear), _ptr(out["T"]),
                                    _ptr(out["U"]), _ptr(out["H"]), _ptr(out.get("C")),
                                    _ptr(out.get("c_last")), _ptr(ws),
                                    need if ws is not None else 0, _stream())
@@ -266,7 +276,7 @@ def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mas
 
 def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, T, U, C, dH, c0=None, dc_last=None,
                      direction=DIR_FWD, mask=None, gemm_dtype=GEMM_FP32, want_dc0=True, out=None,
-                     ws=None, highway_scale=1.0, reset_new=False):
+                     ws=None, highway_scale=1.0, reset_new=False, linear=False):
     """Backward of forward_lowrank; returns dict(dX, dQ, dP, dv_f, dv_r, db_f,
     db_r, dc0)."""
     L, B, d_in = X.shape
@@ -279,7 +289,8 @@ def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, T, U, C, dH, c0=None, dc_last=
     dev = X.device
     if out is None:
         out = dict(dX=torch.empty_like(X), dQ=torch.empty_like(Q), dP=torch.empty_like(P),
-                   dv_f=torch.empty((ndir, d), device=dev), dv_r=torch.empty((ndir, d), device=dev),
+                   dv_f=None if linear else torch.empty((ndir, d), device=dev),
+                   dv_r=None if linear else torch.empty((ndir, d), device=dev),
                    db_f=torch.empty((ndir, d), device=dev), db_r=torch.empty((ndir, d), device=dev),
                    dc0=torch.empty((B, ndir * d), device=dev) if want_dc0 else None)
     need = lib().sru_backward_lowrank_workspace_bytes(L, B, d_in, d, dp, direction, gemm_dtype)
@@ -287,10 +298,10 @@ def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, T, U, C, dH, c0=None, dc_last=
         ws = workspace(need, dev)
     st = lib().sru_backward_lowrank(_ptr(X), _ptr(Q), _ptr(P), _ptr(v_f), _ptr(v_r), _ptr(b_f),
                                     _ptr(b_r), _ptr(c0), L, B, d_in, d, dp, direction,
-                                    _ptr(mask), gemm_dtype, _options(highway_scale, reset_new),
+                                    _ptr(mask), gemm_dtype, _options(highway_scale, reset_new, linear),
                                     _ptr(T), _ptr(U), _ptr(C), _ptr(dH), _ptr(dc_last),
                                     _ptr(out["dX"]), _ptr(out["dQ"]), _ptr(out["dP"]),
-                                    _ptr(out["dv_f"]), _ptr(out["dv_r"]), _ptr(out["db_f"]),
+                                    _ptr(out.get("dv_f")), _ptr(out.get("dv_r")), _ptr(out["db_f"]),
                                     _ptr(out["db_r"]), _ptr(out.get("dc0")), _ptr(ws),
                                     ws.numel(), _stream())
     _check(st, "sru_backward_lowrank")
@@ -315,7 +326,7 @@ def gemm(op, A, B, M, N, K, gemm_dtype=GEMM_FP32, C=None, ws=None):
 
 
 def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
-                 store_c=True, out=None, highway_scale=1.0, reset_new=False):
+                 store_c=True, out=None, highway_scale=1.0, reset_new=False, linear=False):
     L, B, ndir, k, d = U.shape
     d_in = X.shape[2] if X is not None else (d if k == 3 else -1)
     if k == 4 and X is None:
@@ -328,7 +339,7 @@ def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None
                    c_last=torch.empty((B, ndir * d), device=dev))
     st = lib().sru_scan_forward(_ptr(U), _ptr(X), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r),
                                 _ptr(c0), L, B, d_in, d, direction, _ptr(mask),
-                                _options(highway_scale, reset_new),
+                                _options(highway_scale, reset_new, linear),
                                 _ptr(out["H"]), _ptr(out.get("C")), _ptr(out.get("c_last")),
                                 _ptr(out.get("H_bf16")), _stream())
     _check(st, "sru_scan_forward")
@@ -336,7 +347,8 @@ def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None
 
 
 def scan_backward(U, X, C, dH, v_f, v_r, b_f, b_r, c0=None, dc_last=None, direction=DIR_FWD,
-                  mask=None, d_in=None, out=None, ws=None, highway_scale=1.0, reset_new=False):
+                  mask=None, d_in=None, out=None, ws=None, highway_scale=1.0, reset_new=False,
+                  linear=False):
     L, B, ndir, k, d = U.shape
     if d_in is None:
         d_in = X.shape[2] if X is not None else d
@@ -344,7 +356,8 @@ def scan_backward(U, X, C, dH, v_f, v_r, b_f, b_r, c0=None, dc_last=None, direct
     if out is None:
         out = dict(dU=torch.empty_like(U),
                    dxh=torch.empty((L, B, ndir, d), device=dev) if k == 3 else None,
-                   dv_f=torch.empty((ndir, d), device=dev), dv_r=torch.empty((ndir, d), device=dev),
+                   dv_f=None if linear else torch.empty((ndir, d), device=dev),
+                   dv_r=None if linear else torch.empty((ndir, d), device=dev),
                    db_f=torch.empty((ndir, d), device=dev), db_r=torch.empty((ndir, d), device=dev),
                    dc0=torch.empty((B, ndir * d), device=dev))
     need = lib().sru_scan_backward_workspace_bytes(L, B, d_in, d, direction)
@@ -353,9 +366,9 @@ def scan_backward(U, X, C, dH, v_f, v_r, b_f, b_r, c0=None, dc_last=None, direct
     st = lib().sru_scan_backward(_ptr(U), _ptr(X), _ptr(C), _ptr(dH), _ptr(dc_last),
                                  _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                                  L, B, d_in, d, direction, _ptr(mask),
-                                 _options(highway_scale, reset_new),
-                                 _ptr(out["dU"]), _ptr(out.get("dxh")), _ptr(out["dv_f"]),
-                                 _ptr(out["dv_r"]), _ptr(out["db_f"]), _ptr(out["db_r"]),
+                                 _options(highway_scale, reset_new, linear),
+                                 _ptr(out["dU"]), _ptr(out.get("dxh")), _ptr(out.get("dv_f")),
+                                 _ptr(out.get("dv_r")), _ptr(out["db_f"]), _ptr(out["db_r"]),
                                  _ptr(out.get("dc0")), _ptr(ws), ws.numel(), _stream())
     _check(st, "sru_scan_backward")
     return out
@@ -374,9 +387,9 @@ class Stack:
     """
 
     def __init__(self, layers, L, B, d_in, d, direction, gemm_dtype, device, backward=True,
-                 highway_scale=1.0, reset_new=False, store_c=True):
+                 highway_scale=1.0, reset_new=False, store_c=True, linear=False):
         self.layers = layers
-        self.variant = dict(highway_scale=highway_scale, reset_new=reset_new)
+        self.variant = dict(highway_scale=highway_scale, reset_new=reset_new, linear=linear)
         self.L, self.B, self.d, self.direction, self.gemm_dtype = L, B, d, direction, gemm_dtype
         ndir = 2 if direction == DIR_BI else 1
         self.ndir = ndir
@@ -405,8 +418,8 @@ class Stack:
             self.fw.append(o)
             if backward:
                 g = dict(dX=torch.empty((L, B, din), device=device),
-                         dv_f=torch.empty((ndir, d), device=device),
-                         dv_r=torch.empty((ndir, d), device=device),
+                         dv_f=None if linear else torch.empty((ndir, d), device=device),
+                         dv_r=None if linear else torch.empty((ndir, d), device=device),
                          db_f=torch.empty((ndir, d), device=device),
                          db_r=torch.empty((ndir, d), device=device), dc0=None)
                 if low:

@@ -49,6 +49,7 @@ class Workload:
     seed: int
     store_c: bool = True    # keep every state C (False: inference, no backward)
     dp: int | None = None   # projection rank: Wcat = P Q^T (Sec. 4.4), else dense
+    linear: bool = False    # v * c removed from both gates (ablation (1), Sec. 4.5)
 
     @property
     def ndir(self) -> int:
@@ -67,7 +68,10 @@ class Workload:
 # The five workloads of the build target (sizes and distributions as stated
 # there), then the inference shape of the SRU that replaces a Transformer's
 # feed-forward layer (Sec. 4.3: d_model = 512 in, d_sru = 2048, batches of
-# about 5120 tokens; forward only, no C); seeds are the workload index.
+# about 5120 tokens; forward only, no C), the 6-layer stack with the
+# projection trick, and workload 2 with the linear recurrence; seeds are
+# the workload index.  The linear workload still draws v_f, v_r (same draw
+# order as the others); nothing reads them.
 WORKLOADS = [
     Workload("sru1_L32_B4_d128_fp32_fwd", 1, DIR_FWD, 32, 4, 128, 128,
              GEMM_FP32, False, None, False, 0),
@@ -84,6 +88,10 @@ WORKLOADS = [
     # the headline stack with the projection trick at the paper's rank 512
     Workload("sru6_L256_B64_d1024_dp512_bf16", 6, DIR_FWD, 256, 64, 1024, 1024,
              GEMM_BF16, True, None, True, 6, dp=512),
+    # the question-answering shape of workload 2 without the v * c terms: the
+    # recurrence is linear in c, so its scans also run parallel over time
+    Workload("bisru3_L400_B32_d128_fp32_masked_linear", 3, DIR_BI, 400, 32, 128, 128,
+             GEMM_FP32, True, 200, False, 7, linear=True),
 ]
 
 
@@ -96,7 +104,7 @@ def scaled(w: Workload, *, L=None, B=None, d=None, layers=None, name=None) -> Wo
     dp = None if w.dp is None else max(8, (w.dp * d) // w.d)
     return Workload(name or f"{w.name}@L{L}_B{B or w.B}_d{d}", layers or w.layers,
                     w.direction, L, B or w.B, d_in, d, w.gemm_dtype, w.backward,
-                    len_lo, w.bf_uniform, w.seed, w.store_c, dp)
+                    len_lo, w.bf_uniform, w.seed, w.store_c, dp, w.linear)
 
 
 def lengths_to_mask(lengths: np.ndarray, L: int) -> np.ndarray:

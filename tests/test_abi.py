@@ -184,6 +184,30 @@ def test_valid_options_pass_validation():
     assert abs(sru.highway_scale_for_bias(0.0) - 3.0 ** 0.5) < 1e-15
 
 
+@pytest.mark.parametrize("recurrence", [2, -1])
+def test_invalid_recurrence_rejected(recurrence):
+    lib = sru.lib()
+    bad = ctypes.byref(sru.Options(1.0, sru.RESET_PREV, recurrence))
+    assert _fwd(lib, opts=bad) == E_FLAG
+    assert _bwd(lib, opts=bad) == E_FLAG
+
+
+def test_linear_recurrence_needs_no_v():
+    """Ablation (1) has no v: v_f, v_r, dv_f, dv_r may be NULL (the calls go
+    on to the next check); the gated recurrence still requires them."""
+    lib = sru.lib()
+    lin = ctypes.byref(sru.Options(1.0, sru.RESET_PREV, sru.RECURRENCE_LINEAR))
+    assert _fwd(lib, opts=lin, v_f=None, v_r=None, H=FAKE_MIS) == E_ALIGN
+    assert _bwd(lib, opts=lin, v_f=None, v_r=None, dv_f=None, dv_r=None) == E_WS
+    assert _fwd(lib, v_f=None, v_r=None) == E_NULL
+    assert _bwd(lib, dv_r=None) == E_NULL
+    assert lib.sru_scan_forward(FAKE, FAKE, None, None, FAKE, FAKE, None, 4, 2, 8, 8, 0, None,
+                                lin, FAKE_MIS, None, None, None, None) == E_ALIGN
+    args = [FAKE, FAKE, FAKE, FAKE, None, None, None, FAKE, FAKE, None, 4, 2, 8, 8, 0, None,
+            lin, FAKE, FAKE, None, None, FAKE, FAKE, None, None, 0, None]
+    assert lib.sru_scan_backward(*args) == E_WS
+
+
 def test_lowrank_argument_checks():
     lib = sru.lib()
     f = lib.sru_forward_lowrank
