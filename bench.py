@@ -127,11 +127,12 @@ def kernel_work(w, splits, bf16):
         "scan_bwd": dict(bytes=elems * (24.0 + du_b * k + (4.0 if k == 3 else 0.0))),
         "reduce_vb": dict(bytes=4.0 * (nq * w.B * nfeat + nq * nfeat)),
         "splitk_reduce": dict(bytes=4.0 * (splits + 1) * N * K),
-        # fp32 -> bf16 copies of the product operands: Wcat, X (first layer),
-        # and Wcat^T where dX cannot read Wcat row-contiguous
+        # fp32 -> bf16 copies of the product operands: Wcat, X (first layer);
+        # Wcat^T for dX, transposed from the forward's bf16 Wcat (the stack
+        # hands it over: 2 B read, 2 B written per element)
         "bf16_w": dict(bytes=(4.0 + 2.0) * N * K),
         "bf16_x": dict(bytes=(4.0 + 2.0) * M * K),
-        "bf16_wt": dict(bytes=(4.0 + 2.0) * N * K),
+        "bf16_wt": dict(bytes=(2.0 + 2.0) * N * K),
         **low,
     }
 

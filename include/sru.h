@@ -162,7 +162,8 @@ SRU_API int sru_forward(const float* X, const float* W,
  *        [ndir, d], dc0 [B, ndir*d] (NULL = do not compute).
  *   bf16 companions (SRU_GEMM_BF16 only, else NULL; each may be NULL; as
  *   in sru_forward): X_bf16 = X rounded to bf16; W_bf16 = Wcat rounded to
- *   bf16 (the W_bf16 sru_forward wrote).  NULL: rounded into the workspace.
+ *   bf16 (the W_bf16 sru_forward wrote; the dX product reads its transposed
+ *   copy, made in the workspace).  NULL: rounded into the workspace.
  */
 SRU_API int sru_backward(const float* X, const float* W,
                  const float* v_f, const float* v_r, const float* b_f, const float* b_r,

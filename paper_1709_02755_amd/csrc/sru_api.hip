@@ -143,7 +143,7 @@ sru::GemmDesc dw_desc(const Dims& s, bool bf16, const void* dU, const void* X, f
 
 // Backward workspace layout:
 //   [dU (fp32, or bf16 in bf16 mode) | dxh (k = 3) | v/b partials |
-//    Wcat (or Wcat^T) and X in bf16 (bf16 mode) | dW split partials]
+//    Wcat^T and X in bf16 (bf16 mode) | dW split partials]
 struct BwdLayout {
   size_t dU, dxh, partial, wt, xb, splitk, total;
   int splits;
@@ -415,25 +415,18 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
     return e;
 
   // 2. dX = dU Wcat (+ the highway gradient of every direction when k = 3).
-  //    bf16 mode: Wcat in bf16 (W_bf16, or rounded into the workspace) read
-  //    row-contiguous by the direct kernel; where that path does not apply,
-  //    Wcat^T is rounded into the workspace and the product is an NT one.
+  //    bf16 mode: Wcat^T rounded to bf16 into the workspace (a transposed
+  //    copy of W_bf16 when the caller holds it, else rounded from W), so
+  //    both operands are K-contiguous: the product then runs at the speed
+  //    of the projection, faster than with Wcat read row-contiguous.
   sru::GemmDesc gx;
   if (bf16) {
-    gx = gemm_desc(SRU_OP_NN, true, (int)s.M, d_in, (int)s.N, dU, s.N, W_bf16 ? W_bf16 : wt,
-                   d_in, dX, d_in);
+    const hipError_t te = W_bf16
+        ? sru::to_bf16_t_launch(W_bf16, true, (int)s.N, d_in, wt, stream, "bf16_wt")
+        : sru::to_bf16_t_launch(W, false, (int)s.N, d_in, wt, stream, "bf16_wt");
+    if (int e = hip_status(te)) return e;
+    gx = gemm_desc(SRU_OP_NT, true, (int)s.M, d_in, (int)s.N, dU, s.N, wt, s.N, dX, d_in);
     gx.a_bf16 = gx.b_bf16 = true;
-    if (sru::gemm_is_direct(gx)) {
-      if (!W_bf16) {
-        if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wt, false, stream, "bf16_w")))
-          return e;
-      }
-    } else {
-      if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wt, true, stream, "bf16_wt")))
-        return e;
-      gx = gemm_desc(SRU_OP_NT, true, (int)s.M, d_in, (int)s.N, dU, s.N, wt, s.N, dX, d_in);
-      gx.a_bf16 = gx.b_bf16 = true;
-    }
   } else {
     gx = gemm_desc(SRU_OP_NN, false, (int)s.M, d_in, (int)s.N, dU, s.N, W, d_in, dX, d_in);
   }

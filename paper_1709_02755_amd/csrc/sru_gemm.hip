@@ -806,20 +806,69 @@ __global__ __launch_bounds__(256) void to_bf16_kernel(const float* __restrict__ 
 }
 
 // Transposed: dst[c*rows + r] = bf16(src[r*cols + c]) through a 64x64 LDS tile.
-__global__ __launch_bounds__(256) void to_bf16_t_kernel(const float* __restrict__ src, int rows,
+// Source element as fp32: fp32 as is, bf16 (raw bits) widened exactly.
+__device__ __forceinline__ float src_f32(float v) { return v; }
+__device__ __forceinline__ float src_f32(uint16_t v) {
+  return __builtin_bit_cast(float, (unsigned)v << 16);
+}
+
+template <class S>
+__global__ __launch_bounds__(256) void to_bf16_t_kernel(const S* __restrict__ src, int rows,
                                                         int cols, uint16_t* __restrict__ dst) {
   __shared__ float tile[64][65];
   const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   for (int i = ty; i < 64; i += 4) {
     const int r = r0 + i, c = c0 + tx;
-    tile[i][tx] = (r < rows && c < cols) ? src[(long long)r * cols + c] : 0.f;
+    tile[i][tx] = (r < rows && c < cols) ? src_f32(src[(long long)r * cols + c]) : 0.f;
   }
   __syncthreads();
   for (int i = ty; i < 64; i += 4) {
     const int c = c0 + i, r = r0 + tx;
     if (c < cols && r < rows)
       dst[(long long)c * rows + r] = __builtin_bit_cast(uint16_t, (__bf16)tile[tx][i]);
+  }
+}
+
+// The same for whole 64 x 64 tiles with 16-byte accesses on both sides: each
+// lane loads 16 bytes of a source row (4 fp32 or 8 bf16 elements) into the
+// LDS tile, then packs 8 elements of a tile column into one 16-byte segment
+// of an output row.  With the row pitch of 65 floats both the row writes and
+// the column reads of the tile hit 64 distinct banks.
+template <class S>
+__global__ __launch_bounds__(256) void to_bf16_t_tiled_kernel(const S* __restrict__ src, int rows,
+                                                              int cols, uint16_t* __restrict__ dst) {
+  __shared__ float tile[64][65];
+  constexpr int E = 16 / (int)sizeof(S);  // source elements per 16-byte load
+  constexpr int TPR = 64 / E;             // lanes per tile row
+  constexpr int RPR = 256 / TPR;          // tile rows per pass
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int t = threadIdx.x;
+  const int lc = (t % TPR) * E;
+  for (int i = t / TPR; i < 64; i += RPR) {
+    const S* row = src + (long long)(r0 + i) * cols + c0 + lc;
+    if constexpr (sizeof(S) == 4) {
+      // loaded as floats: a bit cast of a vector element would read element 0
+      const floatx4 v = *reinterpret_cast<const floatx4*>(row);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) tile[i][lc + w] = v[w];
+    } else {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(row);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const unsigned x = v[w];
+        tile[i][lc + 2 * w] = __builtin_bit_cast(float, x << 16);
+        tile[i][lc + 2 * w + 1] = __builtin_bit_cast(float, x & 0xFFFF0000u);
+      }
+    }
+  }
+  __syncthreads();
+  const int q = t & 7;  // 8-element segment of the output row
+  for (int c = t >> 3; c < 64; c += 32) {
+    u32x4 w;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w[j] = pack_bf16(tile[8 * q + 2 * j][c], tile[8 * q + 2 * j + 1][c]);
+    *reinterpret_cast<u32x4*>(dst + (long long)(c0 + c) * rows + r0 + 8 * q) = w;
   }
 }
 
@@ -1078,12 +1127,32 @@ hipError_t gemm_launch(const GemmDesc& g, hipStream_t st) {
   return g.bf16 ? launch_layout<CfgBF16>(g, st) : launch_layout<CfgF32>(g, st);
 }
 
+template <class S>
+void launch_transpose(const S* src, int rows, int cols, uint16_t* dst, hipStream_t st) {
+  const dim3 grid((cols + 63) / 64, (rows + 63) / 64);
+  const bool tiled = rows % 64 == 0 && cols % 64 == 0 &&
+                     (reinterpret_cast<uintptr_t>(src) & 15) == 0 &&
+                     (reinterpret_cast<uintptr_t>(dst) & 15) == 0;
+  if (tiled)
+    hipLaunchKernelGGL(to_bf16_t_tiled_kernel<S>, grid, dim3(256), 0, st, src, rows, cols, dst);
+  else
+    hipLaunchKernelGGL(to_bf16_t_kernel<S>, grid, dim3(256), 0, st, src, rows, cols, dst);
+}
+
+hipError_t to_bf16_t_launch(const void* src, bool src_bf16, int rows, int cols, uint16_t* dst,
+                            hipStream_t st, const char* label) {
+  timing_before(label, st);
+  if (src_bf16) launch_transpose(static_cast<const uint16_t*>(src), rows, cols, dst, st);
+  else launch_transpose(static_cast<const float*>(src), rows, cols, dst, st);
+  timing_after(st);
+  return hipGetLastError();
+}
+
 hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, bool transpose,
                           hipStream_t st, const char* label) {
   timing_before(label, st);
   if (transpose) {
-    dim3 grid((cols + 63) / 64, (rows + 63) / 64);
-    hipLaunchKernelGGL(to_bf16_t_kernel, grid, dim3(256), 0, st, src, rows, cols, dst);
+    launch_transpose(src, rows, cols, dst, st);
   } else {
     const long long n = (long long)rows * cols;
     const long long threads = (n + 7) / 8;
