@@ -93,7 +93,7 @@ def kernel_work(w, splits, bf16):
     elems = M * nfeat
     du_b = 2.0 if bf16 else 4.0
     nq = 2 if w.linear else 4  # v/b sums per feature (no v in the linear variant)
-    hb = 2.0 * (w.layers - 1) / w.layers if bf16 and w.dp is None else 0.0  # bf16 copy of H
+    hb = 2.0 * (w.layers - 1) / w.layers if bf16 else 0.0  # bf16 copy of H (not the top's)
     if w.dp is not None:  # low-rank layers: Wcat = P Q^T, rank dp
         dp = w.dp
         low = {
@@ -104,10 +104,8 @@ def kernel_work(w, splits, bf16):
             "gemm_dp": dict(flops=2.0 * N * dp * M),   # dP = dU^T T
             "gemm_dq": dict(flops=2.0 * K * dp * M),   # dQ = X^T dT
             "bf16_x": dict(bytes=(4.0 + 2.0) * M * K),
-            "bf16_q": dict(bytes=(4.0 + 2.0) * K * dp),
-            "bf16_p": dict(bytes=(4.0 + 2.0) * N * dp),
-            "bf16_t": dict(bytes=(4.0 + 2.0) * M * dp),
-            "bf16_dt": dict(bytes=(4.0 + 2.0) * M * dp),
+            "bf16_q": dict(bytes=(4.0 + 2.0) * K * dp),   # Q, or Q^T
+            "bf16_p": dict(bytes=(4.0 + 2.0) * N * dp),   # P, or P^T
             "splitk_reduce": dict(),  # two reductions of different sizes: time only
         }
     else:
@@ -354,7 +352,7 @@ def main():
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {tokens_per_s:.4g} tokens/s")
 
     # --- per-kernel durations: the library brackets each launch with events
-    per_step = w.layers * 16  # upper bound on kernels per layer and step
+    per_step = w.layers * 32  # upper bound on kernels per layer and step
     ev = HipEvents(2 * per_step * args.profile_steps + 2)
     lib = sru.lib()
     lib.sru_timing_begin(ev.events, ev.n)
@@ -364,6 +362,8 @@ def main():
     finally:
         nk = lib.sru_timing_end()
     torch.cuda.synchronize()
+    if 2 * nk + 2 > ev.n:  # the hook ran out of events: the counts would be short
+        raise RuntimeError(f"per-launch timing ran out of events ({nk} kernels)")
     agg = {}
     for i in range(nk):
         lab = lib.sru_timing_label(i).decode()

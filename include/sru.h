@@ -188,6 +188,11 @@ SRU_API int sru_backward(const float* X, const float* W,
  * bf16 mode rounds the operands of each product (X and Q, T and P, dU and
  * P, dT and Q, dU and T, X and dT), and needs d_in, dp and ndir*k*d to be
  * multiples of 8 (else SRU_E_SHAPE).  Workspace as queried.
+ * bf16 companions (SRU_GEMM_BF16 only, else NULL; each may be NULL; as for
+ * sru_forward / sru_backward): X_bf16 [M, d_in] in -- X rounded to bf16
+ * (e.g. the H_bf16 of the layer below); T_bf16 [M, dp] -- out of the
+ * forward (T rounded to bf16, written with T), in to the backward (it must
+ * be that rounding of T); H_bf16 [L, B, ndir*d] out -- H rounded to bf16.
  */
 SRU_API size_t sru_forward_lowrank_workspace_bytes(int L, int B, int d_in, int d, int dp,
                                                    int direction, int gemm_dtype);
@@ -198,6 +203,7 @@ SRU_API int sru_forward_lowrank(const float* X, const float* Q, const float* P,
                         const float* c0, int L, int B, int d_in, int d, int dp, int direction,
                         const uint8_t* pad_mask, int gemm_dtype, const sru_options* options,
                         float* T, float* U, float* H, float* C, float* c_last,
+                        const uint16_t* X_bf16, uint16_t* T_bf16, uint16_t* H_bf16,
                         void* workspace, size_t workspace_bytes, hipStream_t stream);
 SRU_API int sru_backward_lowrank(const float* X, const float* Q, const float* P,
                          const float* v_f, const float* v_r, const float* b_f, const float* b_r,
@@ -206,6 +212,7 @@ SRU_API int sru_backward_lowrank(const float* X, const float* Q, const float* P,
                          const float* T, const float* U, const float* C, const float* dH,
                          const float* dc_last, float* dX, float* dQ, float* dP,
                          float* dv_f, float* dv_r, float* db_f, float* db_r, float* dc0,
+                         const uint16_t* X_bf16, const uint16_t* T_bf16,
                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------

@@ -172,25 +172,29 @@ BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
 
 // ---------------------------------------------------------------- low rank
 // Wcat = P Q^T (Sec. 4.4).  Products, with M = L*B, N = ndir*k*d, dp = d':
-//   forward : T = X Q (NN, K = d_in), U = T P^T (NT, K = dp)
-//   backward: dT = dU P (NN, K = N), dX = dT Q^T (NT, K = dp; + highway),
+//   forward : T = X Q (K = d_in), U = T P^T (NT, K = dp)
+//   backward: dT = dU P (K = N), dX = dT Q^T (NT, K = dp; + highway),
 //             dP = dU^T T (TN, K = M), dQ = X^T dT (TN, K = M)
-// In bf16 mode every operand is rounded into the workspace, so each product
-// runs on the direct kernel; that needs whole 16-byte chunks.
+// fp32 mode runs T and dT as NN products.  bf16 mode rounds every operand
+// (into the workspace unless the caller holds the copy) and runs each
+// product on the direct kernel, which needs whole 16-byte chunks: T and dT
+// as NT products on transposed bf16 copies of Q and P (K-contiguous, like
+// the projection), T written in fp32 and bf16 at once, dT in bf16 only
+// (only its rounding is ever read).
 bool lowrank_dims_ok(const Dims& s, int dp, int gemm_dtype) {
   if (gemm_dtype != SRU_GEMM_BF16) return true;
   return s.d_in % 8 == 0 && dp % 8 == 0 && s.N % 8 == 0;
 }
 
 struct LrFwdLayout {
-  size_t xb, qb, tb, pb, total;
+  size_t xb, qt, tb, pb, total;
 };
 LrFwdLayout lr_fwd_layout(const Dims& s, int dp, int gemm_dtype) {
   LrFwdLayout w{};
   if (gemm_dtype != SRU_GEMM_BF16) return w;
   size_t off = 0;
   w.xb = off; off += align_up(2 * (size_t)s.M * s.d_in);
-  w.qb = off; off += align_up(2 * (size_t)s.d_in * dp);
+  w.qt = off; off += align_up(2 * (size_t)s.d_in * dp);  // Q^T [dp, d_in]
   w.tb = off; off += align_up(2 * (size_t)s.M * dp);
   w.pb = off; off += align_up(2 * (size_t)s.N * dp);
   w.total = off;
@@ -214,7 +218,7 @@ sru::GemmDesc lr_dq_desc(const Dims& s, int dp, bool bf16, const void* X, const 
 }
 
 struct LrBwdLayout {
-  size_t dU, dxh, partial, dT, pb, qb, tb, xb, dtb, splitk, total;
+  size_t dU, dxh, partial, dT, pt, qb, tb, xb, dtb, splitk, total;
   int splits_p, splits_q;
 };
 LrBwdLayout lr_bwd_layout(const Dims& s, int dp, int gemm_dtype) {
@@ -224,9 +228,9 @@ LrBwdLayout lr_bwd_layout(const Dims& s, int dp, int gemm_dtype) {
   w.dU = off; off += align_up((bf16 ? 2 : 4) * (size_t)s.M * s.N);
   w.dxh = off; if (s.k == 3) off += align_up(4 * (size_t)s.M * s.nfeat);
   w.partial = off; off += align_up(16 * (size_t)s.B * s.nfeat);
-  w.dT = off; off += align_up(4 * (size_t)s.M * dp);
+  w.dT = off; if (!bf16) off += align_up(4 * (size_t)s.M * dp);  // bf16: dT in bf16 only
   if (bf16) {
-    w.pb = off; off += align_up(2 * (size_t)s.N * dp);
+    w.pt = off; off += align_up(2 * (size_t)s.N * dp);  // P^T [dp, N]
     w.qb = off; off += align_up(2 * (size_t)s.d_in * dp);
     w.tb = off; off += align_up(2 * (size_t)s.M * dp);
     w.xb = off; off += align_up(2 * (size_t)s.M * s.d_in);
@@ -555,8 +559,9 @@ int sru_forward_lowrank(const float* X, const float* Q, const float* P, const fl
                         const float* v_r, const float* b_f, const float* b_r, const float* c0,
                         int L, int B, int d_in, int d, int dp, int direction,
                         const uint8_t* pad_mask, int gemm_dtype, const sru_options* options,
-                        float* T, float* U, float* H, float* C, float* c_last, void* workspace,
-                        size_t workspace_bytes, hipStream_t stream) {
+                        float* T, float* U, float* H, float* C, float* c_last,
+                        const uint16_t* X_bf16, uint16_t* T_bf16, uint16_t* H_bf16,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
   Dims s;
   int st = make_dims(L, B, d_in, d, direction, s);
   if (st != SRU_OK) return st;
@@ -570,6 +575,7 @@ int sru_forward_lowrank(const float* X, const float* Q, const float* P, const fl
   const void* ptrs[] = {X, Q, P, v_f, v_r, b_f, b_r, c0, T, U, H, C, c_last};
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
+  if (int e = check_bf16_side(gemm_dtype, {X_bf16, T_bf16, H_bf16})) return e;
   const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
   const LrFwdLayout lay = lr_fwd_layout(s, dp, gemm_dtype);
   if (lay.total > 0) {
@@ -582,30 +588,42 @@ int sru_forward_lowrank(const float* X, const float* Q, const float* P, const fl
     return hip_status(sru::to_bf16_launch(src, rows, cols, dst, false, stream, label));
   };
 
-  // T = X Q
-  if (bf16) {
-    if (int e = round(X, (int)s.M, d_in, bf(lay.xb), "bf16_x")) return e;
-    if (int e = round(Q, d_in, dp, bf(lay.qb), "bf16_q")) return e;
-  }
-  sru::GemmDesc gt = gemm_desc(SRU_OP_NN, bf16, (int)s.M, dp, d_in,
-                               bf16 ? (const void*)bf(lay.xb) : X, d_in,
-                               bf16 ? (const void*)bf(lay.qb) : Q, dp, T, dp);
-  gt.a_bf16 = gt.b_bf16 = bf16;
-  gt.label = "gemm_t";
-  if (int e = hip_status(sru::gemm_launch(gt, stream))) return e;
-  // U = T P^T
-  if (bf16) {
-    if (int e = round(T, (int)s.M, dp, bf(lay.tb), "bf16_t")) return e;
+  if (!bf16) {
+    // T = X Q, U = T P^T
+    sru::GemmDesc gt = gemm_desc(SRU_OP_NN, false, (int)s.M, dp, d_in, X, d_in, Q, dp, T, dp);
+    gt.label = "gemm_t";
+    if (int e = hip_status(sru::gemm_launch(gt, stream))) return e;
+    sru::GemmDesc gu = gemm_desc(SRU_OP_NT, false, (int)s.M, (int)s.N, dp, T, dp, P, dp, U, s.N);
+    gu.label = "gemm_u";
+    if (int e = hip_status(sru::gemm_launch(gu, stream))) return e;
+  } else {
+    // T = X Q as X (Q^T)^T: both operands K-contiguous; T in fp32 and bf16
+    const uint16_t* xb = X_bf16;
+    if (!xb) {
+      if (int e = round(X, (int)s.M, d_in, bf(lay.xb), "bf16_x")) return e;
+      xb = bf(lay.xb);
+    }
+    if (int e = hip_status(sru::to_bf16_t_launch(Q, false, d_in, dp, bf(lay.qt), stream,
+                                                 "bf16_q")))
+      return e;
+    uint16_t* tb = T_bf16 ? T_bf16 : bf(lay.tb);
+    sru::GemmDesc gt = gemm_desc(SRU_OP_NT, true, (int)s.M, dp, d_in, xb, d_in, bf(lay.qt), d_in,
+                                 T, dp);
+    gt.a_bf16 = gt.b_bf16 = true;
+    gt.Cb = tb;
+    gt.ldcb = dp;
+    gt.label = "gemm_t";
+    if (int e = hip_status(sru::gemm_launch(gt, stream))) return e;
+    // U = T P^T
     if (int e = round(P, (int)s.N, dp, bf(lay.pb), "bf16_p")) return e;
+    sru::GemmDesc gu = gemm_desc(SRU_OP_NT, true, (int)s.M, (int)s.N, dp, tb, dp, bf(lay.pb), dp,
+                                 U, s.N);
+    gu.a_bf16 = gu.b_bf16 = true;
+    gu.label = "gemm_u";
+    if (int e = hip_status(sru::gemm_launch(gu, stream))) return e;
   }
-  sru::GemmDesc gu = gemm_desc(SRU_OP_NT, bf16, (int)s.M, (int)s.N, dp,
-                               bf16 ? (const void*)bf(lay.tb) : T, dp,
-                               bf16 ? (const void*)bf(lay.pb) : P, dp, U, s.N);
-  gu.a_bf16 = gu.b_bf16 = bf16;
-  gu.label = "gemm_u";
-  if (int e = hip_status(sru::gemm_launch(gu, stream))) return e;
 
-  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, nullptr};
+  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16};
   return hip_status(sru::scan_forward_launch(scan_shape(s, direction, op), a, stream));
 }
 
@@ -615,7 +633,8 @@ int sru_backward_lowrank(const float* X, const float* Q, const float* P, const f
                          const uint8_t* pad_mask, int gemm_dtype, const sru_options* options,
                          const float* T, const float* U, const float* C, const float* dH,
                          const float* dc_last, float* dX, float* dQ, float* dP, float* dv_f,
-                         float* dv_r, float* db_f, float* db_r, float* dc0, void* workspace,
+                         float* dv_r, float* db_f, float* db_r, float* dc0,
+                         const uint16_t* X_bf16, const uint16_t* T_bf16, void* workspace,
                          size_t workspace_bytes, hipStream_t stream) {
   Dims s;
   int st = make_dims(L, B, d_in, d, direction, s);
@@ -632,6 +651,7 @@ int sru_backward_lowrank(const float* X, const float* Q, const float* P, const f
                         dv_r, db_f, db_r, dc0};
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
+  if (int e = check_bf16_side(gemm_dtype, {X_bf16, T_bf16})) return e;
   const LrBwdLayout lay = lr_bwd_layout(s, dp, gemm_dtype);
   if (!workspace || workspace_bytes < lay.total) return SRU_E_WORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
@@ -644,9 +664,10 @@ int sru_backward_lowrank(const float* X, const float* Q, const float* P, const f
   float* partial = reinterpret_cast<float*>(ws + lay.partial);
   float* dT = reinterpret_cast<float*>(ws + lay.dT);
   float* splitk = reinterpret_cast<float*>(ws + lay.splitk);
-  sru::GemmDesc gp = lr_dp_desc(s, dp, bf16, dU, bf16 ? (const void*)bf(lay.tb) : T, dP);
-  sru::GemmDesc gq = lr_dq_desc(s, dp, bf16, bf16 ? (const void*)bf(lay.xb) : X,
-                                bf16 ? (const void*)bf(lay.dtb) : dT, dQ);
+  const void* tb = !bf16 ? static_cast<const void*>(T) : T_bf16 ? T_bf16 : bf(lay.tb);
+  const void* xb = !bf16 ? static_cast<const void*>(X) : X_bf16 ? X_bf16 : bf(lay.xb);
+  sru::GemmDesc gp = lr_dp_desc(s, dp, bf16, dU, tb, dP);
+  sru::GemmDesc gq = lr_dq_desc(s, dp, bf16, xb, bf16 ? (const void*)bf(lay.dtb) : dT, dQ);
   gp.partials = gq.partials = splitk;
   // the split partials were sized for these plans: refuse before enqueueing
   if (sru::gemm_splits(gp) > lay.splits_p || sru::gemm_splits(gq) > lay.splits_q)
@@ -660,18 +681,24 @@ int sru_backward_lowrank(const float* X, const float* Q, const float* P, const f
                      pad_mask, dU, bf16, dxh, partial, dc0, dv_f, dv_r, db_f, db_r};
   if (int e = hip_status(sru::scan_backward_launch(scan_shape(s, direction, op), a, stream)))
     return e;
-  // 2. dT = dU P
+  // 2. dT = dU P (bf16: as dU (P^T)^T, written in bf16 only)
+  sru::GemmDesc gd;
   if (bf16) {
-    if (int e = round(P, (int)s.N, dp, bf(lay.pb), "bf16_p")) return e;
+    if (int e = hip_status(sru::to_bf16_t_launch(P, false, (int)s.N, dp, bf(lay.pt), stream,
+                                                 "bf16_p")))
+      return e;
+    gd = gemm_desc(SRU_OP_NT, true, (int)s.M, dp, (int)s.N, dU, s.N, bf(lay.pt), s.N, nullptr,
+                   dp);
+    gd.a_bf16 = gd.b_bf16 = true;
+    gd.Cb = bf(lay.dtb);
+    gd.ldcb = dp;
+  } else {
+    gd = gemm_desc(SRU_OP_NN, false, (int)s.M, dp, (int)s.N, dU, s.N, P, dp, dT, dp);
   }
-  sru::GemmDesc gd = gemm_desc(SRU_OP_NN, bf16, (int)s.M, dp, (int)s.N, dU, s.N,
-                               bf16 ? (const void*)bf(lay.pb) : P, dp, dT, dp);
-  gd.a_bf16 = gd.b_bf16 = bf16;
   gd.label = "gemm_dt";
   if (int e = hip_status(sru::gemm_launch(gd, stream))) return e;
   // 3. dX = dT Q^T (+ the highway gradient of every direction when k = 3)
   if (bf16) {
-    if (int e = round(dT, (int)s.M, dp, bf(lay.dtb), "bf16_dt")) return e;
     if (int e = round(Q, d_in, dp, bf(lay.qb), "bf16_q")) return e;
   }
   sru::GemmDesc gx = gemm_desc(SRU_OP_NT, bf16, (int)s.M, d_in, dp,
@@ -687,11 +714,11 @@ int sru_backward_lowrank(const float* X, const float* Q, const float* P, const f
   }
   if (int e = hip_status(sru::gemm_launch(gx, stream))) return e;
   // 4. dP = dU^T T, 5. dQ = X^T dT (reductions over all tokens)
-  if (bf16) {
+  if (bf16 && !T_bf16) {
     if (int e = round(T, (int)s.M, dp, bf(lay.tb), "bf16_t")) return e;
   }
   if (int e = hip_status(sru::gemm_launch(gp, stream))) return e;
-  if (bf16) {
+  if (bf16 && !X_bf16) {
     if (int e = round(X, (int)s.M, d_in, bf(lay.xb), "bf16_x")) return e;
   }
   return hip_status(sru::gemm_launch(gq, stream));

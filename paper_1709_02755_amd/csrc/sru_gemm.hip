@@ -272,6 +272,8 @@ struct KernelArgs {
   long long add_ld, add_off;
   int add_count;
   int vec_out;  // output (and addend) rows allow 16-byte accesses: see write_tile_rows
+  uint16_t* outb;  // bf16 copy of the result (direct kernel, OB), out may be nullptr
+  long long ldob;
 };
 
 // Epilogue shared by the kernels.  32x32 accumulator layout: element e of
@@ -318,12 +320,60 @@ __device__ __forceinline__ void write_tile_add(const KernelArgs& g,
 // group of four elements is four consecutive columns of one row, written
 // (and its addend read) as one 16-byte access when the tile lies wholly
 // inside the output and vec_out holds (16-byte aligned rows).
-template <class C, int ADD>
+// OB: also (or, when g.out is null, only) write the bf16 rounding of the
+// result to g.outb (four columns as one 8-byte store); no addend then.
+template <class C, int ADD, bool OB = false>
 __device__ __forceinline__ void write_tile_rows(const KernelArgs& g,
                                                 const floatx16 (&acc)[C::FM][C::FN], int m0,
                                                 int n0, int wm0, int wn0, int lane, int split) {
-  float* out = g.out + (long long)split * g.split_stride;
+  static_assert(!OB || ADD == 0, "the bf16 result takes no addend");
+  float* out = g.out ? g.out + (long long)split * g.split_stride : nullptr;
   const int cl = 4 * (lane >> 5);
+  if constexpr (OB) {
+    if (g.vec_out && m0 + C::BM <= g.M && n0 + C::BN <= g.N) {
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i) {
+        const int m = m0 + wm0 + i * 32 + (lane & 31);
+        const long long col = n0 + wn0 + cl;
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float a0 = acc[i][j][4 * q], a1 = acc[i][j][4 * q + 1];
+            const float a2 = acc[i][j][4 * q + 2], a3 = acc[i][j][4 * q + 3];
+            u32x2 w;
+            w[0] = pack_bf16(a0, a1);
+            w[1] = pack_bf16(a2, a3);
+            *reinterpret_cast<u32x2*>(g.outb + m * g.ldob + col + j * 32 + 8 * q) = w;
+            if (out) {
+              floatx4 v;
+              v[0] = a0;
+              v[1] = a1;
+              v[2] = a2;
+              v[3] = a3;
+              *reinterpret_cast<floatx4*>(out + m * g.ldo + col + j * 32 + 8 * q) = v;
+            }
+          }
+      }
+      return;
+    }
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j) {
+        const int m = m0 + wm0 + i * 32 + (lane & 31);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int n = n0 + wn0 + j * 32 + 8 * (e >> 2) + cl + (e & 3);
+          if (m < g.M && n < g.N) {
+            const float v = acc[i][j][e];
+            g.outb[(long long)m * g.ldob + n] = __builtin_bit_cast(uint16_t, (__bf16)v);
+            if (out) out[(long long)m * g.ldo + n] = v;
+          }
+        }
+      }
+    return;
+  }
   if (g.vec_out && m0 + C::BM <= g.M && n0 + C::BN <= g.N) {
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -541,6 +591,7 @@ struct DCfg {
 using DirectTall = DCfg<256, 128, 32, 2, 2, 3>;  // 4 waves, 2 workgroups per CU
 using DirectWide = DCfg<256, 256, 32, 2, 4, 4>;  // 8 waves, 1 workgroup per CU
 using DirectLine = DCfg<256, 256, 64, 2, 4, 2>;  // 8 waves, whole-line loads
+using DirectNarrow = DCfg<256, 128, 64, 2, 2, 2>;  // 4 waves, whole-line loads, half the columns
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_t;
@@ -621,7 +672,7 @@ struct DirectOperand {
   }
 };
 
-template <class C, int ADD, bool A_RC, bool B_RC>
+template <class C, int ADD, bool A_RC, bool B_RC, bool OB>
 __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelArgs g) {
   constexpr int STAGES = C::STAGES;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
@@ -754,12 +805,12 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
       mfmas(f[sl & 1]);
     }
   }
-  write_tile_rows<C, ADD>(g, acc, m0, n0, wm0, wn0, lane, ti.split);
+  write_tile_rows<C, ADD, OB>(g, acc, m0, n0, wm0, wn0, lane, ti.split);
 }
 
-template <class C, int ADD, bool A_RC, bool B_RC>
+template <class C, int ADD, bool A_RC, bool B_RC, bool OB = false>
 void launch_direct(const KernelArgs& a, int nwg, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_direct_kernel<C, ADD, A_RC, B_RC>), dim3(nwg), dim3(C::THREADS), 0, st,
+  hipLaunchKernelGGL((gemm_direct_kernel<C, ADD, A_RC, B_RC, OB>), dim3(nwg), dim3(C::THREADS), 0, st,
                      a);
 }
 
@@ -1003,25 +1054,41 @@ int direct_splits_cfg(const GemmDesc& g) {
 }
 
 using CfgDirect = DirectLine;
+// K-contiguous products whose 256 x 256 tiles would leave CUs idle (N of a
+// few hundred, e.g. the rank-dp products of the projection trick) use
+// 256 x 128 tiles: twice the workgroups.
+using CfgNarrow = DirectNarrow;
 
 int direct_splits(const GemmDesc& g) { return direct_splits_cfg<CfgDirect>(g); }
 
+bool use_narrow(const GemmDesc& g) {
+  if (!g.a_kc || !g.b_kc || g.add_count != 0) return false;
+  const long long tiles = (long long)((g.M + CfgDirect::BM - 1) / CfgDirect::BM) *
+                          ((g.N + CfgDirect::BN - 1) / CfgDirect::BN);
+  return tiles < 256;
+}
+
 // Explicit instantiations: the host pass did not emit the launch stubs of
 // every specialisation referenced through launch_direct_cfg.
-#define SRU_DIRECT_INST(ADD, ARC, BRC) \
-  template __global__ void gemm_direct_kernel<CfgDirect, ADD, ARC, BRC>(KernelArgs);
-SRU_DIRECT_INST(0, false, false)
-SRU_DIRECT_INST(1, false, false)
-SRU_DIRECT_INST(2, false, false)
-SRU_DIRECT_INST(0, true, true)
-SRU_DIRECT_INST(1, true, true)
-SRU_DIRECT_INST(2, true, true)
-SRU_DIRECT_INST(0, false, true)
-SRU_DIRECT_INST(1, false, true)
-SRU_DIRECT_INST(2, false, true)
+#define SRU_DIRECT_INST(CFG, ADD, ARC, BRC, OB) \
+  template __global__ void gemm_direct_kernel<CFG, ADD, ARC, BRC, OB>(KernelArgs);
+SRU_DIRECT_INST(CfgDirect, 0, false, false, false)
+SRU_DIRECT_INST(CfgDirect, 1, false, false, false)
+SRU_DIRECT_INST(CfgDirect, 2, false, false, false)
+SRU_DIRECT_INST(CfgDirect, 0, true, true, false)
+SRU_DIRECT_INST(CfgDirect, 1, true, true, false)
+SRU_DIRECT_INST(CfgDirect, 2, true, true, false)
+SRU_DIRECT_INST(CfgDirect, 0, false, true, false)
+SRU_DIRECT_INST(CfgDirect, 1, false, true, false)
+SRU_DIRECT_INST(CfgDirect, 2, false, true, false)
+SRU_DIRECT_INST(CfgDirect, 0, false, false, true)
+SRU_DIRECT_INST(CfgNarrow, 0, false, false, false)
+SRU_DIRECT_INST(CfgNarrow, 1, false, false, false)  // referenced by the launcher's
+SRU_DIRECT_INST(CfgNarrow, 2, false, false, false)  // addend switch, never launched
+SRU_DIRECT_INST(CfgNarrow, 0, false, false, true)
 #undef SRU_DIRECT_INST
 
-template <class C, bool A_RC, bool B_RC>
+template <class C, bool A_RC, bool B_RC, bool OB = false>
 hipError_t launch_direct_cfg(const GemmDesc& g, hipStream_t st) {
   const int splits = direct_splits_cfg<C>(g);
   const int kt = (g.K + C::BK - 1) / C::BK;
@@ -1053,11 +1120,15 @@ hipError_t launch_direct_cfg(const GemmDesc& g, hipStream_t st) {
     a.add_off = g.add_off;
   }
   auto al16 = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
-  a.vec_out = a.ldo % 4 == 0 && a.split_stride % 4 == 0 && al16(a.out) &&
-              (a.add_count == 0 || (a.add_ld % 4 == 0 && a.add_off % 4 == 0 && al16(a.add)));
+  a.outb = g.Cb;
+  a.ldob = g.ldcb;
+  a.vec_out = a.ldo % 4 == 0 && a.split_stride % 4 == 0 && (!a.out || al16(a.out)) &&
+              (a.add_count == 0 || (a.add_ld % 4 == 0 && a.add_off % 4 == 0 && al16(a.add))) &&
+              (!OB || (a.ldob % 4 == 0 && ((uintptr_t)a.outb & 7) == 0));
   const int nwg = a.tiles_m * a.tiles_n * splits;
   timing_before(g.label ? g.label : !g.b_kc ? (g.a_kc ? "gemm_nn" : "gemm_tn") : "gemm_nt", st);
-  if (a.add_count == 2) launch_direct<C, 2, A_RC, B_RC>(a, nwg, st);
+  if constexpr (OB) launch_direct<C, 0, A_RC, B_RC, true>(a, nwg, st);
+  else if (a.add_count == 2) launch_direct<C, 2, A_RC, B_RC>(a, nwg, st);
   else if (a.add_count == 1) launch_direct<C, 1, A_RC, B_RC>(a, nwg, st);
   else launch_direct<C, 0, A_RC, B_RC>(a, nwg, st);
   timing_after(st);
@@ -1120,10 +1191,18 @@ size_t gemm_partial_bytes(int M, int N, int splits) {
 hipError_t gemm_launch(const GemmDesc& g, hipStream_t st) {
   if ((g.a_bf16 || g.b_bf16) && !g.bf16) return hipErrorInvalidValue;
   if (direct_ok(g)) {
+    if (g.Cb) {
+      // bf16 result: K-contiguous operands, no addend (never split)
+      if (!g.a_kc || !g.b_kc || g.add_count != 0) return hipErrorInvalidValue;
+      return use_narrow(g) ? launch_direct_cfg<CfgNarrow, false, false, true>(g, st)
+                           : launch_direct_cfg<CfgDirect, false, false, true>(g, st);
+    }
     if (!g.a_kc) return launch_direct_cfg<CfgDirect, true, true>(g, st);
     if (!g.b_kc) return launch_direct_cfg<CfgDirect, false, true>(g, st);
+    if (use_narrow(g)) return launch_direct_cfg<CfgNarrow, false, false>(g, st);
     return launch_direct_cfg<CfgDirect, false, false>(g, st);
   }
+  if (g.Cb) return hipErrorInvalidValue;  // a bf16 result needs the direct path
   return g.bf16 ? launch_layout<CfgBF16>(g, st) : launch_layout<CfgF32>(g, st);
 }
 

@@ -34,6 +34,11 @@ struct GemmDesc {
   const float* add;
   long long add_ld, add_off;
   int add_count;
+  // Optional bf16 (RNE) copy of the result, row pitch ldcb; C may then be
+  // nullptr (bf16 result only).  Direct path only, both operands
+  // K-contiguous, no addend, no split; ldcb % 4 == 0, 8-byte aligned.
+  uint16_t* Cb;
+  long long ldcb;
   const char* label;  // name for the measurement hook (nullptr: by layout)
 };
 

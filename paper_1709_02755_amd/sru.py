@@ -47,9 +47,10 @@ _SIGNATURES = {
     "sru_scan_backward": (_I, [_P] * 10 + [_I] * 5 + [_P, _P] + [_P] * 7 + [_P, _S, _P]),
     "sru_forward_lowrank_workspace_bytes": (_S, [_I] * 7),
     "sru_backward_lowrank_workspace_bytes": (_S, [_I] * 7),
-    "sru_forward_lowrank": (_I, [_P] * 8 + [_I] * 6 + [_P, _I, _P] + [_P] * 5 + [_P, _S, _P]),
+    "sru_forward_lowrank": (_I, [_P] * 8 + [_I] * 6 + [_P, _I, _P] + [_P] * 5 + [_P] * 3
+                            + [_P, _S, _P]),
     "sru_backward_lowrank": (_I, [_P] * 8 + [_I] * 6 + [_P, _I, _P] + [_P] * 5 + [_P] * 8
-                             + [_P, _S, _P]),
+                             + [_P] * 2 + [_P, _S, _P]),
     "sru_timing_begin": (_I, [_P, _I]),
     "sru_timing_end": (_I, []),
     "sru_timing_label": (ctypes.c_char_p, [_I]),
@@ -240,9 +241,13 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
 
 def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
                     gemm_dtype=GEMM_FP32, store_c=True, out=None, ws=None, highway_scale=1.0,
-                    reset_new=False, linear=False):
+                    reset_new=False, linear=False, X_bf16=None):
     """Layer with Wcat = P Q^T (Sec. 4.4); Q [d_in, dp], P [ndir, k, d, dp].
-    Returns dict(T, U, H, C, c_last); T = X Q is needed by the backward."""
+    Returns dict(T, U, H, C, c_last); T = X Q is needed by the backward.
+
+    bf16 GEMMs only: X_bf16 replaces the rounding of X; entries T_bf16 /
+    H_bf16 of `out` (bfloat16 tensors), if present, receive T and H rounded
+    to bf16."""
     L, B, d_in = X.shape
     ndir, k, d, dp = P.shape
     _req(X, "X", (L, B, d_in))
@@ -268,7 +273,8 @@ def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mas
                                    _ptr(b_r), _ptr(c0), L, B, d_in, d, dp, direction, _ptr(mask),
                                    gemm_dtype, _options(highway_scale, reset_new, linear), _ptr(out["T"]),
                                    _ptr(out["U"]), _ptr(out["H"]), _ptr(out.get("C")),
-                                   _ptr(out.get("c_last")), _ptr(ws),
+                                   _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("T_bf16")),
+                                   _ptr(out.get("H_bf16")), _ptr(ws),
                                    need if ws is not None else 0, _stream())
     _check(st, "sru_forward_lowrank")
     return out
@@ -276,9 +282,11 @@ def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mas
 
 def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, T, U, C, dH, c0=None, dc_last=None,
                      direction=DIR_FWD, mask=None, gemm_dtype=GEMM_FP32, want_dc0=True, out=None,
-                     ws=None, highway_scale=1.0, reset_new=False, linear=False):
+                     ws=None, highway_scale=1.0, reset_new=False, linear=False, X_bf16=None,
+                     T_bf16=None):
     """Backward of forward_lowrank; returns dict(dX, dQ, dP, dv_f, dv_r, db_f,
-    db_r, dc0)."""
+    db_r, dc0).  bf16 GEMMs only: X_bf16 / T_bf16 (the roundings of X and T,
+    as forward_lowrank writes them) replace the library's own rounding."""
     L, B, d_in = X.shape
     ndir, k, d, dp = P.shape
     _req(T, "T", (L, B, dp))
@@ -302,8 +310,8 @@ def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, T, U, C, dH, c0=None, dc_last=
                                     _ptr(T), _ptr(U), _ptr(C), _ptr(dH), _ptr(dc_last),
                                     _ptr(out["dX"]), _ptr(out["dQ"]), _ptr(out["dP"]),
                                     _ptr(out.get("dv_f")), _ptr(out.get("dv_r")), _ptr(out["db_f"]),
-                                    _ptr(out["db_r"]), _ptr(out.get("dc0")), _ptr(ws),
-                                    ws.numel(), _stream())
+                                    _ptr(out["db_r"]), _ptr(out.get("dc0")), _ptr(X_bf16),
+                                    _ptr(T_bf16), _ptr(ws), ws.numel(), _stream())
     _check(st, "sru_backward_lowrank")
     return out
 
@@ -380,10 +388,11 @@ class Stack:
 
     `layers` holds per-layer dicts of GPU tensors v_f, v_r, b_f, b_r and
     either W (dense) or Q, P (the low-rank projection, Wcat = P Q^T).
-    With bf16 GEMMs each dense layer's forward also writes bf16 copies of
-    Wcat and (below the top layer) H: the next layer's projection and every
-    backward product read those instead of rounding X and W again.  Without
-    a backward pass, store_c=False skips the states C (inference).
+    With bf16 GEMMs each layer's forward also writes bf16 copies of H (below
+    the top layer) and of Wcat (dense) or T (low-rank): the next layer's
+    projection and the backward products read those instead of rounding the
+    same values again.  Without a backward pass, store_c=False skips the
+    states C (inference).
     """
 
     def __init__(self, layers, L, B, d_in, d, direction, gemm_dtype, device, backward=True,
@@ -405,16 +414,16 @@ class Stack:
                      H=torch.empty((L, B, ndir * d), device=device),
                      C=torch.empty((L, B, ndir * d), device=device) if keep_c else None,
                      c_last=torch.empty((B, ndir * d), device=device))
+            bf = dict(dtype=torch.bfloat16, device=device)
             if low:
                 dp = p["Q"].shape[1]
                 o["T"] = torch.empty((L, B, dp), device=device)
+                if gemm_dtype == GEMM_BF16:
+                    o["T_bf16"] = torch.empty((L, B, dp), **bf)
             elif gemm_dtype == GEMM_BF16:
-                o["W_bf16"] = torch.empty(tuple(p["W"].shape), dtype=torch.bfloat16,
-                                          device=device)
-                nxt = layers[li + 1] if li + 1 < len(layers) else None
-                if nxt is not None and "Q" not in nxt:  # the next dense layer's operand
-                    o["H_bf16"] = torch.empty((L, B, ndir * d), dtype=torch.bfloat16,
-                                              device=device)
+                o["W_bf16"] = torch.empty(tuple(p["W"].shape), **bf)
+            if gemm_dtype == GEMM_BF16 and li + 1 < len(layers):
+                o["H_bf16"] = torch.empty((L, B, ndir * d), **bf)  # the next layer's operand
             self.fw.append(o)
             if backward:
                 g = dict(dX=torch.empty((L, B, din), device=device),
@@ -446,7 +455,8 @@ class Stack:
             v = (p["v_f"], p["v_r"], p["b_f"], p["b_r"], None, self.direction, mask,
                  self.gemm_dtype)
             if "Q" in p:
-                forward_lowrank(x, p["Q"], p["P"], *v, out=o, ws=self.ws, **self.variant)
+                forward_lowrank(x, p["Q"], p["P"], *v, out=o, ws=self.ws, X_bf16=xb,
+                                **self.variant)
             else:
                 forward(x, p["W"], *v, out=o, ws=self.ws, X_bf16=xb, **self.variant)
             x, xb = o["H"], o.get("H_bf16")
@@ -458,12 +468,12 @@ class Stack:
             p, o, b = self.layers[li], self.fw[li], self.bw[li]
             x = X if li == 0 else self.fw[li - 1]["H"]
             v = (p["v_f"], p["v_r"], p["b_f"], p["b_r"])
+            xb = None if li == 0 else self.fw[li - 1].get("H_bf16")
             if "Q" in p:
                 backward_lowrank(x, p["Q"], p["P"], *v, o["T"], o["U"], o["C"], g, None, None,
                                  self.direction, mask, self.gemm_dtype, want_dc0=False, out=b,
-                                 ws=self.ws, **self.variant)
+                                 ws=self.ws, X_bf16=xb, T_bf16=o.get("T_bf16"), **self.variant)
             else:
-                xb = None if li == 0 else self.fw[li - 1].get("H_bf16")
                 backward(x, p["W"], *v, o["U"], o["C"], g, None, None, self.direction, mask,
                          self.gemm_dtype, want_dc0=False, out=b, ws=self.ws, X_bf16=xb,
                          W_bf16=o.get("W_bf16"), **self.variant)

@@ -213,11 +213,14 @@ def test_lowrank_argument_checks():
     f = lib.sru_forward_lowrank
 
     def fwd(**kw):
-        a = dict(L=4, B=2, d_in=8, d=8, dp=8, direction=0, gemm=0, T=FAKE, ws=None, ws_bytes=0)
+        a = dict(L=4, B=2, d_in=8, d=8, dp=8, direction=0, gemm=0, T=FAKE, Xb=None, Tb=None,
+                 Hb=None, ws=None, ws_bytes=0)
         a.update(kw)
         return f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, a["L"], a["B"], a["d_in"], a["d"],
                  a["dp"], a["direction"], None, a["gemm"], None, a["T"], FAKE, FAKE, FAKE, None,
-                 a["ws"], a["ws_bytes"], None)
+                 a["Xb"], a["Tb"], a["Hb"], a["ws"], a["ws_bytes"], None)
+    assert fwd(Tb=FAKE) == E_FLAG              # bf16 companions need bf16 products
+    assert fwd(gemm=1, Tb=ctypes.c_void_p(0x10008)) == E_ALIGN  # 16-byte aligned
     assert fwd(dp=0) == E_SHAPE
     assert fwd(gemm=1, dp=6) == E_SHAPE        # bf16 products need dp % 8 == 0
     assert fwd(gemm=1, d_in=12) == E_SHAPE
@@ -228,3 +231,9 @@ def test_lowrank_argument_checks():
     assert fwd(gemm=1) == E_WS
     assert lib.sru_backward_lowrank_workspace_bytes(4, 2, 8, 8, 8, 0, 0) > 0
     assert lib.sru_backward_lowrank_workspace_bytes(4, 2, 8, 8, 0, 0, 0) == 0
+    b = lib.sru_backward_lowrank
+    args = [FAKE] * 7 + [None, 4, 2, 8, 8, 8, 0, None, 0, None] + [FAKE] * 4 + [None] + \
+        [FAKE] * 7 + [None] + [FAKE, None, None, 0, None]
+    assert b(*args) == E_FLAG                   # X_bf16 with fp32 products
+    args[-5] = None
+    assert b(*args) == E_WS

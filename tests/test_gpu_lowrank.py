@@ -68,3 +68,85 @@ def test_lowrank_bf16_rejects_unaligned_rank():
     z = torch.zeros((1, d), device="cuda")
     with pytest.raises(sru.SruError, match="SHAPE"):
         sru.forward_lowrank(X, Q, P, z, z, z, z, gemm_dtype=O.GEMM_BF16)
+
+
+@pytest.mark.parametrize("direction,d_in,d,dp", [(O.DIR_FWD, 256, 256, 64),
+                                                 (O.DIR_BI, 128, 64, 40)])
+def test_lowrank_companions_bit_identical(direction, d_in, d, dp):
+    """bf16 products: the copies forward_lowrank writes (T_bf16, H_bf16) are
+    exactly the RNE roundings of T and H, and handing X_bf16 / T_bf16 to the
+    calls gives bit-identical results to letting the library round."""
+    L, B = 37, 5
+    print(f"lowrank companions dir={direction} d_in={d_in} d={d} dp={dp}", flush=True)
+    rng = np.random.default_rng(dp)
+    c = random_layer_case(rng, L, B, d_in, d, direction, masked=True, c0=True, dc_last=True,
+                          bias_scale=0.5)
+    ndir, k = c["W"].shape[:2]
+    Q = dev((rng.uniform(-1, 1, (d_in, dp)) * np.sqrt(3.0 / d_in)).astype(np.float32))
+    P = dev((rng.uniform(-1, 1, (ndir, k, d, dp)) * np.sqrt(3.0 / dp)).astype(np.float32))
+    p = [dev(c[key]) for key in ("v_f", "v_r", "b_f", "b_r")]
+    X = dev(c["X"])
+    kw = dict(c0=dev(c["c0"]), direction=direction, mask=dev(c["mask"]), gemm_dtype=O.GEMM_BF16)
+    bits = lambda t: t.contiguous().view(torch.int16)
+    fw0 = sru.forward_lowrank(X, Q, P, *p, **kw)
+    out = dict(T=torch.empty((L, B, dp), device="cuda"),
+               U=torch.empty((L, B, ndir, k, d), device="cuda"),
+               H=torch.empty((L, B, ndir * d), device="cuda"),
+               C=torch.empty((L, B, ndir * d), device="cuda"),
+               c_last=torch.empty((B, ndir * d), device="cuda"),
+               T_bf16=torch.empty((L, B, dp), dtype=torch.bfloat16, device="cuda"),
+               H_bf16=torch.empty((L, B, ndir * d), dtype=torch.bfloat16, device="cuda"))
+    fw1 = sru.forward_lowrank(X, Q, P, *p, out=out, X_bf16=X.to(torch.bfloat16), **kw)
+    torch.cuda.synchronize()
+    for key in ("T", "U", "H", "C", "c_last"):
+        assert torch.equal(fw0[key], fw1[key]), key
+    assert torch.equal(bits(fw1["T_bf16"]), bits(fw1["T"].to(torch.bfloat16)))
+    assert torch.equal(bits(fw1["H_bf16"]), bits(fw1["H"].to(torch.bfloat16)))
+    args = (fw0["T"], fw0["U"], fw0["C"], dev(c["dH"]))
+    bkw = dict(kw, dc_last=dev(c["dc_last"]))
+    bw0 = sru.backward_lowrank(X, Q, P, *p, *args, **bkw)
+    bw1 = sru.backward_lowrank(X, Q, P, *p, *args, X_bf16=X.to(torch.bfloat16),
+                               T_bf16=fw1["T_bf16"], **bkw)
+    torch.cuda.synchronize()
+    for key in bw0:
+        if bw0[key] is not None:
+            assert torch.equal(bw0[key], bw1[key]), key
+
+
+def test_lowrank_stack_wiring_equals_plain_calls():
+    """The Stack hands each layer's H_bf16 and T_bf16 on; its results equal
+    per-layer calls that round everything themselves."""
+    L, B, d, dp, nl = 24, 6, 128, 64, 3
+    rng = np.random.default_rng(9)
+    layers = []
+    for _ in range(nl):
+        layers.append(dict(
+            Q=dev((rng.uniform(-1, 1, (d, dp)) * np.sqrt(3.0 / d)).astype(np.float32)),
+            P=dev((rng.uniform(-1, 1, (1, 3, d, dp)) * np.sqrt(3.0 / dp)).astype(np.float32)),
+            v_f=dev(rng.uniform(-0.5, 0.5, (1, d)).astype(np.float32)),
+            v_r=dev(rng.uniform(-0.5, 0.5, (1, d)).astype(np.float32)),
+            b_f=dev(rng.uniform(-1, 1, (1, d)).astype(np.float32)),
+            b_r=dev(np.zeros((1, d), np.float32))))
+    X = dev(rng.standard_normal((L, B, d)).astype(np.float32))
+    dH = dev(rng.standard_normal((L, B, d)).astype(np.float32))
+    st = sru.Stack(layers, L, B, d, d, O.DIR_FWD, O.GEMM_BF16, "cuda")
+    st.forward(X)
+    st.backward(X, dH)
+    xs, fws = [X], []
+    for p in layers:
+        v = (p["v_f"], p["v_r"], p["b_f"], p["b_r"])
+        fws.append(sru.forward_lowrank(xs[-1], p["Q"], p["P"], *v, gemm_dtype=O.GEMM_BF16))
+        xs.append(fws[-1]["H"])
+    g, bws = dH, [None] * nl
+    for li in range(nl - 1, -1, -1):
+        p, f = layers[li], fws[li]
+        bws[li] = sru.backward_lowrank(xs[li], p["Q"], p["P"], p["v_f"], p["v_r"], p["b_f"],
+                                       p["b_r"], f["T"], f["U"], f["C"], g,
+                                       gemm_dtype=O.GEMM_BF16)
+        g = bws[li]["dX"]
+    torch.cuda.synchronize()
+    for li in range(nl):
+        for key in ("T", "U", "H", "C"):
+            assert torch.equal(st.fw[li][key], fws[li][key]), (li, key)
+        for key in ("dX", "dQ", "dP", "dv_f", "dv_r", "db_f", "db_r"):
+            assert torch.equal(st.bw[li][key], bws[li][key]), (li, key)
