@@ -246,11 +246,13 @@ KERNEL_KEYS = [(("scan_fwd_kernel",), "scan_fwd"), (("scan_bwd_kernel",), "scan_
                (("scan_fwd_lin_kernel",), "scan_fwd"), (("scan_bwd_lin_kernel",), "scan_bwd"),
                (("reduce_vb_kernel",), "reduce_vb"), (("splitk_reduce_kernel",), "splitk_reduce"),
                (("to_bf16_kernel",), "bf16_x"),
-               # the three products of the bf16 path (template args after the
-               # tile configuration: addend count, A row-contiguous, B row-contiguous)
-               (("gemm_direct_kernel", ">, 0, false, false>"), "gemm_u"),
-               (("gemm_direct_kernel", ">, 1, false, true>"), "gemm_dx"),
-               (("gemm_direct_kernel", ">, 0, true, true>"), "gemm_dw")]
+               # the three products of the dense bf16 path (template args after
+               # the 256 x 256 tile configuration: addend count, A row-contiguous,
+               # B row-contiguous, bf16 result)
+               (("gemm_direct_kernel", "256, 256, 64", ">, 0, false, false, false>"), "gemm_u"),
+               (("gemm_direct_kernel", "256, 256, 64", ">, 1, false, false, false>"), "gemm_dx"),
+               (("gemm_direct_kernel", "256, 256, 64", ">, 2, false, false, false>"), "gemm_dx"),
+               (("gemm_direct_kernel", "256, 256, 64", ">, 0, true, true, false>"), "gemm_dw")]
 
 
 def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out):
