@@ -374,7 +374,54 @@ __device__ __forceinline__ void write_tile_rows(const KernelArgs& g,
       }
     return;
   }
-  if (g.vec_out && m0 + C::BM <= g.M && n0 + C::BN <= g.N) {
+  if constexpr (ADD > 0) {
+    if (g.vec_out && m0 + C::BM <= g.M && n0 + C::BN <= g.N) {
+      // Addends of one row of MFMA tiles are loaded one row ahead, before
+      // the stores of the current row: the loads never wait behind stores
+      // (which the compiler would otherwise keep in program order, since
+      // it cannot rule out aliasing), so a wave has one exposed memory
+      // round trip instead of one per MFMA tile.
+      constexpr int NA = C::FN * 4;  // 16-byte addend chunks per tile row
+      floatx4 buf[2][ADD][NA];
+      auto load_row = [&](int i, floatx4 (&a)[ADD][NA]) {
+        const int m = m0 + wm0 + i * 32 + (lane & 31);
+        const float* arow = g.add + (long long)m * g.add_ld + n0 + wn0 + cl;
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            a[0][j * 4 + q] = *reinterpret_cast<const floatx4*>(arow + j * 32 + 8 * q);
+            if constexpr (ADD > 1)
+              a[1][j * 4 + q] =
+                  *reinterpret_cast<const floatx4*>(arow + g.add_off + j * 32 + 8 * q);
+          }
+      };
+      load_row(0, buf[0]);
+#pragma unroll
+      for (int i = 0; i < C::FM; ++i) {
+        floatx4 v[NA];
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[j * 4 + q][e] = acc[i][j][4 * q + e];
+            v[j * 4 + q] += buf[i & 1][0][j * 4 + q];
+            if constexpr (ADD > 1) v[j * 4 + q] += buf[i & 1][1][j * 4 + q];
+          }
+        if (i + 1 < C::FM) load_row(i + 1, buf[(i + 1) & 1]);
+        const int m = m0 + wm0 + i * 32 + (lane & 31);
+        float* orow = out + (long long)m * g.ldo + n0 + wn0 + cl;
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<floatx4*>(orow + j * 32 + 8 * q) = v[j * 4 + q];
+      }
+      return;
+    }
+  }
+  if (ADD == 0 && g.vec_out && m0 + C::BM <= g.M && n0 + C::BN <= g.N) {
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
       const int m = m0 + wm0 + i * 32 + (lane & 31);
