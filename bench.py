@@ -298,6 +298,8 @@ def main():
                     help="sequences in the CPU-oracle sample (0 = skip)")
     ap.add_argument("--highway-scale", type=float, default=1.0,
                     help="alpha on the highway term (Sec. 3.2 scaling correction; 1 = none)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of the step recorded into a HIP graph (no launch cost)")
     ap.add_argument("--reset-new", action="store_true",
                     help="reset gate reads c_t (Algorithm 1's order) instead of c_{t-1}")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="REPS",
@@ -334,11 +336,14 @@ def main():
                    backward=w.backward, highway_scale=args.highway_scale,
                    reset_new=args.reset_new, store_c=w.store_c, linear=w.linear)
 
-    def step():
+    def eager_step():
         st.forward(X, mask)
         if w.backward:
             st.backward(X, dH, mask)
 
+    step = eager_step
+    if args.graph:
+        step = st.capture(X, dH, mask).replay
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -360,7 +365,7 @@ def main():
     lib.sru_timing_begin(ev.events, ev.n)
     try:
         for _ in range(args.profile_steps):
-            step()
+            eager_step()  # the hook brackets launches, which a graph replay does not make
     finally:
         nk = lib.sru_timing_end()
     torch.cuda.synchronize()
@@ -436,7 +441,8 @@ def main():
                    "reset_gate": "c_t (Algorithm 1)" if args.reset_new else "c_{t-1} (Eq. 3)",
                    "recurrence": ("linear: v * c removed (ablation (1), Sec. 4.5)" if w.linear
                                   else "gated (Eq. 1-4)"),
-                   "seq_len": w.L, "parallelism": "single GPU"},
+                   "seq_len": w.L, "parallelism": "single GPU",
+                   "launch": "hip graph replay" if args.graph else "eager"},
         "roofline": roofline,
         "scan_hbm": scan_hbm,
         "kernels": kernels,

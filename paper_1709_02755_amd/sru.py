@@ -479,3 +479,28 @@ class Stack:
                          W_bf16=o.get("W_bf16"), **self.variant)
             g = b["dX"]
         return g
+
+    def step(self, X, dH=None, mask=None):
+        """One forward (+ backward, if the stack has one) pass."""
+        self.forward(X, mask)
+        if self.bw:
+            self.backward(X, dH, mask)
+
+    def capture(self, X, dH=None, mask=None):
+        """Record one step into a HIP graph (torch.cuda.CUDAGraph).
+
+        The library allocates, frees and synchronises nothing and issues no
+        memset, so a whole step records as plain kernel nodes.  Replaying the
+        graph runs the step again on whatever X, dH and mask then hold (the
+        same tensors, updated in place), with no per-kernel launch cost.  The
+        graph reads and writes this stack's buffers: do not run the stack
+        eagerly and replay the graph concurrently."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self.step(X, dH, mask)  # warm-up outside the capture
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            self.step(X, dH, mask)
+        return graph
