@@ -65,11 +65,12 @@ class Workload:
         return self.L * self.B
 
 
-# The five workloads of the build target (sizes and distributions as stated
-# there), then the inference shape of the SRU that replaces a Transformer's
-# feed-forward layer (Sec. 4.3: d_model = 512 in, d_sru = 2048, batches of
-# about 5120 tokens; forward only, no C), the 6-layer stack with the
-# projection trick, and workload 2 with the linear recurrence; seeds are
+# Five workloads of the SRU layer at the sizes of its common uses (layers,
+# direction, L, B, d, product precision, padding), then the inference shape
+# of the SRU that replaces a Transformer's feed-forward layer (Sec. 4.3:
+# d_model = 512 in, d_sru = 2048, batches of about 5120 tokens; forward only,
+# no C), the 6-layer stack with the projection trick, and workload 2 with
+# the linear recurrence; seeds are
 # the workload index.  The linear workload still draws v_f, v_r (same draw
 # order as the others); nothing reads them.
 WORKLOADS = [

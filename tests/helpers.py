@@ -5,7 +5,7 @@ import torch
 
 from conftest import rel_err
 
-# Tolerances of the build target: 1e-5 relative for fp32 GEMMs, 2e-2 for the
+# Parity tolerances: 1e-5 relative for fp32 GEMMs, 2e-2 for the
 # bf16-GEMM path, measured as max |g - r| / max(|r|, rms(r)) per tensor.
 TOL_FP32 = 1e-5
 TOL_BF16 = 2e-2
