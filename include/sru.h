@@ -226,6 +226,13 @@ typedef enum {
   SRU_OP_TN = 2  /* C[M,N] = A[K,M]^T * B[K,N]   (dW = dU^T X)   */
 } sru_gemm_op;
 
+/* bf16 rounding (round to nearest even) of n fp32 values: the operand copy
+ * the bf16 companions expect.  A caller that feeds the same X to a layer's
+ * forward and backward rounds it once here and passes the copy as X_bf16 to
+ * both.  src, dst: device memory, 16-byte aligned, not overlapping; n >= 0
+ * (0 enqueues nothing). */
+SRU_API int sru_round_bf16(const float* src, size_t n, uint16_t* dst, hipStream_t stream);
+
 /* Matrix product on the MFMA units (the batched projection of Sec. 3.1 and
  * its two backward products).  Row-major operands with leading dimensions
  * lda, ldb, ldc (elements).  gemm_dtype as above.  TN may split the

@@ -453,6 +453,16 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   return hip_status(sru::gemm_launch(gw, stream));
 }
 
+int sru_round_bf16(const float* src, size_t n, uint16_t* dst, hipStream_t stream) {
+  if (n == 0) return SRU_OK;
+  if (!src || !dst) return SRU_E_NULLPTR;
+  if (n > (size_t)kMaxElems) return SRU_E_SHAPE;
+  if (!aligned16(src) || !aligned16(dst)) return SRU_E_ALIGN;
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+  if (s0 < d0 + 2 * n && d0 < s0 + 4 * n) return SRU_E_SHAPE;  // overlapping buffers
+  return hip_status(sru::to_bf16_n_launch(src, (long long)n, dst, stream, "bf16_x"));
+}
+
 size_t sru_gemm_workspace_bytes(int op, int M, int N, int K, int gemm_dtype) {
   if (op < SRU_OP_NT || op > SRU_OP_TN || !valid_dtype(gemm_dtype)) return 0;
   if (M <= 0 || N <= 0 || K <= 0) return 0;

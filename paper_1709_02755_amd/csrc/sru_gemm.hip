@@ -1274,17 +1274,28 @@ hipError_t to_bf16_t_launch(const void* src, bool src_bf16, int rows, int cols, 
   return hipGetLastError();
 }
 
+void launch_copy(const float* src, long long n, uint16_t* dst, hipStream_t st) {
+  const long long threads = (n + 7) / 8;
+  hipLaunchKernelGGL(to_bf16_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
+                     src, n, dst);
+}
+
 hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, bool transpose,
                           hipStream_t st, const char* label) {
   timing_before(label, st);
   if (transpose) {
     launch_transpose(src, rows, cols, dst, st);
   } else {
-    const long long n = (long long)rows * cols;
-    const long long threads = (n + 7) / 8;
-    hipLaunchKernelGGL(to_bf16_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
-                       src, n, dst);
+    launch_copy(src, (long long)rows * cols, dst, st);
   }
+  timing_after(st);
+  return hipGetLastError();
+}
+
+hipError_t to_bf16_n_launch(const float* src, long long n, uint16_t* dst, hipStream_t st,
+                            const char* label) {
+  timing_before(label, st);
+  launch_copy(src, n, dst, st);
   timing_after(st);
   return hipGetLastError();
 }

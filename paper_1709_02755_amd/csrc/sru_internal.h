@@ -46,6 +46,9 @@ struct GemmDesc {
 // when `transpose`.
 hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, bool transpose,
                           hipStream_t stream, const char* label);
+// The same for n contiguous elements (n up to 2^40).
+hipError_t to_bf16_n_launch(const float* src, long long n, uint16_t* dst, hipStream_t stream,
+                            const char* label);
 // Transposed copy [cols, rows] in bf16 (RNE) of a [rows, cols] matrix held in
 // fp32, or in bf16 (src_bf16; then an exact copy of its values).
 hipError_t to_bf16_t_launch(const void* src, bool src_bf16, int rows, int cols, uint16_t* dst,

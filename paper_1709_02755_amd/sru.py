@@ -51,6 +51,7 @@ _SIGNATURES = {
                             + [_P, _S, _P]),
     "sru_backward_lowrank": (_I, [_P] * 8 + [_I] * 6 + [_P, _I, _P] + [_P] * 5 + [_P] * 8
                              + [_P] * 2 + [_P, _S, _P]),
+    "sru_round_bf16": (_I, [_P, _S, _P, _P]),
     "sru_timing_begin": (_I, [_P, _I]),
     "sru_timing_end": (_I, []),
     "sru_timing_label": (ctypes.c_char_p, [_I]),
@@ -316,6 +317,16 @@ def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, T, U, C, dH, c0=None, dc_last=
     return out
 
 
+def round_bf16(src, out=None):
+    """bf16 (RNE) copy of an fp32 tensor, as the bf16 companions expect."""
+    _req(src, "src", tuple(src.shape))
+    if out is None:
+        out = torch.empty(tuple(src.shape), dtype=torch.bfloat16, device=src.device)
+    _req(out, "out", tuple(src.shape), dtype=torch.bfloat16)
+    _check(lib().sru_round_bf16(_ptr(src), src.numel(), _ptr(out), _stream()), "sru_round_bf16")
+    return out
+
+
 def gemm(op, A, B, M, N, K, gemm_dtype=GEMM_FP32, C=None, ws=None):
     """C[M,N] for op NT (A[M,K] B[N,K]^T), NN (A[M,K] B[K,N]) or TN (A[K,M]^T B[K,N])."""
     a_shape = (K, M) if op == OP_TN else (M, K)
@@ -448,9 +459,15 @@ class Stack:
                 ws_bytes = max(ws_bytes, forward_workspace_bytes(L, B, din, d, direction,
                                                                  gemm_dtype))
         self.ws = workspace(ws_bytes, device)
+        # bf16 products: the first layer's input is rounded once per step and
+        # the copy serves its forward and its backward
+        self.xb0 = (torch.empty((L, B, d_in), dtype=torch.bfloat16, device=device)
+                    if gemm_dtype == GEMM_BF16 else None)
 
     def forward(self, X, mask=None):
         x, xb = X, None
+        if self.xb0 is not None:
+            xb = round_bf16(X, self.xb0)
         for p, o in zip(self.layers, self.fw):
             v = (p["v_f"], p["v_r"], p["b_f"], p["b_r"], None, self.direction, mask,
                  self.gemm_dtype)
@@ -463,12 +480,13 @@ class Stack:
         return x
 
     def backward(self, X, dH, mask=None):
+        """Backward of the last forward(), which must have run on the same X."""
         g = dH
         for li in range(len(self.layers) - 1, -1, -1):
             p, o, b = self.layers[li], self.fw[li], self.bw[li]
             x = X if li == 0 else self.fw[li - 1]["H"]
             v = (p["v_f"], p["v_r"], p["b_f"], p["b_r"])
-            xb = None if li == 0 else self.fw[li - 1].get("H_bf16")
+            xb = self.xb0 if li == 0 else self.fw[li - 1].get("H_bf16")
             if "Q" in p:
                 backward_lowrank(x, p["Q"], p["P"], *v, o["T"], o["U"], o["C"], g, None, None,
                                  self.direction, mask, self.gemm_dtype, want_dc0=False, out=b,

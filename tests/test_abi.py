@@ -237,3 +237,12 @@ def test_lowrank_argument_checks():
     assert b(*args) == E_FLAG                   # X_bf16 with fp32 products
     args[-5] = None
     assert b(*args) == E_WS
+
+
+def test_round_bf16_argument_checks():
+    lib = sru.lib()
+    f = lib.sru_round_bf16
+    assert f(None, 0, None, None) == OK                       # nothing to do
+    assert f(None, 8, FAKE, None) == E_NULL
+    assert f(FAKE, 8, ctypes.c_void_p(0x10008), None) == E_ALIGN
+    assert f(ctypes.c_void_p(0x20000), 8, ctypes.c_void_p(0x20010), None) == E_SHAPE  # overlap

@@ -106,3 +106,15 @@ def test_stack_wiring_equals_plain_calls():
     for li in range(layers):
         for key, v in grads[li].items():
             assert torch.equal(v, ref[li][key]), (li, key)
+
+
+@pytest.mark.parametrize("n", [1, 7, 8, 4099, 1 << 20])
+def test_round_bf16_equals_rne_cast(n):
+    """sru_round_bf16 gives torch's round-to-nearest-even bf16 bit for bit,
+    including ties, infinities and a ragged tail."""
+    x = torch.randn(n, device="cuda") * 10.0
+    if n >= 8:
+        x[:4] = torch.tensor([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, float("inf"), -0.0])
+    got = sru.round_bf16(x)
+    torch.cuda.synchronize()
+    assert torch.equal(bits(got), bits(x.to(torch.bfloat16)))
