@@ -132,6 +132,11 @@ SRU_API size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int d
  *        H [L, B, ndir*d];
  *        C [L, B, ndir*d] -- every state c_t, needed by sru_backward
  *        (NULL = do not store: inference);
+ *        U may be NULL too when C is NULL and sru_forward_fused_available
+ *        says so (bf16 products, d % 64 == 0): the projection and the scan
+ *        then run as one kernel and U never reaches memory (H and c_last
+ *        are bit-identical to the unfused call's).  Otherwise a NULL U is
+ *        SRU_E_NULLPTR;
  *        c_last [B, ndir*d] -- state after each sequence's last valid step
  *        (NULL = do not store).
  *   bf16 companions (gemm_dtype = SRU_GEMM_BF16 only, else they must be
@@ -144,6 +149,11 @@ SRU_API size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int d
  *        H_bf16 [L, B, ndir*d] out -- H rounded to bf16 (the next layer's
  *        X_bf16).
  */
+/* 1 when sru_forward accepts U = NULL with C = NULL for these sizes (the
+ * fused projection + scan of inference), else 0. */
+SRU_API int sru_forward_fused_available(int L, int B, int d_in, int d, int direction,
+                                        int gemm_dtype);
+
 SRU_API int sru_forward(const float* X, const float* W,
                 const float* v_f, const float* v_r, const float* b_f, const float* b_r,
                 const float* c0, int L, int B, int d_in, int d, int direction,

@@ -124,6 +124,21 @@ sru::GemmDesc gemm_desc(int op, bool bf16, int M, int N, int K, const void* A, l
   return g;
 }
 
+// Where inference (U and C not kept) runs the projection and the scan as one
+// kernel: bf16 products, whole groups of 64 hidden units, whole 16-byte
+// chunks of X rows, and operands within the 2 GiB byte range of buffer loads.
+bool fused_ok(const Dims& s, int gemm_dtype) {
+  return gemm_dtype == SRU_GEMM_BF16 && s.d % 64 == 0 && s.d_in % 8 == 0 &&
+         2 * s.M * s.d_in < (1LL << 31) && 2 * s.N * s.d_in < (1LL << 31);
+}
+// Sequences per fused tile: the tile holds 256 rows of (step, sequence)
+// pairs; short sequences share a tile (up to 8, one scan wave each).
+int fused_seqs_per_tile(int L) {
+  int bb = 1;
+  while (bb < 8 && 256 / (2 * bb) >= L) bb *= 2;
+  return bb;
+}
+
 // Forward workspace: bf16 mode keeps bf16 copies of W [N, d_in] and
 // X [M, d_in] (the operands of the projection).
 size_t fwd_workspace(const Dims& s, int gemm_dtype) {
@@ -318,6 +333,12 @@ size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int direction
   return bwd_layout(s, gemm_dtype).total;
 }
 
+int sru_forward_fused_available(int L, int B, int d_in, int d, int direction, int gemm_dtype) {
+  Dims s;
+  if (make_dims(L, B, d_in, d, direction, s) != SRU_OK || !valid_dtype(gemm_dtype)) return 0;
+  return fused_ok(s, gemm_dtype) ? 1 : 0;
+}
+
 int sru_forward(const float* X, const float* W, const float* v_f, const float* v_r,
                 const float* b_f, const float* b_r, const float* c0, int L, int B, int d_in,
                 int d, int direction, const uint8_t* pad_mask, int gemm_dtype,
@@ -330,7 +351,11 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
   if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
   Opts op;
   if (int e = read_options(options, op)) return e;
-  if (!X || !W || missing_v(op, v_f, v_r) || !b_f || !b_r || !U || !H) return SRU_E_NULLPTR;
+  // U may be omitted only where the fused projection + scan applies
+  // (inference with bf16 products: C omitted too)
+  const bool fused = !U && fused_ok(s, gemm_dtype) && !C;
+  if (!X || !W || missing_v(op, v_f, v_r) || !b_f || !b_r || (!U && !fused) || !H)
+    return SRU_E_NULLPTR;
   const void* ptrs[] = {X, W, v_f, v_r, b_f, b_r, c0, U, H, C, c_last};
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
@@ -359,6 +384,37 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
       if (int e = hip_status(sru::to_bf16_launch(X, (int)s.M, d_in, xb, false, stream, "bf16_x"))) return e;
       Xop = xb;
     }
+  }
+  if (fused) {
+    sru::FusedFwdArgs f{};
+    f.Xb = static_cast<const uint16_t*>(Xop);
+    f.Wb = static_cast<const uint16_t*>(Wop);
+    f.a_bytes = (unsigned)(2 * s.M * d_in);
+    f.b_bytes = (unsigned)(2 * s.N * d_in);
+    f.X = X;
+    f.v_f = op.linear ? nullptr : v_f;
+    f.v_r = op.linear ? nullptr : v_r;
+    f.b_f = b_f;
+    f.b_r = b_r;
+    f.c0 = c0;
+    f.mask = pad_mask;
+    f.H = H;
+    f.Hb = H_bf16;
+    f.c_last = c_last;
+    f.L = L;
+    f.B = B;
+    f.d_in = d_in;
+    f.d = d;
+    f.ndir = s.ndir;
+    f.k = s.k;
+    f.direction = direction;
+    f.bb = fused_seqs_per_tile(L);
+    f.ngroups = d / 64;
+    f.nbgroups = (B + f.bb - 1) / f.bb;
+    f.alpha = op.alpha;
+    f.reset_new = op.reset_new;
+    f.linear = op.linear;
+    return hip_status(sru::proj_scan_forward_launch(f, stream));
   }
   sru::GemmDesc g = gemm_desc(SRU_OP_NT, bf16, (int)s.M, (int)s.N, d_in, Xop, d_in, Wop, d_in, U,
                               s.N);

@@ -30,6 +30,7 @@
 #include <algorithm>
 #include <type_traits>
 
+#include "sru_device.h"
 #include "sru_internal.h"
 
 
@@ -682,6 +683,22 @@ struct DirectOperand {
       }
     }
   }
+  // K-contiguous operand whose tile row r is row row_of(r) of the operand,
+  // or a row of zeros where row_of(r) < 0 (no memory is read for it).
+  template <class F>
+  __device__ __forceinline__ void init_rows(int wave, int lane, F row_of, long long ld) {
+    static_assert(!RC, "row maps are for K-contiguous operands");
+#pragma unroll
+    for (int j = 0; j < BPW; ++j) {
+      const int blk = wave * BPW + j;
+      const int r = blk * RPB + lane / LPR;
+      const int chunk = (lane % LPR) ^ swz(r);
+      const long long gr = row_of(r);
+      kk[j] = chunk * 8;
+      off[j] = gr >= 0 ? (unsigned)((gr * ld + chunk * 8) * 2) : 0u;
+      oob[j] = gr >= 0 ? 0u : kOOB;
+    }
+  }
   __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, unsigned char* lds, int wave,
                                         int k0, int kend, long long ld) const {
     const unsigned dk = RC ? (unsigned)((long long)k0 * ld * 2) : (unsigned)(k0 * 2);
@@ -719,40 +736,24 @@ struct DirectOperand {
   }
 };
 
-template <class C, int ADD, bool A_RC, bool B_RC, bool OB>
-__global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelArgs g) {
+// The main loop of the direct products: the tile whose operand loads la and
+// lb were set up, accumulated over k in [kbeg, kend) into acc.
+template <class C, class OpA, class OpB>
+__device__ __forceinline__ void direct_mainloop(unsigned char* smem, const OpA& la,
+                                                const OpB& lb, __amdgpu_buffer_rsrc_t ra,
+                                                __amdgpu_buffer_rsrc_t rb, long long lda,
+                                                long long ldb, int kbeg, int kend, int wave,
+                                                int lane, int wm0, int wn0,
+                                                floatx16 (&acc)[C::FM][C::FN]) {
   constexpr int STAGES = C::STAGES;
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
-
-  const TileIdx ti = tile_of(g);
-  const int m0 = ti.tm * C::BM;
-  const int n0 = ti.tn * C::BN;
-  const int kbeg = ti.split * g.k_per_split;
-  const int kend = min(g.K, kbeg + g.k_per_split);
   const int nk = (kend - kbeg + C::BK - 1) / C::BK;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm0 = (wave / C::WAVES_N) * C::WM;
-  const int wn0 = (wave % C::WAVES_N) * C::WN;
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(g.A, g.a_bytes);
-  const __amdgpu_buffer_rsrc_t rb = make_rsrc(g.B, g.b_bytes);
-
-  using OpA = DirectOperand<C::BM, A_RC, C::A_BPW, C::BK>;
-  using OpB = DirectOperand<C::BN, B_RC, C::B_BPW, C::BK>;
-  OpA la;
-  OpB lb;
-  la.init(wave, lane, m0, g.M, g.lda);
-  lb.init(wave, lane, n0, g.N, g.ldb);
   auto issue = [&](int kt) {
     unsigned char* st = smem + (kt % STAGES) * C::STB;
     const int k0 = kbeg + kt * C::BK;
-    la.issue(ra, st, wave, k0, kend, g.lda);
-    lb.issue(rb, st + C::A_OPB, wave, k0, kend, g.ldb);
+    la.issue(ra, st, wave, k0, kend, lda);
+    lb.issue(rb, st + C::A_OPB, wave, k0, kend, ldb);
   };
 
-  floatx16 acc[C::FM][C::FN];
 #pragma unroll
   for (int i = 0; i < C::FM; ++i)
 #pragma unroll
@@ -852,7 +853,203 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
       mfmas(f[sl & 1]);
     }
   }
+}
+
+template <class C, int ADD, bool A_RC, bool B_RC, bool OB>
+__global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelArgs g) {
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
+
+  const TileIdx ti = tile_of(g);
+  const int m0 = ti.tm * C::BM;
+  const int n0 = ti.tn * C::BN;
+  const int kbeg = ti.split * g.k_per_split;
+  const int kend = min(g.K, kbeg + g.k_per_split);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm0 = (wave / C::WAVES_N) * C::WM;
+  const int wn0 = (wave % C::WAVES_N) * C::WN;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(g.A, g.a_bytes);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(g.B, g.b_bytes);
+
+  using OpA = DirectOperand<C::BM, A_RC, C::A_BPW, C::BK>;
+  using OpB = DirectOperand<C::BN, B_RC, C::B_BPW, C::BK>;
+  OpA la;
+  OpB lb;
+  la.init(wave, lane, m0, g.M, g.lda);
+  lb.init(wave, lane, n0, g.N, g.ldb);
+  floatx16 acc[C::FM][C::FN];
+  direct_mainloop<C>(smem, la, lb, ra, rb, g.lda, g.ldb, kbeg, kend, wave, lane, wm0, wn0,
+                     acc);
   write_tile_rows<C, ADD, OB>(g, acc, m0, n0, wm0, wn0, lane, ti.split);
+}
+
+// ---- fused projection + forward scan (inference: neither U nor C kept) ----
+// One workgroup per (direction, group of 64 hidden units, group of BB
+// sequences).  Per time block of 256 / BB steps it computes the tile of U
+// whose rows are the (step, sequence) pairs of the block and whose columns
+// are the gate blocks of its 64 units, with the main loop of the direct
+// products.  It stages the tile through LDS in two halves of 128 rows and
+// runs Eq. 1-4 for its lanes from there: wave s scans sequence s of the
+// group, lane j unit j, the state c held in a register across halves and
+// blocks.  U never reaches memory.  The scan arithmetic is the forward scan
+// kernel's, in the same order, so H equals the unfused path's bit for bit.
+// With k = 3 the fourth column block multiplies zero rows, and its LDS slot
+// holds x, the highway input, instead.
+constexpr int kFusedPitch = 68;  // floats per staged row: 64 + 4 keeps 16-byte writes conflict-free
+constexpr int kFusedStage = 4 * 128 * kFusedPitch * 4;  // bytes: 4 blocks of 128 rows
+
+template <int KB>
+__global__ __launch_bounds__(DirectLine::THREADS, 1) void proj_scan_fwd_kernel(FusedFwdArgs a) {
+  using C = DirectLine;
+  constexpr int SMEM = C::LDS > kFusedStage ? C::LDS : kFusedStage;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[SMEM];
+  float* stage = reinterpret_cast<float*>(smem);
+
+  // workgroup -> (direction, unit group, sequence group); XCD-aware, so the
+  // workgroups of one XCD share the Wcat rows of a unit group
+  const int nwg = gridDim.x, w = blockIdx.x;
+  const int q8 = nwg / 8, rmd = nwg % 8, x8 = w % 8;
+  const int u = x8 * q8 + (x8 < rmd ? x8 : rmd) + w / 8;
+  const int bg = u % a.nbgroups;
+  const int dg = u / a.nbgroups;
+  const int dir = dg / a.ngroups, g = dg % a.ngroups;
+  const int BB = a.bb, TB = 256 / BB, steps = 128 / BB;
+  const int b0 = bg * BB;
+  const bool rev = a.direction == 1 || (a.direction == 2 && dir == 1);
+  const int L = a.L, Bs = a.B, d = a.d;
+  const long long nfeat = (long long)a.ndir * d;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
+  const int wm0 = wm * C::WM, wn0 = wn * C::WN;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.Xb, a.a_bytes);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.Wb, a.b_bytes);
+  using OpA = DirectOperand<C::BM, false, C::A_BPW, C::BK>;
+  using OpB = DirectOperand<C::BN, false, C::B_BPW, C::BK>;
+  OpB lb;
+  lb.init_rows(
+      wave, lane,
+      [&](int col) -> long long {
+        const int q = col >> 6;
+        return q < KB ? (long long)(dir * KB + q) * d + g * 64 + (col & 63) : -1;
+      },
+      a.d_in);
+
+  // scan lanes: waves 0 .. BB-1, sequence b0 + wave, unit g * 64 + lane
+  const int sb = b0 + wave;
+  const bool scans = wave < BB && sb < Bs;
+  const long long fidx = (long long)dir * d + g * 64 + lane;
+  float vf = 0.f, vr = 0.f, bf = 0.f, br = 0.f, c = 0.f;
+  if (scans) {
+    if (!a.linear) {
+      vf = a.v_f[fidx];
+      vr = a.v_r[fidx];
+    }
+    bf = a.b_f[fidx];
+    br = a.b_r[fidx];
+    c = a.c0 ? a.c0[(long long)sb * nfeat + fidx] : 0.f;
+  }
+  const float alpha = a.alpha;
+  const bool rn = a.reset_new != 0;
+  auto barrier = [] {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // this wave's LDS accesses (lgkmcnt 0) only
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  const int nblk = (L + TB - 1) / TB;
+  for (int ib = 0; ib < nblk; ++ib) {
+    const int t0 = (rev ? nblk - 1 - ib : ib) * TB;
+    OpA la;
+    la.init_rows(
+        wave, lane,
+        [&](int r) -> long long {
+          const int t = t0 + r / BB, b = b0 + r % BB;
+          return t < L && b < Bs ? (long long)t * Bs + b : -1;
+        },
+        a.d_in);
+    floatx16 acc[C::FM][C::FN];
+    direct_mainloop<C>(smem, la, lb, ra, rb, a.d_in, a.d_in, 0, a.d_in, wave, lane, wm0, wn0,
+                       acc);
+    barrier();  // every wave is done with the operand stages
+    for (int ih = 0; ih < 2; ++ih) {
+      const int half = rev ? 1 - ih : ih;
+      if (wm == half) {
+        if (KB == 4 || wn < 3) {
+          // transposed accumulators: lane l holds row l % 32 of each MFMA
+          // tile, columns 8 (e / 4) + 4 (l / 32) + e % 4
+#pragma unroll
+          for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+              for (int eg = 0; eg < 4; ++eg) {
+                floatx4 v;
+                v[0] = acc[i][j][4 * eg];
+                v[1] = acc[i][j][4 * eg + 1];
+                v[2] = acc[i][j][4 * eg + 2];
+                v[3] = acc[i][j][4 * eg + 3];
+                const int row = i * 32 + (lane & 31);
+                const int col = j * 32 + 8 * eg + 4 * (lane >> 5);
+                *reinterpret_cast<floatx4*>(stage + (wn * 128 + row) * kFusedPitch + col) = v;
+              }
+        } else {
+          // k = 3: block 3 holds x for the rows of this half (zero past the end)
+#pragma unroll 4
+          for (int k = 0; k < 32; ++k) {
+            const int ch = k * 64 + lane, row = ch >> 4, cc = (ch & 15) * 4;
+            const int r = half * 128 + row;
+            const int t = t0 + r / BB, b = b0 + r % BB;
+            floatx4 v = {0.f, 0.f, 0.f, 0.f};
+            if (t < L && b < Bs)
+              v = *reinterpret_cast<const floatx4*>(a.X + ((long long)t * Bs + b) * a.d_in +
+                                                    g * 64 + cc);
+            *reinterpret_cast<floatx4*>(stage + (3 * 128 + row) * kFusedPitch + cc) = v;
+          }
+        }
+      }
+      barrier();
+      if (scans) {
+        const int tb = t0 + half * steps;  // first step of this half
+        // padding bits of the half's steps, one per lane, read with readlane
+        int m_lo = 0, m_hi = 0;
+        if (a.mask) {
+          const int t_lo = tb + lane, t_hi = tb + 64 + lane;
+          if (lane < steps && t_lo < L) m_lo = a.mask[(long long)t_lo * Bs + sb];
+          if (lane + 64 < steps && t_hi < L) m_hi = a.mask[(long long)t_hi * Bs + sb];
+        }
+#pragma unroll 4
+        for (int s = 0; s < steps; ++s) {
+          const int tt = rev ? steps - 1 - s : s;
+          const int t = tb + tt;
+          if (t >= L) continue;
+          const float* sp = stage + (tt * BB + wave) * kFusedPitch + lane;
+          const float u0 = sp[0], u1 = sp[128 * kFusedPitch], u2 = sp[2 * 128 * kFusedPitch];
+          const float xh = sp[3 * 128 * kFusedPitch];
+          const int mbit = tt < 64 ? __builtin_amdgcn_readlane(m_lo, tt)
+                                   : __builtin_amdgcn_readlane(m_hi, tt - 64);
+          const float f = sigmoid_fast(fmaf(vf, c, u1 + bf));           // Eq. 1
+          const float cn = fmaf(f, c, (1.0f - f) * u0);                 // Eq. 2
+          const float r = sigmoid_fast(fmaf(vr, rn ? cn : c, u2 + br));  // Eq. 3
+          float h = fmaf(r, cn, (1.0f - r) * (alpha * xh));              // Eq. 4 (Sec. 3.2)
+          if (mbit) {
+            h = 0.0f;
+          } else {
+            c = cn;
+          }
+          const long long o = ((long long)t * Bs + sb) * nfeat + fidx;
+          __builtin_nontemporal_store(h, a.H + o);
+          if (a.Hb) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), a.Hb + o);
+        }
+      }
+      barrier();  // before the next half or block overwrites the stage
+    }
+  }
+  if (scans && a.c_last) a.c_last[(long long)sb * nfeat + fidx] = c;
 }
 
 template <class C, int ADD, bool A_RC, bool B_RC, bool OB = false>
@@ -1288,6 +1485,17 @@ hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, b
   } else {
     launch_copy(src, (long long)rows * cols, dst, st);
   }
+  timing_after(st);
+  return hipGetLastError();
+}
+
+hipError_t proj_scan_forward_launch(const FusedFwdArgs& a, hipStream_t st) {
+  const int grid = a.ndir * a.ngroups * a.nbgroups;
+  timing_before("proj_scan_fwd", st);
+  if (a.k == 3)
+    hipLaunchKernelGGL(proj_scan_fwd_kernel<3>, dim3(grid), dim3(DirectLine::THREADS), 0, st, a);
+  else
+    hipLaunchKernelGGL(proj_scan_fwd_kernel<4>, dim3(grid), dim3(DirectLine::THREADS), 0, st, a);
   timing_after(st);
   return hipGetLastError();
 }

@@ -16,18 +16,13 @@
 // run in a guarded tail.
 #include <type_traits>
 
+#include "sru_device.h"
 #include "sru_internal.h"
 
 namespace sru {
 namespace {
 
 constexpr int kScanThreads = 64;
-
-__device__ __forceinline__ float sigmoid_fast(float z) {
-  // 1 / (1 + e^{-z}); saturates to exactly 0 (e^{-z} = inf) and 1 (e^{-z}
-  // underflows) instead of producing NaN.
-  return __builtin_amdgcn_rcpf(1.0f + __expf(-z));
-}
 
 struct Lane {
   int gid, b, fidx, dir, j;

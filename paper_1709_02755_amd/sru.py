@@ -52,6 +52,7 @@ _SIGNATURES = {
     "sru_backward_lowrank": (_I, [_P] * 8 + [_I] * 6 + [_P, _I, _P] + [_P] * 5 + [_P] * 8
                              + [_P] * 2 + [_P, _S, _P]),
     "sru_round_bf16": (_I, [_P, _S, _P, _P]),
+    "sru_forward_fused_available": (_I, [_I] * 6),
     "sru_timing_begin": (_I, [_P, _I]),
     "sru_timing_end": (_I, []),
     "sru_timing_label": (ctypes.c_char_p, [_I]),
@@ -175,10 +176,18 @@ def workspace(nbytes, device):
     return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
 
 
+def fused_available(L, B, d_in, d, direction, gemm_dtype):
+    """Whether forward() can run without U and C (fused projection + scan)."""
+    return bool(lib().sru_forward_fused_available(L, B, d_in, d, direction, gemm_dtype))
+
+
 def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
             gemm_dtype=GEMM_FP32, store_c=True, out=None, ws=None, X_bf16=None,
-            highway_scale=1.0, reset_new=False, linear=False):
+            highway_scale=1.0, reset_new=False, linear=False, keep_u=True):
     """One layer forward; returns dict(U, H, C, c_last) (C None without store_c).
+
+    keep_u=False with store_c=False: U is not kept either, where
+    fused_available() allows it (U is then None).
 
     bf16 GEMMs only: X_bf16 (torch.bfloat16, X rounded) replaces the
     rounding of X; entries W_bf16 / H_bf16 of `out` (bfloat16 tensors), if
@@ -187,7 +196,9 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
     _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True)
     dev = X.device
     if out is None:
-        out = dict(U=torch.empty((L, B, ndir, k, d), device=dev),
+        no_u = not keep_u and not store_c and fused_available(L, B, d_in, d, direction,
+                                                                gemm_dtype)
+        out = dict(U=None if no_u else torch.empty((L, B, ndir, k, d), device=dev),
                    H=torch.empty((L, B, ndir * d), device=dev),
                    C=torch.empty((L, B, ndir * d), device=dev) if store_c else None,
                    c_last=torch.empty((B, ndir * d), device=dev))
@@ -197,7 +208,7 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
     st = lib().sru_forward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                            L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
                            _options(highway_scale, reset_new, linear),
-                           _ptr(out["U"]), _ptr(out["H"]), _ptr(out.get("C")),
+                           _ptr(out.get("U")), _ptr(out["H"]), _ptr(out.get("C")),
                            _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("W_bf16")),
                            _ptr(out.get("H_bf16")), _ptr(ws), need if ws is not None else 0,
                            _stream())
@@ -421,7 +432,11 @@ class Stack:
             low = "Q" in p
             k = (p["P"] if low else p["W"]).shape[1]
             keep_c = store_c or backward  # the backward reads C
-            o = dict(U=torch.empty((L, B, ndir, k, d), device=device),
+            # inference: dense layers run the fused projection + scan where
+            # available, which keeps no U
+            no_u = (not keep_c and not low and
+                    fused_available(L, B, din, d, direction, gemm_dtype))
+            o = dict(U=None if no_u else torch.empty((L, B, ndir, k, d), device=device),
                      H=torch.empty((L, B, ndir * d), device=device),
                      C=torch.empty((L, B, ndir * d), device=device) if keep_c else None,
                      c_last=torch.empty((B, ndir * d), device=device))

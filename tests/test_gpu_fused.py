@@ -1,0 +1,84 @@
+"""The fused projection + scan of inference (sru_forward with U and C
+omitted): H, c_last and the bf16 copy of H equal the unfused call's bit for
+bit (the scan reads the same fp32 projections, in the same order), across
+tile plans of 1 to 8 sequences, ragged step and sequence counts, k = 3 and 4,
+every direction, padding, c0 and the gate variants; and against the oracle,
+the linear recurrence included."""
+
+import numpy as np
+import pytest
+import torch
+
+from helpers import TOL_BF16, check, dev
+from oracle import sru_oracle as O
+from paper_1709_02755_amd import sru
+from paper_1709_02755_amd.workloads import random_layer_case
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # (L, B, d_in, d, direction, masked, alpha, reset_new)
+    (256, 3, 64, 64, O.DIR_FWD, False, 1.0, False),     # 1 sequence per tile, 1 block
+    (300, 2, 128, 64, O.DIR_REV, True, 1.0, False),     # 2 blocks, ragged, k = 4
+    (100, 5, 128, 128, O.DIR_BI, True, 1.7, True),      # 2 per tile, ragged B
+    (64, 9, 512, 192, O.DIR_FWD, True, 1.0, False),     # 4 per tile (the FFN plan), k = 4
+    (17, 11, 64, 64, O.DIR_BI, False, float(np.sqrt(3.0)), False),  # 8 per tile
+    (1, 4, 256, 128, O.DIR_REV, False, 1.0, True),      # a single step
+]
+
+
+def _case(L, B, d_in, d, direction, masked, seed):
+    return random_layer_case(np.random.default_rng(seed), L, B, d_in, d, direction,
+                             masked=masked, c0=True, bias_scale=0.5, v_scale=0.8)
+
+
+def _run(c, direction, gv, fused, linear=False):
+    L, B, d_in = c["X"].shape
+    ndir, k, d = c["W"].shape[:3]
+    X, W = dev(c["X"]), dev(c["W"])
+    p = [None, None] if linear else [dev(c["v_f"]), dev(c["v_r"])]
+    p += [dev(c["b_f"]), dev(c["b_r"])]
+    out = dict(U=None if fused else torch.empty((L, B, ndir, k, d), device="cuda"),
+               H=torch.empty((L, B, ndir * d), device="cuda"), C=None,
+               c_last=torch.empty((B, ndir * d), device="cuda"),
+               H_bf16=torch.empty((L, B, ndir * d), dtype=torch.bfloat16, device="cuda"))
+    sru.forward(X, W, *p, c0=dev(c["c0"]), direction=direction, mask=dev(c["mask"]),
+                gemm_dtype=O.GEMM_BF16, store_c=False, out=out, linear=linear, **gv)
+    return out
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_fused_equals_unfused_bitwise(case):
+    L, B, d_in, d, direction, masked, alpha, reset_new = case
+    print(f"fused L={L} B={B} d_in={d_in} d={d} dir={direction} mask={masked}", flush=True)
+    assert sru.fused_available(L, B, d_in, d, direction, O.GEMM_BF16)
+    c = _case(L, B, d_in, d, direction, masked, L + d)
+    gv = dict(highway_scale=alpha, reset_new=reset_new)
+    ref = _run(c, direction, gv, fused=False)
+    got = _run(c, direction, gv, fused=True)
+    torch.cuda.synchronize()
+    for k in ("H", "c_last"):
+        assert torch.equal(got[k], ref[k]), k
+    assert torch.equal(got["H_bf16"].view(torch.int16), ref["H_bf16"].view(torch.int16))
+
+
+@pytest.mark.parametrize("linear", [False, True])
+def test_fused_matches_oracle(linear):
+    L, B, d_in, d, direction = 90, 6, 192, 128, O.DIR_BI
+    c = _case(L, B, d_in, d, direction, True, 5 + linear)
+    got = _run(c, direction, {}, fused=True, linear=linear)
+    torch.cuda.synchronize()
+    v = (None, None) if linear else (c["v_f"], c["v_r"])
+    rf = O.forward(c["X"], c["W"], *v, c["b_f"], c["b_r"], c["c0"], direction, c["mask"],
+                   O.GEMM_BF16, linear=linear)
+    for k in ("H", "c_last"):
+        check(k, got[k], rf[k], TOL_BF16)
+    m = c["mask"].astype(bool)
+    assert np.all(got["H"].cpu().numpy()[m] == 0.0)
+
+
+def test_fused_not_available_keeps_u_required():
+    """Where the fused kernel does not apply (fp32 products, or d not a
+    multiple of 64) U stays required."""
+    assert not sru.fused_available(8, 2, 64, 64, O.DIR_FWD, O.GEMM_FP32)
+    assert not sru.fused_available(8, 2, 96, 96, O.DIR_FWD, O.GEMM_BF16)
