@@ -112,6 +112,8 @@ def kernel_work(w, splits, bf16):
         low = {}
     return {
         "gemm_u": dict(flops=2.0 * M * N * K),     # U = X W^T
+        # inference with the projection and the scan fused: the product's flops
+        "proj_scan_fwd": dict(flops=2.0 * M * N * K),
         "gemm_dx": dict(flops=2.0 * M * K * N),    # dX = dU W
         "gemm_dw": dict(flops=2.0 * N * K * M),    # dW = dU^T X
         # read U's three blocks and x_hat (x, or U block 3), write h and c

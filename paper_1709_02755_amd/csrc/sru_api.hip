@@ -126,10 +126,15 @@ sru::GemmDesc gemm_desc(int op, bool bf16, int M, int N, int K, const void* A, l
 
 // Where inference (U and C not kept) runs the projection and the scan as one
 // kernel: bf16 products, whole groups of 64 hidden units, whole 16-byte
-// chunks of X rows, and operands within the 2 GiB byte range of buffer loads.
+// chunks of X rows, operands within the 2 GiB byte range of buffer loads;
+// and where it is the faster organisation: four gate blocks (k = 4, a
+// tile's columns are exactly the gates of 64 units) and sequences of at most
+// 64 steps, so at least four sequences share a tile and their scans run side
+// by side.  With one sequence per tile a single wave scans while the matrix
+// units idle, and the separate scan (all lanes at once) is faster.
 bool fused_ok(const Dims& s, int gemm_dtype) {
-  return gemm_dtype == SRU_GEMM_BF16 && s.d % 64 == 0 && s.d_in % 8 == 0 &&
-         2 * s.M * s.d_in < (1LL << 31) && 2 * s.N * s.d_in < (1LL << 31);
+  return gemm_dtype == SRU_GEMM_BF16 && s.k == 4 && s.L <= 64 && s.d % 64 == 0 &&
+         s.d_in % 8 == 0 && 2 * s.M * s.d_in < (1LL << 31) && 2 * s.N * s.d_in < (1LL << 31);
 }
 // Sequences per fused tile: the tile holds 256 rows of (step, sequence)
 // pairs; short sequences share a tile (up to 8, one scan wave each).
@@ -391,7 +396,6 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
     f.Wb = static_cast<const uint16_t*>(Wop);
     f.a_bytes = (unsigned)(2 * s.M * d_in);
     f.b_bytes = (unsigned)(2 * s.N * d_in);
-    f.X = X;
     f.v_f = op.linear ? nullptr : v_f;
     f.v_r = op.linear ? nullptr : v_r;
     f.b_f = b_f;
@@ -406,7 +410,6 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
     f.d_in = d_in;
     f.d = d;
     f.ndir = s.ndir;
-    f.k = s.k;
     f.direction = direction;
     f.bb = fused_seqs_per_tile(L);
     f.ngroups = d / 64;

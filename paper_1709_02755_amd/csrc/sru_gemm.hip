@@ -895,14 +895,14 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
 // group, lane j unit j, the state c held in a register across halves and
 // blocks.  U never reaches memory.  The scan arithmetic is the forward scan
 // kernel's, in the same order, so H equals the unfused path's bit for bit.
-// With k = 3 the fourth column block multiplies zero rows, and its LDS slot
-// holds x, the highway input, instead.
+// k = 4: the four gate blocks (the highway input x_hat is block 3) make the
+// 256 columns of the tile.
 constexpr int kFusedPitch = 68;  // floats per staged row: 64 + 4 keeps 16-byte writes conflict-free
 constexpr int kFusedStage = 4 * 128 * kFusedPitch * 4;  // bytes: 4 blocks of 128 rows
 
-template <int KB>
 __global__ __launch_bounds__(DirectLine::THREADS, 1) void proj_scan_fwd_kernel(FusedFwdArgs a) {
   using C = DirectLine;
+  constexpr int KB = 4;
   constexpr int SMEM = C::LDS > kFusedStage ? C::LDS : kFusedStage;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[SMEM];
   float* stage = reinterpret_cast<float*>(smem);
@@ -932,8 +932,7 @@ __global__ __launch_bounds__(DirectLine::THREADS, 1) void proj_scan_fwd_kernel(F
   lb.init_rows(
       wave, lane,
       [&](int col) -> long long {
-        const int q = col >> 6;
-        return q < KB ? (long long)(dir * KB + q) * d + g * 64 + (col & 63) : -1;
+        return (long long)(dir * KB + (col >> 6)) * d + g * 64 + (col & 63);
       },
       a.d_in);
 
@@ -979,59 +978,48 @@ __global__ __launch_bounds__(DirectLine::THREADS, 1) void proj_scan_fwd_kernel(F
     for (int ih = 0; ih < 2; ++ih) {
       const int half = rev ? 1 - ih : ih;
       if (wm == half) {
-        if (KB == 4 || wn < 3) {
-          // transposed accumulators: lane l holds row l % 32 of each MFMA
-          // tile, columns 8 (e / 4) + 4 (l / 32) + e % 4
+        // transposed accumulators: lane l holds row l % 32 of each MFMA
+        // tile, columns 8 (e / 4) + 4 (l / 32) + e % 4
 #pragma unroll
-          for (int i = 0; i < C::FM; ++i)
+        for (int i = 0; i < C::FM; ++i)
 #pragma unroll
-            for (int j = 0; j < C::FN; ++j)
+          for (int j = 0; j < C::FN; ++j)
 #pragma unroll
-              for (int eg = 0; eg < 4; ++eg) {
-                floatx4 v;
-                v[0] = acc[i][j][4 * eg];
-                v[1] = acc[i][j][4 * eg + 1];
-                v[2] = acc[i][j][4 * eg + 2];
-                v[3] = acc[i][j][4 * eg + 3];
-                const int row = i * 32 + (lane & 31);
-                const int col = j * 32 + 8 * eg + 4 * (lane >> 5);
-                *reinterpret_cast<floatx4*>(stage + (wn * 128 + row) * kFusedPitch + col) = v;
-              }
-        } else {
-          // k = 3: block 3 holds x for the rows of this half (zero past the end)
-#pragma unroll 4
-          for (int k = 0; k < 32; ++k) {
-            const int ch = k * 64 + lane, row = ch >> 4, cc = (ch & 15) * 4;
-            const int r = half * 128 + row;
-            const int t = t0 + r / BB, b = b0 + r % BB;
-            floatx4 v = {0.f, 0.f, 0.f, 0.f};
-            if (t < L && b < Bs)
-              v = *reinterpret_cast<const floatx4*>(a.X + ((long long)t * Bs + b) * a.d_in +
-                                                    g * 64 + cc);
-            *reinterpret_cast<floatx4*>(stage + (3 * 128 + row) * kFusedPitch + cc) = v;
-          }
-        }
+            for (int eg = 0; eg < 4; ++eg) {
+              floatx4 v;
+              v[0] = acc[i][j][4 * eg];
+              v[1] = acc[i][j][4 * eg + 1];
+              v[2] = acc[i][j][4 * eg + 2];
+              v[3] = acc[i][j][4 * eg + 3];
+              const int row = i * 32 + (lane & 31);
+              const int col = j * 32 + 8 * eg + 4 * (lane >> 5);
+              *reinterpret_cast<floatx4*>(stage + (wn * 128 + row) * kFusedPitch + col) = v;
+            }
       }
       barrier();
       if (scans) {
         const int tb = t0 + half * steps;  // first step of this half
+        // steps tt < nv of the half lie inside the sequence
+        const int nv = max(0, min(steps, L - tb));
         // padding bits of the half's steps, one per lane, read with readlane
         int m_lo = 0, m_hi = 0;
         if (a.mask) {
-          const int t_lo = tb + lane, t_hi = tb + 64 + lane;
-          if (lane < steps && t_lo < L) m_lo = a.mask[(long long)t_lo * Bs + sb];
-          if (lane + 64 < steps && t_hi < L) m_hi = a.mask[(long long)t_hi * Bs + sb];
+          if (lane < nv) m_lo = a.mask[(long long)(tb + lane) * Bs + sb];
+          if (lane + 64 < nv) m_hi = a.mask[(long long)(tb + 64 + lane) * Bs + sb];
         }
-#pragma unroll 4
-        for (int s = 0; s < steps; ++s) {
-          const int tt = rev ? steps - 1 - s : s;
-          const int t = tb + tt;
-          if (t >= L) continue;
-          const float* sp = stage + (tt * BB + wave) * kFusedPitch + lane;
-          const float u0 = sp[0], u1 = sp[128 * kFusedPitch], u2 = sp[2 * 128 * kFusedPitch];
-          const float xh = sp[3 * 128 * kFusedPitch];
-          const int mbit = tt < 64 ? __builtin_amdgcn_readlane(m_lo, tt)
-                                   : __builtin_amdgcn_readlane(m_hi, tt - 64);
+        // pointers at the half's first step in the direction's order, moved
+        // one step per iteration: no branch and no index arithmetic in the
+        // loop, so the LDS reads of later steps are issued ahead of the chain
+        const int tt0 = rev ? nv - 1 : 0;
+        const int dtt = rev ? -1 : 1;
+        const float* sp = stage + (tt0 * BB + wave) * kFusedPitch + lane;
+        const long long o0 = ((long long)(tb + tt0) * Bs + sb) * nfeat + fidx;
+        float* hp = a.H + o0;
+        uint16_t* hbp = a.Hb ? a.Hb + o0 : nullptr;
+        const long long dstep = (long long)dtt * Bs * nfeat;
+        const int sstep = dtt * BB * kFusedPitch;
+        auto step = [&](int tt, float u0, float u1, float u2, float xh) {
+          const int mbit = __builtin_amdgcn_readlane(tt < 64 ? m_lo : m_hi, tt & 63);
           const float f = sigmoid_fast(fmaf(vf, c, u1 + bf));           // Eq. 1
           const float cn = fmaf(f, c, (1.0f - f) * u0);                 // Eq. 2
           const float r = sigmoid_fast(fmaf(vr, rn ? cn : c, u2 + br));  // Eq. 3
@@ -1041,9 +1029,29 @@ __global__ __launch_bounds__(DirectLine::THREADS, 1) void proj_scan_fwd_kernel(F
           } else {
             c = cn;
           }
-          const long long o = ((long long)t * Bs + sb) * nfeat + fidx;
-          __builtin_nontemporal_store(h, a.H + o);
-          if (a.Hb) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), a.Hb + o);
+          __builtin_nontemporal_store(h, hp);
+          if (hbp) {
+            __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), hbp);
+            hbp += dstep;
+          }
+          hp += dstep;
+        };
+        constexpr int P = 128 * kFusedPitch;  // floats between gate blocks
+        int s = 0;
+        // four steps at a time: their LDS reads first, then the dependent chain
+        for (; s + 4 <= nv; s += 4) {
+          float u[4][4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) u[q][e] = sp[q * sstep + e * P];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) step(tt0 + dtt * (s + q), u[q][0], u[q][1], u[q][2], u[q][3]);
+          sp += 4 * sstep;
+        }
+        for (; s < nv; ++s) {
+          step(tt0 + dtt * s, sp[0], sp[P], sp[2 * P], sp[3 * P]);
+          sp += sstep;
         }
       }
       barrier();  // before the next half or block overwrites the stage
@@ -1492,10 +1500,7 @@ hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, b
 hipError_t proj_scan_forward_launch(const FusedFwdArgs& a, hipStream_t st) {
   const int grid = a.ndir * a.ngroups * a.nbgroups;
   timing_before("proj_scan_fwd", st);
-  if (a.k == 3)
-    hipLaunchKernelGGL(proj_scan_fwd_kernel<3>, dim3(grid), dim3(DirectLine::THREADS), 0, st, a);
-  else
-    hipLaunchKernelGGL(proj_scan_fwd_kernel<4>, dim3(grid), dim3(DirectLine::THREADS), 0, st, a);
+  hipLaunchKernelGGL(proj_scan_fwd_kernel, dim3(grid), dim3(DirectLine::THREADS), 0, st, a);
   timing_after(st);
   return hipGetLastError();
 }

@@ -250,12 +250,14 @@ def test_round_bf16_argument_checks():
 
 def test_forward_without_u_needs_the_fused_path():
     lib = sru.lib()
-    assert lib.sru_forward_fused_available(4, 2, 64, 64, 0, 1) == 1
-    assert lib.sru_forward_fused_available(4, 2, 64, 64, 0, 0) == 0   # fp32 products
+    assert lib.sru_forward_fused_available(4, 2, 128, 64, 0, 1) == 1
+    assert lib.sru_forward_fused_available(4, 2, 128, 64, 0, 0) == 0  # fp32 products
+    assert lib.sru_forward_fused_available(4, 2, 64, 64, 0, 1) == 0   # k = 3
     assert lib.sru_forward_fused_available(4, 2, 60, 64, 0, 1) == 0   # d_in % 8
     assert lib.sru_forward_fused_available(4, 2, 64, 32, 0, 1) == 0   # d % 64
+    assert lib.sru_forward_fused_available(65, 2, 128, 64, 0, 1) == 0  # L > 64
     # U omitted: fp32 products, or C kept, leave U required
-    assert _fwd(lib, d_in=64, d=64, U=None, C=None) == E_NULL
-    assert _fwd(lib, d_in=64, d=64, gemm=1, U=None, C=FAKE) == E_NULL
+    assert _fwd(lib, d_in=128, d=64, U=None, C=None) == E_NULL
+    assert _fwd(lib, d_in=128, d=64, gemm=1, U=None, C=FAKE) == E_NULL
     # bf16, C omitted: U may be omitted (the call goes on to the workspace check)
-    assert _fwd(lib, d_in=64, d=64, gemm=1, U=None, C=None) == E_WS
+    assert _fwd(lib, d_in=128, d=64, gemm=1, U=None, C=None) == E_WS

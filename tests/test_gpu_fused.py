@@ -1,9 +1,9 @@
 """The fused projection + scan of inference (sru_forward with U and C
-omitted): H, c_last and the bf16 copy of H equal the unfused call's bit for
-bit (the scan reads the same fp32 projections, in the same order), across
-tile plans of 1 to 8 sequences, ragged step and sequence counts, k = 3 and 4,
-every direction, padding, c0 and the gate variants; and against the oracle,
-the linear recurrence included."""
+omitted; k = 4 and at most 64 steps): H, c_last and the bf16 copy of H equal
+the unfused call's bit for bit (the scan reads the same fp32 projections, in
+the same order), across tile plans of 4 and 8 sequences, ragged step and
+sequence counts, every direction, padding, c0 and the gate variants; and
+against the oracle, the linear recurrence included."""
 
 import numpy as np
 import pytest
@@ -17,13 +17,13 @@ from paper_1709_02755_amd.workloads import random_layer_case
 pytestmark = pytest.mark.gpu
 
 CASES = [
-    # (L, B, d_in, d, direction, masked, alpha, reset_new)
-    (256, 3, 64, 64, O.DIR_FWD, False, 1.0, False),     # 1 sequence per tile, 1 block
-    (300, 2, 128, 64, O.DIR_REV, True, 1.0, False),     # 2 blocks, ragged, k = 4
-    (100, 5, 128, 128, O.DIR_BI, True, 1.7, True),      # 2 per tile, ragged B
-    (64, 9, 512, 192, O.DIR_FWD, True, 1.0, False),     # 4 per tile (the FFN plan), k = 4
-    (17, 11, 64, 64, O.DIR_BI, False, float(np.sqrt(3.0)), False),  # 8 per tile
+    # (L, B, d_in, d, direction, masked, alpha, reset_new); d_in != d: k = 4
+    (64, 9, 512, 192, O.DIR_FWD, True, 1.0, False),     # 4 per tile (the FFN plan), ragged B
+    (50, 6, 128, 64, O.DIR_REV, True, 1.0, False),      # 4 per tile, ragged L
+    (40, 5, 256, 128, O.DIR_BI, True, 1.7, True),       # both directions, variants
+    (17, 11, 128, 64, O.DIR_BI, False, float(np.sqrt(3.0)), False),  # 8 per tile
     (1, 4, 256, 128, O.DIR_REV, False, 1.0, True),      # a single step
+    (64, 80, 512, 2048, O.DIR_FWD, False, 1.0, False),  # the Transformer-FFN shape
 ]
 
 
@@ -64,7 +64,7 @@ def test_fused_equals_unfused_bitwise(case):
 
 @pytest.mark.parametrize("linear", [False, True])
 def test_fused_matches_oracle(linear):
-    L, B, d_in, d, direction = 90, 6, 192, 128, O.DIR_BI
+    L, B, d_in, d, direction = 60, 6, 192, 128, O.DIR_BI
     c = _case(L, B, d_in, d, direction, True, 5 + linear)
     got = _run(c, direction, {}, fused=True, linear=linear)
     torch.cuda.synchronize()
@@ -78,7 +78,10 @@ def test_fused_matches_oracle(linear):
 
 
 def test_fused_not_available_keeps_u_required():
-    """Where the fused kernel does not apply (fp32 products, or d not a
-    multiple of 64) U stays required."""
-    assert not sru.fused_available(8, 2, 64, 64, O.DIR_FWD, O.GEMM_FP32)
-    assert not sru.fused_available(8, 2, 96, 96, O.DIR_FWD, O.GEMM_BF16)
+    """Where the fused kernel does not apply (fp32 products, k = 3, sequences
+    over 64 steps, d not a multiple of 64) U stays required."""
+    assert sru.fused_available(64, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
+    assert not sru.fused_available(8, 2, 128, 64, O.DIR_FWD, O.GEMM_FP32)
+    assert not sru.fused_available(8, 2, 64, 64, O.DIR_FWD, O.GEMM_BF16)   # k = 3
+    assert not sru.fused_available(65, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
+    assert not sru.fused_available(8, 2, 96, 32, O.DIR_FWD, O.GEMM_BF16)
