@@ -285,12 +285,16 @@ SRU_API int sru_scan_backward(const float* U, const float* X, const float* C, co
  * kernel i runs between events[2i] and events[2i+1].  When the events run
  * out, further kernels are not bracketed.  sru_timing_end disarms the hook
  * and returns the number of kernels bracketed; sru_timing_label(i) names
- * kernel i ("gemm_u", "gemm_dx", "gemm_dw" inside the layer calls,
- * "gemm_nt", "gemm_nn", "gemm_tn" from sru_gemm, "splitk_reduce",
- * "bf16_w", "bf16_x", "bf16_wt" (fp32 -> bf16 operand copies), "scan_fwd", "scan_bwd", "reduce_vb"; "" out of
- * range) until the next
- * sru_timing_begin.  The caller owns the events and reads them after
- * synchronising.  Disarmed (the default), launches record nothing.
+ * kernel i until the next sru_timing_begin ("" out of range):
+ *   products: "gemm_u", "gemm_dx", "gemm_dw" (layer calls), "gemm_t",
+ *     "gemm_dt", "gemm_dp", "gemm_dq" (low-rank calls), "gemm_nt",
+ *     "gemm_nn", "gemm_tn" (sru_gemm), "splitk_reduce";
+ *   bf16 operand copies: "bf16_w", "bf16_x", "bf16_wt", "bf16_q", "bf16_p",
+ *     "bf16_t";
+ *   scans: "scan_fwd", "scan_bwd", "reduce_vb", and "proj_scan_fwd" (the
+ *     fused projection + scan of inference).
+ * The caller owns the events and reads them after synchronising.
+ * Disarmed (the default), launches record nothing.
  * ------------------------------------------------------------------------- */
 SRU_API int sru_timing_begin(hipEvent_t* events, int capacity);
 SRU_API int sru_timing_end(void);

@@ -323,7 +323,7 @@ const char* sru_status_string(int status) {
 
 int sru_last_hip_error(void) { return g_last_hip_error; }
 
-int sru_version(void) { return (1 << 16) | 0; }
+int sru_version(void) { return (1 << 16) | 1; }
 
 size_t sru_forward_workspace_bytes(int L, int B, int d_in, int d, int direction, int gemm_dtype) {
   Dims s;
