@@ -81,15 +81,26 @@ class HipEvents:
 
 # ------------------------------------------------------------------ work model
 def kernel_work(w, splits, bf16):
-    """Algorithmic bytes / flops per launch of each kernel at workload w
-    (first layer shape; all layers of the stacks benchmarked match, except
-    that the top layer writes no bf16 copy of H: averaged over layers).
-    Bytes count each element read or written once: fp32 4 B, bf16 2 B."""
+    """Algorithmic bytes / flops per launch of each kernel at workload w,
+    averaged over the stack's layers (a layer above a bidirectional one
+    takes 2d inputs); the input rounding runs once per step, on the first
+    layer's input.  Bytes count each element read or written once: fp32
+    4 B, bf16 2 B."""
+    per = [_layer_work(w, li, splits, bf16) for li in range(w.layers)]
+    out = {}
+    for key in per[0]:
+        vals = [p[key] for p in per]
+        out[key] = {m: sum(v[m] for v in vals) / len(vals) for m in vals[0]}
+    out["bf16_x"] = per[0]["bf16_x"]
+    return out
+
+
+def _layer_work(w, li, splits, bf16):
+    """Algorithmic bytes / flops per launch of each kernel for layer li."""
     M = w.L * w.B
     nfeat = w.ndir * w.d
-    k = 3 if w.d_in == w.d else 4
+    K, k = w.layer_dims(li)
     N = w.ndir * k * w.d
-    K = w.d_in
     elems = M * nfeat
     du_b = 2.0 if bf16 else 4.0
     nq = 2 if w.linear else 4  # v/b sums per feature (no v in the linear variant)
