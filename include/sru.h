@@ -96,8 +96,11 @@ typedef enum { SRU_GEMM_FP32 = 0, SRU_GEMM_BF16 = 1 } sru_gemm_dtype;
  *     are then not read, dv_f and dv_r not written (all may be NULL), and
  *     reset_state has no effect (r reads no state).  The scans then run in
  *     parallel over chunks of time as well as over (b, direction, j), which
- *     keeps the GPU busy when B*ndir*d is small.  Anything else is
- *     SRU_E_FLAG. */
+ *     keeps the GPU busy when B*ndir*d is small; with fewer than 128*64
+ *     such lanes, time is also cut into segments run by separate
+ *     workgroups, whose maps are kept in the workspace (the queried sizes
+ *     always include this scratch, so the gated recurrence may be passed a
+ *     workspace sized for either).  Anything else is SRU_E_FLAG. */
 typedef enum { SRU_RESET_PREV = 0, SRU_RESET_NEW = 1 } sru_reset_state;
 typedef enum { SRU_RECURRENCE_GATED = 0, SRU_RECURRENCE_LINEAR = 1 } sru_recurrence;
 typedef struct {
@@ -117,7 +120,8 @@ SRU_API int sru_version(void);
 
 /* Workspace bytes sru_forward / sru_backward need for these sizes (0 means
  * none; NULL may then be passed).  Returns 0 for invalid arguments as well;
- * the compute call reports those. */
+ * the compute call reports those.  The sizes cover both recurrences; an
+ * fp32 forward of the gated recurrence needs none and accepts NULL. */
 SRU_API size_t sru_forward_workspace_bytes(int L, int B, int d_in, int d, int direction,
                                    int gemm_dtype);
 SRU_API size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int direction,
@@ -254,12 +258,16 @@ SRU_API int sru_gemm(int op, int gemm_dtype, int M, int N, int K,
 
 /* The fused forward scan (Algorithm 1 with the Eq. 3 reading) on a given U.
  * X is read only when k = 3 (d_in == d).  C, c_last and H_bf16 (bf16 copy
- * of H, 2-byte aligned) may be NULL. */
+ * of H, 2-byte aligned) may be NULL.  Workspace:
+ * sru_scan_forward_workspace_bytes, used by the linear recurrence only (the
+ * gated one accepts NULL); 256-byte aligned. */
+SRU_API size_t sru_scan_forward_workspace_bytes(int L, int B, int d_in, int d, int direction);
 SRU_API int sru_scan_forward(const float* U, const float* X,
                      const float* v_f, const float* v_r, const float* b_f, const float* b_r,
                      const float* c0, int L, int B, int d_in, int d, int direction,
                      const uint8_t* pad_mask, const sru_options* options, float* H, float* C,
-                     float* c_last, uint16_t* H_bf16, hipStream_t stream);
+                     float* c_last, uint16_t* H_bf16, void* workspace, size_t workspace_bytes,
+                     hipStream_t stream);
 
 /* The reverse-time gradient scan on a given U, C, dH.
  *   out: dU [L, B, ndir, k, d] (gradient w.r.t. the projections; when k = 4

@@ -144,11 +144,32 @@ int fused_seqs_per_tile(int L) {
   return bb;
 }
 
-// Forward workspace: bf16 mode keeps bf16 copies of W [N, d_in] and
-// X [M, d_in] (the operands of the projection).
-size_t fwd_workspace(const Dims& s, int gemm_dtype) {
+// Scratch of the scans.  The linear recurrence's scans cut time into
+// segments when the lanes alone cannot fill the chip, and keep the segments'
+// maps (and, backward, one row of partial sums per segment); the sizes
+// depend on L, B, d and the number of directions only, and the workspace
+// sizes cover both recurrences, so one size serves every option.
+sru::ScanShape linear_shape(const Dims& s) {
+  Opts op;
+  op.linear = 1;
+  return scan_shape(s, 0, op);
+}
+size_t scan_fwd_scratch(const Dims& s) {
+  return align_up(sru::scan_forward_scratch_bytes(linear_shape(s)));
+}
+size_t scan_bwd_partial(const Dims& s) {
+  return align_up(std::max(sru::scan_backward_partial_bytes(scan_shape(s, 0)),
+                           sru::scan_backward_partial_bytes(linear_shape(s))));
+}
+
+// Forward workspace: [bf16 copies of W [N, d_in] and X [M, d_in] (bf16
+// mode: the operands of the projection) | scan scratch].
+size_t fwd_bf16_bytes(const Dims& s, int gemm_dtype) {
   if (gemm_dtype != SRU_GEMM_BF16) return 0;
   return align_up(2 * (size_t)s.N * (size_t)s.d_in) + align_up(2 * (size_t)s.M * (size_t)s.d_in);
+}
+size_t fwd_workspace(const Dims& s, int gemm_dtype) {
+  return fwd_bf16_bytes(s, gemm_dtype) + scan_fwd_scratch(s);
 }
 
 // The dW product of sru_backward (the workspace is sized from this same
@@ -178,7 +199,7 @@ BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
   w.dxh = off;
   if (s.k == 3) off += align_up(sizeof(float) * (size_t)s.M * (size_t)s.nfeat);
   w.partial = off;
-  off += align_up(sizeof(float) * 4 * (size_t)s.B * (size_t)s.nfeat);
+  off += scan_bwd_partial(s);
   w.wt = off;
   if (bf16) off += align_up(2 * (size_t)s.N * (size_t)s.d_in);
   w.xb = off;
@@ -206,17 +227,21 @@ bool lowrank_dims_ok(const Dims& s, int dp, int gemm_dtype) {
   return s.d_in % 8 == 0 && dp % 8 == 0 && s.N % 8 == 0;
 }
 
+// [bf16 operands (bf16 mode) | scan scratch (last, so the gated
+// recurrence needs only the first scr bytes)]
 struct LrFwdLayout {
-  size_t xb, qt, tb, pb, total;
+  size_t xb, qt, tb, pb, scr, total;
 };
 LrFwdLayout lr_fwd_layout(const Dims& s, int dp, int gemm_dtype) {
   LrFwdLayout w{};
-  if (gemm_dtype != SRU_GEMM_BF16) return w;
   size_t off = 0;
-  w.xb = off; off += align_up(2 * (size_t)s.M * s.d_in);
-  w.qt = off; off += align_up(2 * (size_t)s.d_in * dp);  // Q^T [dp, d_in]
-  w.tb = off; off += align_up(2 * (size_t)s.M * dp);
-  w.pb = off; off += align_up(2 * (size_t)s.N * dp);
+  if (gemm_dtype == SRU_GEMM_BF16) {
+    w.xb = off; off += align_up(2 * (size_t)s.M * s.d_in);
+    w.qt = off; off += align_up(2 * (size_t)s.d_in * dp);  // Q^T [dp, d_in]
+    w.tb = off; off += align_up(2 * (size_t)s.M * dp);
+    w.pb = off; off += align_up(2 * (size_t)s.N * dp);
+  }
+  w.scr = off; off += scan_fwd_scratch(s);
   w.total = off;
   return w;
 }
@@ -247,7 +272,7 @@ LrBwdLayout lr_bwd_layout(const Dims& s, int dp, int gemm_dtype) {
   size_t off = 0;
   w.dU = off; off += align_up((bf16 ? 2 : 4) * (size_t)s.M * s.N);
   w.dxh = off; if (s.k == 3) off += align_up(4 * (size_t)s.M * s.nfeat);
-  w.partial = off; off += align_up(16 * (size_t)s.B * s.nfeat);
+  w.partial = off; off += scan_bwd_partial(s);
   w.dT = off; if (!bf16) off += align_up(4 * (size_t)s.M * dp);  // bf16: dT in bf16 only
   if (bf16) {
     w.pt = off; off += align_up(2 * (size_t)s.N * dp);  // P^T [dp, N]
@@ -323,7 +348,7 @@ const char* sru_status_string(int status) {
 
 int sru_last_hip_error(void) { return g_last_hip_error; }
 
-int sru_version(void) { return (1 << 16) | 1; }
+int sru_version(void) { return (1 << 16) | 2; }
 
 size_t sru_forward_workspace_bytes(int L, int B, int d_in, int d, int direction, int gemm_dtype) {
   Dims s;
@@ -366,7 +391,8 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
     if (p && !aligned4(p)) return SRU_E_ALIGN;
   if (int e = check_bf16_side(gemm_dtype, {X_bf16, W_bf16, H_bf16})) return e;
   const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
-  const size_t need = fwd_workspace(s, gemm_dtype);
+  const size_t bf16_bytes = fwd_bf16_bytes(s, gemm_dtype);
+  const size_t need = bf16_bytes + (op.linear && !fused ? scan_fwd_scratch(s) : 0);
   if (need > 0) {
     if (!workspace || workspace_bytes < need) return SRU_E_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
@@ -425,7 +451,8 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
   g.label = "gemm_u";
   if (int e = hip_status(sru::gemm_launch(g, stream))) return e;
 
-  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16};
+  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16,
+                     static_cast<unsigned char*>(workspace) + bf16_bytes};
   return hip_status(sru::scan_forward_launch(scan_shape(s, direction, op), a, stream));
 }
 
@@ -552,10 +579,17 @@ int sru_gemm(int op, int gemm_dtype, int M, int N, int K, const float* A, int ld
   return hip_status(sru::gemm_launch(g, stream));
 }
 
+size_t sru_scan_forward_workspace_bytes(int L, int B, int d_in, int d, int direction) {
+  Dims s;
+  if (make_dims(L, B, d_in, d, direction, s) != SRU_OK) return 0;
+  return scan_fwd_scratch(s);
+}
+
 int sru_scan_forward(const float* U, const float* X, const float* v_f, const float* v_r,
                      const float* b_f, const float* b_r, const float* c0, int L, int B, int d_in,
                      int d, int direction, const uint8_t* pad_mask, const sru_options* options,
-                     float* H, float* C, float* c_last, uint16_t* H_bf16, hipStream_t stream) {
+                     float* H, float* C, float* c_last, uint16_t* H_bf16, void* workspace,
+                     size_t workspace_bytes, hipStream_t stream) {
   Dims s;
   int st = make_dims(L, B, d_in, d, direction, s);
   if (st != SRU_OK) return st;
@@ -567,14 +601,19 @@ int sru_scan_forward(const float* U, const float* X, const float* v_f, const flo
   for (const void* p : ptrs)
     if (p && !aligned4(p)) return SRU_E_ALIGN;
   if ((reinterpret_cast<uintptr_t>(H_bf16) & 1) != 0) return SRU_E_ALIGN;
-  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16};
+  const size_t need = op.linear ? scan_fwd_scratch(s) : 0;
+  if (need > 0) {
+    if (!workspace || workspace_bytes < need) return SRU_E_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
+  }
+  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16, workspace};
   return hip_status(sru::scan_forward_launch(scan_shape(s, direction, op), a, stream));
 }
 
 size_t sru_scan_backward_workspace_bytes(int L, int B, int d_in, int d, int direction) {
   Dims s;
   if (make_dims(L, B, d_in, d, direction, s) != SRU_OK) return 0;
-  return align_up(sru::scan_backward_partial_bytes(scan_shape(s, direction)));
+  return scan_bwd_partial(s);
 }
 
 int sru_scan_backward(const float* U, const float* X, const float* C, const float* dH,
@@ -647,8 +686,9 @@ int sru_forward_lowrank(const float* X, const float* Q, const float* P, const fl
   if (int e = check_bf16_side(gemm_dtype, {X_bf16, T_bf16, H_bf16})) return e;
   const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
   const LrFwdLayout lay = lr_fwd_layout(s, dp, gemm_dtype);
-  if (lay.total > 0) {
-    if (!workspace || workspace_bytes < lay.total) return SRU_E_WORKSPACE;
+  const size_t need = op.linear ? lay.total : lay.scr;
+  if (need > 0) {
+    if (!workspace || workspace_bytes < need) return SRU_E_WORKSPACE;
     if ((reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)) != 0) return SRU_E_ALIGN;
   }
   unsigned char* ws = static_cast<unsigned char*>(workspace);
@@ -692,7 +732,7 @@ int sru_forward_lowrank(const float* X, const float* Q, const float* P, const fl
     if (int e = hip_status(sru::gemm_launch(gu, stream))) return e;
   }
 
-  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16};
+  sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16, ws + lay.scr};
   return hip_status(sru::scan_forward_launch(scan_shape(s, direction, op), a, stream));
 }
 

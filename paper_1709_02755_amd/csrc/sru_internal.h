@@ -96,6 +96,13 @@ struct ScanShape {
                   // v_f, v_r, dv_f, dv_r are then unused
 };
 
+// Work plan of the time-chunked scans of the linear recurrence: nw waves per
+// workgroup, groups lane groups of 64, time cut into nseg segments of
+// seg_steps steps (whole blocks), one workgroup per (group, segment).
+struct LinPlan {
+  int nw, groups, nseg, seg_steps;
+};
+
 struct ScanFwdArgs {
   const float* U;
   const float* X;
@@ -109,6 +116,7 @@ struct ScanFwdArgs {
   float* C;
   float* c_last;
   uint16_t* Hb;  // optional bf16 (RNE) copy of H
+  void* scratch;  // linear recurrence: the segment maps (scan_forward_scratch_bytes)
 };
 
 struct ScanBwdArgs {
@@ -126,7 +134,8 @@ struct ScanBwdArgs {
   void* dU;        // fp32, or bf16 bits when du_bf16
   bool du_bf16;
   float* dxh;
-  float* partial;  // [B, 4, ndir*d] per-sequence sums of the v/b gradients
+  float* partial;  // per-sequence sums of the v/b gradients (and, for the
+                   // linear recurrence, the segment maps): scan_backward_partial_bytes
   float* dc0;
   float* dv_f;
   float* dv_r;
@@ -135,6 +144,9 @@ struct ScanBwdArgs {
 };
 
 hipError_t scan_forward_launch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t stream);
+// Scratch the forward scan needs (the linear recurrence's segment maps; the
+// gated one needs none).  Depends on the sizes only.
+size_t scan_forward_scratch_bytes(const ScanShape& s);
 // Enqueues the reverse scan and the fixed-order reduction of `partial`.
 hipError_t scan_backward_launch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t stream);
 size_t scan_backward_partial_bytes(const ScanShape& s);

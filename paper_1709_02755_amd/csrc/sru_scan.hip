@@ -273,6 +273,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
 // block's incoming state.  The backward pass does the
 // same on the carried gradient, g -> f (g + dh r), in reverse step order.
 // No wave leaves early: every wave reaches every barrier.
+//
+// When the lane groups alone would leave CUs idle (small B*ndir*d), time is
+// also cut into segments of whole blocks, one workgroup per (group,
+// segment).  A first kernel folds every segment but the last into its map;
+// the chunked kernel then starts each segment from the maps of the segments
+// before it composed onto c0 (dc_last backward).  That reads two of the
+// inputs twice, and fills the chip.
 constexpr int kLinMaxWaves = 16;
 
 // Workgroup barrier for LDS hand-offs: waits for this wave's LDS accesses
@@ -291,10 +298,10 @@ __device__ __forceinline__ void lds_barrier() {
 // from threadIdx.x mod 64.  Lanes past the end (live = false) take the last
 // lane's coordinates, so every address they form is in range; they store
 // nothing.
-__device__ __forceinline__ bool decode_lane_lin(const ScanShape& s, Lane& ln) {
+__device__ __forceinline__ bool decode_lane_lin(const ScanShape& s, Lane& ln, int group) {
   const int nfeat = s.ndir * s.d;
   const int total = s.B * nfeat;
-  const int gid = blockIdx.x * 64 + (threadIdx.x & 63);
+  const int gid = group * 64 + (threadIdx.x & 63);
   const bool live = gid < total;
   ln.gid = live ? gid : total - 1;
   ln.b = ln.gid / nfeat;
@@ -305,13 +312,104 @@ __device__ __forceinline__ bool decode_lane_lin(const ScanShape& s, Lane& ln) {
   return live;
 }
 
+// The backward's segment maps follow its partial rows [nseg * B, 4, ndir*d].
+__host__ __device__ __forceinline__ float2* lin_bwd_maps(float* partial, const ScanShape& s,
+                                                        const LinPlan& pl) {
+  return reinterpret_cast<float2*>(partial + (long long)pl.nseg * s.B * 4 * s.ndir * s.d);
+}
+
+// Segment maps: every segment but the last folded into (A, S) per lane, in
+// the order of the chunked kernels' first phase (chunks of CH steps per wave,
+// the waves' maps composed in wave order, block after block).  MAPB selects
+// the backward's map, g -> f (g + dh r), in reverse step order.
+template <bool MASK, bool MAPB, int CH>
+__global__ __launch_bounds__(64 * kLinMaxWaves) void scan_lin_maps_kernel(ScanShape s,
+                                                                          ScanFwdArgs fa,
+                                                                          ScanBwdArgs ba,
+                                                                          LinPlan pl) {
+  __shared__ float2 red[kLinMaxWaves][64];
+  Lane ln;
+  const int group = blockIdx.x % pl.groups, seg = blockIdx.x / pl.groups;
+  const bool live = decode_lane_lin(s, ln, group);
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int NW = blockDim.x >> 6;
+  const int L = s.L;
+  const int d = s.d;
+  const long long nfeat = (long long)s.ndir * s.d;
+  const int KB = s.k;
+  const long long u_step = (long long)s.B * s.ndir * KB * s.d;
+  const long long h_step = (long long)s.B * nfeat;
+  const float* up = (MAPB ? ba.U : fa.U) + ((long long)ln.b * s.ndir + ln.dir) * KB * s.d + ln.j;
+  const uint8_t* mk = MAPB ? ba.mask : fa.mask;
+  const uint8_t* mp = MASK ? mk + ln.b : nullptr;
+  const float* dhp = MAPB ? ba.dH + ln.gid : nullptr;
+  const float bf = (MAPB ? ba.b_f : fa.b_f)[ln.fidx];
+  const float br = MAPB ? ba.b_r[ln.fidx] : 0.0f;
+  // time index of a position of this segment in the pass's order
+  auto tof = [&](int st) {
+    const int pos = MAPB ? L - 1 - st : st;  // forward-order position
+    return (long long)(ln.rev ? L - 1 - pos : pos);
+  };
+  const int sbeg = seg * pl.seg_steps, send = min(L, sbeg + pl.seg_steps);
+  float A = 1.0f, S = 0.0f;
+  for (int base = sbeg; base < send; base += NW * CH) {
+    const int st0 = base + w * CH;
+    float r1[CH], r2[CH], rd[CH];
+    bool act[CH];
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const long long t = tof(st0 + i < send ? st0 + i : send - 1);
+      r1[i] = __builtin_nontemporal_load(up + t * u_step + d);
+      if constexpr (MAPB) {
+        r2[i] = __builtin_nontemporal_load(up + t * u_step + 2 * d);
+        rd[i] = __builtin_nontemporal_load(dhp + t * h_step);
+      } else {
+        r2[i] = __builtin_nontemporal_load(up + t * u_step);  // u0
+        rd[i] = 0.0f;
+      }
+      act[i] = st0 + i < send;
+      if constexpr (MASK) act[i] = act[i] && mp[t * s.B] == 0;
+    }
+    float Aw = 1.0f, Sw = 0.0f;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const float f = sigmoid_fast(r1[i] + bf);
+      if (act[i]) {
+        if constexpr (MAPB) {
+          const float r = sigmoid_fast(r2[i] + br);
+          Sw = f * fmaf(rd[i], r, Sw);
+        } else {
+          Sw = fmaf(f, Sw, (1.0f - f) * r2[i]);
+        }
+        Aw *= f;
+      }
+    }
+    red[w][lane] = make_float2(Aw, Sw);
+    lds_barrier();
+    for (int m = 0; m < NW; ++m) {
+      const float2 q = red[m][lane];
+      S = fmaf(q.x, S, q.y);
+      A *= q.x;
+    }
+    lds_barrier();  // before the next block's chunk maps
+  }
+  if (w == 0 && live) {
+    float2* out = MAPB ? lin_bwd_maps(ba.partial, s, pl)
+                       : reinterpret_cast<float2*>(fa.scratch);
+    out[((long long)group * pl.nseg + seg) * 64 + lane] = make_float2(A, S);
+  }
+}
+
 template <int KB, bool MASK, bool STORE_C, bool STORE_HB, int CH>
 __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_fwd_lin_kernel(ScanShape s,
-                                                                         ScanFwdArgs a) {
+                                                                         ScanFwdArgs a,
+                                                                         LinPlan pl) {
   __shared__ float2 agg[2][kLinMaxWaves][64];  // (A, S) per block parity, wave, lane
   __shared__ float carry_lds[2][64];           // block's final state, per parity
   Lane ln;
-  const bool live = decode_lane_lin(s, ln);
+  const int group = blockIdx.x % pl.groups, seg = blockIdx.x / pl.groups;
+  const bool live = decode_lane_lin(s, ln, group);
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int NW = blockDim.x >> 6;
@@ -326,18 +424,28 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_fwd_lin_kernel(ScanSha
   const uint8_t* mp = MASK ? a.mask + ln.b : nullptr;
   const float bf = a.b_f[ln.fidx], br = a.b_r[ln.fidx];
   const float alpha = s.alpha;
+  // this workgroup's steps [sbeg, send) of the direction's order; the
+  // incoming state: c0 through the maps of the segments before this one
+  const int sbeg = seg * pl.seg_steps, send = min(L, sbeg + pl.seg_steps);
   float carry = a.c0 ? a.c0[ln.gid] : 0.0f;
+  {
+    const float2* sm = reinterpret_cast<const float2*>(a.scratch) + (long long)group * pl.nseg * 64;
+    for (int q = 0; q < seg; ++q) {
+      const float2 m = sm[q * 64 + lane];
+      carry = fmaf(m.x, carry, m.y);
+    }
+  }
   auto tindex = [&](int st) { return ln.rev ? L - 1 - st : st; };
 
   int blk = 0;
-  for (int base = 0; base < L; base += NW * CH, ++blk) {
+  for (int base = sbeg; base < send; base += NW * CH, ++blk) {
     const int p = blk & 1;
     const int st0 = base + w * CH;
     float ru0[CH], rf[CH], ru2[CH], rx[CH];
     bool act[CH];
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
-      const int st = st0 + i < L ? st0 + i : L - 1;
+      const int st = st0 + i < send ? st0 + i : send - 1;
       const long long t = tindex(st);
       const float* u = up + t * u_step;
       ru0[i] = __builtin_nontemporal_load(u);
@@ -345,7 +453,7 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_fwd_lin_kernel(ScanSha
       ru2[i] = __builtin_nontemporal_load(u + 2 * d);
       if constexpr (KB == 4) rx[i] = __builtin_nontemporal_load(u + 3 * d);
       else rx[i] = xp[t * x_step];
-      act[i] = st0 + i < L;
+      act[i] = st0 + i < send;
       if constexpr (MASK) act[i] = act[i] && mp[t * s.B] == 0;
     }
     // 1. this chunk's map
@@ -371,7 +479,7 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_fwd_lin_kernel(ScanSha
     // 3. rescan
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
-      if (st0 + i >= L) break;
+      if (st0 + i >= send) break;
       const long long t = tindex(st0 + i);
       const float f = rf[i];
       const float cn = fmaf(f, c, (1.0f - f) * ru0[i]);            // Eq. 2
@@ -388,10 +496,10 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_fwd_lin_kernel(ScanSha
       }
     }
     // the wave holding the block's last step publishes the rescanned state
-    const int w_last = (min(L - base, NW * CH) - 1) / CH;
+    const int w_last = (min(send - base, NW * CH) - 1) / CH;
     if (w == w_last) {
       carry_lds[p][lane] = c;
-      if (base + NW * CH >= L && live && a.c_last) a.c_last[ln.gid] = c;
+      if (base + NW * CH >= send && send == L && live && a.c_last) a.c_last[ln.gid] = c;
     }
   }
 }
@@ -406,11 +514,13 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_fwd_lin_kernel(ScanSha
 // over the workgroup's waves.
 template <int KB, bool MASK, bool DUB, int CH>
 __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_lin_kernel(ScanShape s,
-                                                                         ScanBwdArgs a) {
+                                                                         ScanBwdArgs a,
+                                                                         LinPlan pl) {
   __shared__ float2 agg[2][kLinMaxWaves][64];
   __shared__ float carry_lds[2][64];
   Lane ln;
-  const bool live = decode_lane_lin(s, ln);
+  const int group = blockIdx.x % pl.groups, seg = blockIdx.x / pl.groups;
+  const bool live = decode_lane_lin(s, ln, group);
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int NW = blockDim.x >> 6;
@@ -431,7 +541,17 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_lin_kernel(ScanSha
   const float bf = a.b_f[ln.fidx], br = a.b_r[ln.fidx];
   const float alpha = s.alpha;
   const float c0v = a.c0 ? a.c0[ln.gid] : 0.0f;
+  // processing indices [sbeg, send) of this workgroup; the incoming
+  // gradient: dc_last through the maps of the segments before this one
+  const int sbeg = seg * pl.seg_steps, send = min(L, sbeg + pl.seg_steps);
   float carry = a.dc_last ? a.dc_last[ln.gid] : 0.0f;
+  {
+    const float2* sm = lin_bwd_maps(a.partial, s, pl) + (long long)group * pl.nseg * 64;
+    for (int q = 0; q < seg; ++q) {
+      const float2 m = sm[q * 64 + lane];
+      carry = fmaf(m.x, carry, m.y);
+    }
+  }
   float sum_df = 0.f, sum_dr = 0.f;
   // time index of processing index i (clamped into range)
   auto tproc = [&](int i) {
@@ -440,7 +560,7 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_lin_kernel(ScanSha
   };
 
   int blk = 0;
-  for (int base = 0; base < L; base += NW * CH, ++blk) {
+  for (int base = sbeg; base < send; base += NW * CH, ++blk) {
     const int p = blk & 1;
     const int i0 = base + w * CH;
     float ru0[CH], rf[CH], rr[CH], rx[CH], rdh[CH], rc[CH + 1];
@@ -456,7 +576,7 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_lin_kernel(ScanSha
       else rx[m] = xp[t * x_step];
       rdh[m] = __builtin_nontemporal_load(dhp + t * h_step);
       rc[m] = cpp[t * h_step];
-      act[m] = i0 + m < L;
+      act[m] = i0 + m < send;
       if constexpr (MASK) act[m] = act[m] && mp[t * s.B] == 0;
     }
     {
@@ -487,7 +607,7 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_lin_kernel(ScanSha
     // 3. rescan
 #pragma unroll
     for (int m = 0; m < CH; ++m) {
-      if (i0 + m >= L) break;
+      if (i0 + m >= send) break;
       const long long t = tproc(i0 + m);
       const float f = rf[m], r = rr[m];
       const float c_t = rc[m];
@@ -520,10 +640,10 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_lin_kernel(ScanSha
         else __builtin_nontemporal_store(dx, a.dxh + ln.gid + t * h_step);
       }
     }
-    const int w_last = (min(L - base, NW * CH) - 1) / CH;
+    const int w_last = (min(send - base, NW * CH) - 1) / CH;
     if (w == w_last) {
       carry_lds[p][lane] = g;
-      if (base + NW * CH >= L && live && a.dc0) a.dc0[ln.gid] = g;
+      if (base + NW * CH >= send && send == L && live && a.dc0) a.dc0[ln.gid] = g;
     }
   }
   // fixed-order sum of the waves' b sums (agg is free: every wave is past
@@ -538,7 +658,8 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_lin_kernel(ScanSha
       sdf += q.x;
       sdr += q.y;
     }
-    float* part = a.partial + (long long)ln.b * 4 * nfeat + ln.fidx;
+    // one row of partials per (segment, sequence)
+    float* part = a.partial + ((long long)seg * s.B + ln.b) * 4 * nfeat + ln.fidx;
     part[2 * nfeat] = sdf;
     part[3 * nfeat] = sdr;
   }
@@ -585,23 +706,42 @@ constexpr int kBwdPF = 6;
 constexpr int kFwdLinCH = 12;
 constexpr int kBwdLinCH = 8;
 
-// Waves per workgroup of the chunked scans: enough chunks that the launch
-// holds about 4096 waves (4 per SIMD), at most 16 per workgroup and no more
-// chunks than the sequence has steps.
-int lin_waves(const ScanShape& s, int ch) {
-  const int groups = (s.B * s.ndir * s.d + 63) / 64;
+// Plan of the chunked scans: waves per workgroup so that the launch holds
+// about 4096 waves (4 per SIMD), at most 16 per workgroup and no more chunks
+// than the sequence has steps.  With lane groups for fewer than half the CUs,
+// time is also cut into segments of whole blocks, for up to about two
+// workgroups per CU: the segments' maps cost an extra pass over half of the
+// scan's input, which pays where the scan is bound by its serial latency
+// and not where half the chip already streams from HBM.
+LinPlan lin_plan(const ScanShape& s, int ch) {
+  LinPlan pl{};
+  pl.groups = (s.B * s.ndir * s.d + 63) / 64;
   int nw = 1;
-  while (nw < kLinMaxWaves && groups * nw * 2 <= 4096 && nw * ch < s.L) nw *= 2;
-  return nw;
+  while (nw < kLinMaxWaves && pl.groups * nw * 2 <= 4096 && nw * ch < s.L) nw *= 2;
+  pl.nw = nw;
+  const int block = nw * ch;
+  const int nblk = (s.L + block - 1) / block;
+  int nseg = 1;
+  if (pl.groups < 128) nseg = std::min(nblk, (512 + pl.groups - 1) / pl.groups);
+  pl.seg_steps = ((nblk + nseg - 1) / nseg) * block;
+  pl.nseg = (s.L + pl.seg_steps - 1) / pl.seg_steps;
+  return pl;
 }
 
 template <int KB, bool MASK, bool STORE_C, bool STORE_HB>
 hipError_t fwd_lin_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st) {
-  const int grid = (s.B * s.ndir * s.d + 63) / 64;
-  const int nw = lin_waves(s, kFwdLinCH);
+  const LinPlan pl = lin_plan(s, kFwdLinCH);
+  if (pl.nseg > 1) {
+    timing_before("scan_maps", st);
+    hipLaunchKernelGGL((scan_lin_maps_kernel<MASK, false, kFwdLinCH>),
+                       dim3(pl.groups * (pl.nseg - 1)), dim3(64 * pl.nw), 0, st, s, a,
+                       ScanBwdArgs{}, pl);
+    timing_after(st);
+    if (hipError_t e = hipGetLastError()) return e;
+  }
   timing_before("scan_fwd", st);
-  hipLaunchKernelGGL((scan_fwd_lin_kernel<KB, MASK, STORE_C, STORE_HB, kFwdLinCH>), dim3(grid),
-                     dim3(64 * nw), 0, st, s, a);
+  hipLaunchKernelGGL((scan_fwd_lin_kernel<KB, MASK, STORE_C, STORE_HB, kFwdLinCH>),
+                     dim3(pl.groups * pl.nseg), dim3(64 * pl.nw), 0, st, s, a, pl);
   timing_after(st);
   return hipGetLastError();
 }
@@ -641,17 +781,28 @@ template <int KB, bool MASK>
 hipError_t bwd_dispatch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t st) {
   const int lanes = s.B * s.ndir * s.d;
   const int grid = (lanes + kScanThreads - 1) / kScanThreads;
-  timing_before("scan_bwd", st);
   if (s.linear) {
-    const int g = (lanes + 63) / 64;
-    const int nw = lin_waves(s, kBwdLinCH);
+    const LinPlan pl = lin_plan(s, kBwdLinCH);
+    if (pl.nseg > 1) {
+      timing_before("scan_maps", st);
+      hipLaunchKernelGGL((scan_lin_maps_kernel<MASK, true, kBwdLinCH>),
+                         dim3(pl.groups * (pl.nseg - 1)), dim3(64 * pl.nw), 0, st, s,
+                         ScanFwdArgs{}, a, pl);
+      timing_after(st);
+      if (hipError_t e = hipGetLastError()) return e;
+    }
+    timing_before("scan_bwd", st);
     if (a.du_bf16)
-      hipLaunchKernelGGL((scan_bwd_lin_kernel<KB, MASK, true, kBwdLinCH>), dim3(g), dim3(64 * nw),
-                         0, st, s, a);
+      hipLaunchKernelGGL((scan_bwd_lin_kernel<KB, MASK, true, kBwdLinCH>),
+                         dim3(pl.groups * pl.nseg), dim3(64 * pl.nw), 0, st, s, a, pl);
     else
-      hipLaunchKernelGGL((scan_bwd_lin_kernel<KB, MASK, false, kBwdLinCH>), dim3(g),
-                         dim3(64 * nw), 0, st, s, a);
-  } else if (a.du_bf16 && s.reset_new)
+      hipLaunchKernelGGL((scan_bwd_lin_kernel<KB, MASK, false, kBwdLinCH>),
+                         dim3(pl.groups * pl.nseg), dim3(64 * pl.nw), 0, st, s, a, pl);
+    timing_after(st);
+    return hipGetLastError();
+  }
+  timing_before("scan_bwd", st);
+  if (a.du_bf16 && s.reset_new)
     hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, true, true, kBwdPF>), dim3(grid),
                        dim3(kScanThreads), 0, st, s, a);
   else if (a.du_bf16)
@@ -676,7 +827,16 @@ hipError_t scan_forward_launch(const ScanShape& s, const ScanFwdArgs& a, hipStre
 }
 
 size_t scan_backward_partial_bytes(const ScanShape& s) {
-  return sizeof(float) * 4ull * (size_t)s.B * (size_t)s.ndir * (size_t)s.d;
+  const size_t row = sizeof(float) * 4ull * (size_t)s.ndir * (size_t)s.d;
+  if (!s.linear) return row * (size_t)s.B;
+  const LinPlan pl = lin_plan(s, kBwdLinCH);
+  return row * (size_t)s.B * (size_t)pl.nseg + sizeof(float2) * 64ull * pl.groups * pl.nseg;
+}
+
+size_t scan_forward_scratch_bytes(const ScanShape& s) {
+  if (!s.linear) return 0;
+  const LinPlan pl = lin_plan(s, kFwdLinCH);
+  return pl.nseg > 1 ? sizeof(float2) * 64ull * pl.groups * pl.nseg : 0;
 }
 
 hipError_t scan_backward_launch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t st) {
@@ -688,8 +848,10 @@ hipError_t scan_backward_launch(const ScanShape& s, const ScanBwdArgs& a, hipStr
   const int nfeat = s.ndir * s.d;
   const int qlo = s.linear ? 2 : 0;
   const int grid = ((4 - qlo) * nfeat + 63) / 64;
+  // the linear scans leave one row of partials per (segment, sequence)
+  const int rows = s.linear ? s.B * lin_plan(s, kBwdLinCH).nseg : s.B;
   timing_before("reduce_vb", st);
-  hipLaunchKernelGGL(reduce_vb_kernel, dim3(grid), dim3(64 * kVbWaves), 0, st, a.partial, s.B,
+  hipLaunchKernelGGL(reduce_vb_kernel, dim3(grid), dim3(64 * kVbWaves), 0, st, a.partial, rows,
                      nfeat, qlo, a.dv_f, a.dv_r, a.db_f, a.db_r);
   timing_after(st);
   return hipGetLastError();

@@ -42,7 +42,8 @@ _SIGNATURES = {
                      + [_P, _S, _P]),
     "sru_gemm_workspace_bytes": (_S, [_I] * 5),
     "sru_gemm": (_I, [_I] * 5 + [_P, _I, _P, _I, _P, _I] + [_P, _S, _P]),
-    "sru_scan_forward": (_I, [_P] * 7 + [_I] * 5 + [_P, _P] + [_P] * 3 + [_P] + [_P]),
+    "sru_scan_forward_workspace_bytes": (_S, [_I] * 5),
+    "sru_scan_forward": (_I, [_P] * 7 + [_I] * 5 + [_P, _P] + [_P] * 3 + [_P] + [_P, _S, _P]),
     "sru_scan_backward_workspace_bytes": (_S, [_I] * 5),
     "sru_scan_backward": (_I, [_P] * 10 + [_I] * 5 + [_P, _P] + [_P] * 7 + [_P, _S, _P]),
     "sru_forward_lowrank_workspace_bytes": (_S, [_I] * 7),
@@ -356,7 +357,8 @@ def gemm(op, A, B, M, N, K, gemm_dtype=GEMM_FP32, C=None, ws=None):
 
 
 def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
-                 store_c=True, out=None, highway_scale=1.0, reset_new=False, linear=False):
+                 store_c=True, out=None, ws=None, highway_scale=1.0, reset_new=False,
+                 linear=False):
     L, B, ndir, k, d = U.shape
     d_in = X.shape[2] if X is not None else (d if k == 3 else -1)
     if k == 4 and X is None:
@@ -367,11 +369,14 @@ def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None
         out = dict(H=torch.empty((L, B, ndir * d), device=dev),
                    C=torch.empty((L, B, ndir * d), device=dev) if store_c else None,
                    c_last=torch.empty((B, ndir * d), device=dev))
+    need = lib().sru_scan_forward_workspace_bytes(L, B, d_in, d, direction)
+    if ws is None:
+        ws = workspace(need, dev)
     st = lib().sru_scan_forward(_ptr(U), _ptr(X), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r),
                                 _ptr(c0), L, B, d_in, d, direction, _ptr(mask),
                                 _options(highway_scale, reset_new, linear),
                                 _ptr(out["H"]), _ptr(out.get("C")), _ptr(out.get("c_last")),
-                                _ptr(out.get("H_bf16")), _stream())
+                                _ptr(out.get("H_bf16")), _ptr(ws), need, _stream())
     _check(st, "sru_scan_forward")
     return out
 

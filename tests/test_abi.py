@@ -153,11 +153,11 @@ def test_scan_argument_checks():
     lib = sru.lib()
     f = lib.sru_scan_forward
     assert f(FAKE, None, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 0, None, None, FAKE, None,
-             None, None, None) == E_NULL                   # k = 3 needs X
+             None, None, None, 0, None) == E_NULL          # k = 3 needs X
     assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 9, None, None, FAKE, None,
-             None, None, None) == E_FLAG
+             None, None, None, 0, None) == E_FLAG
     assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 8, 8, 0, None, None, FAKE, None,
-             None, ctypes.c_void_p(0x10001), None) == E_ALIGN  # bf16 H: 2-byte aligned
+             None, ctypes.c_void_p(0x10001), None, 0, None) == E_ALIGN  # bf16 H: 2-byte aligned
     b = lib.sru_scan_backward
     args = [FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, 4, 2, 16, 8, 0, None,
             None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, None]
@@ -202,7 +202,18 @@ def test_linear_recurrence_needs_no_v():
     assert _fwd(lib, v_f=None, v_r=None) == E_NULL
     assert _bwd(lib, dv_r=None) == E_NULL
     assert lib.sru_scan_forward(FAKE, FAKE, None, None, FAKE, FAKE, None, 4, 2, 8, 8, 0, None,
-                                lin, FAKE_MIS, None, None, None, None) == E_ALIGN
+                                lin, FAKE_MIS, None, None, None, None, 0, None) == E_ALIGN
+    # few lanes: the linear scans cut time into segments and need scratch,
+    # which the gated scan does not
+    need = lib.sru_scan_forward_workspace_bytes(4000, 2, 64, 64, 0)
+    assert need > 0 and need % 256 == 0
+    fargs = [FAKE, FAKE, None, None, FAKE, FAKE, None, 4000, 2, 64, 64, 0, None, lin, FAKE, None,
+             None, None, None, 0, None]
+    assert lib.sru_scan_forward(*fargs) == E_WS
+    fargs[18], fargs[19] = FAKE_MIS, need
+    assert lib.sru_scan_forward(*fargs) == E_ALIGN      # 256-byte aligned workspace
+    # many lanes: one segment, no scratch
+    assert lib.sru_scan_forward_workspace_bytes(64, 64, 1024, 1024, 0) == 0
     args = [FAKE, FAKE, FAKE, FAKE, None, None, None, FAKE, FAKE, None, 4, 2, 8, 8, 0, None,
             lin, FAKE, FAKE, None, None, FAKE, FAKE, None, None, 0, None]
     assert lib.sru_scan_backward(*args) == E_WS

@@ -1,9 +1,11 @@
 """GPU parity of the linear recurrence (ablation (1) of Sec. 4.5: v * c_{t-1}
 removed from both gates) against the oracle.  The GPU scans this variant in
-parallel over chunks of time; the cases below span one chunk per lane up to
-16 chunks per workgroup, several time blocks with a ragged last block,
-lanes past the end of the last workgroup, masks, both directions, k = 3 and
-4, and the layer calls in fp32 and bf16."""
+parallel over chunks of time, and with few lanes also over segments of time
+run by separate workgroups; the cases below span one chunk per lane up to
+16 chunks per workgroup, several time blocks with a ragged last block, one
+to 32 segments with a short last one, lanes past the end of the last
+workgroup, masks, both directions, k = 3 and 4, and the layer calls in fp32
+and bf16."""
 
 import numpy as np
 import pytest
@@ -24,6 +26,8 @@ SCAN_CASES = [
     (400, 32, 128, 128, O.DIR_BI, True),  # workload-2 shape: 16 chunks, ragged blocks
     (1000, 1, 130, 65, O.DIR_REV, True),  # many blocks, a partial workgroup, k = 4
     (37, 64, 1024, 1024, O.DIR_FWD, True),  # many lanes: few chunks per workgroup
+    (4000, 2, 64, 64, O.DIR_FWD, True),   # two lane groups: 21 / 32 segments
+    (777, 3, 96, 96, O.DIR_BI, False),    # 9 lane groups: 5 / 7 segments, short last one
 ]
 
 

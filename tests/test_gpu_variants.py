@@ -111,7 +111,7 @@ def test_default_options_equal_no_options():
         st = sru.lib().sru_scan_forward(sru._ptr(Ud), sru._ptr(Xd), *[sru._ptr(t) for t in p],
                                         sru._ptr(dev(c["c0"])), L, B, d, d, O.DIR_BI,
                                         sru._ptr(dev(c["mask"])), opts, sru._ptr(H), None, None,
-                                        None, sru._stream())
+                                        None, None, 0, sru._stream())
         assert st == 0
         outs.append(H)
     torch.cuda.synchronize()
