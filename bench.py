@@ -173,17 +173,80 @@ def source_hash():
     return h.hexdigest()[:16]
 
 
-def pmc_traffic(label):
+def pmc_traffic(label, workload):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if
-    it was taken on the current kernel sources; else None."""
+    it was taken on the current kernel sources and this workload; else None."""
     p = os.path.join(ROOT, "profiles", "pmc_traffic.json")
     if not os.path.exists(p):
         return None
     d = json.load(open(p))
-    if d.get("source_hash") != source_hash():
+    if d.get("source_hash") != source_hash() or d.get("workload") != workload:
         return None
     k = d.get("kernels", {}).get(label)
     return None if k is None else k.get("hbm_bytes_per_launch")
+
+
+def cold_scans(w, st, X, dH, mask, reps, highway_scale, reset_new):
+    """The two scans of layer 0, timed cold: a 512 MiB buffer is
+    overwritten right before every launch, so none of the scan's input is
+    left in the 256 MB last-level cache.  These are the plain scan calls
+    (fp32 dU, no bf16 copy of H), so each carries its own algorithmic bytes:
+    forward, U's k blocks, x (k = 3), h and c; backward, U's k blocks, x
+    (k = 3), c, dh, dU's k blocks and dx_hat (k = 3)."""
+    import torch
+
+    from paper_1709_02755_amd import sru
+    f0 = st.fw[0]
+    if f0["U"] is None or f0["C"] is None:
+        return None
+    U, C = f0["U"], f0["C"]
+    L, B, ndir, k, d = U.shape
+    p = st.layers[0]
+    v = dict(highway_scale=highway_scale, reset_new=reset_new, linear=w.linear)
+    par = (p["v_f"], p["v_r"], p["b_f"], p["b_r"])
+    elems = L * B * ndir * d
+    xb = 4.0 if k == 3 else 0.0
+    fbytes = elems * (4.0 * k + xb + 8.0)
+    bbytes = elems * (4.0 * k + xb + 8.0 + 4.0 * k + xb)
+    fout = dict(H=torch.empty_like(f0["H"]), C=torch.empty_like(C),
+                c_last=torch.empty_like(f0["c_last"]))
+    fws = sru.workspace(sru.lib().sru_scan_forward_workspace_bytes(L, B, X.shape[2], d,
+                                                                   w.direction), U.device)
+    calls = {"scan_fwd": (fbytes, lambda: sru.scan_forward(
+        U, X, *par, direction=w.direction, mask=mask, out=fout, ws=fws, **v))}
+    if w.backward:
+        bout = dict(dU=torch.empty_like(U),
+                    dxh=torch.empty((L, B, ndir, d), device=U.device) if k == 3 else None,
+                    dv_f=None if w.linear else torch.empty((ndir, d), device=U.device),
+                    dv_r=None if w.linear else torch.empty((ndir, d), device=U.device),
+                    db_f=torch.empty((ndir, d), device=U.device),
+                    db_r=torch.empty((ndir, d), device=U.device),
+                    dc0=torch.empty((B, ndir * d), device=U.device))
+        bws = sru.workspace(sru.lib().sru_scan_backward_workspace_bytes(L, B, X.shape[2], d,
+                                                                        w.direction), U.device)
+        calls["scan_bwd"] = (bbytes, lambda: sru.scan_backward(
+            U, X, C, dH, *par, direction=w.direction, mask=mask, d_in=X.shape[2], out=bout,
+            ws=bws, **v))
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=U.device)
+    res = {}
+    for name, (nbytes, call) in calls.items():
+        call()  # warm the launch path
+        times = []
+        for i in range(reps):
+            flush.fill_(i & 0xFF)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            call()
+            e1.record()
+            e1.synchronize()
+            times.append(e0.elapsed_time(e1) * 1e-3)
+        t = sorted(times)[len(times) // 2]
+        gbps = nbytes / t / 1e9
+        res[name] = {"avg_us": round(t * 1e6, 2), "GBps": round(gbps, 1),
+                     "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                     "bytes_per_elem": nbytes / elems, "reps": reps, "stat": "median"}
+    del flush
+    return res
 
 
 # ------------------------------------------------------------------ CPU oracle
@@ -268,7 +331,7 @@ KERNEL_KEYS = [(("scan_fwd_kernel",), "scan_fwd"), (("scan_bwd_kernel",), "scan_
                (("gemm_direct_kernel", "256, 256, 64", ">, 0, true, true, false>"), "gemm_dw")]
 
 
-def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out):
+def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out, workload):
     """Turn four rocprofv3 --pmc runs (FETCH_SIZE and WRITE_SIZE of the bench
     and of the calibration copy) into per-launch HBM bytes for the scans."""
     def one(d, counter, key):
@@ -291,7 +354,7 @@ def summarize_pmc(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, out):
             continue
         kernels[label] = {"fetch_bytes_per_launch": f, "write_bytes_per_launch": w,
                           "hbm_bytes_per_launch": f + w}
-    res = {"source_hash": source_hash(), "copy_scale_fetch": scale_f,
+    res = {"source_hash": source_hash(), "workload": workload, "copy_scale_fetch": scale_f,
            "copy_scale_write": scale_w, "kernels": kernels}
     with open(out, "w") as fh:
         json.dump(res, fh, indent=1)
@@ -315,6 +378,9 @@ def main():
                     help="time replays of the step recorded into a HIP graph (no launch cost)")
     ap.add_argument("--reset-new", action="store_true",
                     help="reset gate reads c_t (Algorithm 1's order) instead of c_{t-1}")
+    ap.add_argument("--cold-reps", type=int, default=7,
+                    help="launches of each scan timed cold (0 = skip; the counter runs skip "
+                         "them so that only the step's launches are counted)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="REPS",
                     help="only run a 1 GiB copy REPS times (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=5,
@@ -322,7 +388,8 @@ def main():
                     help="build the per-launch HBM traffic table from rocprofv3 --pmc runs")
     args = ap.parse_args()
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc)
+        from paper_1709_02755_amd.workloads import WORKLOADS
+        summarize_pmc(*args.summarize_pmc, WORKLOADS[args.workload].name)
         return
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
@@ -414,13 +481,22 @@ def main():
     d = kernels[dominant]
     roofline = {"kernel": dominant, "bound": d.get("bound"), "achieved": d.get("achieved"),
                 "peak": d.get("peak"), "unit": d.get("unit"), "frac": d.get("frac"),
-                "avg_us": d["avg_us"], "traffic": pmc_traffic(dominant)}
+                "avg_us": d["avg_us"], "traffic": pmc_traffic(dominant, w.name)}
     scan_hbm = {k: {"GBps": kernels[k]["achieved"], "frac": kernels[k]["frac"],
-                    "avg_us": kernels[k]["avg_us"], "traffic": pmc_traffic(k)}
+                    "avg_us": kernels[k]["avg_us"], "traffic": pmc_traffic(k, w.name)}
                 for k in ("scan_fwd", "scan_bwd") if k in kernels}
     for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms_per_step"]):
         log(f"  {k:14s} {v['avg_us']:9.2f} us x{v['launches_per_step']}  "
             f"{v.get('achieved', '-')} {v.get('unit', '')} ({v.get('frac', '-')})")
+
+    cold = None
+    if args.cold_reps > 0:
+        cold = cold_scans(w, st, X, dH, mask, args.cold_reps, args.highway_scale,
+                          args.reset_new)
+    if cold:
+        for k, v in cold.items():
+            log(f"  cold {k}: {v['avg_us']} us, {v['GBps']} GB/s ({v['frac']})")
+    valid = None if inp["mask"] is None else int((inp["mask"] == 0).sum())
 
     cpu = None
     if args.cpu_seqs > 0:
@@ -435,6 +511,7 @@ def main():
                    f"SRU {'fwd+bwd' if w.backward else 'fwd'} tokens/s at {w.name}"),
         "value": tokens_per_s,
         "unit": "tokens/s",
+        "valid_tokens_per_s": None if valid is None else valid * args.steps / secs,
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -450,6 +527,7 @@ def main():
                    "passes": "fwd+bwd" if w.backward else "fwd",
                    "gemm": "bf16 operands, fp32 accumulate" if w.gemm_dtype else "fp32",
                    "scan": "fp32", "tokens_per_step": w.tokens, "global_batch": w.B,
+                   "valid_tokens_per_step": valid,
                    "highway_scale": args.highway_scale,
                    "reset_gate": "c_t (Algorithm 1)" if args.reset_new else "c_{t-1} (Eq. 3)",
                    "recurrence": ("linear: v * c removed (ablation (1), Sec. 4.5)" if w.linear
@@ -458,6 +536,7 @@ def main():
                    "launch": "hip graph replay" if args.graph else "eager"},
         "roofline": roofline,
         "scan_hbm": scan_hbm,
+        "scan_cold": cold,
         "kernels": kernels,
         "cpu_baseline": cpu,
     }

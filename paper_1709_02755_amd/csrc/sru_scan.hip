@@ -701,8 +701,16 @@ __global__ __launch_bounds__(64 * kVbWaves) void reduce_vb_kernel(const float* _
   }
 }
 
-constexpr int kFwdPF = 8;
+// Steps of loads a lane keeps in flight (its register ring).  Measured on
+// MI355X over the workloads' shapes: deeper rings are slower once every SIMD
+// holds a wave (the memory system is then saturated and shorter per-wave
+// queues serve it better); with fewer waves than SIMDs the backward needs a
+// ring of 6 to cover the memory latency, and the forward does best with 6
+// everywhere.
+constexpr int kFwdPF = 6;
 constexpr int kBwdPF = 6;
+constexpr int kBwdPFFull = 4;
+constexpr int kFullLanes = 256 * 4 * 64;  // one wave on each of the 1024 SIMDs
 constexpr int kFwdLinCH = 12;
 constexpr int kBwdLinCH = 8;
 
@@ -777,6 +785,22 @@ hipError_t fwd_dispatch_c(const ScanShape& s, const ScanFwdArgs& a, hipStream_t 
              : fwd_dispatch<KB, MASK, false, false>(s, a, st);
 }
 
+template <int KB, bool MASK, int PF>
+void bwd_launch(const ScanShape& s, const ScanBwdArgs& a, int grid, hipStream_t st) {
+  if (a.du_bf16 && s.reset_new)
+    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, true, true, PF>), dim3(grid),
+                       dim3(kScanThreads), 0, st, s, a);
+  else if (a.du_bf16)
+    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, true, false, PF>), dim3(grid),
+                       dim3(kScanThreads), 0, st, s, a);
+  else if (s.reset_new)
+    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, false, true, PF>), dim3(grid),
+                       dim3(kScanThreads), 0, st, s, a);
+  else
+    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, false, false, PF>), dim3(grid),
+                       dim3(kScanThreads), 0, st, s, a);
+}
+
 template <int KB, bool MASK>
 hipError_t bwd_dispatch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t st) {
   const int lanes = s.B * s.ndir * s.d;
@@ -802,18 +826,8 @@ hipError_t bwd_dispatch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t st
     return hipGetLastError();
   }
   timing_before("scan_bwd", st);
-  if (a.du_bf16 && s.reset_new)
-    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, true, true, kBwdPF>), dim3(grid),
-                       dim3(kScanThreads), 0, st, s, a);
-  else if (a.du_bf16)
-    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, true, false, kBwdPF>), dim3(grid),
-                       dim3(kScanThreads), 0, st, s, a);
-  else if (s.reset_new)
-    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, false, true, kBwdPF>), dim3(grid),
-                       dim3(kScanThreads), 0, st, s, a);
-  else
-    hipLaunchKernelGGL((scan_bwd_kernel<KB, MASK, false, false, kBwdPF>), dim3(grid),
-                       dim3(kScanThreads), 0, st, s, a);
+  if (lanes >= kFullLanes) bwd_launch<KB, MASK, kBwdPFFull>(s, a, grid, st);
+  else bwd_launch<KB, MASK, kBwdPF>(s, a, grid, st);
   timing_after(st);
   return hipGetLastError();
 }

@@ -71,6 +71,10 @@ SCAN_CASES = [
     (33, 4, 128, 128, O.DIR_BI, False),
     (40, 5, 64, 64, O.DIR_FWD, True),
     (23, 2, 96, 48, O.DIR_REV, True),
+    # a wave on every SIMD (B*ndir*d >= 65536): the backward's shorter ring,
+    # with a ragged tail (L % 4 != 0), k = 3 and 4
+    (7, 64, 1024, 1024, O.DIR_FWD, True),
+    (13, 32, 512, 1024, O.DIR_BI, True),
 ]
 
 

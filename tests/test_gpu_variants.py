@@ -22,6 +22,7 @@ SCAN_CASES = [
     (13, 3, 65, 65, O.DIR_REV, True),
     (33, 4, 96, 64, O.DIR_BI, False),
     (40, 5, 128, 128, O.DIR_BI, True),
+    (11, 64, 1024, 1024, O.DIR_REV, True),  # a wave on every SIMD: shorter backward ring
 ]
 
 
