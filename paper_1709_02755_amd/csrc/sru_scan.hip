@@ -65,11 +65,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
   float c = a.c0 ? a.c0[ln.gid] : 0.0f;
 
   float r0[PF], r1[PF], r2[PF], rx[PF];
-  uint8_t rm[PF];
+  // mask bytes held one per register: a byte array would be packed four to
+  // a register, and packing waits for the loads that fill it
+  unsigned rm[PF];
   (void)rm;
 
   auto tindex = [&](int st) { return ln.rev ? L - 1 - st : st; };
-  auto load = [&](int st, float& u0, float& u1, float& u2, float& xh, uint8_t& m) {
+  auto load = [&](int st, float& u0, float& u1, float& u2, float& xh, unsigned& m) {
     const long long t = tindex(st);
     const float* u = up + t * u_step;
     u0 = __builtin_nontemporal_load(u);
@@ -79,7 +81,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
     else xh = xp[t * x_step];
     if constexpr (MASK) m = mp[t * s.B];
   };
-  auto step = [&](int st, float u0, float u1, float u2, float xh, uint8_t m) {
+  auto step = [&](int st, float u0, float u1, float u2, float xh, unsigned m) {
     const long long t = tindex(st);
     const float f = sigmoid_fast(fmaf(vf, c, u1 + bf));   // Eq. 1
     const float cn = fmaf(f, c, (1.0f - f) * u0);         // Eq. 2
@@ -162,11 +164,13 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
   float c_t = cpp[(long long)tpos(L - 1) * h_step];
 
   float r0[PF], r1[PF], r2[PF], rx[PF], rdh[PF], rcp[PF];
-  uint8_t rm[PF];
+  // mask bytes held one per register: a byte array would be packed four to
+  // a register, and packing waits for the loads that fill it
+  unsigned rm[PF];
   (void)rm;
 
   auto load = [&](int i, float& u0, float& u1, float& u2, float& xh, float& dh, float& cprev,
-                  uint8_t& m) {
+                  unsigned& m) {
     const int pos = L - 1 - i;
     const long long t = tpos(pos);
     const float* u = up + t * u_step;
@@ -181,7 +185,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
     if constexpr (MASK) m = mp[t * s.B];
   };
   auto step = [&](int i, float u0, float u1, float u2, float xh, float dh, float cprev,
-                  uint8_t m) {
+                  unsigned m) {
     const int pos = L - 1 - i;
     const long long t = tpos(pos);
     const float c_p = pos > 0 ? cprev : c0v;
