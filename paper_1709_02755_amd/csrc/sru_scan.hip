@@ -51,13 +51,21 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
   const long long u_step = (long long)s.B * s.ndir * KB * s.d;
   const long long x_step = (long long)s.B * s.d_in;
   const long long h_step = (long long)s.B * nfeat;
-  const float* up = a.U + ((long long)ln.b * s.ndir + ln.dir) * KB * s.d + ln.j;
-  const float* xp = KB == 3 ? a.X + (long long)ln.b * s.d_in + ln.j : nullptr;
-  const uint8_t* mp = MASK ? a.mask + ln.b : nullptr;
-  float* hp = a.H + ln.gid;
-  float* cp = STORE_C ? a.C + ln.gid : nullptr;
-  uint16_t* hbp = STORE_HB ? a.Hb + ln.gid : nullptr;
   const int d = s.d;
+  // Addresses are cursors that move one step at a time in the direction's
+  // order (no per-step 64-bit products): the load cursors run PF steps
+  // ahead of the store cursors and stop at the last step, so the loads past
+  // the end of the sequence re-read it.
+  const long long t0 = ln.rev ? L - 1 : 0;
+  const long long sg = ln.rev ? -1 : 1;
+  const long long su = sg * u_step, sx = sg * x_step, sh = sg * h_step, sm = sg * s.B;
+  const float* lu = a.U + ((long long)ln.b * s.ndir + ln.dir) * KB * s.d + ln.j + t0 * u_step;
+  const float* lx = KB == 3 ? a.X + (long long)ln.b * s.d_in + ln.j + t0 * x_step : nullptr;
+  const uint8_t* lm = MASK ? a.mask + ln.b + t0 * s.B : nullptr;
+  float* hp = a.H + ln.gid + t0 * h_step;
+  float* cp = STORE_C ? a.C + ln.gid + t0 * h_step : nullptr;
+  uint16_t* hbp = STORE_HB ? a.Hb + ln.gid + t0 * h_step : nullptr;
+  int ls = 0;  // the step the load cursors point at
 
   const float vf = a.v_f[ln.fidx], vr = a.v_r[ln.fidx];
   const float bf = a.b_f[ln.fidx], br = a.b_r[ln.fidx];
@@ -70,19 +78,20 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
   unsigned rm[PF];
   (void)rm;
 
-  auto tindex = [&](int st) { return ln.rev ? L - 1 - st : st; };
-  auto load = [&](int st, float& u0, float& u1, float& u2, float& xh, unsigned& m) {
-    const long long t = tindex(st);
-    const float* u = up + t * u_step;
-    u0 = __builtin_nontemporal_load(u);
-    u1 = __builtin_nontemporal_load(u + d);
-    u2 = __builtin_nontemporal_load(u + 2 * d);
-    if constexpr (KB == 4) xh = __builtin_nontemporal_load(u + 3 * d);
-    else xh = xp[t * x_step];
-    if constexpr (MASK) m = mp[t * s.B];
+  auto load = [&](float& u0, float& u1, float& u2, float& xh, unsigned& m) {
+    u0 = __builtin_nontemporal_load(lu);
+    u1 = __builtin_nontemporal_load(lu + d);
+    u2 = __builtin_nontemporal_load(lu + 2 * d);
+    if constexpr (KB == 4) xh = __builtin_nontemporal_load(lu + 3 * d);
+    else xh = *lx;
+    if constexpr (MASK) m = *lm;
+    const bool adv = ls + 1 < L;  // the same for the whole wave
+    ls += adv;
+    lu = adv ? lu + su : lu;
+    if constexpr (KB == 3) lx = adv ? lx + sx : lx;
+    if constexpr (MASK) lm = adv ? lm + sm : lm;
   };
-  auto step = [&](int st, float u0, float u1, float u2, float xh, unsigned m) {
-    const long long t = tindex(st);
+  auto step = [&](float u0, float u1, float u2, float xh, unsigned m) {
     const float f = sigmoid_fast(fmaf(vf, c, u1 + bf));   // Eq. 1
     const float cn = fmaf(f, c, (1.0f - f) * u0);         // Eq. 2
     const float r = sigmoid_fast(fmaf(vr, RN ? cn : c, u2 + br));  // Eq. 3
@@ -94,29 +103,30 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
     } else {
       c = cn;
     }
-    __builtin_nontemporal_store(h, hp + t * h_step);
-    if constexpr (STORE_C) __builtin_nontemporal_store(c, cp + t * h_step);
-    if constexpr (STORE_HB)
-      __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), hbp + t * h_step);
+    __builtin_nontemporal_store(h, hp);
+    if constexpr (STORE_C) __builtin_nontemporal_store(c, cp);
+    if constexpr (STORE_HB) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), hbp);
+    hp += sh;
+    if constexpr (STORE_C) cp += sh;
+    if constexpr (STORE_HB) hbp += sh;
   };
 
 #pragma unroll
-  for (int p = 0; p < PF; ++p) load(p < L ? p : L - 1, r0[p], r1[p], r2[p], rx[p], rm[p]);
+  for (int p = 0; p < PF; ++p) load(r0[p], r1[p], r2[p], rx[p], rm[p]);
 
   int s0 = 0;
   for (; s0 + PF <= L; s0 += PF) {
 #pragma unroll
     for (int p = 0; p < PF; ++p) {
-      step(s0 + p, r0[p], r1[p], r2[p], rx[p], rm[p]);
-      const int sn = s0 + p + PF < L ? s0 + p + PF : L - 1;
-      load(sn, r0[p], r1[p], r2[p], rx[p], rm[p]);
+      step(r0[p], r1[p], r2[p], rx[p], rm[p]);
+      load(r0[p], r1[p], r2[p], rx[p], rm[p]);  // step s0 + p + PF (or the last)
       // keep each prefetch where it is: sunk loads shorten the distance
       __builtin_amdgcn_sched_barrier(0);
     }
   }
 #pragma unroll
   for (int p = 0; p < PF; ++p)
-    if (s0 + p < L) step(s0 + p, r0[p], r1[p], r2[p], rx[p], rm[p]);
+    if (s0 + p < L) step(r0[p], r1[p], r2[p], rx[p], rm[p]);
 
   if (a.c_last) a.c_last[ln.gid] = c;
 }
@@ -144,14 +154,25 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
   const long long x_step = (long long)s.B * s.d_in;
   const long long h_step = (long long)s.B * nfeat;
   const long long u_off = ((long long)ln.b * s.ndir + ln.dir) * KB * s.d + ln.j;
-  const float* up = a.U + u_off;
   using DuT = typename std::conditional<DUB, uint16_t, float>::type;
-  DuT* dup = static_cast<DuT*>(a.dU) + u_off;
-  const float* xp = KB == 3 ? a.X + (long long)ln.b * s.d_in + ln.j : nullptr;
-  const uint8_t* mp = MASK ? a.mask + ln.b : nullptr;
   const float* cpp = a.C + ln.gid;
-  const float* dhp = a.dH + ln.gid;
-  float* dxp = KB == 3 ? a.dxh + ln.gid : nullptr;
+  // Cursors, as in the forward scan, moving one step per load or store in
+  // the reverse of the direction's order: the load cursors (U, x, dh, mask
+  // at t(pos); C at t(pos - 1)) run PF steps ahead of the store cursors and
+  // stop at the first position.
+  auto tpos = [&](int pos) { return (long long)(ln.rev ? L - 1 - pos : pos); };
+  const long long t0 = tpos(L - 1);
+  const long long sg = ln.rev ? 1 : -1;
+  const long long su = sg * u_step, sx = sg * x_step, sh = sg * h_step, sm = sg * s.B;
+  const float* lu = a.U + u_off + t0 * u_step;
+  const float* lx = KB == 3 ? a.X + (long long)ln.b * s.d_in + ln.j + t0 * x_step : nullptr;
+  const uint8_t* lm = MASK ? a.mask + ln.b + t0 * s.B : nullptr;
+  const float* ldh = a.dH + ln.gid + t0 * h_step;
+  const float* lc = cpp + tpos(L > 1 ? L - 2 : 0) * h_step;
+  DuT* dup = static_cast<DuT*>(a.dU) + u_off + t0 * u_step;
+  float* dxp = KB == 3 ? a.dxh + ln.gid + t0 * h_step : nullptr;
+  int nl = 0;  // loads issued
+  int is = 0;  // steps done
 
   const float vf = a.v_f[ln.fidx], vr = a.v_r[ln.fidx];
   const float bf = a.b_f[ln.fidx], br = a.b_r[ln.fidx];
@@ -160,8 +181,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
   float g = a.dc_last ? a.dc_last[ln.gid] : 0.0f;
   float sum_df_c = 0.f, sum_dr_c = 0.f, sum_df = 0.f, sum_dr = 0.f;
 
-  auto tpos = [&](int pos) { return ln.rev ? L - 1 - pos : pos; };
-  float c_t = cpp[(long long)tpos(L - 1) * h_step];
+  float c_t = cpp[t0 * h_step];
 
   float r0[PF], r1[PF], r2[PF], rx[PF], rdh[PF], rcp[PF];
   // mask bytes held one per register: a byte array would be packed four to
@@ -169,26 +189,29 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
   unsigned rm[PF];
   (void)rm;
 
-  auto load = [&](int i, float& u0, float& u1, float& u2, float& xh, float& dh, float& cprev,
+  auto load = [&](float& u0, float& u1, float& u2, float& xh, float& dh, float& cprev,
                   unsigned& m) {
-    const int pos = L - 1 - i;
-    const long long t = tpos(pos);
-    const float* u = up + t * u_step;
-    u0 = __builtin_nontemporal_load(u);
-    u1 = __builtin_nontemporal_load(u + d);
-    u2 = __builtin_nontemporal_load(u + 2 * d);
-    if constexpr (KB == 4) xh = __builtin_nontemporal_load(u + 3 * d);
-    else xh = xp[t * x_step];
-    dh = __builtin_nontemporal_load(dhp + t * h_step);
-    const long long tp = tpos(pos > 0 ? pos - 1 : 0);
-    cprev = cpp[tp * h_step];
-    if constexpr (MASK) m = mp[t * s.B];
+    u0 = __builtin_nontemporal_load(lu);
+    u1 = __builtin_nontemporal_load(lu + d);
+    u2 = __builtin_nontemporal_load(lu + 2 * d);
+    if constexpr (KB == 4) xh = __builtin_nontemporal_load(lu + 3 * d);
+    else xh = *lx;
+    dh = __builtin_nontemporal_load(ldh);
+    cprev = *lc;
+    if constexpr (MASK) m = *lm;
+    // the same for the whole wave: load nl + 1 is at position L-2-nl, its
+    // C one position earlier
+    const bool adv = nl + 1 < L, advc = nl + 2 < L;
+    ++nl;
+    lu = adv ? lu + su : lu;
+    if constexpr (KB == 3) lx = adv ? lx + sx : lx;
+    ldh = adv ? ldh + sh : ldh;
+    if constexpr (MASK) lm = adv ? lm + sm : lm;
+    lc = advc ? lc + sh : lc;
   };
-  auto step = [&](int i, float u0, float u1, float u2, float xh, float dh, float cprev,
-                  unsigned m) {
-    const int pos = L - 1 - i;
-    const long long t = tpos(pos);
-    const float c_p = pos > 0 ? cprev : c0v;
+  auto step = [&](float u0, float u1, float u2, float xh, float dh, float cprev, unsigned m) {
+    const float c_p = is + 1 < L ? cprev : c0v;  // position 0 starts from c0
+    ++is;
     const float c_r = RN ? c_t : c_p;  // the state the reset gate reads
     const float f = sigmoid_fast(fmaf(vf, c_p, u1 + bf));
     const float r = sigmoid_fast(fmaf(vr, c_r, u2 + br));
@@ -216,16 +239,17 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
     sum_dr += dr;
     const float gn = RN ? fmaf(df, vf, gc * f) : fmaf(dr, vr, fmaf(df, vf, gc * f));
     g = pad ? g : gn;
-    DuT* du = dup + t * u_step;
     auto put = [](float v, DuT* p) {
       if constexpr (DUB) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)v), p);
       else __builtin_nontemporal_store(v, p);
     };
-    put(du0, du);
-    put(df, du + d);
-    put(dr, du + 2 * d);
-    if constexpr (KB == 4) put(dx, du + 3 * d);
-    else __builtin_nontemporal_store(dx, dxp + t * h_step);
+    put(du0, dup);
+    put(df, dup + d);
+    put(dr, dup + 2 * d);
+    if constexpr (KB == 4) put(dx, dup + 3 * d);
+    else __builtin_nontemporal_store(dx, dxp);
+    dup += su;
+    if constexpr (KB == 3) dxp += sh;
     // c_t takes the value in a register of its own.  Were it to share
     // cprev's register, the ring's registers would shift by one slot per
     // step and the loop would copy still-loading values at its back edge.
@@ -233,21 +257,19 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
   };
 
 #pragma unroll
-  for (int p = 0; p < PF; ++p)
-    load(p < L ? p : L - 1, r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);
+  for (int p = 0; p < PF; ++p) load(r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);
   int i0 = 0;
   for (; i0 + PF <= L; i0 += PF) {
 #pragma unroll
     for (int p = 0; p < PF; ++p) {
-      step(i0 + p, r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);
-      const int in = i0 + p + PF < L ? i0 + p + PF : L - 1;
-      load(in, r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);
+      step(r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);
+      load(r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);  // index i0 + p + PF (or the last)
       __builtin_amdgcn_sched_barrier(0);  // as in the forward scan
     }
   }
 #pragma unroll
   for (int p = 0; p < PF; ++p)
-    if (i0 + p < L) step(i0 + p, r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);
+    if (i0 + p < L) step(r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);
 
   float* part = a.partial + (long long)ln.b * 4 * nfeat + ln.fidx;
   part[0] = sum_df_c;
