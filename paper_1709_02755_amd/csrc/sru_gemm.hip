@@ -542,8 +542,16 @@ __device__ __forceinline__ TileIdx tile_of(const KernelArgs& g) {
   TileIdx r;
   r.split = u / nt;
   const int t = u - r.split * nt;
-  r.tm = t / g.tiles_n;
-  r.tn = t - r.tm * g.tiles_n;
+  // tiles in groups of GM tile rows, column by column within a group: the
+  // 32 tiles an XCD runs at once then span 8 A panels x 4 B panels instead
+  // of 3 x 12 (gemm_u's 12 column tiles), fewer distinct panels in its L2
+  constexpr int GM = 8;
+  const int gsz = GM * g.tiles_n;
+  const int first = (t / gsz) * GM;
+  const int rows = min(g.tiles_m - first, GM);
+  const int tg = t - (t / gsz) * gsz;
+  r.tm = first + tg % rows;
+  r.tn = tg / rows;
   return r;
 }
 
