@@ -662,12 +662,16 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
 //   bounds the load rate.  A fragment is one ds_read_b128.
 // Row-contiguous (RC = true; dW = dU^T X, both operands [K, rows]):
 //   the tile is kept as loaded, k-row s at s*2R bytes (R rows of bf16), its
-//   R/8 16-byte row-chunks permuted as slot = chunk ^ 2*(s & 3).  A wave
+//   R/8 16-byte row-chunks permuted as slot = chunk ^ 4*(s & 3).  A wave
 //   load fills 512/R k-rows.  A fragment (8 consecutive k of one row) is two
 //   ds_read_b64_tr_b16: within each group of 16 lanes, input lane 4s+q names
 //   k-row s, rows 4q..4q+3 of the group's 16 rows, and output lane i
-//   receives that k-run of row i.  The four k-rows x 32 bytes one group
-//   reads land on 8 distinct 16-byte slots.
+//   receives that k-run of row i.  A k-row is a multiple of 256 bytes, so
+//   its slot p sits on banks 4p..4p+3 (mod 64) whatever s is; the two groups
+//   of a half wave read chunks c..c+3 (c a multiple of 4) of the same four
+//   k-rows, and the XOR by 4*(s & 3) puts those 16 chunks on 16 distinct
+//   slots mod 16, i.e. all 64 banks once.  (An XOR by 2*(s & 3) put both
+//   groups on the same 8 slots: a two-way conflict on every read.)
 //
 // Each wave owns a 128 x 64 block of the tile (4 x 2 MFMA tiles of 32 x 32,
 // 128 accumulator registers per lane); two waves share each SIMD, so one's
@@ -737,8 +741,9 @@ struct DirectOperand {
         oob[j] = 0;  // rows past the end are clamped: they feed discarded outputs
       } else {
         constexpr int CPK = R / 8;  // 16-byte chunks per k-row
+        static_assert(CPK >= 16, "the k-row swizzle XORs chunk indices with up to 12");
         const int srow = blk * (512 / R) + lane / CPK;
-        const int chunk = (lane % CPK) ^ (2 * (srow & 3));
+        const int chunk = (lane % CPK) ^ (4 * (srow & 3));
         const int r = r0 + chunk * 8;
         kk[j] = srow;
         off[j] = (unsigned)(((long long)srow * ld + min(r, rows - 8)) * 2);
@@ -785,7 +790,7 @@ struct DirectOperand {
       const int r = (row & ~15) + 4 * (gl & 3);
       const int kr = c * 8 + (gl >> 2);
       auto addr = [&](int k) {
-        return base + k * (2 * R) + (((r >> 3) ^ (2 * (k & 3))) << 4) + (r & 7) * 2;
+        return base + k * (2 * R) + (((r >> 3) ^ (4 * (k & 3))) << 4) + (r & 7) * 2;
       };
       const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(addr(kr)));
       const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(addr(kr + 4)));
