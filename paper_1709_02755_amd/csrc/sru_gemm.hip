@@ -1186,6 +1186,51 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
+// The same for rows of 16-byte aligned groups of 4 (N % 4 == 0): one group
+// per thread, the partials read as 16-byte loads.  The per-element sum is
+// the same sequence of additions, so the result is bit-identical.
+__global__ __launch_bounds__(256) void splitk_reduce4_kernel(const float* __restrict__ part,
+                                                             int splits, int M, int N,
+                                                             float* C, long long ldc,
+                                                             const float* add, long long add_ld,
+                                                             long long add_off, int add_count) {
+  const long long total = (long long)M * N;
+  const long long i = ((long long)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i >= total) return;
+  const int m = (int)(i / N);
+  const int n = (int)(i - (long long)m * N);
+  floatx4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+  for (int z = 0; z < splits; ++z) s += *reinterpret_cast<const floatx4*>(part + z * total + i);
+  if (add_count > 0) {
+    const float* ar = add + (long long)m * add_ld + n;
+    s += *reinterpret_cast<const floatx4*>(ar);
+    if (add_count > 1) s += *reinterpret_cast<const floatx4*>(ar + add_off);
+  }
+  *reinterpret_cast<floatx4*>(C + (long long)m * ldc + n) = s;
+}
+
+hipError_t launch_splitk_reduce(const float* part, int splits, int M, int N, float* C,
+                                long long ldc, const float* add, long long add_ld,
+                                long long add_off, int add_count, hipStream_t st) {
+  const long long total = (long long)M * N;
+  auto al16 = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  const bool vec = N % 4 == 0 && ldc % 4 == 0 && al16(part) && al16(C) &&
+                   (add_count == 0 || (add_ld % 4 == 0 && add_off % 4 == 0 && al16(add)));
+  timing_before("splitk_reduce", st);
+  if (vec) {
+    const long long groups = total / 4;
+    hipLaunchKernelGGL(splitk_reduce4_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256),
+                       0, st, part, splits, M, N, C, ldc, add, add_ld, add_off, add_count);
+  } else {
+    const int grid = (int)std::min<long long>((total + 255) / 256, 8192);
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, st, part, splits, M, N,
+                       C, ldc, add, add_ld, add_off, add_count);
+  }
+  timing_after(st);
+  return hipGetLastError();
+}
+
 // fp32 -> bf16 conversions (RNE).  Plain copy: 8 elements per thread (two
 // 16-byte loads, one 16-byte store).
 __global__ __launch_bounds__(256) void to_bf16_kernel(const float* __restrict__ src,
@@ -1363,13 +1408,8 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
   timing_after(st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
-  const long long total = (long long)g.M * g.N;
-  const int grid = (int)std::min<long long>((total + 255) / 256, 8192);
-  timing_before("splitk_reduce", st);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, st, g.partials, a.splits,
-                     g.M, g.N, g.C, g.ldc, g.add, g.add_ld, g.add_off, g.add_count);
-  timing_after(st);
-  return hipGetLastError();
+  return launch_splitk_reduce(g.partials, a.splits, g.M, g.N, g.C, g.ldc, g.add, g.add_ld,
+                              g.add_off, g.add_count, st);
 }
 
 // ---- the direct path: plan (shared by workspace sizing and launch) ----
@@ -1488,13 +1528,8 @@ hipError_t launch_direct_cfg(const GemmDesc& g, hipStream_t st) {
   timing_after(st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
-  const long long total = (long long)g.M * g.N;
-  const int grid = (int)std::min<long long>((total + 255) / 256, 8192);
-  timing_before("splitk_reduce", st);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, st, g.partials, a.splits,
-                     g.M, g.N, g.C, g.ldc, g.add, g.add_ld, g.add_off, g.add_count);
-  timing_after(st);
-  return hipGetLastError();
+  return launch_splitk_reduce(g.partials, a.splits, g.M, g.N, g.C, g.ldc, g.add, g.add_ld,
+                              g.add_off, g.add_count, st);
 }
 
 // Operand-type combinations that are instantiated: fp32 x fp32 for every

@@ -44,10 +44,13 @@ def test_gemm_matches_matmul(op, dtype, shape):
 
 
 @pytest.mark.parametrize("dtype", [sru.GEMM_FP32, sru.GEMM_BF16])
-def test_gemm_long_reduction_split(dtype):
-    """dW-shaped product with K = tokens (split over K, fixed-order sum)."""
-    M, N, K = 384, 256, 12800
-    print(f"gemm TN long K dtype={dtype}", flush=True)
+@pytest.mark.parametrize("shape", [(384, 256, 12800), (130, 63, 4100), (257, 100, 3000)])
+def test_gemm_long_reduction_split(dtype, shape):
+    """dW-shaped product with K = tokens (split over K, fixed-order sum).
+    N = 63 sums the splits element by element, N = 100 and 256 in groups of
+    four; M = 130 and 257 leave ragged edge tiles."""
+    M, N, K = shape
+    print(f"gemm TN long K dtype={dtype} M={M} N={N} K={K}", flush=True)
     rng = np.random.default_rng(5)
     A = rng.standard_normal((K, M)).astype(np.float32)
     B = rng.standard_normal((K, N)).astype(np.float32)
