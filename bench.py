@@ -187,12 +187,17 @@ def pmc_traffic(label, workload):
 
 
 def cold_scans(w, st, X, dH, mask, reps, highway_scale, reset_new):
-    """The two scans of layer 0, timed cold: a 512 MiB buffer is
-    overwritten right before every launch, so none of the scan's input is
-    left in the 256 MB last-level cache.  These are the plain scan calls
-    (fp32 dU, no bf16 copy of H), so each carries its own algorithmic bytes:
-    forward, U's k blocks, x (k = 3), h and c; backward, U's k blocks, x
-    (k = 3), c, dh, dU's k blocks and dx_hat (k = 3)."""
+    """The two scans of layer 0, timed cold: a 512 MiB buffer is overwritten
+    right before every call, so none of the scan's input is left in the
+    256 MB last-level cache.  The scan kernels are the ones the step runs:
+    the forward is the plain scan call with the step's outputs (H, C and, with
+    bf16 products, the bf16 copy of H); the backward is the whole layer-0
+    backward call, whose first kernel is the gradient scan (bf16 dU with bf16
+    products).  Each time is the scan kernel's own, from the per-launch event
+    hook, over its algorithmic bytes: forward, U's k blocks, x (k = 3), h, c
+    (and bf16 h); backward, U's k blocks, x (k = 3), c, dh, dU's k blocks
+    (fp32 or bf16) and dx_hat (k = 3).  The linear recurrence's maps kernel,
+    when it runs, is timed with its scan."""
     import torch
 
     from paper_1709_02755_amd import sru
@@ -202,49 +207,59 @@ def cold_scans(w, st, X, dH, mask, reps, highway_scale, reset_new):
     U, C = f0["U"], f0["C"]
     L, B, ndir, k, d = U.shape
     p = st.layers[0]
+    bf16 = w.gemm_dtype == sru.GEMM_BF16
     v = dict(highway_scale=highway_scale, reset_new=reset_new, linear=w.linear)
     par = (p["v_f"], p["v_r"], p["b_f"], p["b_r"])
     elems = L * B * ndir * d
     xb = 4.0 if k == 3 else 0.0
-    fbytes = elems * (4.0 * k + xb + 8.0)
-    bbytes = elems * (4.0 * k + xb + 8.0 + 4.0 * k + xb)
+    fbytes = elems * (4.0 * k + xb + 8.0 + (2.0 if bf16 else 0.0))
+    bbytes = elems * (4.0 * k + xb + 8.0 + (2.0 if bf16 else 4.0) * k + xb)
     fout = dict(H=torch.empty_like(f0["H"]), C=torch.empty_like(C),
                 c_last=torch.empty_like(f0["c_last"]))
+    if bf16:
+        fout["H_bf16"] = torch.empty(f0["H"].shape, dtype=torch.bfloat16, device=U.device)
     fws = sru.workspace(sru.lib().sru_scan_forward_workspace_bytes(L, B, X.shape[2], d,
                                                                    w.direction), U.device)
-    calls = {"scan_fwd": (fbytes, lambda: sru.scan_forward(
+    calls = {"scan_fwd": (fbytes, ("scan_fwd", "scan_maps"), lambda: sru.scan_forward(
         U, X, *par, direction=w.direction, mask=mask, out=fout, ws=fws, **v))}
     if w.backward:
-        bout = dict(dU=torch.empty_like(U),
-                    dxh=torch.empty((L, B, ndir, d), device=U.device) if k == 3 else None,
-                    dv_f=None if w.linear else torch.empty((ndir, d), device=U.device),
-                    dv_r=None if w.linear else torch.empty((ndir, d), device=U.device),
-                    db_f=torch.empty((ndir, d), device=U.device),
-                    db_r=torch.empty((ndir, d), device=U.device),
-                    dc0=torch.empty((B, ndir * d), device=U.device))
-        bws = sru.workspace(sru.lib().sru_scan_backward_workspace_bytes(L, B, X.shape[2], d,
-                                                                        w.direction), U.device)
-        calls["scan_bwd"] = (bbytes, lambda: sru.scan_backward(
-            U, X, C, dH, *par, direction=w.direction, mask=mask, d_in=X.shape[2], out=bout,
-            ws=bws, **v))
+        # the layer-0 call of the step's backward (dH has layer 0's output shape)
+        if "Q" in p:
+            bcall = lambda: sru.backward_lowrank(
+                X, p["Q"], p["P"], *par, f0["T"], U, C, dH, None, None, w.direction, mask,
+                w.gemm_dtype, want_dc0=False, out=st.bw[0], ws=st.ws, X_bf16=st.xb0,
+                T_bf16=f0.get("T_bf16"), **v)
+        else:
+            bcall = lambda: sru.backward(
+                X, p["W"], *par, U, C, dH, None, None, w.direction, mask, w.gemm_dtype,
+                want_dc0=False, out=st.bw[0], ws=st.ws, X_bf16=st.xb0,
+                W_bf16=f0.get("W_bf16"), **v)
+        calls["scan_bwd"] = (bbytes, ("scan_bwd", "scan_maps"), bcall)
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=U.device)
+    lib = sru.lib()
+    ev = HipEvents(2 * 64 + 2)
     res = {}
-    for name, (nbytes, call) in calls.items():
-        call()  # warm the launch path
-        times = []
-        for i in range(reps):
-            flush.fill_(i & 0xFF)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            call()
-            e1.record()
-            e1.synchronize()
-            times.append(e0.elapsed_time(e1) * 1e-3)
-        t = sorted(times)[len(times) // 2]
-        gbps = nbytes / t / 1e9
-        res[name] = {"avg_us": round(t * 1e6, 2), "GBps": round(gbps, 1),
-                     "frac": round(gbps / HBM_PEAK_GBPS, 4),
-                     "bytes_per_elem": nbytes / elems, "reps": reps, "stat": "median"}
+    try:
+        for name, (nbytes, labels, call) in calls.items():
+            call()  # warm the launch path
+            times = []
+            for i in range(reps):
+                flush.fill_(i & 0xFF)
+                lib.sru_timing_begin(ev.events, ev.n)
+                try:
+                    call()
+                finally:
+                    nk = lib.sru_timing_end()
+                torch.cuda.synchronize()
+                times.append(sum(ev.elapsed_ms(2 * j, 2 * j + 1) for j in range(nk)
+                                 if lib.sru_timing_label(j).decode() in labels) * 1e-3)
+            t = sorted(times)[len(times) // 2]
+            gbps = nbytes / t / 1e9
+            res[name] = {"avg_us": round(t * 1e6, 2), "GBps": round(gbps, 1),
+                         "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                         "bytes_per_elem": nbytes / elems, "reps": reps, "stat": "median"}
+    finally:
+        ev.close()
     del flush
     return res
 
