@@ -342,6 +342,7 @@ def _per_kernel(rows, counter):
 KERNEL_KEYS = [(("scan_fwd_kernel",), "scan_fwd"), (("scan_bwd_kernel",), "scan_bwd"),
                (("scan_fwd_lin_kernel",), "scan_fwd"), (("scan_bwd_lin_kernel",), "scan_bwd"),
                (("reduce_vb_kernel",), "reduce_vb"), (("splitk_reduce_kernel",), "splitk_reduce"),
+               (("splitk_reduce4_kernel",), "splitk_reduce"),
                (("to_bf16_kernel",), "bf16_x"),
                # the three products of the dense bf16 path (template args after
                # the 256 x 256 tile configuration: addend count, A row-contiguous,
