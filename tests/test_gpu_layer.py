@@ -26,6 +26,9 @@ LAYER_CASES = [
     (33, 9, 260, 260, O.DIR_FWD, False, O.GEMM_BF16),
     (48, 7, 512, 256, O.DIR_REV, True, O.GEMM_BF16),
     (64, 16, 512, 512, O.DIR_FWD, True, O.GEMM_BF16),
+    # bidirectional, k = 3: dX adds both directions' highway gradients; whole
+    # 256 x 256 tiles (epilogue through LDS) and a ragged row of tiles
+    (40, 13, 256, 256, O.DIR_BI, True, O.GEMM_BF16),
 ]
 
 
