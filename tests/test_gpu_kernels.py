@@ -18,8 +18,11 @@ def _bf16(a):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16).double().numpy()
 
 
+# (1500, 520, 200): six tile rows of 256, i.e. one whole group of four tile
+# rows and a partial one in the workgroup -> tile order
 GEMM_SHAPES = [(1, 1, 1), (7, 5, 3), (63, 65, 130), (130, 63, 65), (256, 256, 32),
-               (257, 513, 96), (384, 128, 128), (1000, 300, 260), (2048, 768, 256)]
+               (257, 513, 96), (384, 128, 128), (1000, 300, 260), (2048, 768, 256),
+               (1500, 520, 200)]
 
 
 @pytest.mark.parametrize("op", [sru.OP_NT, sru.OP_NN, sru.OP_TN])
@@ -44,11 +47,13 @@ def test_gemm_matches_matmul(op, dtype, shape):
 
 
 @pytest.mark.parametrize("dtype", [sru.GEMM_FP32, sru.GEMM_BF16])
-@pytest.mark.parametrize("shape", [(384, 256, 12800), (130, 63, 4100), (257, 100, 3000)])
+@pytest.mark.parametrize("shape", [(384, 256, 12800), (130, 63, 4100), (257, 100, 3000),
+                                   (1500, 100, 3000)])
 def test_gemm_long_reduction_split(dtype, shape):
     """dW-shaped product with K = tokens (split over K, fixed-order sum).
     N = 63 sums the splits element by element, N = 100 and 256 in groups of
-    four; M = 130 and 257 leave ragged edge tiles."""
+    four; M = 130, 257 and 1500 leave ragged edge tiles (1500: six tile rows,
+    a partial group of tile rows)."""
     M, N, K = shape
     print(f"gemm TN long K dtype={dtype} M={M} N={N} K={K}", flush=True)
     rng = np.random.default_rng(5)
