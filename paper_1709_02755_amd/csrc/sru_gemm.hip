@@ -1049,6 +1049,9 @@ __global__ __launch_bounds__(DirectLine::THREADS, 1) void proj_scan_fwd_kernel(F
     br = a.b_r[fidx];
     c = a.c0 ? a.c0[(long long)sb * nfeat + fidx] : 0.f;
   }
+  // gate parameters scaled by -log2(e), as in the forward scan
+  const float vfs = vf * kNegLog2e, vrs = vr * kNegLog2e;
+  const float bfs = bf * kNegLog2e, brs = br * kNegLog2e;
   const float alpha = a.alpha;
   const bool rn = a.reset_new != 0;
   auto barrier = [] {
@@ -1119,9 +1122,9 @@ __global__ __launch_bounds__(DirectLine::THREADS, 1) void proj_scan_fwd_kernel(F
         const int sstep = dtt * BB * kFusedPitch;
         auto step = [&](int tt, float u0, float u1, float u2, float xh) {
           const int mbit = __builtin_amdgcn_readlane(tt < 64 ? m_lo : m_hi, tt & 63);
-          const float f = sigmoid_fast(fmaf(vf, c, u1 + bf));           // Eq. 1
-          const float cn = fmaf(f, c, (1.0f - f) * u0);                 // Eq. 2
-          const float r = sigmoid_fast(fmaf(vr, rn ? cn : c, u2 + br));  // Eq. 3
+          const float f = sigmoid_scaled(fmaf(vfs, c, fmaf(u1, kNegLog2e, bfs)));  // Eq. 1
+          const float cn = fmaf(f, c, fmaf(-f, u0, u0));                           // Eq. 2
+          const float r = sigmoid_scaled(fmaf(vrs, rn ? cn : c, fmaf(u2, kNegLog2e, brs)));  // Eq. 3
           float h = fmaf(r, cn, (1.0f - r) * (alpha * xh));              // Eq. 4 (Sec. 3.2)
           if (mbit) {
             h = 0.0f;

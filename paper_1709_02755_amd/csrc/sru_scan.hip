@@ -67,8 +67,9 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
   uint16_t* hbp = STORE_HB ? a.Hb + ln.gid + t0 * h_step : nullptr;
   int ls = 0;  // the step the load cursors point at
 
-  const float vf = a.v_f[ln.fidx], vr = a.v_r[ln.fidx];
-  const float bf = a.b_f[ln.fidx], br = a.b_r[ln.fidx];
+  // gate parameters scaled by -log2(e) (sigmoid_scaled)
+  const float vfs = a.v_f[ln.fidx] * kNegLog2e, vrs = a.v_r[ln.fidx] * kNegLog2e;
+  const float bfs = a.b_f[ln.fidx] * kNegLog2e, brs = a.b_r[ln.fidx] * kNegLog2e;
   const float alpha = s.alpha;
   float c = a.c0 ? a.c0[ln.gid] : 0.0f;
 
@@ -91,10 +92,12 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
     if constexpr (KB == 3) lx = adv ? lx + sx : lx;
     if constexpr (MASK) lm = adv ? lm + sm : lm;
   };
+  // The chain from c to the next c: fma, exp2, add, rcp, fma, fma.  Eq. 2 is
+  // f c + (u0 - f u0), which keeps f = 0 and f = 1 exact (c' = u0, c' = c).
   auto step = [&](float u0, float u1, float u2, float xh, unsigned m) {
-    const float f = sigmoid_fast(fmaf(vf, c, u1 + bf));   // Eq. 1
-    const float cn = fmaf(f, c, (1.0f - f) * u0);         // Eq. 2
-    const float r = sigmoid_fast(fmaf(vr, RN ? cn : c, u2 + br));  // Eq. 3
+    const float f = sigmoid_scaled(fmaf(vfs, c, fmaf(u1, kNegLog2e, bfs)));  // Eq. 1
+    const float cn = fmaf(f, c, fmaf(-f, u0, u0));                           // Eq. 2
+    const float r = sigmoid_scaled(fmaf(vrs, RN ? cn : c, fmaf(u2, kNegLog2e, brs)));  // Eq. 3
     float h = fmaf(r, cn, (1.0f - r) * (alpha * xh));     // Eq. 4 (Sec. 3.2)
     if constexpr (MASK) {
       const bool pad = m != 0;
@@ -175,7 +178,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
   int is = 0;  // steps done
 
   const float vf = a.v_f[ln.fidx], vr = a.v_r[ln.fidx];
-  const float bf = a.b_f[ln.fidx], br = a.b_r[ln.fidx];
+  // the forward scan's gate arithmetic (sigmoid_scaled), so f and r are the
+  // forward's values bit for bit
+  const float vfs = vf * kNegLog2e, vrs = vr * kNegLog2e;
+  const float bfs = a.b_f[ln.fidx] * kNegLog2e, brs = a.b_r[ln.fidx] * kNegLog2e;
   const float alpha = s.alpha;
   const float c0v = a.c0 ? a.c0[ln.gid] : 0.0f;
   float g = a.dc_last ? a.dc_last[ln.gid] : 0.0f;
@@ -213,8 +219,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
     const float c_p = is + 1 < L ? cprev : c0v;  // position 0 starts from c0
     ++is;
     const float c_r = RN ? c_t : c_p;  // the state the reset gate reads
-    const float f = sigmoid_fast(fmaf(vf, c_p, u1 + bf));
-    const float r = sigmoid_fast(fmaf(vr, c_r, u2 + br));
+    const float f = sigmoid_scaled(fmaf(vfs, c_p, fmaf(u1, kNegLog2e, bfs)));
+    const float r = sigmoid_scaled(fmaf(vrs, c_r, fmaf(u2, kNegLog2e, brs)));
     bool pad = false;
     if constexpr (MASK) pad = m != 0;
     const float dhv = pad ? 0.0f : dh;
@@ -224,7 +230,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
     // total gradient into c_t: from later steps, through h, and (RN)
     // through the reset gate
     const float gc = RN ? fmaf(dr, vr, fmaf(dhv, r, g)) : fmaf(dhv, r, g);
-    float df = gc * (c_p - u0) * ff;
+    const float pf = (c_p - u0) * ff;  // df = gc pf
+    float df = gc * pf;
     float du0 = gc * (1.0f - f);
     float dx = dhv * (1.0f - r) * alpha;
     if constexpr (MASK) {
@@ -237,7 +244,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
     sum_dr_c = fmaf(dr, c_r, sum_dr_c);
     sum_df += df;
     sum_dr += dr;
-    const float gn = RN ? fmaf(df, vf, gc * f) : fmaf(dr, vr, fmaf(df, vf, gc * f));
+    // g <- gc f + df v_f (+ dr v_r) = gc (f + pf v_f) (+ dr v_r): two
+    // dependent operations from g to the next g
+    const float gf = fmaf(pf, vf, f);
+    const float gn = RN ? gc * gf : fmaf(gc, gf, dr * vr);
     g = pad ? g : gn;
     auto put = [](float v, DuT* p) {
       if constexpr (DUB) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)v), p);
