@@ -1434,16 +1434,35 @@ bool direct_ok(const GemmDesc& g) {
 }
 
 // Split count for the direct path: the K = tokens product (row-contiguous
-// operands) is cut so that every CU gets its workgroups (at least 8 K steps
-// per split).
+// operands) is cut over K so that the CUs share the work evenly.  The count
+// minimises a cost in K steps: the rounds of workgroups over the CUs times
+// the K steps of a split, plus the split partials' HBM traffic ((s + 1)
+// fp32 outputs written and read) at kSplitBytesPerStep, the bytes HBM moves
+// in the time of one K step (a 64 KiB stage takes ~2 us per CU; ~6 TB/s).
+// At least 8 K steps per split.  E.g. 48 tiles x 256 steps: 5 splits (240
+// workgroups, 52 steps); 192 tiles x 256 steps: 4 splits (768 workgroups,
+// three rounds of 64 steps) rather than 192 workgroups of 256 steps.
+constexpr double kSplitBytesPerStep = 11.0 * (1 << 20);
 template <class C>
 int direct_splits_cfg(const GemmDesc& g) {
   if (g.a_kc) return 1;
-  const int tiles = ((g.M + C::BM - 1) / C::BM) * ((g.N + C::BN - 1) / C::BN);
+  const long long tiles = (long long)((g.M + C::BM - 1) / C::BM) * ((g.N + C::BN - 1) / C::BN);
   const int kt = (g.K + C::BK - 1) / C::BK;
-  int s = max(1, (C::OCC * 256) / tiles);
-  s = min(s, max(1, kt / 8));
-  const int kps = ((kt + s - 1) / s) * C::BK;
+  const long long slots = C::OCC * 256LL;  // workgroups the CUs run at once
+  const double out_bytes = 4.0 * g.M * g.N;
+  int best = 1;
+  double best_cost = 0.0;
+  for (int s = 1; s <= max(1, kt / 8); ++s) {
+    const long long rounds = (tiles * s + slots - 1) / slots;
+    const int steps = (kt + s - 1) / s;
+    const double cost =
+        (double)(rounds * steps) + (s > 1 ? (s + 1) * out_bytes / kSplitBytesPerStep : 0.0);
+    if (s == 1 || cost < best_cost) {
+      best = s;
+      best_cost = cost;
+    }
+  }
+  const int kps = ((kt + best - 1) / best) * C::BK;
   return (g.K + kps - 1) / kps;
 }
 
