@@ -187,8 +187,23 @@ sru::GemmDesc dw_desc(const Dims& s, bool bf16, const void* dU, const void* X, f
 //    Wcat^T and X in bf16 (bf16 mode) | dW split partials]
 struct BwdLayout {
   size_t dU, dxh, partial, wt, xb, splitk, total;
-  int splits;
+  int splits, splits_dx;
 };
+
+// dX = dU Wcat (+ highway): NN on Wcat in fp32 mode; in bf16 mode NT on the
+// bf16 Wcat^T.  The fp32 product's tiles can be too few to fill the CUs
+// (d_in of a few hundred), so it may be split over K.
+sru::GemmDesc dx_desc(const Dims& s, bool bf16, const void* dU, const void* W, const void* wt,
+                      float* dX) {
+  sru::GemmDesc g = bf16 ? gemm_desc(SRU_OP_NT, true, (int)s.M, s.d_in, (int)s.N, dU, s.N, wt,
+                                     s.N, dX, s.d_in)
+                         : gemm_desc(SRU_OP_NN, false, (int)s.M, s.d_in, (int)s.N, dU, s.N, W,
+                                     s.d_in, dX, s.d_in);
+  g.a_bf16 = g.b_bf16 = bf16;
+  g.kc_split = !bf16;
+  g.label = "gemm_dx";
+  return g;
+}
 
 BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
   const bool bf16 = gemm_dtype == SRU_GEMM_BF16;
@@ -205,8 +220,10 @@ BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
   w.xb = off;
   if (bf16) off += align_up(2 * (size_t)s.M * (size_t)s.d_in);
   w.splits = sru::gemm_splits(dw_desc(s, bf16, nullptr, nullptr, nullptr));
-  w.splitk = off;
-  off += align_up(sru::gemm_partial_bytes((int)s.N, s.d_in, w.splits));
+  w.splits_dx = sru::gemm_splits(dx_desc(s, bf16, nullptr, nullptr, nullptr, nullptr));
+  w.splitk = off;  // shared by the dX and dW partials (they run one after the other)
+  off += align_up(std::max(sru::gemm_partial_bytes((int)s.N, s.d_in, w.splits),
+                           sru::gemm_partial_bytes((int)s.M, s.d_in, w.splits_dx)));
   w.total = off;
   return w;
 }
@@ -509,18 +526,16 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   //    copy of W_bf16 when the caller holds it, else rounded from W), so
   //    both operands are K-contiguous: the product then runs at the speed
   //    of the projection, faster than with Wcat read row-contiguous.
-  sru::GemmDesc gx;
   if (bf16) {
     const hipError_t te = W_bf16
         ? sru::to_bf16_t_launch(W_bf16, true, (int)s.N, d_in, wt, stream, "bf16_wt")
         : sru::to_bf16_t_launch(W, false, (int)s.N, d_in, wt, stream, "bf16_wt");
     if (int e = hip_status(te)) return e;
-    gx = gemm_desc(SRU_OP_NT, true, (int)s.M, d_in, (int)s.N, dU, s.N, wt, s.N, dX, d_in);
-    gx.a_bf16 = gx.b_bf16 = true;
-  } else {
-    gx = gemm_desc(SRU_OP_NN, false, (int)s.M, d_in, (int)s.N, dU, s.N, W, d_in, dX, d_in);
   }
-  gx.label = "gemm_dx";
+  sru::GemmDesc gx = dx_desc(s, bf16, dU, W, wt, dX);
+  gx.partials = splitk;
+  // split as planned, else (a plan that differs at run time) not at all
+  if (sru::gemm_splits(gx) > lay.splits_dx) gx.kc_split = false;
   if (s.k == 3) {
     gx.add = dxh;
     gx.add_ld = s.nfeat;

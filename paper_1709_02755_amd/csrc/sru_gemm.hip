@@ -1324,8 +1324,13 @@ __global__ __launch_bounds__(256) void to_bf16_t_tiled_kernel(const S* __restric
 
 template <class C>
 int splits_for(const GemmDesc& g) {
-  if (g.a_kc) return 1;  // only the K = tokens product (TN) is split
   const int tiles = ((g.M + C::BM - 1) / C::BM) * ((g.N + C::BN - 1) / C::BN);
+  // The K = tokens product (TN) is split.  A K-contiguous one is split only
+  // on request and only when its tiles fill at most a quarter of the CUs:
+  // the 32 tiles of the two-layer d = 256 stack's dX (K = 768) take 21 us
+  // split six ways plus 6 us for the split sum, instead of 66 us; at 100-200
+  // tiles the partials' extra pass costs what the split saves.
+  if (g.a_kc && (!g.kc_split || tiles > 64)) return 1;
   const int kt = (g.K + C::BK - 1) / C::BK;  // K steps
   int s = (2 * 256 + tiles - 1) / tiles;     // aim for two workgroups per CU
   // fp32 accumulation chains stay short (<= 2048 terms per split)

@@ -31,6 +31,9 @@ struct GemmDesc {
   bool bf16;
   int splits;
   float* partials;
+  // a K-contiguous product may be split over K too (register-staged path,
+  // when its tiles would leave CUs idle); partials must then be given
+  bool kc_split;
   const float* add;
   long long add_ld, add_off;
   int add_count;
