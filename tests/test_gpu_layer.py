@@ -161,3 +161,36 @@ def test_chunked_backward_carry_on_gpu(direction, gemm):
     tol = TOL_FP32 if gemm == O.GEMM_FP32 else 1e-5
     for k in ("dW", "dv_f", "dv_r", "db_f", "db_r"):
         check(k, ga[k] + gs[k], host(fb[k]), tol)
+
+
+def test_layers_on_two_streams_equal_serial():
+    """Two layers enqueued at once on two streams (default priority) give the
+    same bits as the same calls one after the other: the library keeps no
+    state between calls, and each call's work stays on its own stream."""
+    print("two streams: bf16 forward L=33 B=8 d=256 | fp32 bidirectional L=20 B=5 d=96", flush=True)
+    cases = [(random_layer_case(np.random.default_rng(11), 33, 8, 256, 256, O.DIR_FWD, masked=True,
+                                c0=True, dc_last=True, bias_scale=0.5), O.DIR_FWD, O.GEMM_BF16),
+             (random_layer_case(np.random.default_rng(12), 20, 5, 96, 96, O.DIR_BI, masked=True,
+                                c0=True, dc_last=True, bias_scale=0.5), O.DIR_BI, O.GEMM_FP32)]
+
+    def enqueue(c, direction, gemm):
+        X, W = dev(c["X"]), dev(c["W"])
+        p = [dev(c[k]) for k in ("v_f", "v_r", "b_f", "b_r")]
+        c0, mask, dcl, dH = dev(c["c0"]), dev(c["mask"]), dev(c["dc_last"]), dev(c["dH"])
+        fw = sru.forward(X, W, *p, c0=c0, direction=direction, mask=mask, gemm_dtype=gemm)
+        bw = sru.backward(X, W, *p, fw["U"], fw["C"], dH, c0=c0, dc_last=dcl,
+                          direction=direction, mask=mask, gemm_dtype=gemm)
+        return {**fw, **bw}
+
+    serial = [enqueue(*a) for a in cases]
+    torch.cuda.synchronize()
+    serial = [{k: host(v) for k, v in r.items() if v is not None} for r in serial]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = []
+    for st, a in zip(streams, cases):
+        with torch.cuda.stream(st):
+            outs.append(enqueue(*a))
+    torch.cuda.synchronize()
+    for ref, got in zip(serial, outs):
+        for k, v in ref.items():
+            assert np.array_equal(host(got[k]), v), k
