@@ -114,6 +114,27 @@ def lengths_to_mask(lengths: np.ndarray, L: int) -> np.ndarray:
     return (t >= np.asarray(lengths)[None, :]).astype(np.uint8)
 
 
+def irregular_mask(rng, L: int, B: int) -> np.ndarray:
+    """[L, B] uint8 padding that is not a suffix, cycling over B by sequence:
+    no padding, every step padded, random holes (about 40 %), the first third
+    padded, a single valid step in the middle.  The layer's mask is any [L, B]
+    pattern; these are the degenerate ones beside the usual padded tails."""
+    m = np.zeros((L, B), np.uint8)
+    for b in range(B):
+        kind = b % 5
+        if kind == 1:
+            m[:, b] = 1
+        elif kind == 2:
+            m[:, b] = rng.random(L) < 0.4
+            m[rng.integers(L), b] = 0
+        elif kind == 3:
+            m[: L // 3, b] = 1
+        elif kind == 4:
+            m[:, b] = 1
+            m[L // 2, b] = 0
+    return m
+
+
 def draw_layer(rng, ndir: int, k: int, d: int, d_in: int, bf_uniform: bool,
                dp: int | None = None) -> dict:
     if dp is None:

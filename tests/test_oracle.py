@@ -12,7 +12,7 @@ import scipy.special
 import torch
 
 from oracle import sru_oracle as O
-from paper_1709_02755_amd.workloads import random_layer_case, lengths_to_mask
+from paper_1709_02755_amd.workloads import irregular_mask, lengths_to_mask, random_layer_case
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 F, R, BI = O.DIR_FWD, O.DIR_REV, O.DIR_BI
@@ -865,3 +865,84 @@ def test_linear_variant_lowrank_equals_dense_product_weight(rng):
     for key in ("dX", "db_f", "db_r", "dc0"):
         np.testing.assert_allclose(lr[key], dn[key], rtol=1e-10, atol=1e-12)
     assert lr["dv_f"] is None
+
+
+# ---------------------------------------------------------------- pin 7b
+def _compacted_reference(c, direction, mask, run):
+    """Per sequence, the unpadded run over its valid steps only (None when it
+    has none): a padded step leaves the state and every gradient untouched,
+    so skipping it must change nothing (Eq. 1-4 apply to the valid steps)."""
+    out = []
+    for b in range(c["X"].shape[1]):
+        valid = mask[:, b] == 0
+        if not valid.any():
+            out.append(None)
+            continue
+        sub = dict(X=c["X"][valid, b:b + 1].copy(), dH=c["dH"][valid, b:b + 1].copy(),
+                   c0=c["c0"][b:b + 1].copy(), dc_last=c["dc_last"][b:b + 1].copy())
+        out.append(run(sub))
+    return out
+
+
+@pytest.mark.parametrize("direction,k4", [(F, False), (R, True), (BI, False), (BI, True)])
+@pytest.mark.parametrize("variant", ["gated", "alpha_reset_new", "linear"])
+def test_irregular_mask_equals_compacted_sequences(rng, direction, k4, variant):
+    """Masks with holes, a fully padded sequence, left padding and a single
+    valid step: on every sequence the masked layer equals the unmasked layer
+    run over that sequence's valid steps alone (H, C, c_last, dX, dc0; C
+    carries the last state over padded steps), the batch sums dW, dv, db are
+    the sums of those runs, and a fully padded sequence passes c0 to c_last
+    and dc_last to dc0 with zero H and dX."""
+    L, B, d = 11, 10, 4
+    d_in = 6 if k4 else d
+    c = _case(rng, L, B, d_in, d, direction, c0=True, dc_last=True, bias_scale=0.5,
+              v_scale=1.2)
+    mask = irregular_mask(rng, L, B)
+    v = dict(gated={}, alpha_reset_new=dict(alpha=1.6, reset_new=True),
+             linear=dict(linear=True))[variant]
+    pw = (c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"])
+
+    def run(a, m=None):
+        fw = O.forward(a["X"], *pw, a["c0"], direction, m, **v)
+        bw = O.backward(a["X"], *pw, a["dH"], a["c0"], direction, m, O.GEMM_FP32,
+                        a["dc_last"], fw=fw, **v)
+        return fw, bw
+
+    fw, bw = run(c, mask)
+    ndir = 2 if direction == BI else 1
+    C = fw["C"].reshape(L, B, ndir, d)
+    tol = dict(rtol=1e-11, atol=1e-12)
+    sums = {k: 0.0 for k in ("dW", "db_f", "db_r") + (() if variant == "linear" else
+                                                       ("dv_f", "dv_r"))}
+    for b, one in enumerate(_compacted_reference(c, direction, mask, run)):
+        valid = mask[:, b] == 0
+        if one is None:
+            assert np.all(fw["H"][:, b] == 0.0) and np.all(bw["dX"][:, b] == 0.0)
+            np.testing.assert_allclose(fw["c_last"][b], c["c0"][b], **tol)
+            np.testing.assert_allclose(bw["dc0"][b], c["dc_last"][b], **tol)
+            np.testing.assert_allclose(C[:, b], np.broadcast_to(
+                c["c0"][b].reshape(ndir, d), (L, ndir, d)), **tol)
+            continue
+        of, ob = one
+        assert np.all(fw["H"][~valid, b] == 0.0) and np.all(bw["dX"][~valid, b] == 0.0)
+        np.testing.assert_allclose(fw["H"][valid, b], of["H"][:, 0], **tol)
+        np.testing.assert_allclose(fw["C"][valid, b], of["C"][:, 0], **tol)
+        np.testing.assert_allclose(fw["c_last"][b], of["c_last"][0], **tol)
+        np.testing.assert_allclose(bw["dX"][valid, b], ob["dX"][:, 0], **tol)
+        np.testing.assert_allclose(bw["dc0"][b], ob["dc0"][0], **tol)
+        # over a padded step C holds the state of the direction's previous
+        # valid step (c0 before the first)
+        oc = of["C"][:, 0].reshape(-1, ndir, d)
+        idx = np.flatnonzero(valid)
+        c0b = c["c0"][b].astype(np.float64).reshape(ndir, d)
+        for dirn in range(ndir):
+            rev = direction == R or dirn == 1
+            for t in np.flatnonzero(~valid):
+                prev = idx[idx > t] if rev else idx[idx < t]
+                want = c0b[dirn] if prev.size == 0 else \
+                    oc[np.searchsorted(idx, prev.min() if rev else prev.max()), dirn]
+                np.testing.assert_allclose(C[t, b, dirn], want, **tol)
+        for k in sums:
+            sums[k] = sums[k] + ob[k]
+    for k, s in sums.items():
+        np.testing.assert_allclose(bw[k], s, **tol)
