@@ -1,16 +1,16 @@
 """GPU parity under padding that is not a suffix: holes inside a sequence, a
 fully padded sequence, left padding and a single valid step (the layer's mask
 is any [L, B] pattern).  Whole layers through the C ABI against the oracle,
-for the gated recurrence, the gate variants and the linear recurrence (whose
-chunked scan composes padded steps as identity maps), fp32 and bf16
-products, every direction, k = 3 and 4, the backward's shorter ring at
-65,536+ lanes, and the fused inference kernel."""
+for the gated recurrence, the gate variants, the projection trick and the
+linear recurrence (whose chunked scan composes padded steps as identity
+maps), fp32 and bf16 products, every direction, k = 3 and 4, the backward's
+shorter ring at 65,536+ lanes, and the fused inference kernel."""
 
 import numpy as np
 import pytest
 import torch
 
-from helpers import TOL_BF16, TOL_FP32, check, dev, host
+from helpers import TOL_BF16, TOL_BF16_LOWRANK, TOL_FP32, check, dev, host
 from oracle import sru_oracle as O
 from paper_1709_02755_amd import sru
 from paper_1709_02755_amd.workloads import irregular_mask, random_layer_case
@@ -107,3 +107,37 @@ def test_fused_inference_with_irregular_mask(linear):
         check(k, out[k], rf[k], TOL_BF16)
     m = c["mask"].astype(bool)
     assert np.all(host(out["H"])[m] == 0.0)
+
+
+@pytest.mark.parametrize("gemm", [O.GEMM_FP32, O.GEMM_BF16])
+def test_lowrank_layer_with_irregular_mask(gemm):
+    """The projection trick (Wcat = P Q^T, Sec. 4.4) under the same masks:
+    T = X Q runs over padded steps too, but no gradient of a padded step
+    reaches dX, dQ or dP."""
+    L, B, d_in, d, dp, direction = 29, 10, 128, 64, 32, O.DIR_BI
+    print(f"lowrank irregular mask gemm={gemm}", flush=True)
+    c = _case(41 + gemm, L, B, d_in, d, direction)
+    rng = np.random.default_rng(43 + gemm)
+    ndir, k = c["W"].shape[:2]
+    Q = (rng.uniform(-1, 1, (d_in, dp)) * np.sqrt(3.0 / d_in)).astype(np.float32)
+    P = (rng.uniform(-1, 1, (ndir, k, d, dp)) * np.sqrt(3.0 / dp)).astype(np.float32)
+    p = [dev(c[key]) for key in ("v_f", "v_r", "b_f", "b_r")]
+    X, Qd, Pd, c0, mask = dev(c["X"]), dev(Q), dev(P), dev(c["c0"]), dev(c["mask"])
+    fw = sru.forward_lowrank(X, Qd, Pd, *p, c0=c0, direction=direction, mask=mask,
+                             gemm_dtype=gemm)
+    bw = sru.backward_lowrank(X, Qd, Pd, *p, fw["T"], fw["U"], fw["C"], dev(c["dH"]), c0=c0,
+                              dc_last=dev(c["dc_last"]), direction=direction, mask=mask,
+                              gemm_dtype=gemm)
+    torch.cuda.synchronize()
+    args = (c["X"], Q, P, c["v_f"], c["v_r"], c["b_f"], c["b_r"])
+    rf = O.forward_lowrank(*args, c["c0"], direction, c["mask"], gemm)
+    rb = O.backward_lowrank(*args, c["dH"], c["c0"], direction, c["mask"], gemm, c["dc_last"],
+                            fw=rf)
+    tol = TOL_FP32 if gemm == O.GEMM_FP32 else TOL_BF16_LOWRANK
+    for key in ("H", "C", "c_last"):
+        check(key, fw[key], rf[key], tol)
+    for key in ("dX", "dQ", "dP", "dv_f", "dv_r", "db_f", "db_r", "dc0"):
+        check(key, bw[key], rb[key], tol)
+    m = c["mask"].astype(bool)
+    assert np.all(host(fw["H"])[m] == 0.0)
+    assert np.all(host(bw["dX"])[m] == 0.0)
