@@ -272,3 +272,21 @@ def test_forward_without_u_needs_the_fused_path():
     assert _fwd(lib, d_in=128, d=64, gemm=1, U=None, C=FAKE) == E_NULL
     # bf16, C omitted: U may be omitted (the call goes on to the workspace check)
     assert _fwd(lib, d_in=128, d=64, gemm=1, U=None, C=None) == E_WS
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """With no library and no way to build one, the binding raises; there is
+    no other path to the results (no CPU fallback)."""
+    from paper_1709_02755_amd import build as build_mod
+
+    def no_build():
+        raise RuntimeError("hipcc unavailable")
+
+    monkeypatch.setattr(sru, "_lib", None)
+    monkeypatch.setattr(sru, "LIB_PATH", str(tmp_path / "libsru.so"))
+    monkeypatch.setattr(build_mod, "build", no_build)
+    with pytest.raises(RuntimeError, match="hipcc unavailable"):
+        sru.lib()
+    (tmp_path / "libsru.so").write_bytes(b"not a shared object")
+    with pytest.raises(OSError):
+        sru.lib()
