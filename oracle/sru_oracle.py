@@ -70,6 +70,24 @@ def _f64(a):
     return None if a is None else np.asarray(a, dtype=np.float64)
 
 
+# Precision in which the matrix products accumulate: fp64 (exact for the
+# oracle's purposes).  A test may set it to np.float32 to evaluate the same
+# method the way an fp32-accumulating implementation does, which measures how
+# far accumulation order alone can move a bf16-mode result (each product's
+# output then differs by fp32 rounding, and a value that crosses a bf16
+# rounding boundary changes the next product's operand by a whole bf16 step).
+PRODUCT_ACCUMULATION = np.float64
+
+
+def _mm(a, b):
+    """The matrix product a @ b, accumulated in PRODUCT_ACCUMULATION,
+    returned as fp64."""
+    if PRODUCT_ACCUMULATION is np.float64:
+        return np.asarray(a, np.float64) @ np.asarray(b, np.float64)
+    acc = PRODUCT_ACCUMULATION
+    return (np.asarray(a, acc) @ np.asarray(b, acc)).astype(np.float64)
+
+
 def bf16_round(a):
     """Round to the nearest bfloat16 value (ties to even), returned as fp64.
 
@@ -163,7 +181,7 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
         for t in steps:
             x_t = X[t]
             xp = bf16_round(x_t) if bf16 else x_t
-            u = [xp @ Wp[dirn, q].T for q in range(k)]          # W x_t, W_f x_t, ...
+            u = [_mm(xp, Wp[dirn, q].T) for q in range(k)]          # W x_t, W_f x_t, ...
             x_hat = x_t if k == 3 else u[3]
             f = sigmoid(u[1] + v_f[dirn] * c + b_f[dirn])        # Eq. 1
             c_new = f * c + (1.0 - f) * u[0]                      # Eq. 2
@@ -270,8 +288,8 @@ def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
             du_p = bf16_round(du_t) if bf16 else du_t
             xp = bf16_round(x_t) if bf16 else x_t
             for q in range(k):
-                dX[t] += du_p[:, q] @ Wp[dirn, q]
-                dW[dirn, q] += du_p[:, q].T @ xp
+                dX[t] += _mm(du_p[:, q], Wp[dirn, q])
+                dW[dirn, q] += _mm(du_p[:, q].T, xp)
             if k == 3:
                 dX[t] += dxh[t, :, dirn]
         dc0[:, dirn] = g
@@ -281,48 +299,24 @@ def backward(X, W, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD,
                 dc0=dc0.reshape(B, ndir * d), dU=dU, dxh=dxh)
 
 
-def forward_alg1_scalar(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
-                        pad_mask=None, alpha=1.0, reset_new=False, linear=False):
-    """Tiny-shape cross-check in the shape of Algorithm 1 (fp32 GEMM mode).
-
-    The projections for all steps come first as one batched product (Sec. 3.1),
-    then independent scalar recurrences run per (example i, dimension j),
-    reading the gate columns at offsets j, j+d, j+2d of the batched tensor.
-    The reset gate uses the previous state (Eq. 3 reading) unless reset_new,
-    where it follows Algorithm 1's order (r after c).  Pure Python loops:
-    only for tiny shapes.
-    """
+def forward_batched(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, pad_mask=None,
+                    alpha=1.0, reset_new=False, linear=False):
+    """Sec. 3.1's organisation of the same layer, as a cross-check of
+    forward() (fp32-GEMM mode): the projections of all L*B tokens come from
+    one matrix product with the stacked weight [W; W_f; W_r(; W_h)] first,
+    and the step loop of Eq. 1-4 then only reads its gate inputs from that
+    batched tensor.  forward() instead multiplies inside the step loop, so
+    agreement checks the reorganisation rather than assuming it.
+    Returns dict(U, H, C, c_last)."""
     X = _f64(X)
     W = _f64(W)
     L, B, d_in, ndir, k, d = _check_shapes(X, W, direction)
-    v_f, v_r = _gate_weights(v_f, v_r, ndir, d, linear)
-    b_f, b_r = (_f64(a).reshape(ndir, d) for a in (b_f, b_r))
-    c0 = np.zeros((B, ndir, d)) if c0 is None else _f64(c0).reshape(B, ndir, d)
-    pad = np.zeros((L, B), bool) if pad_mask is None else (np.asarray(pad_mask) != 0)
-    # Batched projection: rows (dir, block, j) of the stacked weight.
-    Wcat = W.reshape(ndir * k * d, d_in)
-    Ub = (X.reshape(L * B, d_in) @ Wcat.T).reshape(L, B, ndir, k * d)
-    H = np.zeros((L, B, ndir, d))
-    C = np.zeros((L, B, ndir, d))
-    for dirn in range(ndir):
-        steps = range(L - 1, -1, -1) if _is_reverse(direction, dirn) else range(L)
-        for i in range(B):
-            for j in range(d):
-                c = float(c0[i, dirn, j])
-                for l in steps:
-                    if pad[l, i]:
-                        C[l, i, dirn, j] = c
-                        continue
-                    u = Ub[l, i, dirn]
-                    f = float(sigmoid(u[j + d] + v_f[dirn, j] * c + b_f[dirn, j]))
-                    c_prev = c
-                    c = f * c + (1.0 - f) * u[j]
-                    s = c if reset_new else c_prev
-                    r = float(sigmoid(u[j + 2 * d] + v_r[dirn, j] * s + b_r[dirn, j]))
-                    xh = X[l, i, j] if k == 3 else u[j + 3 * d]
-                    H[l, i, dirn, j] = r * c + (1.0 - r) * xh * alpha
-                    C[l, i, dirn, j] = c
-    return dict(H=H.reshape(L, B, ndir * d), C=C.reshape(L, B, ndir * d))
+    Wcat = W.reshape(ndir * k * d, d_in)                    # rows (dir, block, unit)
+    U = _mm(X.reshape(L * B, d_in), Wcat.T).reshape(L, B, ndir, k, d)
+    out = _scan_on_u(X, U, v_f, v_r, b_f, b_r, c0, direction, pad_mask, alpha, reset_new,
+                     linear)
+    out["U"] = U
+    return out
 
 
 def stack_forward_backward(X, layers, direction, pad_mask, gemm_dtype, dH_top,
@@ -386,8 +380,8 @@ def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD,
     ndir, k, d, dp = P.shape
     bf16 = gemm_dtype == GEMM_BF16
     rnd = bf16_round if bf16 else (lambda a: a)
-    T = rnd(X) @ rnd(Q)                                   # [L, B, dp]
-    U = (rnd(T) @ rnd(P).reshape(ndir * k * d, dp).T).reshape(L, B, ndir, k, d)
+    T = _mm(rnd(X), rnd(Q))                               # [L, B, dp]
+    U = _mm(rnd(T), rnd(P).reshape(ndir * k * d, dp).T).reshape(L, B, ndir, k, d)
     # the scan of Eq. 1-4 on this U: the dense oracle with W chosen so that
     # its per-step projections are exactly U is not available, so the step
     # loop is run here on U directly
@@ -454,12 +448,12 @@ def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, dH, c0=None, direction=DIR_FWD
                   linear=linear)
     dU = bw["dU"].reshape(L, B, ndir * k * d)
     Pm = P.reshape(ndir * k * d, dp)
-    dT = rnd(dU) @ rnd(Pm)                                  # [L, B, dp]
-    dX = rnd(dT) @ rnd(Q).T
+    dT = _mm(rnd(dU), rnd(Pm))                              # [L, B, dp]
+    dX = _mm(rnd(dT), rnd(Q).T)
     if k == 3:
         dX = dX + bw["dxh"].sum(axis=2)
     dUm = rnd(dU).reshape(L * B, -1)
-    dP = (dUm.T @ rnd(fw["T"]).reshape(L * B, dp)).reshape(ndir, k, d, dp)
-    dQ = rnd(X).reshape(L * B, d_in).T @ rnd(dT).reshape(L * B, dp)
+    dP = _mm(dUm.T, rnd(fw["T"]).reshape(L * B, dp)).reshape(ndir, k, d, dp)
+    dQ = _mm(rnd(X).reshape(L * B, d_in).T, rnd(dT).reshape(L * B, dp))
     return dict(dX=dX, dQ=dQ, dP=dP, dv_f=bw["dv_f"], dv_r=bw["dv_r"], db_f=bw["db_f"],
                 db_r=bw["db_r"], dc0=bw["dc0"], dU=bw["dU"], dT=dT, dxh=bw["dxh"])

@@ -85,12 +85,6 @@ def _options(highway_scale=1.0, reset_new=False, linear=False):
                                 RECURRENCE_LINEAR if linear else RECURRENCE_GATED))
 
 
-def highway_scale_for_bias(b):
-    """alpha = sqrt(1 + 2 e^b) for a reset-gate bias b (Sec. 3.2, Appendix A)."""
-    import math
-    return math.sqrt(1.0 + 2.0 * math.exp(b))
-
-
 def lib():
     """Load libsru.so (building it first only if it has never been built)."""
     global _lib
@@ -128,19 +122,47 @@ def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
-def _req(t, name, shape, dtype=torch.float32, optional=False):
+def _on_gpu(t):
+    return t.is_cuda
+
+
+def _req(t, name, shape, dtype=torch.float32, optional=False, device=None):
+    """A GPU tensor of this shape and dtype, contiguous, on `device` (if given)."""
     if t is None:
         if optional:
             return
         raise ValueError(f"{name} is required")
-    if not t.is_cuda:
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if not _on_gpu(t):
         raise ValueError(f"{name} must be a GPU tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
     if t.dtype != dtype:
         raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if tuple(t.shape) != tuple(shape):
         raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def _req_out(out, specs, device):
+    """Check the caller-supplied output buffers of `out` against
+    name -> (shape, dtype, required)."""
+    for name, (shape, dtype, required) in specs.items():
+        _req(out.get(name), name, shape, dtype=dtype, optional=not required, device=device)
+
+
+def _ws(ws, need, device):
+    """(workspace tensor or None, its size in bytes).  A caller's workspace
+    must be a contiguous uint8 GPU tensor on `device`; its real size is what
+    the library is told, so the library's own size check applies."""
+    if ws is None:
+        if not need:
+            return None, 0
+        ws = workspace(need, device)
+    _req(ws, "ws", (ws.numel(),), dtype=torch.uint8, device=device)
+    return ws, ws.numel() * ws.element_size()
 
 
 def dims(X, W):
@@ -150,18 +172,22 @@ def dims(X, W):
 
 
 def _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask):
+    for n, t, nd in (("X", X, 3), ("W", W, 4)):
+        if not isinstance(t, torch.Tensor) or t.dim() != nd:
+            raise ValueError(f"{n} must be a {nd}-d tensor")
+    _req(X, "X", tuple(X.shape))
     L, B, d_in, d, ndir, k = dims(X, W)
     want_nd = 2 if direction == DIR_BI else 1
     if ndir != want_nd or k != (3 if d_in == d else 4):
         raise ValueError(f"W shape {tuple(W.shape)} does not fit d_in={d_in}, direction={direction}")
-    _req(X, "X", (L, B, d_in))
-    _req(W, "W", (ndir, k, d, d_in))
+    dv = X.device
+    _req(W, "W", (ndir, k, d, d_in), device=dv)
     for n, t in (("v_f", v_f), ("v_r", v_r)):
-        _req(t, n, (ndir, d), optional=True)  # the library reports a missing v
+        _req(t, n, (ndir, d), optional=True, device=dv)  # the library reports a missing v
     for n, t in (("b_f", b_f), ("b_r", b_r)):
-        _req(t, n, (ndir, d))
-    _req(c0, "c0", (B, ndir * d), optional=True)
-    _req(mask, "mask", (L, B), dtype=torch.uint8, optional=True)
+        _req(t, n, (ndir, d), device=dv)
+    _req(c0, "c0", (B, ndir * d), optional=True, device=dv)
+    _req(mask, "mask", (L, B), dtype=torch.uint8, optional=True, device=dv)
     return L, B, d_in, d, ndir, k
 
 
@@ -194,25 +220,27 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
     rounding of X; entries W_bf16 / H_bf16 of `out` (bfloat16 tensors), if
     present, receive Wcat and H rounded to bf16."""
     L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask)
-    _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True)
-    dev = X.device
+    dv = X.device
+    _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True, device=dv)
     if out is None:
         no_u = not keep_u and not store_c and fused_available(L, B, d_in, d, direction,
                                                                 gemm_dtype)
-        out = dict(U=None if no_u else torch.empty((L, B, ndir, k, d), device=dev),
-                   H=torch.empty((L, B, ndir * d), device=dev),
-                   C=torch.empty((L, B, ndir * d), device=dev) if store_c else None,
-                   c_last=torch.empty((B, ndir * d), device=dev))
-    need = forward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype)
-    if need and ws is None:
-        ws = workspace(need, dev)
+        out = dict(U=None if no_u else torch.empty((L, B, ndir, k, d), device=dv),
+                   H=torch.empty((L, B, ndir * d), device=dv),
+                   C=torch.empty((L, B, ndir * d), device=dv) if store_c else None,
+                   c_last=torch.empty((B, ndir * d), device=dv))
+    f32, b16 = torch.float32, torch.bfloat16
+    _req_out(out, dict(U=((L, B, ndir, k, d), f32, False), H=((L, B, ndir * d), f32, True),
+                       C=((L, B, ndir * d), f32, False), c_last=((B, ndir * d), f32, False),
+                       W_bf16=(tuple(W.shape), b16, False),
+                       H_bf16=((L, B, ndir * d), b16, False)), dv)
+    ws, nbytes = _ws(ws, forward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype), dv)
     st = lib().sru_forward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                            L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
                            _options(highway_scale, reset_new, linear),
                            _ptr(out.get("U")), _ptr(out["H"]), _ptr(out.get("C")),
                            _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("W_bf16")),
-                           _ptr(out.get("H_bf16")), _ptr(ws), need if ws is not None else 0,
-                           _stream())
+                           _ptr(out.get("H_bf16")), _ptr(ws), nbytes, _stream())
     _check(st, "sru_forward")
     return out
 
@@ -225,31 +253,54 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
     bf16 GEMMs only: X_bf16 / W_bf16 (bfloat16 roundings of X and Wcat, as
     forward() writes them) replace the library's own rounding."""
     L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask)
-    _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True)
-    _req(W_bf16, "W_bf16", tuple(W.shape), dtype=torch.bfloat16, optional=True)
-    _req(U, "U", (L, B, ndir, k, d))
-    _req(C, "C", (L, B, ndir * d))
-    _req(dH, "dH", (L, B, ndir * d))
-    _req(dc_last, "dc_last", (B, ndir * d), optional=True)
-    dev = X.device
+    dv = X.device
+    _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True, device=dv)
+    _req(W_bf16, "W_bf16", tuple(W.shape), dtype=torch.bfloat16, optional=True, device=dv)
+    _req(U, "U", (L, B, ndir, k, d), device=dv)
+    _req(C, "C", (L, B, ndir * d), device=dv)
+    _req(dH, "dH", (L, B, ndir * d), device=dv)
+    _req(dc_last, "dc_last", (B, ndir * d), optional=True, device=dv)
     if out is None:
         out = dict(dX=torch.empty_like(X), dW=torch.empty_like(W),
-                   dv_f=None if linear else torch.empty((ndir, d), device=dev),
-                   dv_r=None if linear else torch.empty((ndir, d), device=dev),
-                   db_f=torch.empty((ndir, d), device=dev), db_r=torch.empty((ndir, d), device=dev),
-                   dc0=torch.empty((B, ndir * d), device=dev) if want_dc0 else None)
-    need = backward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype)
-    if ws is None:
-        ws = workspace(need, dev)
+                   dv_f=None if linear else torch.empty((ndir, d), device=dv),
+                   dv_r=None if linear else torch.empty((ndir, d), device=dv),
+                   db_f=torch.empty((ndir, d), device=dv), db_r=torch.empty((ndir, d), device=dv),
+                   dc0=torch.empty((B, ndir * d), device=dv) if want_dc0 else None)
+    f32 = torch.float32
+    vec = ((ndir, d), f32, False)
+    _req_out(out, dict(dX=(tuple(X.shape), f32, True), dW=(tuple(W.shape), f32, True),
+                       dv_f=vec, dv_r=vec, db_f=((ndir, d), f32, True),
+                       db_r=((ndir, d), f32, True), dc0=((B, ndir * d), f32, False)), dv)
+    ws, nbytes = _ws(ws, backward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype), dv)
     st = lib().sru_backward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                             L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
                             _options(highway_scale, reset_new, linear),
                             _ptr(U), _ptr(C), _ptr(dH), _ptr(dc_last),
                             _ptr(out["dX"]), _ptr(out["dW"]), _ptr(out.get("dv_f")), _ptr(out.get("dv_r")),
                             _ptr(out["db_f"]), _ptr(out["db_r"]), _ptr(out.get("dc0")),
-                            _ptr(X_bf16), _ptr(W_bf16), _ptr(ws), ws.numel(), _stream())
+                            _ptr(X_bf16), _ptr(W_bf16), _ptr(ws), nbytes, _stream())
     _check(st, "sru_backward")
     return out
+
+
+def _check_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0, mask):
+    """Shapes, dtypes and device of a low-rank layer's inputs."""
+    for n, t, nd in (("X", X, 3), ("Q", Q, 2), ("P", P, 4)):
+        if not isinstance(t, torch.Tensor) or t.dim() != nd:
+            raise ValueError(f"{n} must be a {nd}-d tensor")
+    L, B, d_in = X.shape
+    ndir, k, d, dp = P.shape
+    dv = X.device
+    _req(X, "X", (L, B, d_in))
+    _req(Q, "Q", (d_in, dp), device=dv)
+    _req(P, "P", (ndir, k, d, dp), device=dv)
+    for n, t in (("v_f", v_f), ("v_r", v_r)):
+        _req(t, n, (ndir, d), optional=True, device=dv)
+    for n, t in (("b_f", b_f), ("b_r", b_r)):
+        _req(t, n, (ndir, d), device=dv)
+    _req(c0, "c0", (B, ndir * d), optional=True, device=dv)
+    _req(mask, "mask", (L, B), dtype=torch.uint8, optional=True, device=dv)
+    return L, B, d_in, d, dp, ndir, k
 
 
 def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
@@ -261,34 +312,28 @@ def forward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mas
     bf16 GEMMs only: X_bf16 replaces the rounding of X; entries T_bf16 /
     H_bf16 of `out` (bfloat16 tensors), if present, receive T and H rounded
     to bf16."""
-    L, B, d_in = X.shape
-    ndir, k, d, dp = P.shape
-    _req(X, "X", (L, B, d_in))
-    _req(Q, "Q", (d_in, dp))
-    _req(P, "P", (ndir, k, d, dp))
-    for n, t in (("v_f", v_f), ("v_r", v_r)):
-        _req(t, n, (ndir, d), optional=True)
-    for n, t in (("b_f", b_f), ("b_r", b_r)):
-        _req(t, n, (ndir, d))
-    _req(c0, "c0", (B, ndir * d), optional=True)
-    _req(mask, "mask", (L, B), dtype=torch.uint8, optional=True)
-    dev = X.device
+    L, B, d_in, d, dp, ndir, k = _check_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0, mask)
+    dv = X.device
+    _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True, device=dv)
     if out is None:
-        out = dict(T=torch.empty((L, B, dp), device=dev),
-                   U=torch.empty((L, B, ndir, k, d), device=dev),
-                   H=torch.empty((L, B, ndir * d), device=dev),
-                   C=torch.empty((L, B, ndir * d), device=dev) if store_c else None,
-                   c_last=torch.empty((B, ndir * d), device=dev))
+        out = dict(T=torch.empty((L, B, dp), device=dv),
+                   U=torch.empty((L, B, ndir, k, d), device=dv),
+                   H=torch.empty((L, B, ndir * d), device=dv),
+                   C=torch.empty((L, B, ndir * d), device=dv) if store_c else None,
+                   c_last=torch.empty((B, ndir * d), device=dv))
+    f32, b16 = torch.float32, torch.bfloat16
+    _req_out(out, dict(T=((L, B, dp), f32, True), U=((L, B, ndir, k, d), f32, True),
+                       H=((L, B, ndir * d), f32, True), C=((L, B, ndir * d), f32, False),
+                       c_last=((B, ndir * d), f32, False), T_bf16=((L, B, dp), b16, False),
+                       H_bf16=((L, B, ndir * d), b16, False)), dv)
     need = lib().sru_forward_lowrank_workspace_bytes(L, B, d_in, d, dp, direction, gemm_dtype)
-    if need and ws is None:
-        ws = workspace(need, dev)
+    ws, nbytes = _ws(ws, need, dv)
     st = lib().sru_forward_lowrank(_ptr(X), _ptr(Q), _ptr(P), _ptr(v_f), _ptr(v_r), _ptr(b_f),
                                    _ptr(b_r), _ptr(c0), L, B, d_in, d, dp, direction, _ptr(mask),
                                    gemm_dtype, _options(highway_scale, reset_new, linear), _ptr(out["T"]),
                                    _ptr(out["U"]), _ptr(out["H"]), _ptr(out.get("C")),
                                    _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("T_bf16")),
-                                   _ptr(out.get("H_bf16")), _ptr(ws),
-                                   need if ws is not None else 0, _stream())
+                                   _ptr(out.get("H_bf16")), _ptr(ws), nbytes, _stream())
     _check(st, "sru_forward_lowrank")
     return out
 
@@ -300,23 +345,29 @@ def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, T, U, C, dH, c0=None, dc_last=
     """Backward of forward_lowrank; returns dict(dX, dQ, dP, dv_f, dv_r, db_f,
     db_r, dc0).  bf16 GEMMs only: X_bf16 / T_bf16 (the roundings of X and T,
     as forward_lowrank writes them) replace the library's own rounding."""
-    L, B, d_in = X.shape
-    ndir, k, d, dp = P.shape
-    _req(T, "T", (L, B, dp))
-    _req(U, "U", (L, B, ndir, k, d))
-    _req(C, "C", (L, B, ndir * d))
-    _req(dH, "dH", (L, B, ndir * d))
-    _req(dc_last, "dc_last", (B, ndir * d), optional=True)
-    dev = X.device
+    L, B, d_in, d, dp, ndir, k = _check_lowrank(X, Q, P, v_f, v_r, b_f, b_r, c0, mask)
+    dv = X.device
+    _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True, device=dv)
+    _req(T_bf16, "T_bf16", (L, B, dp), dtype=torch.bfloat16, optional=True, device=dv)
+    _req(T, "T", (L, B, dp), device=dv)
+    _req(U, "U", (L, B, ndir, k, d), device=dv)
+    _req(C, "C", (L, B, ndir * d), device=dv)
+    _req(dH, "dH", (L, B, ndir * d), device=dv)
+    _req(dc_last, "dc_last", (B, ndir * d), optional=True, device=dv)
     if out is None:
         out = dict(dX=torch.empty_like(X), dQ=torch.empty_like(Q), dP=torch.empty_like(P),
-                   dv_f=None if linear else torch.empty((ndir, d), device=dev),
-                   dv_r=None if linear else torch.empty((ndir, d), device=dev),
-                   db_f=torch.empty((ndir, d), device=dev), db_r=torch.empty((ndir, d), device=dev),
-                   dc0=torch.empty((B, ndir * d), device=dev) if want_dc0 else None)
+                   dv_f=None if linear else torch.empty((ndir, d), device=dv),
+                   dv_r=None if linear else torch.empty((ndir, d), device=dv),
+                   db_f=torch.empty((ndir, d), device=dv), db_r=torch.empty((ndir, d), device=dv),
+                   dc0=torch.empty((B, ndir * d), device=dv) if want_dc0 else None)
+    f32 = torch.float32
+    vec = ((ndir, d), f32, False)
+    _req_out(out, dict(dX=(tuple(X.shape), f32, True), dQ=(tuple(Q.shape), f32, True),
+                       dP=(tuple(P.shape), f32, True), dv_f=vec, dv_r=vec,
+                       db_f=((ndir, d), f32, True), db_r=((ndir, d), f32, True),
+                       dc0=((B, ndir * d), f32, False)), dv)
     need = lib().sru_backward_lowrank_workspace_bytes(L, B, d_in, d, dp, direction, gemm_dtype)
-    if ws is None:
-        ws = workspace(need, dev)
+    ws, nbytes = _ws(ws, need, dv)
     st = lib().sru_backward_lowrank(_ptr(X), _ptr(Q), _ptr(P), _ptr(v_f), _ptr(v_r), _ptr(b_f),
                                     _ptr(b_r), _ptr(c0), L, B, d_in, d, dp, direction,
                                     _ptr(mask), gemm_dtype, _options(highway_scale, reset_new, linear),
@@ -324,17 +375,19 @@ def backward_lowrank(X, Q, P, v_f, v_r, b_f, b_r, T, U, C, dH, c0=None, dc_last=
                                     _ptr(out["dX"]), _ptr(out["dQ"]), _ptr(out["dP"]),
                                     _ptr(out.get("dv_f")), _ptr(out.get("dv_r")), _ptr(out["db_f"]),
                                     _ptr(out["db_r"]), _ptr(out.get("dc0")), _ptr(X_bf16),
-                                    _ptr(T_bf16), _ptr(ws), ws.numel(), _stream())
+                                    _ptr(T_bf16), _ptr(ws), nbytes, _stream())
     _check(st, "sru_backward_lowrank")
     return out
 
 
 def round_bf16(src, out=None):
     """bf16 (RNE) copy of an fp32 tensor, as the bf16 companions expect."""
+    if not isinstance(src, torch.Tensor):
+        raise ValueError("src must be a torch tensor")
     _req(src, "src", tuple(src.shape))
     if out is None:
         out = torch.empty(tuple(src.shape), dtype=torch.bfloat16, device=src.device)
-    _req(out, "out", tuple(src.shape), dtype=torch.bfloat16)
+    _req(out, "out", tuple(src.shape), dtype=torch.bfloat16, device=src.device)
     _check(lib().sru_round_bf16(_ptr(src), src.numel(), _ptr(out), _stream()), "sru_round_bf16")
     return out
 
@@ -344,39 +397,60 @@ def gemm(op, A, B, M, N, K, gemm_dtype=GEMM_FP32, C=None, ws=None):
     a_shape = (K, M) if op == OP_TN else (M, K)
     b_shape = (N, K) if op == OP_NT else (K, N)
     _req(A, "A", a_shape)
-    _req(B, "B", b_shape)
+    dv = A.device
+    _req(B, "B", b_shape, device=dv)
     if C is None:
-        C = torch.empty((M, N), device=A.device)
-    need = lib().sru_gemm_workspace_bytes(op, M, N, K, gemm_dtype)
-    if need and ws is None:
-        ws = workspace(need, A.device)
+        C = torch.empty((M, N), device=dv)
+    _req(C, "C", (M, N), device=dv)
+    ws, nbytes = _ws(ws, lib().sru_gemm_workspace_bytes(op, M, N, K, gemm_dtype), dv)
     st = lib().sru_gemm(op, gemm_dtype, M, N, K, _ptr(A), a_shape[1], _ptr(B), b_shape[1],
-                        _ptr(C), N, _ptr(ws), need if need else 0, _stream())
+                        _ptr(C), N, _ptr(ws), nbytes, _stream())
     _check(st, "sru_gemm")
     return C
+
+
+def _check_scan_params(U, v_f, v_r, b_f, b_r, c0, mask):
+    if not isinstance(U, torch.Tensor) or U.dim() != 5:
+        raise ValueError("U must be a 5-d tensor [L, B, ndir, k, d]")
+    L, B, ndir, k, d = U.shape
+    _req(U, "U", (L, B, ndir, k, d))
+    dv = U.device
+    for n, t in (("v_f", v_f), ("v_r", v_r)):
+        _req(t, n, (ndir, d), optional=True, device=dv)
+    for n, t in (("b_f", b_f), ("b_r", b_r)):
+        _req(t, n, (ndir, d), device=dv)
+    _req(c0, "c0", (B, ndir * d), optional=True, device=dv)
+    _req(mask, "mask", (L, B), dtype=torch.uint8, optional=True, device=dv)
+    return L, B, ndir, k, d
 
 
 def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
                  store_c=True, out=None, ws=None, highway_scale=1.0, reset_new=False,
                  linear=False):
-    L, B, ndir, k, d = U.shape
-    d_in = X.shape[2] if X is not None else (d if k == 3 else -1)
+    L, B, ndir, k, d = _check_scan_params(U, v_f, v_r, b_f, b_r, c0, mask)
+    dv = U.device
     if k == 4 and X is None:
         raise ValueError("pass X (or its shape via d_in) for k = 4")
-    _req(U, "U", (L, B, ndir, k, d))
-    dev = U.device
+    if X is not None:
+        if not isinstance(X, torch.Tensor) or X.dim() != 3:
+            raise ValueError("X must be a 3-d tensor [L, B, d_in]")
+        _req(X, "X", (L, B, X.shape[2]), device=dv)
+    d_in = X.shape[2] if X is not None else d
     if out is None:
-        out = dict(H=torch.empty((L, B, ndir * d), device=dev),
-                   C=torch.empty((L, B, ndir * d), device=dev) if store_c else None,
-                   c_last=torch.empty((B, ndir * d), device=dev))
+        out = dict(H=torch.empty((L, B, ndir * d), device=dv),
+                   C=torch.empty((L, B, ndir * d), device=dv) if store_c else None,
+                   c_last=torch.empty((B, ndir * d), device=dv))
+    f32 = torch.float32
+    _req_out(out, dict(H=((L, B, ndir * d), f32, True), C=((L, B, ndir * d), f32, False),
+                       c_last=((B, ndir * d), f32, False),
+                       H_bf16=((L, B, ndir * d), torch.bfloat16, False)), dv)
     need = lib().sru_scan_forward_workspace_bytes(L, B, d_in, d, direction)
-    if ws is None:
-        ws = workspace(need, dev)
+    ws, nbytes = _ws(ws, need, dv)
     st = lib().sru_scan_forward(_ptr(U), _ptr(X), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r),
                                 _ptr(c0), L, B, d_in, d, direction, _ptr(mask),
                                 _options(highway_scale, reset_new, linear),
                                 _ptr(out["H"]), _ptr(out.get("C")), _ptr(out.get("c_last")),
-                                _ptr(out.get("H_bf16")), _ptr(ws), need, _stream())
+                                _ptr(out.get("H_bf16")), _ptr(ws), nbytes, _stream())
     _check(st, "sru_scan_forward")
     return out
 
@@ -384,27 +458,38 @@ def scan_forward(U, X, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None
 def scan_backward(U, X, C, dH, v_f, v_r, b_f, b_r, c0=None, dc_last=None, direction=DIR_FWD,
                   mask=None, d_in=None, out=None, ws=None, highway_scale=1.0, reset_new=False,
                   linear=False):
-    L, B, ndir, k, d = U.shape
+    L, B, ndir, k, d = _check_scan_params(U, v_f, v_r, b_f, b_r, c0, mask)
+    dv = U.device
+    if X is not None:
+        if not isinstance(X, torch.Tensor) or X.dim() != 3:
+            raise ValueError("X must be a 3-d tensor [L, B, d_in]")
+        _req(X, "X", (L, B, X.shape[2]), device=dv)
     if d_in is None:
         d_in = X.shape[2] if X is not None else d
-    dev = U.device
+    _req(C, "C", (L, B, ndir * d), device=dv)
+    _req(dH, "dH", (L, B, ndir * d), device=dv)
+    _req(dc_last, "dc_last", (B, ndir * d), optional=True, device=dv)
     if out is None:
         out = dict(dU=torch.empty_like(U),
-                   dxh=torch.empty((L, B, ndir, d), device=dev) if k == 3 else None,
-                   dv_f=None if linear else torch.empty((ndir, d), device=dev),
-                   dv_r=None if linear else torch.empty((ndir, d), device=dev),
-                   db_f=torch.empty((ndir, d), device=dev), db_r=torch.empty((ndir, d), device=dev),
-                   dc0=torch.empty((B, ndir * d), device=dev))
+                   dxh=torch.empty((L, B, ndir, d), device=dv) if k == 3 else None,
+                   dv_f=None if linear else torch.empty((ndir, d), device=dv),
+                   dv_r=None if linear else torch.empty((ndir, d), device=dv),
+                   db_f=torch.empty((ndir, d), device=dv), db_r=torch.empty((ndir, d), device=dv),
+                   dc0=torch.empty((B, ndir * d), device=dv))
+    f32 = torch.float32
+    vec = ((ndir, d), f32, False)
+    _req_out(out, dict(dU=((L, B, ndir, k, d), f32, True), dxh=((L, B, ndir, d), f32, False),
+                       dv_f=vec, dv_r=vec, db_f=((ndir, d), f32, True),
+                       db_r=((ndir, d), f32, True), dc0=((B, ndir * d), f32, False)), dv)
     need = lib().sru_scan_backward_workspace_bytes(L, B, d_in, d, direction)
-    if ws is None:
-        ws = workspace(need, dev)
+    ws, nbytes = _ws(ws, need, dv)
     st = lib().sru_scan_backward(_ptr(U), _ptr(X), _ptr(C), _ptr(dH), _ptr(dc_last),
                                  _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
                                  L, B, d_in, d, direction, _ptr(mask),
                                  _options(highway_scale, reset_new, linear),
                                  _ptr(out["dU"]), _ptr(out.get("dxh")), _ptr(out.get("dv_f")),
                                  _ptr(out.get("dv_r")), _ptr(out["db_f"]), _ptr(out["db_r"]),
-                                 _ptr(out.get("dc0")), _ptr(ws), ws.numel(), _stream())
+                                 _ptr(out.get("dc0")), _ptr(ws), nbytes, _stream())
     _check(st, "sru_scan_backward")
     return out
 

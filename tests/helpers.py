@@ -9,10 +9,12 @@ from conftest import rel_err
 # bf16-GEMM path, measured as max |g - r| / max(|r|, rms(r)) per tensor.
 TOL_FP32 = 1e-5
 TOL_BF16 = 2e-2
-# The low-rank projection (Wcat = P Q^T) computes each projection as two
-# chained products, so every gradient passes twice as many bf16-rounded
-# operands as on the dense path; independent roundings add in quadrature,
-# which scales the dense bar by sqrt(2) (2.8e-2), rounded up.
+# The low-rank projection (Wcat = P Q^T) computes each projection and each
+# gradient as two chained products, so bf16 rounding flips caused by the
+# order of fp32 accumulation carry further.  The bar is the dense 2e-2
+# scaled by how far the oracle itself moves when its products accumulate in
+# fp32, low-rank stack over dense stack (1.90e-2 / 1.07e-2), rounded down;
+# tests/test_tolerance_bound.py measures both.
 TOL_BF16_LOWRANK = 3e-2
 
 

@@ -181,7 +181,6 @@ def test_valid_options_pass_validation():
     ok = ctypes.byref(sru.Options(3.0 ** 0.5, sru.RESET_NEW))
     assert _fwd(lib, opts=ok, H=FAKE_MIS) == E_ALIGN
     assert _bwd(lib, opts=ok) == E_WS
-    assert abs(sru.highway_scale_for_bias(0.0) - 3.0 ** 0.5) < 1e-15
 
 
 @pytest.mark.parametrize("recurrence", [2, -1])

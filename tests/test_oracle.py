@@ -325,18 +325,18 @@ def test_masked_equals_truncated_sequences(rng):
 @pytest.mark.parametrize("direction", [F, R, BI])
 @pytest.mark.parametrize("k4", [False, True])
 def test_batched_reorganisation_equals_per_step(direction, k4):
-    """Sec. 3.1: batching the projections over all steps and then running the
-    scalar element-wise loop (Algorithm 1, reset gate on c_{t-1}) gives the
-    same result as Eq. 1-4 step by step."""
+    """Sec. 3.1: one product for the projections of all steps, then the
+    element-wise recurrence reading its gate inputs from that batched tensor,
+    gives the same result as Eq. 1-4 step by step."""
     rng = np.random.default_rng(3)
     d = 3
     c = _case(rng, 6, 2, 2 * d if k4 else d, d, direction, c0=True, masked=True,
               bias_scale=0.5)
     a = _fw(c, direction)
-    b = O.forward_alg1_scalar(c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"],
-                              c["c0"], direction, c["mask"])
-    np.testing.assert_allclose(a["H"], b["H"], rtol=1e-13, atol=1e-14)
-    np.testing.assert_allclose(a["C"], b["C"], rtol=1e-13, atol=1e-14)
+    b = O.forward_batched(c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"],
+                          c["c0"], direction, c["mask"])
+    for key in ("U", "H", "C", "c_last"):
+        np.testing.assert_allclose(a[key], b[key], rtol=1e-13, atol=1e-14)
 
 
 # ---------------------------------------------------------------- pin 9
@@ -617,13 +617,13 @@ def test_scaling_correction_variance_appendix(b):
 
 
 @pytest.mark.parametrize("alpha,reset_new", VARIANTS)
-def test_alg1_scalar_loop_matches_variants(rng, alpha, reset_new):
-    """The per-(i, j) scalar loop in Algorithm 1's shape agrees with the
-    vectorised per-step forward for both variants."""
+def test_batched_organisation_matches_variants(rng, alpha, reset_new):
+    """The batched organisation (one product, then the recurrence) agrees with
+    the per-step forward for both variants."""
     c = _case(rng, 6, 2, 5, 3, BI, c0=True, masked=True, bias_scale=0.5, v_scale=1.5)
     args = (c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"], c["c0"], BI, c["mask"])
     a = O.forward(*args, alpha=alpha, reset_new=reset_new)
-    b = O.forward_alg1_scalar(*args, alpha=alpha, reset_new=reset_new)
+    b = O.forward_batched(*args, alpha=alpha, reset_new=reset_new)
     for k in ("H", "C"):
         np.testing.assert_allclose(a[k], b[k], rtol=1e-12, atol=1e-13)
 
@@ -946,3 +946,124 @@ def test_irregular_mask_equals_compacted_sequences(rng, direction, k4, variant):
             sums[k] = sums[k] + ob[k]
     for k, s in sums.items():
         np.testing.assert_allclose(bw[k], s, **tol)
+
+
+# ---------------------------------------------------------------- stacked layers
+# stack_forward_backward feeds layer l's H to layer l+1 and chains each
+# layer's dX down as the next dH.  Central differences of the top layer's
+# loss sum(H_top * dH) against every parameter of every layer (and the
+# stack's input) pin the chaining: a layer run on the wrong input, the wrong
+# layer's dX passed down, or a low-rank layer handled as a dense one fails.
+
+def _stack_layer(rng, ndir, d, d_in, low_rank_dp=None):
+    k = 3 if d_in == d else 4
+    p = dict(v_f=rng.uniform(-0.8, 0.8, (ndir, d)), v_r=rng.uniform(-0.8, 0.8, (ndir, d)),
+             b_f=rng.uniform(-0.6, 0.6, (ndir, d)), b_r=rng.uniform(-0.6, 0.6, (ndir, d)))
+    if low_rank_dp is None:
+        p["W"] = rng.uniform(-0.9, 0.9, (ndir, k, d, d_in))
+    else:
+        p["Q"] = rng.uniform(-0.9, 0.9, (d_in, low_rank_dp))
+        p["P"] = rng.uniform(-0.9, 0.9, (ndir, k, d, low_rank_dp))
+    return p
+
+
+def _check_stack_gradients(X, layers, direction, mask, dH, linear=False):
+    def loss(Xv, ls):
+        out = O.stack_forward_backward(Xv, ls, direction, mask, O.GEMM_FP32, dH,
+                                       need_backward=False, linear=linear)
+        return float(np.sum(out["Hs"][-1] * dH))
+
+    ref = O.stack_forward_backward(X, layers, direction, mask, O.GEMM_FP32, dH, linear=linear)
+    grads = ref["grads"]
+    assert len(grads) == len(layers)
+    h = 1e-6
+
+    def fd(get, put, shape):
+        num = np.zeros(int(np.prod(shape)))
+        for i in range(num.size):
+            for sgn in (1.0, -1.0):
+                Xv, ls = get()
+                put(Xv, ls, i, sgn * h)
+                num[i] += sgn * loss(Xv, ls) / (2 * h)
+        return num.reshape(shape)
+
+    def compare(ana, num, what):
+        scale = max(np.max(np.abs(num)), 1e-3)
+        err = np.max(np.abs(np.asarray(ana) - num)) / scale
+        assert err <= 1e-6, (what, err)
+
+    def fresh():
+        return X.copy(), [{k: v.copy() for k, v in p.items()} for p in layers]
+
+    def put_x(Xv, ls, i, dh):
+        Xv.reshape(-1)[i] += dh
+
+    compare(grads[0]["dX"], fd(fresh, put_x, X.shape), "dX of layer 1")
+    names = dict(W="dW", Q="dQ", P="dP", v_f="dv_f", v_r="dv_r", b_f="db_f", b_r="db_r")
+    for li, p in enumerate(layers):
+        for pname, gname in names.items():
+            if pname not in p or (linear and pname in ("v_f", "v_r")):
+                continue
+
+            def put_p(Xv, ls, i, dh, li=li, pname=pname):
+                ls[li][pname].reshape(-1)[i] += dh
+            compare(grads[li][gname], fd(fresh, put_p, p[pname].shape), f"{gname} of layer {li + 1}")
+        if linear:
+            assert grads[li]["dv_f"] is None and grads[li]["dv_r"] is None
+
+
+def test_stack_gradients_bidirectional_masked():
+    """Three bidirectional layers (k = 3, then k = 4 on the 2d-wide input of
+    the layers above), padded sequences, nonzero biases: every layer's dW,
+    dv, db and the stack's dX against central differences."""
+    rng = np.random.default_rng(21)
+    L, B, d = 4, 2, 2
+    layers = [_stack_layer(rng, 2, d, d), _stack_layer(rng, 2, d, 2 * d),
+              _stack_layer(rng, 2, d, 2 * d)]
+    X = rng.standard_normal((L, B, d))
+    mask = lengths_to_mask(np.array([L, 2]), L)
+    dH = rng.standard_normal((L, B, 2 * d))
+    _check_stack_gradients(X, layers, BI, mask, dH)
+
+
+def test_stack_gradients_low_rank_and_dense_layers():
+    """A stack mixing low-rank layers (Wcat = P Q^T, Sec. 4.4) and a dense
+    one: dQ, dP, dW, dv, db of every layer and the stack's dX."""
+    rng = np.random.default_rng(22)
+    L, B, d = 4, 2, 3
+    layers = [_stack_layer(rng, 1, d, d, low_rank_dp=2), _stack_layer(rng, 1, d, d),
+              _stack_layer(rng, 1, d, d, low_rank_dp=2)]
+    X = rng.standard_normal((L, B, d))
+    mask = lengths_to_mask(np.array([L, 3]), L)
+    dH = rng.standard_normal((L, B, d))
+    _check_stack_gradients(X, layers, R, mask, dH)
+
+
+def test_stack_gradients_linear_recurrence():
+    """A bidirectional stack of the linear recurrence (ablation (1), Sec. 4.5):
+    v is not a parameter (no gradient), the rest as above."""
+    rng = np.random.default_rng(23)
+    L, B, d = 4, 2, 2
+    layers = [_stack_layer(rng, 2, d, d), _stack_layer(rng, 2, d, 2 * d)]
+    X = rng.standard_normal((L, B, d))
+    mask = lengths_to_mask(np.array([3, L]), L)
+    dH = rng.standard_normal((L, B, 2 * d))
+    _check_stack_gradients(X, layers, BI, mask, dH, linear=True)
+
+
+def test_stack_forward_chains_layer_outputs():
+    """Layer l+1 of the stack is the single layer run on layer l's H (so a
+    stack cannot silently run every layer on the stack's input)."""
+    rng = np.random.default_rng(24)
+    L, B, d = 5, 3, 3
+    layers = [_stack_layer(rng, 1, d, d) for _ in range(3)]
+    X = rng.standard_normal((L, B, d))
+    out = O.stack_forward_backward(X, layers, F, None, O.GEMM_FP32, None, need_backward=False)
+    x = X
+    for li, p in enumerate(layers):
+        h = O.forward(x, p["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"])["H"]
+        np.testing.assert_array_equal(out["Hs"][li], h)
+        x = h
+    assert not np.allclose(out["Hs"][2], O.forward(X, layers[2]["W"], layers[2]["v_f"],
+                                                   layers[2]["v_r"], layers[2]["b_f"],
+                                                   layers[2]["b_r"])["H"])
