@@ -270,12 +270,14 @@ def cpu_baseline(w, inp, nseq):
     first `nseq` sequences of the same inputs: the full stack, forward and
     (when the workload has one) backward."""
     from oracle import sru_oracle as O
+    affinity = len(os.sched_getaffinity(0))
     try:
         from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 1) for i in threadpool_info()
-                       if i.get("user_api") == "blas"), default=1)
-    except Exception:  # threadpoolctl missing: report the affinity set
-        threads = len(os.sched_getaffinity(0))
+        blas = max((i.get("num_threads", 1) for i in threadpool_info()
+                    if i.get("user_api") == "blas"), default=1)
+    except Exception:  # threadpoolctl missing: the BLAS pool is not known
+        blas = None
+    threads = blas if blas is not None else affinity
     nseq = min(nseq, w.B)
     sl = slice(0, nseq)
     X = inp["X"][:, sl]
@@ -293,7 +295,7 @@ def cpu_baseline(w, inp, nseq):
     tokens = w.L * nseq * reps
     passes = "fwd+bwd" if w.backward else "fwd"
     return {"value": tokens / secs, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "seconds": secs,
+            "blas_threads": blas, "affinity_cores": affinity, "seconds": secs,
             "sample": f"{w.layers}-layer {passes} stack on {nseq} of {w.B} sequences, "
                       f"{reps} run(s) ({tokens} tokens), fp64 NumPy, per-step projections"}
 
@@ -451,14 +453,21 @@ def main():
     torch.cuda.synchronize()
     log(f"warmup {args.warmup} done")
 
+    # the library launches on torch's current stream, so torch's events
+    # bracket each step; the wall clock brackets all of them
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    marks[0].record()
+    for i in range(args.steps):
         step()
+        marks[i + 1].record()
     torch.cuda.synchronize()
     secs = time.perf_counter() - t0
+    step_ms = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
     ms_per_step = 1e3 * secs / args.steps
     tokens_per_s = w.tokens * args.steps / secs
-    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {tokens_per_s:.4g} tokens/s")
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {tokens_per_s:.4g} tokens/s "
+        f"(median {step_ms[len(step_ms) // 2]:.3f}, min {step_ms[0]:.3f} ms)")
 
     # --- per-kernel durations: the library brackets each launch with events
     per_step = w.layers * 32  # upper bound on kernels per layer and step
@@ -538,6 +547,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "ms_per_step_median": step_ms[len(step_ms) // 2],
+        "ms_per_step_min": step_ms[0],
+        "tokens_per_s_median": w.tokens / (step_ms[len(step_ms) // 2] * 1e-3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

@@ -69,9 +69,9 @@ class Workload:
 # direction, L, B, d, product precision, padding), then the inference shape
 # of the SRU that replaces a Transformer's feed-forward layer (Sec. 4.3:
 # d_model = 512 in, d_sru = 2048, batches of about 5120 tokens; forward only,
-# no C), the 6-layer stack with the projection trick, and workload 2 with
-# the linear recurrence; seeds are
-# the workload index.  The linear workload still draws v_f, v_r (same draw
+# no C), the 6-layer stack with the projection trick, workload 2 with
+# the linear recurrence, and one GPU's shard of the headline stack; seeds
+# are the workload index.  The linear workload still draws v_f, v_r (same draw
 # order as the others); nothing reads them.
 WORKLOADS = [
     Workload("sru1_L32_B4_d128_fp32_fwd", 1, DIR_FWD, 32, 4, 128, 128,
@@ -93,6 +93,11 @@ WORKLOADS = [
     # recurrence is linear in c, so its scans also run parallel over time
     Workload("bisru3_L400_B32_d128_fp32_masked_linear", 3, DIR_BI, 400, 32, 128, 128,
              GEMM_FP32, True, 200, False, 7, linear=True),
+    # one GPU's share of the headline stack under 8-way data parallelism:
+    # the batch of 64 sequences cut into 8 shards of 8 (sequences never
+    # interact, so each GPU runs the whole stack on its shard)
+    Workload("sru6_L256_B8_d1024_bf16_dp8_shard", 6, DIR_FWD, 256, 8, 1024, 1024,
+             GEMM_BF16, True, None, True, 8),
 ]
 
 
