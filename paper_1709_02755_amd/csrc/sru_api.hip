@@ -191,8 +191,9 @@ struct BwdLayout {
 };
 
 // dX = dU Wcat (+ highway): NN on Wcat in fp32 mode; in bf16 mode NT on the
-// bf16 Wcat^T.  The fp32 product's tiles can be too few to fill the CUs
-// (d_in of a few hundred), so it may be split over K.
+// bf16 Wcat^T.  Its tiles can be too few to fill the CUs (d_in of a few
+// hundred, or few tokens: one GPU's share of a batch), so it may be split
+// over K; the launcher's plan decides.
 sru::GemmDesc dx_desc(const Dims& s, bool bf16, const void* dU, const void* W, const void* wt,
                       float* dX) {
   sru::GemmDesc g = bf16 ? gemm_desc(SRU_OP_NT, true, (int)s.M, s.d_in, (int)s.N, dU, s.N, wt,
@@ -200,7 +201,7 @@ sru::GemmDesc dx_desc(const Dims& s, bool bf16, const void* dU, const void* W, c
                          : gemm_desc(SRU_OP_NN, false, (int)s.M, s.d_in, (int)s.N, dU, s.N, W,
                                      s.d_in, dX, s.d_in);
   g.a_bf16 = g.b_bf16 = bf16;
-  g.kc_split = !bf16;
+  g.kc_split = true;
   g.label = "gemm_dx";
   return g;
 }

@@ -1439,7 +1439,10 @@ bool direct_ok(const GemmDesc& g) {
 }
 
 // Split count for the direct path: the K = tokens product (row-contiguous
-// operands) is cut over K so that the CUs share the work evenly.  The count
+// operands) is cut over K so that the CUs share the work evenly, and so is a
+// K-contiguous product whose caller asks for it (kc_split: dX of a small
+// batch, whose few tiles would leave most CUs idle).  A bf16 result (Cb) is
+// never split.  The count
 // minimises a cost in K steps: the rounds of workgroups over the CUs times
 // the K steps of a split, plus the split partials' HBM traffic ((s + 1)
 // fp32 outputs written and read) at kSplitBytesPerStep, the bytes HBM moves
@@ -1450,7 +1453,7 @@ bool direct_ok(const GemmDesc& g) {
 constexpr double kSplitBytesPerStep = 11.0 * (1 << 20);
 template <class C>
 int direct_splits_cfg(const GemmDesc& g) {
-  if (g.a_kc) return 1;
+  if (g.Cb || (g.a_kc && !g.kc_split)) return 1;
   const long long tiles = (long long)((g.M + C::BM - 1) / C::BM) * ((g.N + C::BN - 1) / C::BN);
   const int kt = (g.K + C::BK - 1) / C::BK;
   const long long slots = C::OCC * 256LL;  // workgroups the CUs run at once
@@ -1481,13 +1484,18 @@ using CfgDirectKC = DirectLineA3;
 // 256 x 128 tiles: twice the workgroups.
 using CfgNarrow = DirectNarrow;
 
-int direct_splits(const GemmDesc& g) { return direct_splits_cfg<CfgDirect>(g); }
-
 bool use_narrow(const GemmDesc& g) {
   if (!g.a_kc || !g.b_kc || g.add_count != 0) return false;
   const long long tiles = (long long)((g.M + CfgDirect::BM - 1) / CfgDirect::BM) *
                           ((g.N + CfgDirect::BN - 1) / CfgDirect::BN);
   return tiles < 256;
+}
+
+// The split count of the configuration gemm_launch runs g on.
+int direct_splits(const GemmDesc& g) {
+  if (!g.a_kc || !g.b_kc) return direct_splits_cfg<CfgDirect>(g);
+  if (use_narrow(g)) return direct_splits_cfg<CfgNarrow>(g);
+  return direct_splits_cfg<CfgDirectKC>(g);
 }
 
 // Explicit instantiations: the host pass did not emit the launch stubs of

@@ -9,13 +9,14 @@ from conftest import rel_err
 # bf16-GEMM path, measured as max |g - r| / max(|r|, rms(r)) per tensor.
 TOL_FP32 = 1e-5
 TOL_BF16 = 2e-2
-# The low-rank projection (Wcat = P Q^T) computes each projection and each
+# A stack of low-rank layers (Wcat = P Q^T) computes each projection and each
 # gradient as two chained products, so bf16 rounding flips caused by the
-# order of fp32 accumulation carry further.  The bar is the dense 2e-2
-# scaled by how far the oracle itself moves when its products accumulate in
-# fp32, low-rank stack over dense stack (1.90e-2 / 1.07e-2), rounded down;
-# tests/test_tolerance_bound.py measures both.
-TOL_BF16_LOWRANK = 3e-2
+# order of fp32 accumulation carry further through the stack.  Its bar is the
+# dense 2e-2 scaled by how far the oracle itself moves when its products
+# accumulate in fp32, low-rank stack over dense stack (1.90e-2 / 1.07e-2),
+# rounded down; tests/test_tolerance_bound.py measures both.  A single
+# low-rank layer is held to the dense bar.
+TOL_BF16_LOWRANK_STACK = 3e-2
 
 
 def dev(a, dtype=None):

@@ -29,6 +29,8 @@ LAYER_CASES = [
     # bidirectional, k = 3: dX adds both directions' highway gradients; whole
     # 256 x 256 tiles (epilogue through LDS) and a ragged row of tiles
     (40, 13, 256, 256, O.DIR_BI, True, O.GEMM_BF16),
+    # one GPU's share of the headline batch (B = 8): 32 tiles of dX, split over K
+    (256, 8, 1024, 1024, O.DIR_FWD, False, O.GEMM_BF16),
 ]
 
 

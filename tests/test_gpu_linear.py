@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 import torch
 
-from helpers import TOL_BF16, TOL_BF16_LOWRANK, TOL_FP32, check, dev
+from helpers import TOL_BF16, TOL_FP32, check, dev
 from oracle import sru_oracle as O
 from paper_1709_02755_amd import sru
 from paper_1709_02755_amd.workloads import random_layer_case
@@ -190,6 +190,6 @@ def test_linear_lowrank_layer():
     rb = O.backward_lowrank(*args, c["dH"], c["c0"], direction, c["mask"], gemm, c["dc_last"],
                             fw=rf, linear=True)
     for k in ("H", "C", "c_last"):
-        check(k, fw[k], rf[k], TOL_BF16_LOWRANK)
+        check(k, fw[k], rf[k], TOL_BF16)
     for k in ("dX", "dQ", "dP", "db_f", "db_r", "dc0"):
-        check(k, bw[k], rb[k], TOL_BF16_LOWRANK)
+        check(k, bw[k], rb[k], TOL_BF16)
