@@ -167,6 +167,32 @@ SRU_API int sru_forward(const float* X, const float* W,
                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * sru_forward without a caller workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, hosts
+ * that forbid allocation): the same arguments, results and errors as
+ * sru_forward, minus workspace and workspace_bytes.  Its workspace lives in
+ * a static device array of SRU_NOALLOC_SCRATCH_BYTES (128 MiB) that each GPU
+ * the library runs on holds until the process ends; the call itself
+ * allocates and frees nothing.  Shapes whose forward workspace
+ * (sru_forward_workspace_bytes) exceeds that size return SRU_E_WORKSPACE
+ * before anything is enqueued.  It runs on the current device, which
+ * `stream` must belong to; the first call on a device looks up the array's
+ * address there (a HIP failure then returns SRU_E_HIP).  Every call on one
+ * device shares that device's array: calls whose execution overlaps on one
+ * GPU (other streams, other threads) race on it and must be serialised by
+ * the caller.  The array keeps the last call's contents; nothing in it needs
+ * to start at zero.
+ */
+#define SRU_NOALLOC_SCRATCH_BYTES (128u << 20)
+SRU_API int sru_forward_noalloc(const float* X, const float* W,
+                const float* v_f, const float* v_r, const float* b_f, const float* b_r,
+                const float* c0, int L, int B, int d_in, int d, int direction,
+                const uint8_t* pad_mask, int gemm_dtype, const sru_options* options,
+                float* U, float* H, float* C, float* c_last,
+                const uint16_t* X_bf16, uint16_t* W_bf16, uint16_t* H_bf16,
+                hipStream_t stream);
+
+/*
  * Backward pass of one layer: the chain rule of Eq. 1-4 taken in reverse
  * step order (the paper trains by back-propagation but does not state it).
  *   in : the forward inputs, U and C from sru_forward on those inputs,

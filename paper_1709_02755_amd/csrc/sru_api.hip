@@ -7,6 +7,7 @@
 
 #include <algorithm>
 #include <initializer_list>
+#include <mutex>
 #include <vector>
 
 #include "../../include/sru.h"
@@ -308,6 +309,34 @@ LrBwdLayout lr_bwd_layout(const Dims& s, int dp, int gemm_dtype) {
   return w;
 }
 
+// Scratch of sru_forward_noalloc: the forward's workspace (bf16 operand
+// copies, the linear recurrence's segment maps) in a file-scope device array,
+// so that call allocates nothing.  Host code never passes the array's name to
+// a kernel or a copy (on the host it is only a stand-in symbol): it uses the
+// device address hipGetSymbolAddress returns, looked up once per device with
+// that device current, on the device's first call.
+__device__ __align__(256) unsigned char scratch[SRU_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 256;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device.
+int scratch_on_current_device(void** out) {
+  int dev = -1;
+  if (int e = hip_status(hipGetDevice(&dev))) return e;
+  if (dev < 0 || dev >= kMaxDevices) return SRU_E_SHAPE;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (int e = hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)))) return e;
+    if (!p) return SRU_E_NULLPTR;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SRU_OK;
+}
+
 }  // namespace
 
 namespace sru {
@@ -366,7 +395,7 @@ const char* sru_status_string(int status) {
 
 int sru_last_hip_error(void) { return g_last_hip_error; }
 
-int sru_version(void) { return (1 << 16) | 2; }
+int sru_version(void) { return (1 << 16) | 3; }
 
 size_t sru_forward_workspace_bytes(int L, int B, int d_in, int d, int direction, int gemm_dtype) {
   Dims s;
@@ -472,6 +501,25 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
   sru::ScanFwdArgs a{U, X, v_f, v_r, b_f, b_r, c0, pad_mask, H, C, c_last, H_bf16,
                      static_cast<unsigned char*>(workspace) + bf16_bytes};
   return hip_status(sru::scan_forward_launch(scan_shape(s, direction, op), a, stream));
+}
+
+int sru_forward_noalloc(const float* X, const float* W, const float* v_f, const float* v_r,
+                        const float* b_f, const float* b_r, const float* c0, int L, int B,
+                        int d_in, int d, int direction, const uint8_t* pad_mask, int gemm_dtype,
+                        const sru_options* options, float* U, float* H, float* C,
+                        float* c_last, const uint16_t* X_bf16, uint16_t* W_bf16,
+                        uint16_t* H_bf16, hipStream_t stream) {
+  Dims s;
+  int st = make_dims(L, B, d_in, d, direction, s);
+  if (st != SRU_OK) return st;
+  if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
+  // the whole forward workspace must fit the array (checked before any HIP call)
+  if (fwd_workspace(s, gemm_dtype) > (size_t)SRU_NOALLOC_SCRATCH_BYTES) return SRU_E_WORKSPACE;
+  void* ws = nullptr;
+  if (int e = scratch_on_current_device(&ws)) return e;
+  return sru_forward(X, W, v_f, v_r, b_f, b_r, c0, L, B, d_in, d, direction, pad_mask,
+                     gemm_dtype, options, U, H, C, c_last, X_bf16, W_bf16, H_bf16, ws,
+                     (size_t)SRU_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int sru_backward(const float* X, const float* W, const float* v_f, const float* v_r,

@@ -38,6 +38,8 @@ _SIGNATURES = {
     "sru_backward_workspace_bytes": (_S, [_I] * 6),
     "sru_forward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I, _P] + [_P] * 4 + [_P] * 3
                     + [_P, _S, _P]),
+    "sru_forward_noalloc": (_I, [_P] * 7 + [_I] * 5 + [_P, _I, _P] + [_P] * 4 + [_P] * 3
+                            + [_P]),
     "sru_backward": (_I, [_P] * 7 + [_I] * 5 + [_P, _I, _P] + [_P] * 4 + [_P] * 7 + [_P] * 2
                      + [_P, _S, _P]),
     "sru_gemm_workspace_bytes": (_S, [_I] * 5),
@@ -242,6 +244,36 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
                            _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("W_bf16")),
                            _ptr(out.get("H_bf16")), _ptr(ws), nbytes, _stream())
     _check(st, "sru_forward")
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 128 << 20
+
+
+def forward_noalloc(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
+                    gemm_dtype=GEMM_FP32, out=None, X_bf16=None, highway_scale=1.0,
+                    reset_new=False, linear=False):
+    """forward() through sru_forward_noalloc: the library takes its workspace
+    from a static device array instead of a caller buffer.  `out` (as for
+    forward(); U may be None where fused_available() says so and C is None)
+    is required too, so the call allocates nothing."""
+    L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask)
+    dv = X.device
+    _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True, device=dv)
+    if out is None:
+        raise ValueError("forward_noalloc needs caller-owned outputs (out)")
+    f32, b16 = torch.float32, torch.bfloat16
+    _req_out(out, dict(U=((L, B, ndir, k, d), f32, False), H=((L, B, ndir * d), f32, True),
+                       C=((L, B, ndir * d), f32, False), c_last=((B, ndir * d), f32, False),
+                       W_bf16=(tuple(W.shape), b16, False),
+                       H_bf16=((L, B, ndir * d), b16, False)), dv)
+    st = lib().sru_forward_noalloc(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r),
+                                   _ptr(c0), L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
+                                   _options(highway_scale, reset_new, linear),
+                                   _ptr(out.get("U")), _ptr(out["H"]), _ptr(out.get("C")),
+                                   _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("W_bf16")),
+                                   _ptr(out.get("H_bf16")), _stream())
+    _check(st, "sru_forward_noalloc")
     return out
 
 

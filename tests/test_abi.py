@@ -289,3 +289,33 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     (tmp_path / "libsru.so").write_bytes(b"not a shared object")
     with pytest.raises(OSError):
         sru.lib()
+
+
+def _fwd_noalloc(lib, **kw):
+    a = dict(X=FAKE, W=FAKE, v_f=FAKE, v_r=FAKE, b_f=FAKE, b_r=FAKE, c0=None, L=4, B=2, d_in=8,
+             d=8, direction=0, mask=None, gemm=0, opts=None, U=FAKE, H=FAKE, C=FAKE,
+             c_last=None, Xb=None, Wb=None, Hb=None)
+    a.update(kw)
+    return lib.sru_forward_noalloc(a["X"], a["W"], a["v_f"], a["v_r"], a["b_f"], a["b_r"],
+                                   a["c0"], a["L"], a["B"], a["d_in"], a["d"], a["direction"],
+                                   a["mask"], a["gemm"], a["opts"], a["U"], a["H"], a["C"],
+                                   a["c_last"], a["Xb"], a["Wb"], a["Hb"], None)
+
+
+def test_noalloc_forward_refuses_what_its_scratch_cannot_hold():
+    """The allocation-free forward takes its workspace from a fixed array of
+    SRU_NOALLOC_SCRATCH_BYTES; a shape whose forward workspace is larger is
+    refused before any HIP call (so this runs without a GPU), and so are
+    invalid sizes and flags."""
+    lib = sru.lib()
+    text = open(HEADER).read()
+    assert "#define SRU_NOALLOC_SCRATCH_BYTES (128u << 20)" in text
+    assert sru.NOALLOC_SCRATCH_BYTES == 128 << 20
+    # bf16: the forward workspace holds X and Wcat in bf16
+    L, B, d = 1024, 128, 1024
+    need = lib.sru_forward_workspace_bytes(L, B, d, d, 0, 1)
+    assert need > sru.NOALLOC_SCRATCH_BYTES
+    assert _fwd_noalloc(lib, L=L, B=B, d_in=d, d=d, gemm=1) == E_WS
+    assert _fwd_noalloc(lib, L=0) == E_SHAPE
+    assert _fwd_noalloc(lib, direction=7) == E_FLAG
+    assert _fwd_noalloc(lib, gemm=9) == E_FLAG
