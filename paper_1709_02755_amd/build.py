@@ -64,6 +64,48 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# Host-side AddressSanitizer + UndefinedBehaviorSanitizer build of the C ABI
+# layer (argument checks, workspace planning, dispatch), linked with the
+# normal kernel objects: a CPU test runs the ABI checks against it.  The
+# sanitizers apply to host code only; the device code is unchanged.
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-fno-sanitize-recover=all"]
+SAN_LIB = os.path.join(OBJDIR, "libsru_sanitized.so")
+
+
+def sanitizer_runtime() -> str:
+    """The clang ASan runtime the sanitized library needs preloaded."""
+    llvm = os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "llvm")
+    hits = sorted(glob.glob(os.path.join(llvm, "lib", "clang", "*", "lib", "linux",
+                                         "libclang_rt.asan-x86_64.so")))
+    if not hits:
+        raise RuntimeError("clang ASan runtime not found")
+    return os.path.realpath(hits[-1])
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    if not all(os.path.exists(os.path.join(OBJDIR, os.path.basename(p) + ".o"))
+               for p in glob.glob(os.path.join(CSRC, "*.hip"))):
+        build()
+    api = os.path.join(CSRC, "sru_api.hip")
+    obj = os.path.join(OBJDIR, "sru_api.sanitized.o")
+    flags = [f if f != "-O3" else "-O1" for f in HIP_FLAGS] + ["-g"]
+    cmd = [hipcc(), "-x", "hip", "-c", api, "-o", obj] + flags + SAN_FLAGS
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized compile failed:\n{r.stdout}\n{r.stderr}")
+    others = [os.path.join(OBJDIR, os.path.basename(p) + ".o")
+              for p in sorted(glob.glob(os.path.join(CSRC, "*.hip"))) if p != api]
+    cmd = ([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-shared-libsan", "-o",
+            SAN_LIB, obj] + others + SAN_FLAGS)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized link failed:\n{r.stdout}\n{r.stderr}")
+    if verbose:
+        print(f"built {SAN_LIB}")
+    return SAN_LIB
+
+
 if __name__ == "__main__":
     build(verbose=True)
     sys.exit(0)

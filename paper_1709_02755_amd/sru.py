@@ -15,7 +15,9 @@ import threading
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libsru.so")
+# SRU_LIBRARY names another build of the same library (e.g. the host-side
+# sanitizer build the ABI tests run against); it must exist
+LIB_PATH = os.environ.get("SRU_LIBRARY") or os.path.join(_PKG, "libsru.so")
 
 SRU_OK = 0
 DIR_FWD, DIR_REV, DIR_BI = 0, 1, 2
@@ -93,6 +95,8 @@ def lib():
     with _lock:
         if _lib is None:
             if not os.path.exists(LIB_PATH):
+                if os.environ.get("SRU_LIBRARY"):
+                    raise OSError(f"SRU_LIBRARY={LIB_PATH} does not exist")
                 from . import build as _build
                 _build.build()
             h = ctypes.CDLL(LIB_PATH)

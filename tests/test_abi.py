@@ -281,6 +281,7 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     def no_build():
         raise RuntimeError("hipcc unavailable")
 
+    monkeypatch.delenv("SRU_LIBRARY", raising=False)
     monkeypatch.setattr(sru, "_lib", None)
     monkeypatch.setattr(sru, "LIB_PATH", str(tmp_path / "libsru.so"))
     monkeypatch.setattr(build_mod, "build", no_build)

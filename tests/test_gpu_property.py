@@ -1,0 +1,132 @@
+"""Property tests: the GPU layer equals the oracle on randomly drawn small
+cases (shapes, seeds, directions, padding patterns, gate variants, product
+precision, c0 / dc_last), forward and backward through the C ABI.
+
+Bounded and reproducible: a fixed number of derandomized examples, and no
+shrinking phase, so a failure stops the test at the first failing case
+(whose parameters the assertion prints)."""
+
+import numpy as np
+import pytest
+import torch
+from hypothesis import HealthCheck, Phase, given, settings
+from hypothesis import strategies as st
+
+from helpers import TOL_BF16, TOL_FP32, check, dev, host
+from oracle import sru_oracle as O
+from paper_1709_02755_amd import sru
+from paper_1709_02755_amd.workloads import irregular_mask, lengths_to_mask, random_layer_case
+
+pytestmark = pytest.mark.gpu
+
+SETTINGS = dict(deadline=None, derandomize=True, database=None, phases=[Phase.generate],
+                suppress_health_check=list(HealthCheck))
+
+
+@st.composite
+def layer_cases(draw):
+    d = draw(st.integers(1, 96))
+    k4 = draw(st.booleans())
+    d_in = draw(st.integers(1, 96).filter(lambda x: x != d)) if k4 else d
+    linear = draw(st.booleans())
+    return dict(
+        L=draw(st.integers(1, 40)), B=draw(st.integers(1, 6)), d=d, d_in=d_in,
+        direction=draw(st.sampled_from([O.DIR_FWD, O.DIR_REV, O.DIR_BI])),
+        mask=draw(st.sampled_from(["none", "lengths", "irregular"])),
+        gemm=draw(st.sampled_from([O.GEMM_FP32, O.GEMM_BF16])),
+        alpha=draw(st.sampled_from([1.0, float(np.sqrt(3.0)), 0.6])),
+        reset_new=(not linear) and draw(st.booleans()), linear=linear,
+        c0=draw(st.booleans()), dc_last=draw(st.booleans()),
+        seed=draw(st.integers(0, 2 ** 31 - 1)))
+
+
+def _inputs(case):
+    rng = np.random.default_rng(case["seed"])
+    L, B = case["L"], case["B"]
+    c = random_layer_case(rng, L, B, case["d_in"], case["d"], case["direction"],
+                          c0=case["c0"], dc_last=case["dc_last"], bias_scale=0.7, v_scale=0.8)
+    if case["mask"] == "lengths":
+        c["mask"] = lengths_to_mask(rng.integers(1, L + 1, size=B), L)
+    elif case["mask"] == "irregular":
+        c["mask"] = irregular_mask(rng, L, B)
+    return c
+
+
+@settings(max_examples=150, **SETTINGS)
+@given(case=layer_cases())
+def test_layer_equals_oracle_on_random_cases(case):
+    print(f"property case {case}", flush=True)
+    c = _inputs(case)
+    direction, gemm, linear = case["direction"], case["gemm"], case["linear"]
+    var = dict(highway_scale=case["alpha"], reset_new=case["reset_new"], linear=linear)
+    p = [None if linear else dev(c["v_f"]), None if linear else dev(c["v_r"]),
+         dev(c["b_f"]), dev(c["b_r"])]
+    X, W, c0, mask = dev(c["X"]), dev(c["W"]), dev(c["c0"]), dev(c["mask"])
+    fw = sru.forward(X, W, *p, c0=c0, direction=direction, mask=mask, gemm_dtype=gemm, **var)
+    bw = sru.backward(X, W, *p, fw["U"], fw["C"], dev(c["dH"]), c0=c0,
+                      dc_last=dev(c["dc_last"]), direction=direction, mask=mask,
+                      gemm_dtype=gemm, **var)
+    torch.cuda.synchronize()
+    ov = dict(alpha=case["alpha"], reset_new=case["reset_new"], linear=linear)
+    args = (c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"])
+    rf = O.forward(*args, c["c0"], direction, c["mask"], gemm, **ov)
+    rb = O.backward(*args, c["dH"], c["c0"], direction, c["mask"], gemm, c["dc_last"], fw=rf,
+                    **ov)
+    tol = TOL_FP32 if gemm == O.GEMM_FP32 else TOL_BF16
+    check("U", fw["U"], rf["U"], TOL_FP32)
+    for key in ("H", "C", "c_last"):
+        check(key, fw[key], rf[key], tol)
+    keys = ("dX", "dW", "db_f", "db_r", "dc0") + (() if linear else ("dv_f", "dv_r"))
+    for key in keys:
+        check(key, bw[key], rb[key], tol)
+    if c["mask"] is not None:
+        m = c["mask"].astype(bool)
+        assert np.all(host(fw["H"])[m] == 0.0) and np.all(host(bw["dX"])[m] == 0.0)
+
+
+@st.composite
+def lowrank_cases(draw):
+    d = draw(st.integers(2, 64))
+    k4 = draw(st.booleans())
+    gemm = draw(st.sampled_from([O.GEMM_FP32, O.GEMM_BF16]))
+    if gemm == O.GEMM_BF16:  # bf16 low-rank products need whole 16-byte chunks
+        d = 8 * max(1, d // 8)
+        d_in = 8 * draw(st.integers(1, 12).filter(lambda x: 8 * x != d)) if k4 else d
+        dp = 8 * draw(st.integers(1, 6))
+    else:
+        d_in = draw(st.integers(1, 80).filter(lambda x: x != d)) if k4 else d
+        dp = draw(st.integers(1, 40))
+    return dict(L=draw(st.integers(1, 32)), B=draw(st.integers(1, 5)), d=d, d_in=d_in, dp=dp,
+                direction=draw(st.sampled_from([O.DIR_FWD, O.DIR_REV, O.DIR_BI])),
+                mask=draw(st.sampled_from(["none", "lengths", "irregular"])), gemm=gemm,
+                c0=True, dc_last=draw(st.booleans()), seed=draw(st.integers(0, 2 ** 31 - 1)))
+
+
+@settings(max_examples=60, **SETTINGS)
+@given(case=lowrank_cases())
+def test_lowrank_layer_equals_oracle_on_random_cases(case):
+    print(f"property case {case}", flush=True)
+    c = _inputs(case)
+    rng = np.random.default_rng(case["seed"] + 1)
+    ndir, k = c["W"].shape[:2]
+    d_in, d, dp = case["d_in"], case["d"], case["dp"]
+    Q = rng.uniform(-1, 1, (d_in, dp)).astype(np.float32) * np.float32(np.sqrt(3.0 / d_in))
+    P = rng.uniform(-1, 1, (ndir, k, d, dp)).astype(np.float32) * np.float32(np.sqrt(3.0 / dp))
+    direction, gemm = case["direction"], case["gemm"]
+    p = [dev(c[key]) for key in ("v_f", "v_r", "b_f", "b_r")]
+    X, c0, mask = dev(c["X"]), dev(c["c0"]), dev(c["mask"])
+    fw = sru.forward_lowrank(X, dev(Q), dev(P), *p, c0=c0, direction=direction, mask=mask,
+                             gemm_dtype=gemm)
+    bw = sru.backward_lowrank(X, dev(Q), dev(P), *p, fw["T"], fw["U"], fw["C"], dev(c["dH"]),
+                              c0=c0, dc_last=dev(c["dc_last"]), direction=direction, mask=mask,
+                              gemm_dtype=gemm)
+    torch.cuda.synchronize()
+    args = (c["X"], Q, P, c["v_f"], c["v_r"], c["b_f"], c["b_r"])
+    rf = O.forward_lowrank(*args, c["c0"], direction, c["mask"], gemm)
+    rb = O.backward_lowrank(*args, c["dH"], c["c0"], direction, c["mask"], gemm, c["dc_last"],
+                            fw=rf)
+    tol = TOL_FP32 if gemm == O.GEMM_FP32 else TOL_BF16
+    for key in ("T", "U", "H", "C", "c_last"):
+        check(key, fw[key], rf[key], tol)
+    for key in ("dX", "dQ", "dP", "dv_f", "dv_r", "db_f", "db_r", "dc0"):
+        check(key, bw[key], rb[key], tol)
