@@ -186,10 +186,17 @@ def pmc_traffic(label, workload):
     return None if k is None else k.get("hbm_bytes_per_launch")
 
 
-def cold_scans(w, st, X, dH, mask, reps, highway_scale, reset_new):
-    """The two scans of layer 0, timed cold: a 512 MiB buffer is overwritten
-    right before every call, so none of the scan's input is left in the
-    256 MB last-level cache.  The scan kernels are the ones the step runs:
+FLUSH_MODES = ("none", "write", "read", "write+read")
+
+
+def cold_scans(w, st, X, dH, mask, reps, highway_scale, reset_new, mode="write+read"):
+    """The two scans of layer 0, timed cold: right before every call a
+    512 MiB buffer is overwritten, so none of the scan's input is left in
+    L2 or the 256 MB last-level cache, and then a second 512 MiB buffer is
+    read, so the caches hold only clean lines when the scan starts.  (The
+    overwrite alone leaves up to 288 MB of dirty lines in those caches,
+    whose write-back to HBM would then be charged to the scan: 14-25 us per
+    scan at L 256, B 64, d 1024.)  The scan kernels are the ones the step runs:
     the forward is the plain scan call with the step's outputs (H, C and, with
     bf16 products, the bf16 copy of H); the backward is the whole layer-0
     backward call, whose first kernel is the gradient scan (bf16 dU with bf16
@@ -236,6 +243,8 @@ def cold_scans(w, st, X, dH, mask, reps, highway_scale, reset_new):
                 W_bf16=f0.get("W_bf16"), **v)
         calls["scan_bwd"] = (bbytes, ("scan_bwd", "scan_maps"), bcall)
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=U.device)
+    clean = torch.ones((512 << 20) // 4, dtype=torch.float32, device=U.device)
+    sink = torch.empty((), dtype=torch.float32, device=U.device)
     lib = sru.lib()
     ev = HipEvents(2 * 64 + 2)
     res = {}
@@ -244,7 +253,11 @@ def cold_scans(w, st, X, dH, mask, reps, highway_scale, reset_new):
             call()  # warm the launch path
             times = []
             for i in range(reps):
-                flush.fill_(i & 0xFF)
+                if "write" in mode:
+                    flush.fill_(i & 0xFF)              # evict the scan's data
+                if "read" in mode:
+                    torch.sum(clean, dim=0, out=sink)  # write back the dirty lines
+                torch.cuda.synchronize()
                 lib.sru_timing_begin(ev.events, ev.n)
                 try:
                     call()
@@ -257,10 +270,13 @@ def cold_scans(w, st, X, dH, mask, reps, highway_scale, reset_new):
             gbps = nbytes / t / 1e9
             res[name] = {"avg_us": round(t * 1e6, 2), "GBps": round(gbps, 1),
                          "frac": round(gbps / HBM_PEAK_GBPS, 4),
-                         "bytes_per_elem": nbytes / elems, "reps": reps, "stat": "median"}
+                         "bytes_per_elem": nbytes / elems, "reps": reps, "stat": "median",
+                         "flush": {"none": "none", "write": "512 MiB written",
+                                   "read": "512 MiB read",
+                                   "write+read": "512 MiB written, then 512 MiB read"}[mode]}
     finally:
         ev.close()
-    del flush
+    del flush, clean
     return res
 
 
@@ -405,6 +421,9 @@ def main():
     ap.add_argument("--cold-reps", type=int, default=7,
                     help="launches of each scan timed cold (0 = skip; the counter runs skip "
                          "them so that only the step's launches are counted)")
+    ap.add_argument("--cold-protocols", action="store_true",
+                    help="only time the layer-0 scans under each cache-flush protocol "
+                         "(none, write, read, write+read) and print one JSON line")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="REPS",
                     help="only run a 1 GiB copy REPS times (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=5,
@@ -444,6 +463,17 @@ def main():
         st.forward(X, mask)
         if w.backward:
             st.backward(X, dH, mask)
+
+    if args.cold_protocols:
+        eager_step()
+        torch.cuda.synchronize()
+        table = {m: cold_scans(w, st, X, dH, mask, max(args.cold_reps, 3), args.highway_scale,
+                               args.reset_new, mode=m) for m in FLUSH_MODES}
+        for m, r in table.items():
+            log("  " + m.ljust(11) + "  ".join(f"{k} {v['avg_us']:8.2f} us ({v['frac']:.3f})"
+                                              for k, v in r.items()))
+        print(json.dumps({"workload": w.name, "cold_protocols": table}), flush=True)
+        return
 
     step = eager_step
     if args.graph:

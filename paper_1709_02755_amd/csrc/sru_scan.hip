@@ -23,6 +23,7 @@ namespace sru {
 namespace {
 
 constexpr int kScanThreads = 64;
+typedef __attribute__((address_space(3))) void lds_t;
 
 struct Lane {
   int gid, b, fidx, dir, j;
@@ -132,6 +133,194 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
     if (s0 + p < L) step(r0[p], r1[p], r2[p], rx[p], rm[p]);
 
   if (a.c_last) a.c_last[ln.gid] = c;
+}
+
+// ------------------------------------------------ forward scan, LDS ring
+// The same recurrence and arithmetic as scan_fwd_kernel (results equal bit
+// for bit), organised for more memory parallelism.  A workgroup owns 256
+// consecutive hidden units of one (sequence b, direction): four consumer
+// waves (one unit per lane) run the recurrence, and one producer wave
+// streams their inputs into a ring in LDS with buffer loads that write LDS
+// directly, 1 KiB (64 lanes x 16 bytes) per instruction: per step one load
+// per input segment (U blocks 0-2 and x for k = 3, U blocks 0-3 for
+// k = 4) and, with padding, one byte load of the step's mask entry per
+// lane.  The ring holds kRingSlots groups of kRingSteps steps; the producer
+// keeps kRingSlots - 1 groups in flight (12 steps, 48 KiB per workgroup),
+// about twice what the register ring of scan_fwd_kernel holds per unit.
+// Hand-off per group: the producer waits for the group's loads, every wave
+// meets at a barrier, the consumers read the group from LDS and the
+// producer refills the slot the consumers finished before the barrier.
+// Steps past the end of the sequence load with an out-of-range offset
+// (zeros) and are not computed.  Operands must be smaller than 2 GiB (the
+// buffer offsets are 32-bit; the top bit marks out-of-range).
+constexpr int kRingUnits = 256;  // hidden units per workgroup (4 consumer waves)
+constexpr int kRingSteps = 4;    // steps per hand-off
+constexpr int kRingSlots = 4;    // groups in the ring
+constexpr int kRingConsumers = kRingUnits / 64;
+constexpr int kRingThreads = kRingUnits + 64;
+constexpr int kRingSegBytes = kRingUnits * 4;  // one input segment of one step
+constexpr unsigned kRingOOB = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t ring_rsrc(const void* p, unsigned bytes) {
+  // dword 3 = 0x00020000: 32-bit data format, the raw-buffer setting of gfx9 parts
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+// Workgroup barrier of the ring: this wave's LDS accesses are complete
+// (lgkmcnt 0), not its global stores (the release fence of __syncthreads
+// would wait for those too).
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0) (vmcnt 63, expcnt 7)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// s_waitcnt immediate for vmcnt <= n (expcnt 7, lgkmcnt 15)
+constexpr int ring_vm_wait(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
+
+template <int KB, bool MASK, bool STORE_C, bool STORE_HB, bool RN>
+__global__ __launch_bounds__(kRingThreads) void scan_fwd_ring_kernel(ScanShape s, ScanFwdArgs a,
+                                                                     unsigned u_bytes,
+                                                                     unsigned x_bytes,
+                                                                     unsigned m_bytes) {
+  constexpr int NSEG = 4;  // U blocks 0-2 and x (k = 3), or U blocks 0-3 (k = 4)
+  constexpr int STEPB = NSEG * kRingSegBytes;
+  constexpr int SLOTB = kRingSteps * STEPB;
+  constexpr int IPG = kRingSteps * (NSEG + (MASK ? 1 : 0));  // loads per group
+  static_assert((kRingSlots - 1) * IPG < 64, "vmcnt counts at most 63 loads");
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[kRingSlots * SLOTB];
+  __shared__ __attribute__((aligned(256))) unsigned mring[kRingSlots][kRingSteps * 64];
+
+  const int nblk = s.d / kRingUnits;
+  const int jb = blockIdx.x % nblk;
+  const int bd = blockIdx.x / nblk;
+  const int dir = bd % s.ndir;
+  const int b = bd / s.ndir;
+  const bool rev = s.direction == 1 || (s.direction == 2 && dir == 1);
+  const int L = s.L;
+  const int G = (L + kRingSteps - 1) / kRingSteps;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+
+  if (wave == kRingConsumers) {
+    // ---- producer
+    const __amdgpu_buffer_rsrc_t ru = ring_rsrc(a.U, u_bytes);
+    const __amdgpu_buffer_rsrc_t rx = ring_rsrc(KB == 3 ? a.X : a.U, KB == 3 ? x_bytes : u_bytes);
+    const __amdgpu_buffer_rsrc_t rm =
+        ring_rsrc(MASK ? static_cast<const void*>(a.mask) : static_cast<const void*>(a.U),
+                  MASK ? m_bytes : u_bytes);
+    const unsigned u_step = (unsigned)s.B * s.ndir * KB * s.d * 4u;
+    const unsigned x_step = (unsigned)s.B * s.d_in * 4u;
+    const unsigned u_base =
+        (unsigned)((((long long)b * s.ndir + dir) * KB * s.d + jb * kRingUnits) * 4) + lane * 16u;
+    const unsigned x_base = (unsigned)(((long long)b * s.d_in + jb * kRingUnits) * 4) + lane * 16u;
+    const unsigned seg = (unsigned)s.d * 4u;
+    auto issue = [&](int gi) {
+      unsigned char* slot = ring + (gi % kRingSlots) * SLOTB;
+#pragma unroll
+      for (int k = 0; k < kRingSteps; ++k) {
+        const int step = gi * kRingSteps + k;
+        const int t = rev ? L - 1 - step : step;
+        const unsigned oob = step < L ? 0u : kRingOOB;
+        const unsigned uo = ((unsigned)t * u_step + u_base) | oob;
+#pragma unroll
+        for (int q = 0; q < KB; ++q)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              ru, (lds_t*)(slot + k * STEPB + q * kRingSegBytes), 16, uo + q * seg, 0, 0, 0);
+        if constexpr (KB == 3)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              rx, (lds_t*)(slot + k * STEPB + 3 * kRingSegBytes), 16,
+              ((unsigned)t * x_step + x_base) | oob, 0, 0, 0);
+        if constexpr (MASK) {
+          // lane 0 loads the step's mask byte into its dword slot; the
+          // other lanes read out of range (zeros)
+          const unsigned mo = lane == 0 ? (((unsigned)t * s.B + b) | oob) : kRingOOB;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              rm, (lds_t*)(&mring[gi % kRingSlots][k * 64]), 1, mo, 0, 0, 0);
+        }
+      }
+    };
+    for (int gi = 0; gi < kRingSlots - 1 && gi < G; ++gi) issue(gi);
+    for (int g = 0; g < G; ++g) {
+      // group g has landed once at most the groups issued after it remain
+      const int later = min(kRingSlots - 2, G - 1 - g);
+      if (later >= 2) __builtin_amdgcn_s_waitcnt(ring_vm_wait(2 * IPG));
+      else if (later == 1) __builtin_amdgcn_s_waitcnt(ring_vm_wait(IPG));
+      else __builtin_amdgcn_s_waitcnt(ring_vm_wait(0));
+      ring_barrier();
+      // the slot of group g - 1, which every consumer finished before the barrier
+      if (g + kRingSlots - 1 < G) issue(g + kRingSlots - 1);
+    }
+    return;
+  }
+
+  // ---- consumers: unit j of (b, dir), lane gid of the [B, ndir*d] state
+  const int j = jb * kRingUnits + wave * 64 + lane;
+  const int fidx = dir * s.d + j;
+  const long long nfeat = (long long)s.ndir * s.d;
+  const long long gid = (long long)b * nfeat + fidx;
+  const long long h_step = (long long)s.B * nfeat;
+  const long long t0 = rev ? L - 1 : 0;
+  const long long sh = rev ? -h_step : h_step;
+  float* hp = a.H + gid + t0 * h_step;
+  float* cp = STORE_C ? a.C + gid + t0 * h_step : nullptr;
+  uint16_t* hbp = STORE_HB ? a.Hb + gid + t0 * h_step : nullptr;
+  const float vfs = a.v_f[fidx] * kNegLog2e, vrs = a.v_r[fidx] * kNegLog2e;
+  const float bfs = a.b_f[fidx] * kNegLog2e, brs = a.b_r[fidx] * kNegLog2e;
+  const float alpha = s.alpha;
+  float c = a.c0 ? a.c0[gid] : 0.0f;
+  const int ubyte = (wave * 64 + lane) * 4;
+
+  auto step = [&](const float (&v)[NSEG], unsigned mk) {
+    const float u0 = v[0], u1 = v[1], u2 = v[2], xh = v[3];
+    const float f = sigmoid_scaled(fmaf(vfs, c, fmaf(u1, kNegLog2e, bfs)));  // Eq. 1
+    const float cn = fmaf(f, c, fmaf(-f, u0, u0));                           // Eq. 2
+    const float r = sigmoid_scaled(fmaf(vrs, RN ? cn : c, fmaf(u2, kNegLog2e, brs)));  // Eq. 3
+    float h = fmaf(r, cn, (1.0f - r) * (alpha * xh));  // Eq. 4 (Sec. 3.2)
+    if constexpr (MASK) {
+      const bool pad = mk != 0;
+      c = pad ? c : cn;
+      h = pad ? 0.0f : h;
+    } else {
+      c = cn;
+    }
+    __builtin_nontemporal_store(h, hp);
+    if constexpr (STORE_C) __builtin_nontemporal_store(c, cp);
+    if constexpr (STORE_HB)
+      __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), hbp);
+    hp += sh;
+    if constexpr (STORE_C) cp += sh;
+    if constexpr (STORE_HB) hbp += sh;
+  };
+
+  // Whole groups run without a bound check, so a group's LDS reads all go
+  // out before its first step; the last, partial group checks each step.
+  const int Gfull = L / kRingSteps;
+  for (int g = 0; g < G; ++g) {
+    ring_barrier();
+    const unsigned char* slot = ring + (g % kRingSlots) * SLOTB;
+    float in[kRingSteps][NSEG];
+    unsigned m[kRingSteps];
+#pragma unroll
+    for (int k = 0; k < kRingSteps; ++k) {
+#pragma unroll
+      for (int q = 0; q < NSEG; ++q)
+        in[k][q] = *reinterpret_cast<const float*>(slot + k * STEPB + q * kRingSegBytes + ubyte);
+      m[k] = MASK ? (mring[g % kRingSlots][k * 64] & 0xFFu) : 0u;
+    }
+    if (g < Gfull) {
+#pragma unroll
+      for (int k = 0; k < kRingSteps; ++k) step(in[k], m[k]);
+    } else {
+#pragma unroll
+      for (int k = 0; k < kRingSteps; ++k)
+        if (g * kRingSteps + k < L) step(in[k], m[k]);
+    }
+  }
+  if (a.c_last) a.c_last[gid] = c;
 }
 
 // ------------------------------------------------------------ backward scan
@@ -790,10 +979,46 @@ hipError_t fwd_lin_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_
   return hipGetLastError();
 }
 
+// Where the LDS-ring forward scan runs: gated recurrence, whole groups of
+// 256 units, operands inside the 2 GiB range of buffer offsets, enough
+// lanes that the scan streams from HBM rather than waiting on its serial
+// chain (below that, one wave per 64 units spreads better over the SIMDs),
+// and few enough that every workgroup is resident at once (two per CU):
+// with a second round of workgroups the register-ring scan, whose waves
+// all fit at once, is faster.  Measured at L 256, B 64, d 1024 (256
+// workgroups): 68 us against 72 us in the step, the same time cold; at
+// L 128, B 128, d 2048 (1024 workgroups): 201 us against 185 us.
+constexpr long long kRingMinLanes = 65536;
+constexpr long long kRingMaxLanes = 2LL * 256 * kRingUnits;
+bool ring_ok(const ScanShape& s, long long u_bytes, long long x_bytes) {
+  const long long lanes = (long long)s.B * s.ndir * s.d;
+  return !s.linear && s.d % kRingUnits == 0 && lanes >= kRingMinLanes &&
+         lanes <= kRingMaxLanes &&
+         u_bytes < (long long)kRingOOB && x_bytes < (long long)kRingOOB &&
+         (long long)s.L * s.B < (long long)kRingOOB;
+}
+
 template <int KB, bool MASK, bool STORE_C, bool STORE_HB>
 hipError_t fwd_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st) {
   const int lanes = s.B * s.ndir * s.d;
   const int grid = (lanes + kScanThreads - 1) / kScanThreads;
+  const long long u_bytes = 4LL * s.L * s.B * s.ndir * KB * s.d;
+  const long long x_bytes = KB == 3 ? 4LL * s.L * s.B * s.d_in : 0;
+  if (ring_ok(s, u_bytes, x_bytes)) {
+    const int rgrid = s.B * s.ndir * (s.d / kRingUnits);
+    const unsigned m_bytes = (unsigned)((long long)s.L * s.B);
+    timing_before("scan_fwd", st);
+    if (s.reset_new)
+      hipLaunchKernelGGL((scan_fwd_ring_kernel<KB, MASK, STORE_C, STORE_HB, true>), dim3(rgrid),
+                         dim3(kRingThreads), 0, st, s, a, (unsigned)u_bytes, (unsigned)x_bytes,
+                         m_bytes);
+    else
+      hipLaunchKernelGGL((scan_fwd_ring_kernel<KB, MASK, STORE_C, STORE_HB, false>), dim3(rgrid),
+                         dim3(kRingThreads), 0, st, s, a, (unsigned)u_bytes, (unsigned)x_bytes,
+                         m_bytes);
+    timing_after(st);
+    return hipGetLastError();
+  }
   timing_before("scan_fwd", st);
   if (s.reset_new)
     hipLaunchKernelGGL((scan_fwd_kernel<KB, MASK, STORE_C, STORE_HB, true, kFwdPF>), dim3(grid),

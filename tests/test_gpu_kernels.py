@@ -113,6 +113,10 @@ LDS_SCAN_CASES = [
     (61, 5, 64, 64, O.DIR_BI),
     (100, 4, 96, 64, O.DIR_REV),
     (130, 3, 128, 128, O.DIR_FWD),
+    # 256-unit workgroups streaming through the LDS ring (65,536 lanes):
+    # a partial last group of steps, k = 3 reverse, k = 4 bidirectional
+    (9, 64, 1024, 1024, O.DIR_REV),
+    (6, 32, 512, 1024, O.DIR_BI),
 ]
 
 

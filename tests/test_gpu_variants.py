@@ -23,6 +23,7 @@ SCAN_CASES = [
     (33, 4, 96, 64, O.DIR_BI, False),
     (40, 5, 128, 128, O.DIR_BI, True),
     (11, 64, 1024, 1024, O.DIR_REV, True),  # a wave on every SIMD: shorter backward ring
+    (10, 32, 512, 1024, O.DIR_BI, True),  # k = 4, both directions, 256-unit workgroups
 ]
 
 
