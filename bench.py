@@ -280,6 +280,66 @@ def cold_scans(w, st, X, dH, mask, reps, highway_scale, reset_new, mode="write+r
     return res
 
 
+def yardstick(w, st, X, dH, mask, eager_step, reps=20):
+    """The vendor library (torch.mm, i.e. hipBLASLt, bf16 operands, run
+    only) on the first layer's three product shapes, with fp32 and with bf16
+    output, beside this library's own product kernels in the step (the
+    per-launch event hook): medians of `reps` launches, microseconds."""
+    import torch
+
+    from paper_1709_02755_amd import sru
+    M = w.tokens
+    K, k = w.layer_dims(0)
+    N = w.ndir * k * w.d
+    g = torch.Generator(device="cuda").manual_seed(0)
+    rnd = lambda *shape: torch.randn(*shape, device="cuda", generator=g).to(torch.bfloat16)
+    X16, W16, dU16 = rnd(M, K), rnd(N, K), rnd(M, N)
+    # transposed operands are materialised (no transposed views)
+    Wt16, dUt16 = W16.t().contiguous(), dU16.t().contiguous()
+    shapes = {"gemm_u": (lambda od: torch.mm(X16, Wt16, out_dtype=od)),     # U = X W^T
+              "gemm_dx": (lambda od: torch.mm(dU16, W16, out_dtype=od)),    # dX = dU W
+              "gemm_dw": (lambda od: torch.mm(dUt16, X16, out_dtype=od))}   # dW = dU^T X
+
+    def median_us(fn):
+        fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
+        for i in range(reps):
+            ev[2 * i].record()
+            fn()
+            ev[2 * i + 1].record()
+        torch.cuda.synchronize()
+        t = sorted(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(reps))
+        return round(t[reps // 2] * 1e3, 2)
+
+    vendor = {name: {"fp32_out": median_us(lambda: fn(torch.float32)),
+                     "bf16_out": median_us(lambda: fn(torch.bfloat16))}
+              for name, fn in shapes.items()}
+    # this library's kernels: one bracketed step
+    ev = HipEvents(2 * w.layers * 32 + 2)
+    lib = sru.lib()
+    lib.sru_timing_begin(ev.events, ev.n)
+    try:
+        eager_step()
+    finally:
+        nk = lib.sru_timing_end()
+    torch.cuda.synchronize()
+    ours = {}
+    for i in range(nk):
+        lab = lib.sru_timing_label(i).decode()
+        if lab in shapes and lab not in ours:  # the first layer's launch
+            ours[lab] = round(ev.elapsed_ms(2 * i, 2 * i + 1) * 1e3, 2)
+    ev.close()
+    flops = 2.0 * M * N * K
+    for name in shapes:
+        log(f"  {name}: vendor fp32-out {vendor[name]['fp32_out']} us, bf16-out "
+            f"{vendor[name]['bf16_out']} us; ours (fp32 out) {ours.get(name)} us")
+    return {"workload": w.name, "M": M, "N": N, "K": K, "flops": flops, "vendor_us": vendor,
+            "ours_us": ours,
+            "note": "vendor: torch.mm on bf16 operands, median of %d; ours: the step's "
+                    "kernels, first layer" % reps}
+
+
 # ------------------------------------------------------------------ CPU oracle
 def cpu_baseline(w, inp, nseq):
     """The fp64 oracle (test infrastructure, never the product path) on the
@@ -424,6 +484,9 @@ def main():
     ap.add_argument("--cold-protocols", action="store_true",
                     help="only time the layer-0 scans under each cache-flush protocol "
                          "(none, write, read, write+read) and print one JSON line")
+    ap.add_argument("--yardstick", action="store_true",
+                    help="only time the vendor library's bf16 products (torch.mm) on the "
+                         "workload's three product shapes beside the step's own kernels")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="REPS",
                     help="only run a 1 GiB copy REPS times (counter calibration)")
     ap.add_argument("--summarize-pmc", nargs=5,
@@ -463,6 +526,10 @@ def main():
         st.forward(X, mask)
         if w.backward:
             st.backward(X, dH, mask)
+
+    if args.yardstick:
+        print(json.dumps(yardstick(w, st, X, dH, mask, eager_step)), flush=True)
+        return
 
     if args.cold_protocols:
         eager_step()
