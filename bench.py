@@ -417,7 +417,8 @@ def _per_kernel(rows, counter):
 
 
 # kernel-name substrings (all must occur) -> labels of the per-launch table
-KERNEL_KEYS = [(("scan_fwd_kernel",), "scan_fwd"), (("scan_bwd_kernel",), "scan_bwd"),
+KERNEL_KEYS = [(("scan_fwd_kernel",), "scan_fwd"), (("scan_fwd_ring_kernel",), "scan_fwd"),
+               (("scan_bwd_kernel",), "scan_bwd"),
                (("scan_fwd_lin_kernel",), "scan_fwd"), (("scan_bwd_lin_kernel",), "scan_bwd"),
                (("reduce_vb_kernel",), "reduce_vb"), (("splitk_reduce_kernel",), "splitk_reduce"),
                (("splitk_reduce4_kernel",), "splitk_reduce"),
