@@ -105,6 +105,7 @@ def _layer_work(w, li, splits, bf16):
     du_b = 2.0 if bf16 else 4.0
     nq = 2 if w.linear else 4  # v/b sums per feature (no v in the linear variant)
     hb = 2.0 * (w.layers - 1) / w.layers if bf16 else 0.0  # bf16 copy of H (not the top's)
+    vb_bytes = 4.0 * (nq * w.B * nfeat + nq * nfeat)  # per-sequence partials in, sums out
     if w.dp is not None:  # low-rank layers: Wcat = P Q^T, rank dp
         dp = w.dp
         low = {
@@ -136,8 +137,11 @@ def _layer_work(w, li, splits, bf16):
         # the products are bf16) and, for k = 3, dx_hat (4 B): 34 B (bf16) /
         # 40 B (fp32) at k = 3
         "scan_bwd": dict(bytes=elems * (24.0 + du_b * k + (4.0 if k == 3 else 0.0))),
-        "reduce_vb": dict(bytes=4.0 * (nq * w.B * nfeat + nq * nfeat)),
-        "splitk_reduce": dict(bytes=4.0 * (splits + 1) * N * K),
+        "reduce_vb": dict(bytes=vb_bytes),
+        # the dense backward runs the v/b sums as extra workgroups of the dW
+        # product's split-K sum when it has one (else as reduce_vb)
+        "splitk_reduce": dict(bytes=4.0 * (splits + 1) * N * K
+                              + (vb_bytes if w.dp is None and splits > 1 else 0.0)),
         # fp32 -> bf16 copies of the product operands: Wcat, X (first layer);
         # Wcat^T for dX, transposed from the forward's bf16 Wcat (the stack
         # hands it over: 2 B read, 2 B written per element)

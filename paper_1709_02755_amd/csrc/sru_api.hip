@@ -567,6 +567,10 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   //    type of the products that read it
   sru::ScanBwdArgs a{U,   X,    C,   dH,      dc_last, v_f,  v_r,  b_f,  b_r,  c0,
                      pad_mask, dU, bf16, dxh, partial, dc0, dv_f, dv_r, db_f, db_r};
+  // the v/b sums over the batch run with the dW product (in its split-K
+  // sum's launch when it has one)
+  a.defer_vb = true;
+  gw.vb = sru::scan_backward_vb(scan_shape(s, direction, op), a);
   if (int e = hip_status(sru::scan_backward_launch(scan_shape(s, direction, op), a, stream)))
     return e;
 

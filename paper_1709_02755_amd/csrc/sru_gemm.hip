@@ -1192,12 +1192,20 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 
 // The same for rows of 16-byte aligned groups of 4 (N % 4 == 0): one group
 // per thread, the partials read as 16-byte loads.  The per-element sum is
-// the same sequence of additions, so the result is bit-identical.
+// the same sequence of additions, so the result is bit-identical.  Blocks
+// from `main_blocks` on run the v/b sums of the backward pass instead
+// (vb_sum_block: the same bits as their own launch).
 __global__ __launch_bounds__(256) void splitk_reduce4_kernel(const float* __restrict__ part,
                                                              int splits, int M, int N,
                                                              float* C, long long ldc,
                                                              const float* add, long long add_ld,
-                                                             long long add_off, int add_count) {
+                                                             long long add_off, int add_count,
+                                                             unsigned main_blocks, VbSum vb) {
+  if (blockIdx.x >= main_blocks) {
+    __shared__ float red[256];
+    vb_sum_block(vb.partial, vb.rows, vb.nfeat, vb.qlo, vb.out, blockIdx.x - main_blocks, red);
+    return;
+  }
   const long long total = (long long)M * N;
   const long long i = ((long long)blockIdx.x * 256 + threadIdx.x) * 4;
   if (i >= total) return;
@@ -1216,7 +1224,8 @@ __global__ __launch_bounds__(256) void splitk_reduce4_kernel(const float* __rest
 
 hipError_t launch_splitk_reduce(const float* part, int splits, int M, int N, float* C,
                                 long long ldc, const float* add, long long add_ld,
-                                long long add_off, int add_count, hipStream_t st) {
+                                long long add_off, int add_count, const VbSum& vb,
+                                hipStream_t st) {
   const long long total = (long long)M * N;
   auto al16 = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
   const bool vec = N % 4 == 0 && ldc % 4 == 0 && al16(part) && al16(C) &&
@@ -1224,15 +1233,19 @@ hipError_t launch_splitk_reduce(const float* part, int splits, int M, int N, flo
   timing_before("splitk_reduce", st);
   if (vec) {
     const long long groups = total / 4;
-    hipLaunchKernelGGL(splitk_reduce4_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256),
-                       0, st, part, splits, M, N, C, ldc, add, add_ld, add_off, add_count);
+    const unsigned main_blocks = (unsigned)((groups + 255) / 256);
+    const unsigned extra = vb.partial ? (unsigned)vb_sum_blocks(vb) : 0u;
+    hipLaunchKernelGGL(splitk_reduce4_kernel, dim3(main_blocks + extra), dim3(256), 0, st, part,
+                       splits, M, N, C, ldc, add, add_ld, add_off, add_count, main_blocks, vb);
   } else {
     const int grid = (int)std::min<long long>((total + 255) / 256, 8192);
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, st, part, splits, M, N,
                        C, ldc, add, add_ld, add_off, add_count);
   }
   timing_after(st);
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || vec || !vb.partial) return e;
+  return vb_sum_launch(vb, st);
 }
 
 // fp32 -> bf16 conversions (RNE).  Plain copy: 8 elements per thread (two
@@ -1416,9 +1429,10 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
     launch_staged<C, A_KC, B_KC, SA, SB, false>(a, nwg, st);
   timing_after(st);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.splits == 1) return e;
+  if (e != hipSuccess) return e;
+  if (a.splits == 1) return g.vb.partial ? vb_sum_launch(g.vb, st) : hipSuccess;
   return launch_splitk_reduce(g.partials, a.splits, g.M, g.N, g.C, g.ldc, g.add, g.add_ld,
-                              g.add_off, g.add_count, st);
+                              g.add_off, g.add_count, g.vb, st);
 }
 
 // ---- the direct path: plan (shared by workspace sizing and launch) ----
@@ -1563,9 +1577,10 @@ hipError_t launch_direct_cfg(const GemmDesc& g, hipStream_t st) {
   else launch_direct<C, 0, A_RC, B_RC>(a, nwg, st);
   timing_after(st);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || splits == 1) return e;
+  if (e != hipSuccess) return e;
+  if (splits == 1) return g.vb.partial ? vb_sum_launch(g.vb, st) : hipSuccess;
   return launch_splitk_reduce(g.partials, a.splits, g.M, g.N, g.C, g.ldc, g.add, g.add_ld,
-                              g.add_off, g.add_count, st);
+                              g.add_off, g.add_count, g.vb, st);
 }
 
 // Operand-type combinations that are instantiated: fp32 x fp32 for every

@@ -8,6 +8,19 @@
 
 namespace sru {
 
+// The v/b gradient sums over the batch: `rows` rows of per-sequence partials
+// [rows, 4, nfeat] (q = dv_f, dv_r, db_f, db_r) summed in a fixed order into
+// the four [nfeat] outputs, from q = qlo (the linear recurrence has no v:
+// qlo = 2).  partial == nullptr: nothing to do.
+struct VbSum {
+  const float* partial;
+  int rows, nfeat, qlo;
+  float* out[4];
+};
+// Blocks of 256 threads the sums take (64 outputs per block).
+inline int vb_sum_blocks(const VbSum& v) { return ((4 - v.qlo) * v.nfeat + 63) / 64; }
+hipError_t vb_sum_launch(const VbSum& v, hipStream_t stream);
+
 // ----------------------------------------------------------------- GEMM
 // C[M,N] = sum_k A(m,k) B(n,k), fp32 result, MFMA compute.
 //   A(m,k) = a_kc ? A[m*lda + k] : A[k*lda + m]
@@ -43,6 +56,9 @@ struct GemmDesc {
   uint16_t* Cb;
   long long ldcb;
   const char* label;  // name for the measurement hook (nullptr: by layout)
+  // v/b sums to run with this product (vb.partial != nullptr): in the same
+  // launch as the split-K sum when there is one, else right after the product
+  VbSum vb;
 };
 
 // fp32 -> bf16 (RNE) copy of a [rows, cols] matrix; transposed ([cols, rows])
@@ -144,15 +160,20 @@ struct ScanBwdArgs {
   float* dv_r;
   float* db_f;
   float* db_r;
+  // the caller runs the v/b sums (scan_backward_vb) instead of
+  // scan_backward_launch
+  bool defer_vb = false;
 };
 
 hipError_t scan_forward_launch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t stream);
 // Scratch the forward scan needs (the linear recurrence's segment maps; the
 // gated one needs none).  Depends on the sizes only.
 size_t scan_forward_scratch_bytes(const ScanShape& s);
-// Enqueues the reverse scan and the fixed-order reduction of `partial`.
+// Enqueues the reverse scan and (unless a.defer_vb) the fixed-order
+// reduction of `partial`; scan_backward_vb describes that reduction.
 hipError_t scan_backward_launch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t stream);
 size_t scan_backward_partial_bytes(const ScanShape& s);
+VbSum scan_backward_vb(const ScanShape& s, const ScanBwdArgs& a);
 
 // ----------------------------------------------------------------- timing
 // Measurement hook: while a caller has armed it (sru_timing_begin), every

@@ -890,40 +890,14 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_lin_kernel(ScanSha
   }
 }
 
-// Sum of the per-sequence partials over b, in a fixed order (deterministic).
-// A workgroup covers 64 consecutive outputs; its 8 waves take b = w, w+8,
-// ... in sequence, and the 8 wave sums of an output are added as a fixed
-// tree through LDS.  The loads of a lane are independent, so a launch costs
-// about one memory round trip.
-constexpr int kVbWaves = 8;
-// Outputs q = qlo .. 3 (q: dv_f, dv_r, db_f, db_r); the linear variant has
-// no v and sums from q = 2.
-__global__ __launch_bounds__(64 * kVbWaves) void reduce_vb_kernel(const float* __restrict__ partial,
-                                                                  int B, int nfeat, int qlo,
-                                                                  float* dv_f, float* dv_r,
-                                                                  float* db_f, float* db_r) {
-  __shared__ float red[kVbWaves][64];
-  const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
-  const int o = qlo * nfeat + blockIdx.x * 64 + lane;  // output: q * nfeat + f
-  const bool live = o < 4 * nfeat;
-  const long long stride = 4LL * nfeat;
-  float s = 0.f;
-  if (live) {
-    const float* p = partial + o;
-#pragma unroll 8
-    for (int b = w; b < B; b += kVbWaves) s += p[b * stride];
-  }
-  red[w][lane] = s;
-  __syncthreads();
-  if (w == 0 && live) {
-    const float t = ((red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane])) +
-                    ((red[4][lane] + red[5][lane]) + (red[6][lane] + red[7][lane]));
-    const int q = o / nfeat;
-    const int f = o - q * nfeat;
-    float* out = q == 0 ? dv_f : q == 1 ? dv_r : q == 2 ? db_f : db_r;
-    out[f] = t;
-  }
+// Sum of the per-sequence partials over b, in a fixed order (deterministic):
+// vb_sum_block, 64 outputs per workgroup of 4 waves.  The loads of a lane
+// are independent, so a launch costs about one memory round trip.  The same
+// blocks can run inside the split-K sum of the dW product (sru_gemm.hip),
+// which saves this launch; either way the sums are the same bits.
+__global__ __launch_bounds__(256) void reduce_vb_kernel(VbSum v) {
+  __shared__ float red[256];
+  vb_sum_block(v.partial, v.rows, v.nfeat, v.qlo, v.out, blockIdx.x, red);
 }
 
 // Steps of loads a lane keeps in flight (its register ring).  Measured on
@@ -1120,14 +1094,27 @@ hipError_t scan_backward_launch(const ScanShape& s, const ScanBwdArgs& a, hipStr
   if (s.k == 3) e = m ? bwd_dispatch<3, true>(s, a, st) : bwd_dispatch<3, false>(s, a, st);
   else e = m ? bwd_dispatch<4, true>(s, a, st) : bwd_dispatch<4, false>(s, a, st);
   if (e != hipSuccess) return e;
-  const int nfeat = s.ndir * s.d;
-  const int qlo = s.linear ? 2 : 0;
-  const int grid = ((4 - qlo) * nfeat + 63) / 64;
+  if (a.defer_vb) return hipSuccess;
+  return vb_sum_launch(scan_backward_vb(s, a), st);
+}
+
+VbSum scan_backward_vb(const ScanShape& s, const ScanBwdArgs& a) {
+  VbSum v{};
+  v.partial = a.partial;
+  v.nfeat = s.ndir * s.d;
+  v.qlo = s.linear ? 2 : 0;
   // the linear scans leave one row of partials per (segment, sequence)
-  const int rows = s.linear ? s.B * lin_plan(s, kBwdLinCH).nseg : s.B;
+  v.rows = s.linear ? s.B * lin_plan(s, kBwdLinCH).nseg : s.B;
+  v.out[0] = a.dv_f;
+  v.out[1] = a.dv_r;
+  v.out[2] = a.db_f;
+  v.out[3] = a.db_r;
+  return v;
+}
+
+hipError_t vb_sum_launch(const VbSum& v, hipStream_t st) {
   timing_before("reduce_vb", st);
-  hipLaunchKernelGGL(reduce_vb_kernel, dim3(grid), dim3(64 * kVbWaves), 0, st, a.partial, rows,
-                     nfeat, qlo, a.dv_f, a.dv_r, a.db_f, a.db_r);
+  hipLaunchKernelGGL(reduce_vb_kernel, dim3(vb_sum_blocks(v)), dim3(256), 0, st, v);
   timing_after(st);
   return hipGetLastError();
 }

@@ -26,7 +26,7 @@ def test_headline_work_figures():
     scan 24 B per (t, b, j) plus the bf16 copy of h on 5 of the 6 layers; the
     backward scan 24 B read, dU written in bf16 (3 blocks) and the fp32
     highway gradient (34 B); the split-K sum reads S partials and writes
-    the result."""
+    the result, and also sums the v/b partials over the batch."""
     w = _w("sru6_L256_B64_d1024_bf16")
     elems = 256 * 64 * 1024
     work = bench.kernel_work(w, 5, True)
@@ -34,7 +34,8 @@ def test_headline_work_figures():
         assert work[key]["flops"] == 2.0 * 16384 * 3072 * 1024
     assert work["scan_fwd"]["bytes"] == pytest.approx(elems * (24 + 2 * 5 / 6), rel=1e-15)
     assert work["scan_bwd"]["bytes"] == elems * 34
-    assert work["splitk_reduce"]["bytes"] == 4.0 * 6 * 3072 * 1024
+    # with the v/b sums (4 per feature) of the 64 sequences folded in
+    assert work["splitk_reduce"]["bytes"] == 4.0 * 6 * 3072 * 1024 + 4.0 * 4 * 65 * 1024
     assert work["bf16_x"]["bytes"] == 6.0 * 16384 * 1024
 
 
