@@ -92,6 +92,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, unsig
                                            0x00020000);
 }
 
+// Resource for the bytes of an operand from `base` on (extent `bytes`),
+// its range capped below kOOB so that sentinel offsets stay out of range.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t panel_rsrc(const void* p, long long base,
+                                                             long long bytes) {
+  return make_rsrc(static_cast<const unsigned char*>(p) + base,
+                   (unsigned)min(bytes - base, (long long)kOOB - 1));
+}
+
 __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, unsigned off) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
@@ -262,7 +270,10 @@ using Loader =
 struct KernelArgs {
   const void* A;
   const void* B;
-  unsigned a_bytes, b_bytes;  // operand extents for the buffer resources (VEC)
+  // operand extents in bytes: the register-staged kernels address whole
+  // operands through buffer resources (VEC: extents below kOOB); the direct
+  // kernel bases its resources at each workgroup's panels
+  long long a_bytes, b_bytes;
   float* out;               // C, or the split partials
   long long lda, ldb, ldo;
   long long split_stride;   // elements between split outputs (0 when splits == 1)
@@ -577,8 +588,8 @@ __global__ __launch_bounds__(C::THREADS) void gemm_kernel(KernelArgs g) {
 
   Loader<C, C::BM, A_KC, SA, VEC> la;
   Loader<C, C::BN, B_KC, SB, VEC> lb;
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, g.a_bytes);
-  const __amdgpu_buffer_rsrc_t rb = make_rsrc(B, g.b_bytes);
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(A, (unsigned)g.a_bytes);
+  const __amdgpu_buffer_rsrc_t rb = make_rsrc(B, (unsigned)g.b_bytes);
   la.init(g.lda, m0, g.M, tid);
   lb.init(g.ldb, n0, g.N, tid);
 
@@ -717,8 +728,10 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4;
 constexpr int vm_wait(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
 
 // One operand's part of the direct loads: R tile rows, this wave's BPW
-// 1 KiB blocks.  off: byte offset at k0 = 0; kk: k (within a stage) of
-// the lane's data; oob: out-of-range bit for rows past the end (RC).
+// 1 KiB blocks.  off: byte offset at k0 = 0 from the panel's base (init:
+// row r0 of a K-contiguous operand, k-row kbase of a row-contiguous one, see
+// issue; init_rows: the operand's start); kk: k (within a stage) of the
+// lane's data; oob: out-of-range bit for rows past the end (RC).
 template <int R, bool RC, int BPW, int BK>
 struct DirectOperand {
   static constexpr int LPR = BK / 8;    // KC: 16-byte chunks (lanes) per row
@@ -738,7 +751,7 @@ struct DirectOperand {
         const int r = blk * RPB + lane / LPR;
         const int chunk = (lane % LPR) ^ swz(r);
         kk[j] = chunk * 8;
-        off[j] = (unsigned)(((long long)min(r0 + r, rows - 1) * ld + chunk * 8) * 2);
+        off[j] = (unsigned)(((long long)(min(r0 + r, rows - 1) - r0) * ld + chunk * 8) * 2);
         oob[j] = 0;  // rows past the end are clamped: they feed discarded outputs
       } else {
         constexpr int CPK = R / 8;  // 16-byte chunks per k-row
@@ -768,9 +781,11 @@ struct DirectOperand {
       oob[j] = gr >= 0 ? 0u : kOOB;
     }
   }
+  // Loads of the stage at k0 (RC: k-rows from kbase on lie at the panel's
+  // base; KC: the base holds k = 0).
   __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t rs, unsigned char* lds, int wave,
-                                        int k0, int kend, long long ld) const {
-    const unsigned dk = RC ? (unsigned)((long long)k0 * ld * 2) : (unsigned)(k0 * 2);
+                                        int k0, int kend, long long ld, int kbase) const {
+    const unsigned dk = RC ? (unsigned)((long long)(k0 - kbase) * ld * 2) : (unsigned)(k0 * 2);
 #pragma unroll
     for (int j = 0; j < BPW; ++j) {
       // past the end of K: an out-of-range offset, for which the hardware
@@ -819,8 +834,12 @@ __device__ __forceinline__ void direct_mainloop(unsigned char* smem, const OpA& 
   const int nk = (kend - kbeg + C::BK - 1) / C::BK;
   auto a_slot = [&](int kt) { return smem + (kt % SA) * C::A_OPB; };
   auto b_slot = [&](int kt) { return smem + SA * C::A_OPB + (kt % STAGES) * C::B_OPB; };
-  auto issue_a = [&](int kt) { la.issue(ra, a_slot(kt), wave, kbeg + kt * C::BK, kend, lda); };
-  auto issue_b = [&](int kt) { lb.issue(rb, b_slot(kt), wave, kbeg + kt * C::BK, kend, ldb); };
+  auto issue_a = [&](int kt) {
+    la.issue(ra, a_slot(kt), wave, kbeg + kt * C::BK, kend, lda, kbeg);
+  };
+  auto issue_b = [&](int kt) {
+    lb.issue(rb, b_slot(kt), wave, kbeg + kt * C::BK, kend, ldb, kbeg);
+  };
   auto issue = [&](int kt) {
     issue_a(kt);
     issue_b(kt);
@@ -959,8 +978,14 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
   const int wave = tid >> 6;
   const int wm0 = (wave / C::WAVES_N) * C::WM;
   const int wn0 = (wave % C::WAVES_N) * C::WN;
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(g.A, g.a_bytes);
-  const __amdgpu_buffer_rsrc_t rb = make_rsrc(g.B, g.b_bytes);
+  // Buffer resources based at this workgroup's panels: a K-contiguous
+  // operand at the tile's first row, a row-contiguous one at the split's
+  // first k-row.  The loaders' offsets count from there, so they stay below
+  // kOOB however large the operand is (the plan bounds the panels).
+  const __amdgpu_buffer_rsrc_t ra =
+      panel_rsrc(g.A, 2LL * (A_RC ? kbeg : m0) * g.lda, g.a_bytes);
+  const __amdgpu_buffer_rsrc_t rb =
+      panel_rsrc(g.B, 2LL * (B_RC ? kbeg : n0) * g.ldb, g.b_bytes);
 
   using OpA = DirectOperand<C::BM, A_RC, C::A_BPW, C::BK>;
   using OpB = DirectOperand<C::BN, B_RC, C::B_BPW, C::BK>;
@@ -1357,10 +1382,13 @@ int splits_for(const GemmDesc& g) {
 // the row count for RC) and the leading dimension are multiples of a chunk,
 // and an operand smaller than the out-of-range sentinel.
 template <class S>
-bool vec_ok(const void* p, long long ld, int contiguous_extent, long long bytes) {
+bool whole_chunks(const void* p, long long ld, int contiguous_extent) {
   constexpr int E = Src<S>::E;
-  return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % E == 0 &&
-         contiguous_extent % E == 0 && bytes > 0 && bytes < (long long)kOOB;
+  return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % E == 0 && contiguous_extent % E == 0;
+}
+template <class S>
+bool vec_ok(const void* p, long long ld, int contiguous_extent, long long bytes) {
+  return whole_chunks<S>(p, ld, contiguous_extent) && bytes > 0 && bytes < (long long)kOOB;
 }
 
 template <class C, bool A_KC, bool B_KC, class SA, class SB, bool VEC>
@@ -1420,8 +1448,8 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
                                     : (long long)(g.K - 1) * g.ldb + g.N);
   const bool vec = vec_ok<SA>(g.A, g.lda, A_KC ? g.K : g.M, a_bytes) &&
                    vec_ok<SB>(g.B, g.ldb, B_KC ? g.K : g.N, b_bytes);
-  a.a_bytes = vec ? (unsigned)a_bytes : 0u;
-  a.b_bytes = vec ? (unsigned)b_bytes : 0u;
+  a.a_bytes = vec ? a_bytes : 0;
+  a.b_bytes = vec ? b_bytes : 0;
   timing_before(g.label ? g.label : !g.b_kc ? (g.a_kc ? "gemm_nn" : "gemm_tn") : "gemm_nt", st);
   if (vec)
     launch_staged<C, A_KC, B_KC, SA, SB, true>(a, nwg, st);
@@ -1440,16 +1468,37 @@ long long operand_bytes(bool kc, int rows, int K, long long ld, int esz) {
   return (long long)esz * (kc ? (long long)(rows - 1) * ld + K : (long long)(K - 1) * ld + rows);
 }
 
+// The direct kernel addresses each operand from its workgroup's panel (a
+// tile's 256 rows of a K-contiguous operand, a split's k-rows of a
+// row-contiguous one) with 32-bit offsets below kOOB.  Bytes a panel spans:
+long long panel_bytes(bool kc, int rows, int K, long long ld, long long k_rows) {
+  return 2 * (kc ? (long long)(min(rows, 256) - 1) * ld + K : (k_rows - 1) * ld + rows);
+}
+// The largest K range (whole 64-k stages) whose row-contiguous panel fits;
+// 0 if not even one stage does.
+long long rc_max_k(int rows, long long ld) {
+  const long long room = (long long)kOOB - 1 - 2LL * rows;  // bytes for (k_rows - 1) * 2 ld
+  if (room < 0) return 0;
+  return ((room / (2 * ld) + 1) / 64) * 64;
+}
+bool split_allowed(const GemmDesc& g) { return !g.Cb && (!g.a_kc || g.kc_split); }
+
 // bf16 x bf16 operands whose 16-byte chunks are whole (the contiguous
-// extent and leading dimension are multiples of 8 elements) and that are
-// smaller than the out-of-range sentinel.  Layouts: both K-contiguous, both
-// row-contiguous, or A K-contiguous with B row-contiguous (dX = dU W).
+// extent and leading dimension are multiples of 8 elements) and whose
+// panels fit the 32-bit offsets: a K-contiguous operand's 256 rows, a
+// row-contiguous one's whole K when the product is not split, else one
+// 64-k stage (the split count then keeps each split's panel in range, see
+// direct_splits_cfg).  Layouts: both K-contiguous, both row-contiguous, or A
+// K-contiguous with B row-contiguous.
 bool direct_ok(const GemmDesc& g) {
   if (!g.bf16 || !g.a_bf16 || !g.b_bf16 || (!g.a_kc && g.b_kc)) return false;
-  const long long ab = operand_bytes(g.a_kc, g.M, g.K, g.lda, 2);
-  const long long bb = operand_bytes(g.b_kc, g.N, g.K, g.ldb, 2);
-  return vec_ok<uint16_t>(g.A, g.lda, g.a_kc ? g.K : g.M, ab) &&
-         vec_ok<uint16_t>(g.B, g.ldb, g.b_kc ? g.K : g.N, bb);
+  auto fits = [&](bool kc, int rows, long long ld) {
+    if (kc) return panel_bytes(true, rows, g.K, ld, 0) < (long long)kOOB;
+    return split_allowed(g) ? rc_max_k(rows, ld) >= 64 : rc_max_k(rows, ld) >= g.K;
+  };
+  return whole_chunks<uint16_t>(g.A, g.lda, g.a_kc ? g.K : g.M) &&
+         whole_chunks<uint16_t>(g.B, g.ldb, g.b_kc ? g.K : g.N) && g.M > 0 && g.N > 0 &&
+         g.K > 0 && fits(g.a_kc, g.M, g.lda) && fits(g.b_kc, g.N, g.ldb);
 }
 
 // Split count for the direct path: the K = tokens product (row-contiguous
@@ -1467,19 +1516,26 @@ bool direct_ok(const GemmDesc& g) {
 constexpr double kSplitBytesPerStep = 11.0 * (1 << 20);
 template <class C>
 int direct_splits_cfg(const GemmDesc& g) {
-  if (g.Cb || (g.a_kc && !g.kc_split)) return 1;
+  static_assert(C::BK == 64, "rc_max_k counts 64-k stages");
+  if (!split_allowed(g)) return 1;
   const long long tiles = (long long)((g.M + C::BM - 1) / C::BM) * ((g.N + C::BN - 1) / C::BN);
   const int kt = (g.K + C::BK - 1) / C::BK;
   const long long slots = C::OCC * 256LL;  // workgroups the CUs run at once
   const double out_bytes = 4.0 * g.M * g.N;
-  int best = 1;
+  // fewest splits whose row-contiguous panels fit (direct_ok: one stage does)
+  long long kmax = kt;
+  if (!g.a_kc) kmax = min(kmax, rc_max_k(g.M, g.lda) / C::BK);
+  if (!g.b_kc) kmax = min(kmax, rc_max_k(g.N, g.ldb) / C::BK);
+  kmax = max(kmax, 1LL);
+  const int s_min = (int)((kt + kmax - 1) / kmax);
+  int best = s_min;
   double best_cost = 0.0;
-  for (int s = 1; s <= max(1, kt / 8); ++s) {
+  for (int s = s_min; s <= max(s_min, kt / 8); ++s) {
     const long long rounds = (tiles * s + slots - 1) / slots;
     const int steps = (kt + s - 1) / s;
     const double cost =
         (double)(rounds * steps) + (s > 1 ? (s + 1) * out_bytes / kSplitBytesPerStep : 0.0);
-    if (s == 1 || cost < best_cost) {
+    if (s == s_min || cost < best_cost) {
       best = s;
       best_cost = cost;
     }
@@ -1545,8 +1601,8 @@ hipError_t launch_direct_cfg(const GemmDesc& g, hipStream_t st) {
   a.M = g.M;
   a.N = g.N;
   a.K = g.K;
-  a.a_bytes = (unsigned)operand_bytes(g.a_kc, g.M, g.K, g.lda, 2);
-  a.b_bytes = (unsigned)operand_bytes(g.b_kc, g.N, g.K, g.ldb, 2);
+  a.a_bytes = operand_bytes(g.a_kc, g.M, g.K, g.lda, 2);
+  a.b_bytes = operand_bytes(g.b_kc, g.N, g.K, g.ldb, 2);
   a.k_per_split = kps;
   a.tiles_m = (g.M + C::BM - 1) / C::BM;
   a.tiles_n = (g.N + C::BN - 1) / C::BN;
