@@ -57,6 +57,27 @@ def test_dw_split_count_read_from_the_workspace_plan():
     assert bench.dw_splits(sru.lib(), _w("sru6_L256_B64_d1024_bf16")) == 5
 
 
+@pytest.mark.parametrize("L,B,d", [(1024, 384, 1024), (4096, 1024, 2048), (16384, 256, 1024),
+                                   (65536, 64, 512)])
+def test_dw_split_panels_fit_buffer_offsets(L, B, d):
+    """The direct products address a split's panel of a row-contiguous
+    operand (dU [M, N] and X [M, d_in] in bf16, k-rows = tokens) with 32-bit
+    offsets from the split's first k-row.  The plan keeps every split's
+    panel below 2^31 bytes, raising the split count where the cost model
+    alone would not (4M tokens at d = 2048: 12.9 GB per split at its
+    preferred 4 splits)."""
+    w = bench_workload = type(_w("sru6_L256_B64_d1024_bf16"))(
+        f"big_L{L}_B{B}_d{d}", 1, 0, L, B, d, d, 1, True, None, True, 0)
+    s = bench.dw_splits(sru.lib(), bench_workload)
+    M, N = L * B, 3 * d
+    kt = -(-M // 64)
+    kps = -(-kt // s) * 64
+    for rows in (N, w.d_in):  # dU's and X's row lengths (elements)
+        assert (kps - 1) * rows * 2 + rows * 2 < 2 ** 31, (s, kps, rows)
+    if M * N * 2 >= 2 ** 31:
+        assert s > 1
+
+
 def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120, cwd=ROOT)
