@@ -13,9 +13,9 @@ namespace sru {
 // the four [nfeat] outputs, from q = qlo (the linear recurrence has no v:
 // qlo = 2).  partial == nullptr: nothing to do.
 struct VbSum {
-  const float* partial;
-  int rows, nfeat, qlo;
-  float* out[4];
+  const float* partial = nullptr;
+  int rows = 0, nfeat = 0, qlo = 0;
+  float* out[4] = {nullptr, nullptr, nullptr, nullptr};
 };
 // Blocks of 256 threads the sums take (64 outputs per block).
 inline int vb_sum_blocks(const VbSum& v) { return ((4 - v.qlo) * v.nfeat + 63) / 64; }
