@@ -522,6 +522,14 @@ def main():
     dev = torch.device("cuda:0")
     to = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(dev)
     layers = [{k: to(v) for k, v in p.items()} for p in inp["layers"]]
+    # inference with bf16 products holds its weights in bf16, rounded once
+    # (by the library) before the timed steps; training rounds them every
+    # step, since the optimizer changes them
+    held_bf16 = not w.backward and w.gemm_dtype == sru.GEMM_BF16
+    if held_bf16:
+        for p in layers:
+            if "W" in p:
+                p["W"] = sru.round_bf16(p["W"])
     X, dH, mask = to(inp["X"]), to(inp["dH"]), to(inp["mask"])
     st = sru.Stack(layers, w.L, w.B, w.d_in, w.d, w.direction, w.gemm_dtype, dev,
                    backward=w.backward, highway_scale=args.highway_scale,
@@ -662,6 +670,10 @@ def main():
                    "direction": ["forward", "reverse", "bidirectional"][w.direction],
                    "passes": "fwd+bwd" if w.backward else "fwd",
                    "gemm": "bf16 operands, fp32 accumulate" if w.gemm_dtype else "fp32",
+                   "weights": ("bf16, rounded once before the timed steps (inference)"
+                               if held_bf16 else
+                               "fp32, rounded to bf16 in every step" if w.gemm_dtype
+                               else "fp32"),
                    "scan": "fp32", "tokens_per_step": w.tokens, "global_batch": w.B,
                    "valid_tokens_per_step": valid,
                    "highway_scale": args.highway_scale,

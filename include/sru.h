@@ -150,6 +150,10 @@ SRU_API size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int d
  *        layer below; it must equal that rounding of X (it replaces X as the
  *        projection operand).  NULL: X is rounded into the workspace.
  *        W_bf16 [N, d_in] out -- Wcat rounded to bf16, for sru_backward.
+ *        With W = NULL it is an input instead: the weights already rounded
+ *        (e.g. held in bf16 across inference calls, rounded once with
+ *        sru_round_bf16); the forward reads them and rounds nothing.  A
+ *        NULL W with a NULL W_bf16, or in fp32 mode, is SRU_E_NULLPTR.
  *        H_bf16 [L, B, ndir*d] out -- H rounded to bf16 (the next layer's
  *        X_bf16).
  */
@@ -203,7 +207,9 @@ SRU_API int sru_forward_noalloc(const float* X, const float* W,
  *   bf16 companions (SRU_GEMM_BF16 only, else NULL; each may be NULL; as
  *   in sru_forward): X_bf16 = X rounded to bf16; W_bf16 = Wcat rounded to
  *   bf16 (the W_bf16 sru_forward wrote; the dX product reads its transposed
- *   copy, made in the workspace).  NULL: rounded into the workspace.
+ *   copy, made in the workspace).  NULL: rounded into the workspace.  W
+ *   may be NULL when W_bf16 is given (weights held in bf16, as in
+ *   sru_forward); dW is still written in fp32.
  */
 SRU_API int sru_backward(const float* X, const float* W,
                  const float* v_f, const float* v_r, const float* b_f, const float* b_r,

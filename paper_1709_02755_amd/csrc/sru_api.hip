@@ -395,7 +395,7 @@ const char* sru_status_string(int status) {
 
 int sru_last_hip_error(void) { return g_last_hip_error; }
 
-int sru_version(void) { return (1 << 16) | 3; }
+int sru_version(void) { return (1 << 16) | 4; }
 
 size_t sru_forward_workspace_bytes(int L, int B, int d_in, int d, int direction, int gemm_dtype) {
   Dims s;
@@ -431,7 +431,11 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
   // U may be omitted only where the fused projection + scan applies
   // (inference with bf16 products: C omitted too)
   const bool fused = !U && fused_ok(s, gemm_dtype) && !C;
-  if (!X || !W || missing_v(op, v_f, v_r) || !b_f || !b_r || (!U && !fused) || !H)
+  // bf16 products may take the weights already rounded: W = NULL, and
+  // W_bf16 is then the input
+  const bool w_rounded = !W && W_bf16 && gemm_dtype == SRU_GEMM_BF16;
+  if (!X || (!W && !w_rounded) || missing_v(op, v_f, v_r) || !b_f || !b_r ||
+      (!U && !fused) || !H)
     return SRU_E_NULLPTR;
   const void* ptrs[] = {X, W, v_f, v_r, b_f, b_r, c0, U, H, C, c_last};
   for (const void* p : ptrs)
@@ -446,13 +450,17 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
   }
 
   // U = X Wcat^T (Sec. 3.1).  bf16 mode: W and X rounded once (into
-  // W_bf16 / the workspace, unless the caller holds X_bf16), so both
-  // operands of the product are K-contiguous bf16.
+  // W_bf16 / the workspace, unless the caller holds X_bf16 or passes the
+  // weights rounded), so both operands of the product are K-contiguous bf16.
   const void* Wop = W;
   const void* Xop = X;
   if (bf16) {
     uint16_t* wb = W_bf16 ? W_bf16 : static_cast<uint16_t*>(workspace);
-    if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wb, false, stream, "bf16_w"))) return e;
+    if (!w_rounded) {
+      if (int e = hip_status(sru::to_bf16_launch(W, (int)s.N, d_in, wb, false, stream,
+                                                 "bf16_w")))
+        return e;
+    }
     Wop = wb;
     if (X_bf16) {
       Xop = X_bf16;
@@ -536,7 +544,9 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   if (!valid_dtype(gemm_dtype)) return SRU_E_FLAG;
   Opts op;
   if (int e = read_options(options, op)) return e;
-  if (!X || !W || missing_v(op, v_f, v_r) || !b_f || !b_r || !U || !C || !dH || !dX || !dW ||
+  // weights already rounded (bf16 products): W = NULL with W_bf16 given
+  const bool w_ok = W || (W_bf16 && gemm_dtype == SRU_GEMM_BF16);
+  if (!X || !w_ok || missing_v(op, v_f, v_r) || !b_f || !b_r || !U || !C || !dH || !dX || !dW ||
       missing_v(op, dv_f, dv_r) || !db_f || !db_r)
     return SRU_E_NULLPTR;
   const void* ptrs[] = {X, W, v_f, v_r, b_f, b_r, c0, U, C, dH, dc_last, dX, dW, dv_f, dv_r,

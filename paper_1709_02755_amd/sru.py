@@ -177,7 +177,7 @@ def dims(X, W):
     return L, B, d_in, d, ndir, k
 
 
-def _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask):
+def _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask, gemm_dtype=GEMM_FP32):
     for n, t, nd in (("X", X, 3), ("W", W, 4)):
         if not isinstance(t, torch.Tensor) or t.dim() != nd:
             raise ValueError(f"{n} must be a {nd}-d tensor")
@@ -187,7 +187,11 @@ def _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask):
     if ndir != want_nd or k != (3 if d_in == d else 4):
         raise ValueError(f"W shape {tuple(W.shape)} does not fit d_in={d_in}, direction={direction}")
     dv = X.device
-    _req(W, "W", (ndir, k, d, d_in), device=dv)
+    # bf16 products take the weights already rounded as a bfloat16 W
+    w_dtype = torch.bfloat16 if W.dtype == torch.bfloat16 else torch.float32
+    if w_dtype == torch.bfloat16 and gemm_dtype != GEMM_BF16:
+        raise ValueError("a bfloat16 W needs bf16 products (gemm_dtype=GEMM_BF16)")
+    _req(W, "W", (ndir, k, d, d_in), dtype=w_dtype, device=dv)
     for n, t in (("v_f", v_f), ("v_r", v_r)):
         _req(t, n, (ndir, d), optional=True, device=dv)  # the library reports a missing v
     for n, t in (("b_f", b_f), ("b_r", b_r)):
@@ -195,6 +199,16 @@ def _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask):
     _req(c0, "c0", (B, ndir * d), optional=True, device=dv)
     _req(mask, "mask", (L, B), dtype=torch.uint8, optional=True, device=dv)
     return L, B, d_in, d, ndir, k
+
+
+def _weights(W, W_bf16):
+    """(W, W_bf16) as the library takes them: a bfloat16 W is the rounded
+    weights, passed as W_bf16 with W = NULL."""
+    if W.dtype != torch.bfloat16:
+        return W, W_bf16
+    if W_bf16 is not None:
+        raise ValueError("W is already bfloat16: pass no W_bf16 beside it")
+    return None, W
 
 
 def forward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype):
@@ -224,8 +238,11 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
 
     bf16 GEMMs only: X_bf16 (torch.bfloat16, X rounded) replaces the
     rounding of X; entries W_bf16 / H_bf16 of `out` (bfloat16 tensors), if
-    present, receive Wcat and H rounded to bf16."""
-    L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask)
+    present, receive Wcat and H rounded to bf16.  W itself may be bfloat16:
+    the weights already rounded (e.g. by round_bf16, held across inference
+    calls), read as they are; `out` then takes no W_bf16."""
+    L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask,
+                                           gemm_dtype)
     dv = X.device
     _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True, device=dv)
     if out is None:
@@ -240,12 +257,13 @@ def forward(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=None,
                        C=((L, B, ndir * d), f32, False), c_last=((B, ndir * d), f32, False),
                        W_bf16=(tuple(W.shape), b16, False),
                        H_bf16=((L, B, ndir * d), b16, False)), dv)
+    Wf, Wb = _weights(W, out.get("W_bf16"))
     ws, nbytes = _ws(ws, forward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype), dv)
-    st = lib().sru_forward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
-                           L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
+    st = lib().sru_forward(_ptr(X), _ptr(Wf), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r),
+                           _ptr(c0), L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
                            _options(highway_scale, reset_new, linear),
                            _ptr(out.get("U")), _ptr(out["H"]), _ptr(out.get("C")),
-                           _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("W_bf16")),
+                           _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(Wb),
                            _ptr(out.get("H_bf16")), _ptr(ws), nbytes, _stream())
     _check(st, "sru_forward")
     return out
@@ -261,7 +279,8 @@ def forward_noalloc(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=N
     from a static device array instead of a caller buffer.  `out` (as for
     forward(); U may be None where fused_available() says so and C is None)
     is required too, so the call allocates nothing."""
-    L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask)
+    L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask,
+                                           gemm_dtype)
     dv = X.device
     _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True, device=dv)
     if out is None:
@@ -271,11 +290,12 @@ def forward_noalloc(X, W, v_f, v_r, b_f, b_r, c0=None, direction=DIR_FWD, mask=N
                        C=((L, B, ndir * d), f32, False), c_last=((B, ndir * d), f32, False),
                        W_bf16=(tuple(W.shape), b16, False),
                        H_bf16=((L, B, ndir * d), b16, False)), dv)
-    st = lib().sru_forward_noalloc(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r),
-                                   _ptr(c0), L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
-                                   _options(highway_scale, reset_new, linear),
+    Wf, Wb = _weights(W, out.get("W_bf16"))
+    st = lib().sru_forward_noalloc(_ptr(X), _ptr(Wf), _ptr(v_f), _ptr(v_r), _ptr(b_f),
+                                   _ptr(b_r), _ptr(c0), L, B, d_in, d, direction, _ptr(mask),
+                                   gemm_dtype, _options(highway_scale, reset_new, linear),
                                    _ptr(out.get("U")), _ptr(out["H"]), _ptr(out.get("C")),
-                                   _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(out.get("W_bf16")),
+                                   _ptr(out.get("c_last")), _ptr(X_bf16), _ptr(Wb),
                                    _ptr(out.get("H_bf16")), _stream())
     _check(st, "sru_forward_noalloc")
     return out
@@ -287,8 +307,10 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
     """One layer backward; returns dict(dX, dW, dv_f, dv_r, db_f, db_r, dc0).
 
     bf16 GEMMs only: X_bf16 / W_bf16 (bfloat16 roundings of X and Wcat, as
-    forward() writes them) replace the library's own rounding."""
-    L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask)
+    forward() writes them) replace the library's own rounding; a bfloat16 W
+    (the weights held rounded) takes W_bf16's place.  dW is fp32 either way."""
+    L, B, d_in, d, ndir, k = _check_params(X, W, v_f, v_r, b_f, b_r, c0, direction, mask,
+                                           gemm_dtype)
     dv = X.device
     _req(X_bf16, "X_bf16", (L, B, d_in), dtype=torch.bfloat16, optional=True, device=dv)
     _req(W_bf16, "W_bf16", tuple(W.shape), dtype=torch.bfloat16, optional=True, device=dv)
@@ -297,7 +319,7 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
     _req(dH, "dH", (L, B, ndir * d), device=dv)
     _req(dc_last, "dc_last", (B, ndir * d), optional=True, device=dv)
     if out is None:
-        out = dict(dX=torch.empty_like(X), dW=torch.empty_like(W),
+        out = dict(dX=torch.empty_like(X), dW=torch.empty(tuple(W.shape), device=dv),
                    dv_f=None if linear else torch.empty((ndir, d), device=dv),
                    dv_r=None if linear else torch.empty((ndir, d), device=dv),
                    db_f=torch.empty((ndir, d), device=dv), db_r=torch.empty((ndir, d), device=dv),
@@ -307,14 +329,16 @@ def backward(X, W, v_f, v_r, b_f, b_r, U, C, dH, c0=None, dc_last=None, directio
     _req_out(out, dict(dX=(tuple(X.shape), f32, True), dW=(tuple(W.shape), f32, True),
                        dv_f=vec, dv_r=vec, db_f=((ndir, d), f32, True),
                        db_r=((ndir, d), f32, True), dc0=((B, ndir * d), f32, False)), dv)
+    Wf, Wb = _weights(W, W_bf16)
     ws, nbytes = _ws(ws, backward_workspace_bytes(L, B, d_in, d, direction, gemm_dtype), dv)
-    st = lib().sru_backward(_ptr(X), _ptr(W), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r), _ptr(c0),
-                            L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
+    st = lib().sru_backward(_ptr(X), _ptr(Wf), _ptr(v_f), _ptr(v_r), _ptr(b_f), _ptr(b_r),
+                            _ptr(c0), L, B, d_in, d, direction, _ptr(mask), gemm_dtype,
                             _options(highway_scale, reset_new, linear),
                             _ptr(U), _ptr(C), _ptr(dH), _ptr(dc_last),
-                            _ptr(out["dX"]), _ptr(out["dW"]), _ptr(out.get("dv_f")), _ptr(out.get("dv_r")),
-                            _ptr(out["db_f"]), _ptr(out["db_r"]), _ptr(out.get("dc0")),
-                            _ptr(X_bf16), _ptr(W_bf16), _ptr(ws), nbytes, _stream())
+                            _ptr(out["dX"]), _ptr(out["dW"]), _ptr(out.get("dv_f")),
+                            _ptr(out.get("dv_r")), _ptr(out["db_f"]), _ptr(out["db_r"]),
+                            _ptr(out.get("dc0")), _ptr(X_bf16), _ptr(Wb), _ptr(ws), nbytes,
+                            _stream())
     _check(st, "sru_backward")
     return out
 
@@ -540,7 +564,8 @@ class Stack:
     the top layer) and of Wcat (dense) or T (low-rank): the next layer's
     projection and the backward products read those instead of rounding the
     same values again.  Without a backward pass, store_c=False skips the
-    states C (inference).
+    states C (inference).  With bf16 GEMMs a dense layer's W may be held in
+    bfloat16 (rounded once, e.g. for inference): it is then read as it is.
     """
 
     def __init__(self, layers, L, B, d_in, d, direction, gemm_dtype, device, backward=True,
@@ -572,7 +597,7 @@ class Stack:
                 o["T"] = torch.empty((L, B, dp), device=device)
                 if gemm_dtype == GEMM_BF16:
                     o["T_bf16"] = torch.empty((L, B, dp), **bf)
-            elif gemm_dtype == GEMM_BF16:
+            elif gemm_dtype == GEMM_BF16 and p["W"].dtype != torch.bfloat16:
                 o["W_bf16"] = torch.empty(tuple(p["W"].shape), **bf)
             if gemm_dtype == GEMM_BF16 and li + 1 < len(layers):
                 o["H_bf16"] = torch.empty((L, B, ndir * d), **bf)  # the next layer's operand
@@ -589,7 +614,7 @@ class Stack:
                     ws_bytes = max(ws_bytes, lib().sru_backward_lowrank_workspace_bytes(
                         L, B, din, d, dp, direction, gemm_dtype))
                 else:
-                    g["dW"] = torch.empty_like(p["W"])
+                    g["dW"] = torch.empty(tuple(p["W"].shape), device=device)
                     ws_bytes = max(ws_bytes, backward_workspace_bytes(L, B, din, d, direction,
                                                                       gemm_dtype))
                 self.bw.append(g)

@@ -320,3 +320,16 @@ def test_noalloc_forward_refuses_what_its_scratch_cannot_hold():
     assert _fwd_noalloc(lib, L=0) == E_SHAPE
     assert _fwd_noalloc(lib, direction=7) == E_FLAG
     assert _fwd_noalloc(lib, gemm=9) == E_FLAG
+
+
+def test_weights_held_in_bf16():
+    """bf16 products may take the weights already rounded: W = NULL with
+    W_bf16 given (the calls go on to the next check).  A NULL W without
+    W_bf16, or with fp32 products, is still a missing pointer."""
+    lib = sru.lib()
+    assert _fwd(lib, W=None, Wb=FAKE, gemm=1, H=FAKE_MIS) == E_ALIGN
+    assert _bwd(lib, W=None, Wb=FAKE, gemm=1) == E_WS
+    assert _fwd(lib, W=None, gemm=1) == E_NULL
+    assert _bwd(lib, W=None, gemm=1) == E_NULL
+    assert _fwd(lib, W=None, Wb=FAKE, gemm=0) == E_NULL
+    assert _bwd(lib, W=None, Wb=FAKE, gemm=0) == E_NULL

@@ -268,3 +268,29 @@ def test_undersized_workspace_reaches_the_library_check(monkeypatch):
     with pytest.raises(sru.SruError, match="WORKSPACE"):
         sru.forward(X, W, *p, gemm_dtype=sru.GEMM_BF16,
                     ws=torch.zeros(need_f - 256, dtype=torch.uint8))
+
+
+def test_bf16_weights_passed_as_the_rounded_input(stub):
+    """A bfloat16 W (weights held rounded) goes to the library as W_bf16 with
+    W = NULL; it needs bf16 products and takes no second W_bf16; dW stays
+    fp32."""
+    a = fwd_args()
+    Wb = z(1, 3, D, D, dtype=torch.bfloat16)
+    a["W"], a["gemm"] = Wb, sru.GEMM_BF16
+    run_forward(a)
+    name, args = stub.calls[-1]
+    assert name == "sru_forward" and args[1] is None and args[20].value == Wb.data_ptr()
+    with pytest.raises(ValueError, match="bf16 products"):
+        run_forward(dict(a, gemm=sru.GEMM_FP32))
+    with pytest.raises(ValueError, match="already bfloat16"):
+        run_forward(dict(a, out=dict(H=z(L, B, D), W_bf16=z(1, 3, D, D, dtype=torch.bfloat16))))
+    X, p = a["X"], [z(1, D) for _ in range(4)]
+    bw = sru.backward(X, Wb, *p, z(L, B, 1, 3, D), z(L, B, D), z(L, B, D),
+                      gemm_dtype=sru.GEMM_BF16)
+    name, args = stub.calls[-1]
+    assert name == "sru_backward" and args[1] is None and args[27].value == Wb.data_ptr()
+    assert bw["dW"].dtype == F32
+    with pytest.raises(ValueError, match="already bfloat16"):
+        sru.backward(X, Wb, *p, z(L, B, 1, 3, D), z(L, B, D), z(L, B, D),
+                     gemm_dtype=sru.GEMM_BF16, W_bf16=Wb)
+    assert [c[0] for c in stub.calls] == ["sru_forward", "sru_backward"]

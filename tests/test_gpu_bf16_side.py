@@ -4,7 +4,8 @@ X and Wcat instead of rounding them again.  A copy that equals the library's
 own rounding must give bit-identical results; the copies it writes must be
 exactly the round-to-nearest-even bf16 of Wcat and H; and the Stack, which
 wires H_bf16 of one layer into the next, must equal per-layer calls without
-companions."""
+companions.  Weights held in bf16 (a bfloat16 W, passed as the W_bf16 input
+with W = NULL) give the same bits as fp32 weights rounded by the library."""
 
 import numpy as np
 import pytest
@@ -69,11 +70,19 @@ def test_companions_bit_identical(case):
     bw1 = sru.backward(X, W, *p, *args, X_bf16=X.to(torch.bfloat16), W_bf16=fw1["W_bf16"], **bkw)
     bw2 = sru.backward(X, W, *p, *args, W_bf16=fw1["W_bf16"], **bkw)
     torch.cuda.synchronize()
+    # the weights held in bf16 (W = NULL, W_bf16 read as the input)
+    Wb = sru.round_bf16(W)
+    fw3 = sru.forward(X, Wb, *p, **kw)
+    bw3 = sru.backward(X, Wb, *p, *args, **bkw)
+    torch.cuda.synchronize()
+    for key in ("U", "H", "C", "c_last"):
+        assert torch.equal(fw0[key], fw3[key]), key
     for key in bw0:
         if bw0[key] is None:
             continue
         assert torch.equal(bw0[key], bw1[key]), key
         assert torch.equal(bw0[key], bw2[key]), key
+        assert torch.equal(bw0[key], bw3[key]), key
 
 
 def test_stack_wiring_equals_plain_calls():
@@ -106,6 +115,32 @@ def test_stack_wiring_equals_plain_calls():
     for li in range(layers):
         for key, v in grads[li].items():
             assert torch.equal(v, ref[li][key]), (li, key)
+
+
+def test_inference_stack_with_bf16_weights():
+    """Inference at the fused kernel's shape (k = 4, L <= 64) with the
+    weights held in bf16 (rounded once) equals the stack that rounds them on
+    every call, bit for bit; so does the allocation-free forward."""
+    L, B, d_in, d = 24, 10, 64, 128
+    rng = np.random.default_rng(17)
+    c = random_layer_case(rng, L, B, d_in, d, O.DIR_BI, masked=True, bias_scale=0.5)
+    X, mask = dev(c["X"]), dev(c["mask"])
+    p = {k: dev(c[k]) for k in ("W", "v_f", "v_r", "b_f", "b_r")}
+    assert sru.fused_available(L, B, d_in, d, O.DIR_BI, O.GEMM_BF16)
+    a = sru.Stack([p], L, B, d_in, d, O.DIR_BI, O.GEMM_BF16, torch.device("cuda"),
+                  backward=False, store_c=False)
+    b = sru.Stack([dict(p, W=sru.round_bf16(p["W"]))], L, B, d_in, d, O.DIR_BI, O.GEMM_BF16,
+                  torch.device("cuda"), backward=False, store_c=False)
+    Ha = a.forward(X, mask).clone()
+    Hb = b.forward(X, mask).clone()
+    out = dict(H=torch.empty_like(Ha), c_last=torch.empty((B, 2 * d), device="cuda"))
+    sru.forward_noalloc(X, b.layers[0]["W"], p["v_f"], p["v_r"], p["b_f"], p["b_r"],
+                        direction=O.DIR_BI, mask=mask, gemm_dtype=O.GEMM_BF16, out=out)
+    torch.cuda.synchronize()
+    assert a.fw[0]["U"] is None and b.fw[0]["U"] is None  # the fused kernel ran
+    assert torch.equal(Ha, Hb)
+    assert torch.equal(Ha, out["H"])
+    assert torch.equal(a.fw[0]["c_last"], out["c_last"])
 
 
 @pytest.mark.parametrize("n", [1, 7, 8, 4099, 1 << 20])
