@@ -199,23 +199,34 @@ def test_layers_on_two_streams_equal_serial():
 
 
 @pytest.mark.parametrize("case", [
-    (256, 8, 1024, 1024, O.DIR_FWD, False, O.GEMM_BF16),  # dW split: sums in its split-K sum
-    (64, 16, 512, 512, O.DIR_FWD, True, O.GEMM_BF16),
-    (50, 6, 256, 128, O.DIR_BI, True, O.GEMM_FP32),
-    (3, 2, 5, 5, O.DIR_REV, True, O.GEMM_FP32),           # dW not split: their own launch
+    (256, 8, 1024, 1024, O.DIR_FWD, False, O.GEMM_BF16, False),  # dW split: in its split-K sum
+    (64, 16, 512, 512, O.DIR_FWD, True, O.GEMM_BF16, False),
+    (50, 6, 256, 128, O.DIR_BI, True, O.GEMM_FP32, False),
+    (3, 2, 5, 5, O.DIR_REV, True, O.GEMM_FP32, False),           # dW not split: own launch
+    # the linear recurrence: b sums only, over (time segment, sequence) rows
+    (2000, 4, 64, 64, O.DIR_FWD, True, O.GEMM_BF16, True),
+    (400, 2, 64, 64, O.DIR_BI, True, O.GEMM_FP32, True),
 ])
 def test_vb_sums_same_bits_as_standalone_scan(case):
     """The layer backward sums the v/b gradients over the batch inside the
     dW product's launches; the standalone backward scan sums them in its own
     launch.  Both run the same fixed-order sum: identical bits."""
-    L, B, d_in, d, direction, masked, gemm = case
-    print(f"vb sums L={L} B={B} d_in={d_in} d={d} dir={direction} gemm={gemm}", flush=True)
+    L, B, d_in, d, direction, masked, gemm, linear = case
+    print(f"vb sums L={L} B={B} d_in={d_in} d={d} dir={direction} gemm={gemm} "
+          f"linear={linear}", flush=True)
     c = random_layer_case(np.random.default_rng(5 * L + d), L, B, d_in, d, direction,
                           masked=masked, c0=True, dc_last=True, bias_scale=0.5)
-    fw, bw = run_layer(c, direction, gemm)
+    X, W = dev(c["X"]), dev(c["W"])
     p = [dev(c[k]) for k in ("v_f", "v_r", "b_f", "b_r")]
-    sb = sru.scan_backward(fw["U"], dev(c["X"]), fw["C"], dev(c["dH"]), *p, c0=dev(c["c0"]),
-                           dc_last=dev(c["dc_last"]), direction=direction, mask=dev(c["mask"]))
+    kw = dict(c0=dev(c["c0"]), direction=direction, mask=dev(c["mask"]), linear=linear)
+    fw = sru.forward(X, W, *p, gemm_dtype=gemm, **kw)
+    bw = sru.backward(X, W, *p, fw["U"], fw["C"], dev(c["dH"]), dc_last=dev(c["dc_last"]),
+                      gemm_dtype=gemm, **kw)
+    sb = sru.scan_backward(fw["U"], X, fw["C"], dev(c["dH"]), *p, dc_last=dev(c["dc_last"]),
+                           **kw)
     torch.cuda.synchronize()
     for k in ("dv_f", "dv_r", "db_f", "db_r", "dc0"):
+        if linear and k in ("dv_f", "dv_r"):
+            assert bw[k] is None and sb[k] is None
+            continue
         assert torch.equal(bw[k], sb[k]), k
