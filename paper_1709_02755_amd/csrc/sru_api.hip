@@ -195,8 +195,11 @@ struct BwdLayout {
 // bf16 Wcat^T.  Its tiles can be too few to fill the CUs (d_in of a few
 // hundred, or few tokens: one GPU's share of a batch), so it may be split
 // over K; the launcher's plan decides.
+// With k = 3 the product adds every direction's highway gradient dxh.  The
+// addend is part of the descriptor the workspace is sized from, since it
+// decides the tile shape and with it the split count.
 sru::GemmDesc dx_desc(const Dims& s, bool bf16, const void* dU, const void* W, const void* wt,
-                      float* dX) {
+                      float* dX, const float* dxh) {
   sru::GemmDesc g = bf16 ? gemm_desc(SRU_OP_NT, true, (int)s.M, s.d_in, (int)s.N, dU, s.N, wt,
                                      s.N, dX, s.d_in)
                          : gemm_desc(SRU_OP_NN, false, (int)s.M, s.d_in, (int)s.N, dU, s.N, W,
@@ -204,6 +207,12 @@ sru::GemmDesc dx_desc(const Dims& s, bool bf16, const void* dU, const void* W, c
   g.a_bf16 = g.b_bf16 = bf16;
   g.kc_split = true;
   g.label = "gemm_dx";
+  if (s.k == 3) {
+    g.add = dxh;
+    g.add_ld = s.nfeat;
+    g.add_off = s.d;
+    g.add_count = s.ndir;
+  }
   return g;
 }
 
@@ -222,7 +231,7 @@ BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
   w.xb = off;
   if (bf16) off += align_up(2 * (size_t)s.M * (size_t)s.d_in);
   w.splits = sru::gemm_splits(dw_desc(s, bf16, nullptr, nullptr, nullptr));
-  w.splits_dx = sru::gemm_splits(dx_desc(s, bf16, nullptr, nullptr, nullptr, nullptr));
+  w.splits_dx = sru::gemm_splits(dx_desc(s, bf16, nullptr, nullptr, nullptr, nullptr, nullptr));
   w.splitk = off;  // shared by the dX and dW partials (they run one after the other)
   off += align_up(std::max(sru::gemm_partial_bytes((int)s.N, s.d_in, w.splits),
                            sru::gemm_partial_bytes((int)s.M, s.d_in, w.splits_dx)));
@@ -595,16 +604,10 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
         : sru::to_bf16_t_launch(W, false, (int)s.N, d_in, wt, stream, "bf16_wt");
     if (int e = hip_status(te)) return e;
   }
-  sru::GemmDesc gx = dx_desc(s, bf16, dU, W, wt, dX);
+  sru::GemmDesc gx = dx_desc(s, bf16, dU, W, wt, dX, dxh);
   gx.partials = splitk;
   // split as planned, else (a plan that differs at run time) not at all
   if (sru::gemm_splits(gx) > lay.splits_dx) gx.kc_split = false;
-  if (s.k == 3) {
-    gx.add = dxh;
-    gx.add_ld = s.nfeat;
-    gx.add_off = d;
-    gx.add_count = s.ndir;
-  }
   if (int e = hip_status(sru::gemm_launch(gx, stream))) return e;
 
   // 3. dW = dU^T X (reduction over all tokens, split over K).  bf16 mode: X

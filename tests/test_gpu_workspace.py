@@ -1,0 +1,81 @@
+"""The library's writes stay inside the workspace it asks for.  The dX
+product may be split over K; the split partials sit at the end of the
+backward workspace, sized from the same product descriptor the launch
+uses (with the highway addend, which decides the tile shape and with it
+the split count).  Each case runs the backward on a workspace followed by a
+guard region and checks that the guard is untouched and that the results
+equal those of a run on a workspace of exactly the queried size."""
+
+import numpy as np
+import pytest
+import torch
+
+from helpers import dev
+from oracle import sru_oracle as O
+from paper_1709_02755_amd import sru
+from paper_1709_02755_amd.workloads import random_layer_case
+
+pytestmark = pytest.mark.gpu
+
+GUARD = 16 << 20
+FILL = 0xA5
+
+
+@pytest.mark.parametrize("L,B,d,direction", [
+    (256, 16, 1024, O.DIR_FWD),   # dX split 4 ways on 256 x 256 tiles, dW 5 ways
+    (96, 8, 1024, O.DIR_BI),      # two addends (both directions' highway gradients)
+    (128, 8, 2048, O.DIR_FWD),
+    (256, 8, 1024, O.DIR_FWD),    # one GPU's shard of the headline batch
+])
+def test_backward_stays_inside_its_workspace(L, B, d, direction):
+    print(f"workspace guard L={L} B={B} d={d} dir={direction}", flush=True)
+    c = random_layer_case(np.random.default_rng(L + B + d), L, B, d, d, direction,
+                          masked=False, bias_scale=0.5)
+    X, W = dev(c["X"]), dev(c["W"])
+    p = [dev(c[k]) for k in ("v_f", "v_r", "b_f", "b_r")]
+    kw = dict(direction=direction, gemm_dtype=O.GEMM_BF16)
+    fw = sru.forward(X, W, *p, **kw)
+    need = sru.backward_workspace_bytes(L, B, d, d, direction, O.GEMM_BF16)
+    buf = torch.full((need + GUARD,), FILL, dtype=torch.uint8, device="cuda")
+    bw = sru.backward(X, W, *p, fw["U"], fw["C"], dev(c["dH"]), ws=buf[:need], **kw)
+    ref = sru.backward(X, W, *p, fw["U"], fw["C"], dev(c["dH"]),
+                       ws=torch.empty(need, dtype=torch.uint8, device="cuda"), **kw)
+    torch.cuda.synchronize()
+    assert bool(torch.all(buf[need:] == FILL)), "a kernel wrote past the workspace"
+    for k in ("dX", "dW", "dv_f", "dv_r", "db_f", "db_r", "dc0"):
+        assert torch.equal(bw[k], ref[k]), k
+
+
+@pytest.mark.parametrize("linear", [False, True])
+def test_forward_and_lowrank_backward_stay_inside(linear):
+    """The same guard for the forward (bf16 operand copies, the linear
+    recurrence's segment maps) and the low-rank backward (dP and dQ split)."""
+    L, B, d_in, d, dp = 128, 12, 512, 512, 128
+    print(f"workspace guard fwd + lowrank L={L} B={B} d={d} dp={dp} linear={linear}", flush=True)
+    rng = np.random.default_rng(31)
+    c = random_layer_case(rng, L, B, d_in, d, O.DIR_FWD, masked=True, bias_scale=0.5)
+    X = dev(c["X"])
+    p = [dev(c[k]) for k in ("v_f", "v_r", "b_f", "b_r")]
+    Q = dev((rng.uniform(-1, 1, (d_in, dp)) * np.sqrt(3.0 / d_in)).astype(np.float32))
+    P = dev((rng.uniform(-1, 1, (1, 3, d, dp)) * np.sqrt(3.0 / dp)).astype(np.float32))
+    kw = dict(mask=dev(c["mask"]), gemm_dtype=O.GEMM_BF16, linear=linear)
+    lib = sru.lib()
+
+    need_f = sru.forward_workspace_bytes(L, B, d_in, d, O.DIR_FWD, O.GEMM_BF16)
+    buf = torch.full((need_f + GUARD,), FILL, dtype=torch.uint8, device="cuda")
+    fw = sru.forward(X, dev(c["W"]), *p, ws=buf[:need_f], **kw)
+    torch.cuda.synchronize()
+    assert bool(torch.all(buf[need_f:] == FILL)), "the forward wrote past its workspace"
+
+    need_lf = lib.sru_forward_lowrank_workspace_bytes(L, B, d_in, d, dp, O.DIR_FWD, O.GEMM_BF16)
+    need_lb = lib.sru_backward_lowrank_workspace_bytes(L, B, d_in, d, dp, O.DIR_FWD, O.GEMM_BF16)
+    lf = sru.forward_lowrank(X, Q, P, *p, **kw)
+    buf = torch.full((need_lb + GUARD,), FILL, dtype=torch.uint8, device="cuda")
+    lb = sru.backward_lowrank(X, Q, P, *p, lf["T"], lf["U"], lf["C"], dev(c["dH"]),
+                              ws=buf[:need_lb], **kw)
+    ref = sru.backward_lowrank(X, Q, P, *p, lf["T"], lf["U"], lf["C"], dev(c["dH"]), **kw)
+    torch.cuda.synchronize()
+    assert need_lf > 0 and fw["H"] is not None
+    assert bool(torch.all(buf[need_lb:] == FILL)), "the low-rank backward wrote past its workspace"
+    for k in ("dX", "dQ", "dP", "db_f", "db_r", "dc0"):
+        assert torch.equal(lb[k], ref[k]), k
