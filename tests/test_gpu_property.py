@@ -4,7 +4,9 @@ precision, c0 / dc_last), forward and backward through the C ABI.
 
 Bounded and reproducible: a fixed number of derandomized examples, and no
 shrinking phase, so a failure stops the test at the first failing case
-(whose parameters the assertion prints).
+(whose parameters the assertion prints).  Every call runs on a workspace
+of the queried size followed by a guard region that must come back
+untouched.
 
 The cases include one-element tensors and sums whose terms cancel, where a
 relative bar has no RMS to fall back on: beside the parity bars (1e-5 fp32,
@@ -65,6 +67,18 @@ def check_sens(name, got, ref, tol, sens):
 SETTINGS = dict(deadline=None, derandomize=True, database=None, phases=[Phase.generate],
                 suppress_health_check=list(HealthCheck))
 
+GUARD, FILL = 1 << 20, 0xA5
+
+
+def guarded(need):
+    """A workspace of `need` bytes followed by a guard region: (buffer, ws)."""
+    buf = torch.full((max(need, 1) + GUARD,), FILL, dtype=torch.uint8, device="cuda")
+    return buf, buf[:max(need, 1)]
+
+
+def guard_intact(buf, need, what):
+    assert bool(torch.all(buf[max(need, 1):] == FILL)), f"{what} wrote past its workspace"
+
 
 @st.composite
 def layer_cases(draw):
@@ -105,11 +119,18 @@ def test_layer_equals_oracle_on_random_cases(case):
     p = [None if linear else dev(c["v_f"]), None if linear else dev(c["v_r"]),
          dev(c["b_f"]), dev(c["b_r"])]
     X, W, c0, mask = dev(c["X"]), dev(c["W"]), dev(c["c0"]), dev(c["mask"])
-    fw = sru.forward(X, W, *p, c0=c0, direction=direction, mask=mask, gemm_dtype=gemm, **var)
+    L, B, d_in, d = case["L"], case["B"], case["d_in"], case["d"]
+    nf = sru.forward_workspace_bytes(L, B, d_in, d, direction, gemm)
+    nb = sru.backward_workspace_bytes(L, B, d_in, d, direction, gemm)
+    (fbuf, fws), (bbuf, bws) = guarded(nf), guarded(nb)
+    fw = sru.forward(X, W, *p, c0=c0, direction=direction, mask=mask, gemm_dtype=gemm, ws=fws,
+                     **var)
     bw = sru.backward(X, W, *p, fw["U"], fw["C"], dev(c["dH"]), c0=c0,
                       dc_last=dev(c["dc_last"]), direction=direction, mask=mask,
-                      gemm_dtype=gemm, **var)
+                      gemm_dtype=gemm, ws=bws, **var)
     torch.cuda.synchronize()
+    guard_intact(fbuf, nf, "the forward")
+    guard_intact(bbuf, nb, "the backward")
     ov = dict(alpha=case["alpha"], reset_new=case["reset_new"], linear=linear)
 
     def run(x):
@@ -163,12 +184,19 @@ def test_lowrank_layer_equals_oracle_on_random_cases(case):
     direction, gemm = case["direction"], case["gemm"]
     p = [dev(c[key]) for key in ("v_f", "v_r", "b_f", "b_r")]
     X, c0, mask = dev(c["X"]), dev(c["c0"]), dev(c["mask"])
+    lib = sru.lib()
+    L, B = case["L"], case["B"]
+    nf = lib.sru_forward_lowrank_workspace_bytes(L, B, d_in, d, dp, direction, gemm)
+    nb = lib.sru_backward_lowrank_workspace_bytes(L, B, d_in, d, dp, direction, gemm)
+    (fbuf, fws), (bbuf, bws) = guarded(nf), guarded(nb)
     fw = sru.forward_lowrank(X, dev(Q), dev(P), *p, c0=c0, direction=direction, mask=mask,
-                             gemm_dtype=gemm)
+                             gemm_dtype=gemm, ws=fws)
     bw = sru.backward_lowrank(X, dev(Q), dev(P), *p, fw["T"], fw["U"], fw["C"], dev(c["dH"]),
                               c0=c0, dc_last=dev(c["dc_last"]), direction=direction, mask=mask,
-                              gemm_dtype=gemm)
+                              gemm_dtype=gemm, ws=bws)
     torch.cuda.synchronize()
+    guard_intact(fbuf, nf, "the low-rank forward")
+    guard_intact(bbuf, nb, "the low-rank backward")
 
     def run(x):
         args = (x["X"], x["Q"], x["P"], x["v_f"], x["v_r"], x["b_f"], x["b_r"])
