@@ -79,3 +79,30 @@ def test_forward_and_lowrank_backward_stay_inside(linear):
     assert bool(torch.all(buf[need_lb:] == FILL)), "the low-rank backward wrote past its workspace"
     for k in ("dX", "dQ", "dP", "db_f", "db_r", "dc0"):
         assert torch.equal(lb[k], ref[k]), k
+
+
+@pytest.mark.parametrize("linear", [False, True])
+def test_scans_stay_inside(linear):
+    """The scan entry points: the linear recurrence's segment maps and the
+    per-sequence v/b partials live in their workspaces."""
+    L, B, d = 300, 3, 64   # few lane groups: the linear scans cut time into segments
+    print(f"workspace guard scans L={L} B={B} d={d} linear={linear}", flush=True)
+    c = random_layer_case(np.random.default_rng(7), L, B, d, d, O.DIR_BI, masked=True,
+                          c0=True, dc_last=True, bias_scale=0.5)
+    X, W = dev(c["X"]), dev(c["W"])
+    p = [dev(c[k]) for k in ("v_f", "v_r", "b_f", "b_r")]
+    kw = dict(c0=dev(c["c0"]), direction=O.DIR_BI, mask=dev(c["mask"]), linear=linear)
+    fw = sru.forward(X, W, *p, **kw)
+    lib = sru.lib()
+    nf = lib.sru_scan_forward_workspace_bytes(L, B, d, d, O.DIR_BI)
+    nb = lib.sru_scan_backward_workspace_bytes(L, B, d, d, O.DIR_BI)
+    fbuf = torch.full((nf + GUARD,), FILL, dtype=torch.uint8, device="cuda")
+    bbuf = torch.full((nb + GUARD,), FILL, dtype=torch.uint8, device="cuda")
+    sf = sru.scan_forward(fw["U"], X, *p, ws=fbuf[:nf], **kw)
+    sb = sru.scan_backward(fw["U"], X, fw["C"], dev(c["dH"]), *p, dc_last=dev(c["dc_last"]),
+                           ws=bbuf[:nb], **kw)
+    torch.cuda.synchronize()
+    assert nf > 0 and nb > 0
+    assert bool(torch.all(fbuf[nf:] == FILL)), "the forward scan wrote past its workspace"
+    assert bool(torch.all(bbuf[nb:] == FILL)), "the backward scan wrote past its workspace"
+    assert torch.equal(sf["H"], fw["H"]) and torch.equal(sf["c_last"], fw["c_last"])
