@@ -106,3 +106,57 @@ def test_scans_stay_inside(linear):
     assert bool(torch.all(fbuf[nf:] == FILL)), "the forward scan wrote past its workspace"
     assert bool(torch.all(bbuf[nb:] == FILL)), "the backward scan wrote past its workspace"
     assert torch.equal(sf["H"], fw["H"]) and torch.equal(sf["c_last"], fw["c_last"])
+
+
+def _guarded_out(shape, dtype=torch.float32):
+    """An output tensor of `shape` at the start of a buffer whose tail is a guard."""
+    n = int(np.prod(shape))
+    esz = torch.tensor([], dtype=dtype).element_size()
+    buf = torch.full(((n * esz + GUARD_OUT + 15) // 16 * 16,), FILL, dtype=torch.uint8,
+                     device="cuda")
+    return buf, buf[:n * esz].view(dtype).view(shape), n * esz
+
+
+GUARD_OUT = 1 << 16
+
+
+@pytest.mark.parametrize("case", [
+    (37, 5, 130, 65, O.DIR_FWD, O.GEMM_FP32),
+    (20, 3, 63, 63, O.DIR_BI, O.GEMM_FP32),
+    (33, 9, 264, 264, O.DIR_REV, O.GEMM_BF16),
+    (40, 13, 256, 256, O.DIR_BI, O.GEMM_BF16),
+    (17, 6, 200, 72, O.DIR_BI, O.GEMM_BF16),
+])
+def test_outputs_written_within_bounds(case):
+    """Ragged shapes (partial tiles, partial lane groups): every output is
+    the head of a larger buffer, and nothing past it changes."""
+    L, B, d_in, d, direction, gemm = case
+    print(f"output guard L={L} B={B} d_in={d_in} d={d} dir={direction} gemm={gemm}", flush=True)
+    c = random_layer_case(np.random.default_rng(3 * L + d), L, B, d_in, d, direction,
+                          masked=True, c0=True, dc_last=True, bias_scale=0.5)
+    X, W = dev(c["X"]), dev(c["W"])
+    p = [dev(c[k]) for k in ("v_f", "v_r", "b_f", "b_r")]
+    ndir, k = W.shape[0], W.shape[1]
+    nf = ndir * d
+    guards = []
+
+    def out(name, shape, dtype=torch.float32):
+        buf, t, nbytes = _guarded_out(shape, dtype)
+        guards.append((name, buf, nbytes))
+        return t
+    bf = gemm == O.GEMM_BF16
+    fo = dict(U=out("U", (L, B, ndir, k, d)), H=out("H", (L, B, nf)), C=out("C", (L, B, nf)),
+              c_last=out("c_last", (B, nf)))
+    if bf:
+        fo["W_bf16"] = out("W_bf16", tuple(W.shape), torch.bfloat16)
+        fo["H_bf16"] = out("H_bf16", (L, B, nf), torch.bfloat16)
+    kw = dict(c0=dev(c["c0"]), direction=direction, mask=dev(c["mask"]), gemm_dtype=gemm)
+    fw = sru.forward(X, W, *p, out=fo, **kw)
+    bo = dict(dX=out("dX", (L, B, d_in)), dW=out("dW", tuple(W.shape)), dv_f=out("dv_f", (ndir, d)),
+              dv_r=out("dv_r", (ndir, d)), db_f=out("db_f", (ndir, d)), db_r=out("db_r", (ndir, d)),
+              dc0=out("dc0", (B, nf)))
+    sru.backward(X, W, *p, fw["U"], fw["C"], dev(c["dH"]), dc_last=dev(c["dc_last"]), out=bo,
+                 W_bf16=fo.get("W_bf16"), **kw)
+    torch.cuda.synchronize()
+    for name, buf, nbytes in guards:
+        assert bool(torch.all(buf[nbytes:] == FILL)), f"{name} written past its end"
