@@ -8,6 +8,9 @@ backward) against the oracle.
   full oracle, and the full stack against the oracle on a slice of the batch
   (sequences never interact, so the oracle on a batch slice is exact for
   those sequences' H and dX).
+* One GPU's shard of workload 3 (B = 8) runs in full at its full size, and
+  so does the inference workload (on a batch slice), as the benchmark runs
+  them.
 """
 
 import numpy as np
@@ -80,6 +83,18 @@ def test_workload_reduced_size(wi):
 
 
 @pytest.mark.slow
+def test_shard_workload_full_size():
+    """One GPU's share of the headline stack (B = 8 of its 64 sequences) at
+    its full size, the whole batch against the oracle: every layer's H, C,
+    dX, dW and v/b sums."""
+    w = WORKLOADS[8]
+    print(f"workload {w.name}", flush=True)
+    inp = make_inputs(w)
+    st = run_stack(w, inp)
+    compare_stack(w, inp, st)
+
+
+@pytest.mark.slow
 @pytest.mark.parametrize("wi", [3, 4])
 def test_workload_full_size_single_layer(wi):
     """Layer 1 of the workload at full size against the full oracle: every
@@ -125,13 +140,15 @@ def test_workload_full_size_stack_on_batch_slice(wi):
 def test_inference_workload_full_size():
     """The Transformer-FFN inference shape (d_in 512 -> d 2048, k = 4,
     forward only, no C) at its full size in the benchmark's launch
-    configuration; the oracle on a slice of the batch (sequences never
-    interact)."""
+    configuration (weights held in bf16); the oracle on a slice of the batch
+    (sequences never interact)."""
     w = WORKLOADS[5]
     print(f"workload {w.name}", flush=True)
     assert not w.backward and not w.store_c and w.d_in != w.d
     inp = make_inputs(w)
     layers = [layer_to_dev(p) for p in inp["layers"]]
+    for p in layers:  # the benchmark holds inference weights in bf16
+        p["W"] = sru.round_bf16(p["W"])
     st = sru.Stack(layers, w.L, w.B, w.d_in, w.d, w.direction, w.gemm_dtype, "cuda",
                    backward=False, store_c=False)
     H = st.forward(dev(inp["X"]), None)
