@@ -709,7 +709,7 @@ struct DCfg {
   static constexpr int OCC = LDS <= 80 * 1024 ? 2 : 1;  // workgroups per CU
   static_assert(SA == STAGES || SA == STAGES + 1, "A ring depth");
   static_assert(BK == 32 || BK == 64, "k per stage");
-  static_assert(WM == 128 && WN == 64, "wave block");
+  static_assert((WM == 128 && WN == 64) || (WM == 64 && WN == 128), "wave block");
   static_assert(A_BPW * 1024 * WAVES == A_OPB && B_BPW * 1024 * WAVES == B_OPB,
                 "whole 1 KiB load blocks per wave");
   static_assert(LDS <= 160 * 1024 && IPS * (SA - 1) < 64, "LDS and vmcnt");
@@ -821,8 +821,11 @@ struct DirectOperand {
 };
 
 // The main loop of the direct products: the tile whose operand loads la and
-// lb were set up, accumulated over k in [kbeg, kend) into acc.
-template <class C, class OpA, class OpB>
+// lb were set up, accumulated over k in [kbeg, kend) into acc.  TRANS: the
+// MFMAs take B first, so acc holds the transposed tile (lane l: tile row
+// l % 32 of each 32 x 32 block); else lane l holds tile column l % 32, rows
+// 8 (e / 4) + 4 (l / 32) + e % 4 of element e.
+template <class C, bool TRANS = true, class OpA, class OpB>
 __device__ __forceinline__ void direct_mainloop(unsigned char* smem, const OpA& la,
                                                 const OpB& lb, __amdgpu_buffer_rsrc_t ra,
                                                 __amdgpu_buffer_rsrc_t rb, long long lda,
@@ -913,9 +916,12 @@ __device__ __forceinline__ void direct_mainloop(unsigned char* smem, const OpA& 
     for (int i = 0; i < C::FM; ++i)
 #pragma unroll
       for (int j = 0; j < C::FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8, f.b[j]), __builtin_bit_cast(bf16x8, f.a[i]), acc[i][j], 0,
-            0, 0);  // B first: the transposed tile, see write_tile_rows
+        acc[i][j] = TRANS ? __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                __builtin_bit_cast(bf16x8, f.b[j]),
+                                __builtin_bit_cast(bf16x8, f.a[i]), acc[i][j], 0, 0, 0)
+                          : __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                __builtin_bit_cast(bf16x8, f.a[i]),
+                                __builtin_bit_cast(bf16x8, f.b[j]), acc[i][j], 0, 0, 0);
   };
 
   // Software pipeline over the SLABS fragment slabs (16 k each) of a stage:
@@ -1010,62 +1016,92 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
 }
 
 // ---- fused projection + forward scan (inference: neither U nor C kept) ----
-// One workgroup per (direction, group of 64 hidden units, group of BB
-// sequences).  Per time block of 256 / BB steps it computes the tile of U
-// whose rows are the (step, sequence) pairs of the block and whose columns
-// are the gate blocks of its 64 units, with the main loop of the direct
-// products.  It stages the tile through LDS in two halves of 128 rows and
-// runs Eq. 1-4 for its lanes from there: wave s scans sequence s of the
-// group, lane j unit j, the state c held in a register across halves and
-// blocks.  U never reaches memory.  The scan arithmetic is the forward scan
-// kernel's, in the same order, so H equals the unfused path's bit for bit.
-// k = 4: the four gate blocks (the highway input x_hat is block 3) make the
-// 256 columns of the tile.
-constexpr int kFusedPitch = 68;  // floats per staged row: 64 + 4 keeps 16-byte writes conflict-free
-constexpr int kFusedStage = 4 * 128 * kFusedPitch * 4;  // bytes: 4 blocks of 128 rows
+// One workgroup per (direction, group of 64 hidden units, group of bb
+// sequences), bb = 4 or 8; its tile of U has 256 rows, the (step, sequence)
+// pairs of 256 / bb steps, and 256 columns, the four gate blocks of the 64
+// units (k = 4: block 3 is the highway input x_hat).  The MFMAs leave the
+// tile untransposed on 64 x 128 wave blocks, and the operand rows are mapped
+// so that a lane's accumulators are the scan's inputs: lane l of wave
+// (wm, wn) holds column l % 32 of each of its four 32-column MFMA blocks,
+// i.e. the four gates of unit 64 g + 32 wn + l % 32, and rows of one
+// sequence (l / 32 picks one of the wave's two), 16 consecutive steps per
+// 32-row block, so 32 steps in all.  The lane then runs Eq. 1-4 over those
+// steps from its own registers: U is neither written to memory nor staged.
+// With bb = 4 a sequence's 64 steps lie in two waves (time chunks), which
+// scan one after the other and hand c over through LDS.  The scan arithmetic
+// is the forward scan kernel's, in the same order, so H equals the unfused
+// path's bit for bit.
+using FusedCfg = DCfg<256, 256, 64, 4, 2, 2, 3>;  // 8 waves of 64 x 128, A two K steps ahead
 
-__global__ __launch_bounds__(DirectLine::THREADS, 1) void proj_scan_fwd_kernel(FusedFwdArgs a) {
-  using C = DirectLine;
+template <bool B_>
+struct BoolC {
+  static constexpr bool value = B_;
+};
+
+__global__ __launch_bounds__(FusedCfg::THREADS, 1) void proj_scan_fwd_kernel(FusedFwdArgs a) {
+  using C = FusedCfg;
   constexpr int KB = 4;
-  constexpr int SMEM = C::LDS > kFusedStage ? C::LDS : kFusedStage;
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[SMEM];
-  float* stage = reinterpret_cast<float*>(smem);
+  static_assert(C::FM == 2 && C::FN == KB, "a lane: 2 row blocks, one column block per gate");
+  static_assert(C::WAVES_M == 4 && C::WAVES_N == 2, "wave rows and columns");
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
 
   // workgroup -> (direction, unit group, sequence group); XCD-aware, so the
   // workgroups of one XCD share the Wcat rows of a unit group
   const int nwg = gridDim.x, w = blockIdx.x;
   const int q8 = nwg / 8, rmd = nwg % 8, x8 = w % 8;
-  const int u = x8 * q8 + (x8 < rmd ? x8 : rmd) + w / 8;
-  const int bg = u % a.nbgroups;
-  const int dg = u / a.nbgroups;
+  const int wu = x8 * q8 + (x8 < rmd ? x8 : rmd) + w / 8;
+  const int bg = wu % a.nbgroups;
+  const int dg = wu / a.nbgroups;
   const int dir = dg / a.ngroups, g = dg % a.ngroups;
-  const int BB = a.bb, TB = 256 / BB, steps = 128 / BB;
-  const int b0 = bg * BB;
+  const int nchunk = 8 / a.bb;  // time chunks of 32 steps per tile
+  const int b0 = bg * a.bb;
   const bool rev = a.direction == 1 || (a.direction == 2 && dir == 1);
   const int L = a.L, Bs = a.B, d = a.d;
   const long long nfeat = (long long)a.ndir * d;
 
+  // wave -> (time chunk, sequence pair, column half wn): with two chunks,
+  // waves 0-3 scan the first and waves 4-7 the second, one wave per SIMD
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / C::WAVES_N, wn = wave % C::WAVES_N;
-  const int wm0 = wm * C::WM, wn0 = wn * C::WN;
+  const int wn = wave & 1;
+  const int q2 = nchunk == 2 ? wave >> 2 : 0;
+  const int pair = nchunk == 2 ? (wave >> 1) & 1 : wave >> 1;
+  const int wm = pair * nchunk + q2;  // the wave's 64-row block of the tile
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.Xb, a.a_bytes);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.Wb, a.b_bytes);
   using OpA = DirectOperand<C::BM, false, C::A_BPW, C::BK>;
   using OpB = DirectOperand<C::BN, false, C::B_BPW, C::BK>;
+  // tile column 128 cw + 32 gate + u: gate block `gate` of unit 64 g + 32 cw + u
   OpB lb;
   lb.init_rows(
       wave, lane,
       [&](int col) -> long long {
-        return (long long)(dir * KB + (col >> 6)) * d + g * 64 + (col & 63);
+        return (long long)(dir * KB + ((col >> 5) & 3)) * d + g * 64 + (col >> 7) * 32 +
+               (col & 31);
       },
       a.d_in);
+  // tile row r: wave row r / 64 = (sequence pair, time chunk); in a 32-row
+  // block, row rr is sequence (rr / 4) % 2 of the pair at step
+  // 4 (rr / 8) + rr % 4 of the block's 16 (the MFMA's row of element e)
+  OpA la;
+  la.init_rows(
+      wave, lane,
+      [&](int r) -> long long {
+        const int wr = r >> 6, rr = r & 31;
+        const int b = b0 + 2 * (wr / nchunk) + ((rr >> 2) & 1);
+        const int t = 32 * (wr % nchunk) + 16 * ((r >> 5) & 1) + 4 * (rr >> 3) + (rr & 3);
+        return t < L && b < Bs ? (long long)t * Bs + b : -1;
+      },
+      a.d_in);
+  floatx16 acc[C::FM][C::FN];
+  direct_mainloop<C, false>(smem, la, lb, ra, rb, a.d_in, a.d_in, 0, a.d_in, wave, lane,
+                            wm * C::WM, wn * C::WN, acc);
 
-  // scan lanes: waves 0 .. BB-1, sequence b0 + wave, unit g * 64 + lane
-  const int sb = b0 + wave;
-  const bool scans = wave < BB && sb < Bs;
-  const long long fidx = (long long)dir * d + g * 64 + lane;
+  // this lane's scan: sequence sb, unit 64 g + 32 wn + lane % 32, time chunk q2
+  const int sb = b0 + 2 * pair + (lane >> 5);
+  const bool live = sb < Bs;
+  const long long fidx = (long long)dir * d + g * 64 + wn * 32 + (lane & 31);
   float vf = 0.f, vr = 0.f, bf = 0.f, br = 0.f, c = 0.f;
-  if (scans) {
+  if (live) {
     if (!a.linear) {
       vf = a.v_f[fidx];
       vr = a.v_r[fidx];
@@ -1086,105 +1122,95 @@ __global__ __launch_bounds__(DirectLine::THREADS, 1) void proj_scan_fwd_kernel(F
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
   };
+  barrier();  // every wave is done with the operand stages: LDS now holds the hand-over of c
+  float* cx = reinterpret_cast<float*>(smem) + (pair * C::WAVES_N + wn) * 64 + lane;
 
-  const int nblk = (L + TB - 1) / TB;
-  for (int ib = 0; ib < nblk; ++ib) {
-    const int t0 = (rev ? nblk - 1 - ib : ib) * TB;
-    OpA la;
-    la.init_rows(
-        wave, lane,
-        [&](int r) -> long long {
-          const int t = t0 + r / BB, b = b0 + r % BB;
-          return t < L && b < Bs ? (long long)t * Bs + b : -1;
-        },
-        a.d_in);
-    floatx16 acc[C::FM][C::FN];
-    direct_mainloop<C>(smem, la, lb, ra, rb, a.d_in, a.d_in, 0, a.d_in, wave, lane, wm0, wn0,
-                       acc);
-    barrier();  // every wave is done with the operand stages
-    for (int ih = 0; ih < 2; ++ih) {
-      const int half = rev ? 1 - ih : ih;
-      if (wm == half) {
-        // transposed accumulators: lane l holds row l % 32 of each MFMA
-        // tile, columns 8 (e / 4) + 4 (l / 32) + e % 4
+  // the 32 steps of time chunk q (scan order: backward for a reverse
+  // direction); steps at or past L are not computed.  A whole chunk runs
+  // without a branch between its steps, so the compiler can overlap one
+  // step's output (reset gate, h, stores) with the next step's chain.
+  auto scan_chunk = [&](auto rev_c, auto whole_c, auto hb_c, int q) {
+    constexpr bool RV = decltype(rev_c)::value, WHOLE = decltype(whole_c)::value;
+    constexpr bool HB = decltype(hb_c)::value;
+    const int tb = 32 * q;
+    const int nv = min(32, L - tb);
+    // padding bits of the chunk's steps: lane u of each half reads step
+    // tb + u of its sequence, and the ballot hands each half its 32 bits
+    unsigned mbits = 0;
+    if (a.mask) {
+      const int tm = tb + (lane & 31);
+      const bool pad = live && tm < L && a.mask[(long long)tm * Bs + sb] != 0;
+      mbits = (unsigned)(__ballot(pad) >> (32 * (lane >> 5)));
+    }
+    if (!live) return;
+    // output offset at the chunk's first step in scan order, moved one step
+    // at a time (the empty asm keeps the compiler from precomputing every
+    // step's offset)
+    const int tt0 = RV ? (WHOLE ? 31 : nv - 1) : 0;
+    long long o = ((long long)(tb + tt0) * Bs + sb) * nfeat + fidx;
+    const long long dstep = (RV ? -1LL : 1LL) * Bs * nfeat;
+    // A step carries c forward first (Eq. 1-2) and then finishes the
+    // previous step's output (Eq. 3-4, the store), which no longer lies on
+    // the chain from one c to the next.
+    float p_cn = 0.f, p_rin = 0.f, p_zr = 0.f, p_xh = 0.f;
+    bool p_pad = false, pend = false;
+    auto emit = [&]() {
+      const float r = sigmoid_scaled(fmaf(vrs, p_rin, p_zr));        // Eq. 3
+      float h = fmaf(r, p_cn, (1.0f - r) * (alpha * p_xh));          // Eq. 4 (Sec. 3.2)
+      h = p_pad ? 0.0f : h;
+      __builtin_nontemporal_store(h, a.H + o);
+      if constexpr (HB)
+        __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), a.Hb + o);
+      o += dstep;
+      asm volatile("" : "+v"(o));
+    };
 #pragma unroll
-        for (int i = 0; i < C::FM; ++i)
-#pragma unroll
-          for (int j = 0; j < C::FN; ++j)
-#pragma unroll
-            for (int eg = 0; eg < 4; ++eg) {
-              floatx4 v;
-              v[0] = acc[i][j][4 * eg];
-              v[1] = acc[i][j][4 * eg + 1];
-              v[2] = acc[i][j][4 * eg + 2];
-              v[3] = acc[i][j][4 * eg + 3];
-              const int row = i * 32 + (lane & 31);
-              const int col = j * 32 + 8 * eg + 4 * (lane >> 5);
-              *reinterpret_cast<floatx4*>(stage + (wn * 128 + row) * kFusedPitch + col) = v;
-            }
+    for (int s = 0; s < 32; ++s) {
+      const int tt = RV ? 31 - s : s;
+      if (WHOLE || tt < nv) {
+        const float u0 = acc[tt >> 4][0][tt & 15], u1 = acc[tt >> 4][1][tt & 15];
+        const float u2 = acc[tt >> 4][2][tt & 15], xh = acc[tt >> 4][3][tt & 15];
+        const float f = sigmoid_scaled(fmaf(vfs, c, fmaf(u1, kNegLog2e, bfs)));  // Eq. 1
+        const float cn = fmaf(f, c, fmaf(-f, u0, u0));                           // Eq. 2
+        const float rin = rn ? cn : c;
+        const bool pad = (mbits >> tt) & 1u;
+        c = pad ? c : cn;
+        if (WHOLE ? s > 0 : pend) emit();
+        p_cn = cn;
+        p_rin = rin;
+        p_zr = fmaf(u2, kNegLog2e, brs);
+        p_xh = xh;
+        p_pad = pad;
+        pend = true;
       }
+    }
+    if (pend) emit();
+  };
+  // one instantiation per (direction of time, whole chunk, bf16 copy of H)
+  auto scan_any = [&](auto rev_c, int q) {
+    const bool whole = L - 32 * q >= 32;
+    if (whole) {
+      if (a.Hb) scan_chunk(rev_c, BoolC<true>{}, BoolC<true>{}, q);
+      else scan_chunk(rev_c, BoolC<true>{}, BoolC<false>{}, q);
+    } else {
+      if (a.Hb) scan_chunk(rev_c, BoolC<false>{}, BoolC<true>{}, q);
+      else scan_chunk(rev_c, BoolC<false>{}, BoolC<false>{}, q);
+    }
+  };
+  for (int i = 0; i < nchunk; ++i) {
+    const int q = rev ? nchunk - 1 - i : i;  // the chunk scanned now
+    if (i > 0) {
+      // the wave of the previous chunk hands its c over
+      if (q2 == (rev ? q + 1 : q - 1)) *cx = c;
       barrier();
-      if (scans) {
-        const int tb = t0 + half * steps;  // first step of this half
-        // steps tt < nv of the half lie inside the sequence
-        const int nv = max(0, min(steps, L - tb));
-        // padding bits of the half's steps, one per lane, read with readlane
-        int m_lo = 0, m_hi = 0;
-        if (a.mask) {
-          if (lane < nv) m_lo = a.mask[(long long)(tb + lane) * Bs + sb];
-          if (lane + 64 < nv) m_hi = a.mask[(long long)(tb + 64 + lane) * Bs + sb];
-        }
-        // pointers at the half's first step in the direction's order, moved
-        // one step per iteration: no branch and no index arithmetic in the
-        // loop, so the LDS reads of later steps are issued ahead of the chain
-        const int tt0 = rev ? nv - 1 : 0;
-        const int dtt = rev ? -1 : 1;
-        const float* sp = stage + (tt0 * BB + wave) * kFusedPitch + lane;
-        const long long o0 = ((long long)(tb + tt0) * Bs + sb) * nfeat + fidx;
-        float* hp = a.H + o0;
-        uint16_t* hbp = a.Hb ? a.Hb + o0 : nullptr;
-        const long long dstep = (long long)dtt * Bs * nfeat;
-        const int sstep = dtt * BB * kFusedPitch;
-        auto step = [&](int tt, float u0, float u1, float u2, float xh) {
-          const int mbit = __builtin_amdgcn_readlane(tt < 64 ? m_lo : m_hi, tt & 63);
-          const float f = sigmoid_scaled(fmaf(vfs, c, fmaf(u1, kNegLog2e, bfs)));  // Eq. 1
-          const float cn = fmaf(f, c, fmaf(-f, u0, u0));                           // Eq. 2
-          const float r = sigmoid_scaled(fmaf(vrs, rn ? cn : c, fmaf(u2, kNegLog2e, brs)));  // Eq. 3
-          float h = fmaf(r, cn, (1.0f - r) * (alpha * xh));              // Eq. 4 (Sec. 3.2)
-          if (mbit) {
-            h = 0.0f;
-          } else {
-            c = cn;
-          }
-          __builtin_nontemporal_store(h, hp);
-          if (hbp) {
-            __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), hbp);
-            hbp += dstep;
-          }
-          hp += dstep;
-        };
-        constexpr int P = 128 * kFusedPitch;  // floats between gate blocks
-        int s = 0;
-        // four steps at a time: their LDS reads first, then the dependent chain
-        for (; s + 4 <= nv; s += 4) {
-          float u[4][4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) u[q][e] = sp[q * sstep + e * P];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) step(tt0 + dtt * (s + q), u[q][0], u[q][1], u[q][2], u[q][3]);
-          sp += 4 * sstep;
-        }
-        for (; s < nv; ++s) {
-          step(tt0 + dtt * s, sp[0], sp[P], sp[2 * P], sp[3 * P]);
-          sp += sstep;
-        }
-      }
-      barrier();  // before the next half or block overwrites the stage
+      if (q2 == q) c = *cx;
+    }
+    if (q2 == q) {
+      if (rev) scan_any(BoolC<true>{}, q);
+      else scan_any(BoolC<false>{}, q);
     }
   }
-  if (scans && a.c_last) a.c_last[(long long)sb * nfeat + fidx] = c;
+  if (live && a.c_last && q2 == (rev ? 0 : nchunk - 1)) a.c_last[(long long)sb * nfeat + fidx] = c;
 }
 
 template <class C, int ADD, bool A_RC, bool B_RC, bool OB = false>
@@ -1745,9 +1771,11 @@ hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, b
 }
 
 hipError_t proj_scan_forward_launch(const FusedFwdArgs& a, hipStream_t st) {
+  // a tile holds 256 / bb steps of bb sequences, in time chunks of 32 steps
+  if ((a.bb != 4 && a.bb != 8) || a.L > 256 / a.bb) return hipErrorInvalidValue;
   const int grid = a.ndir * a.ngroups * a.nbgroups;
   timing_before("proj_scan_fwd", st);
-  hipLaunchKernelGGL(proj_scan_fwd_kernel, dim3(grid), dim3(DirectLine::THREADS), 0, st, a);
+  hipLaunchKernelGGL(proj_scan_fwd_kernel, dim3(grid), dim3(FusedCfg::THREADS), 0, st, a);
   timing_after(st);
   return hipGetLastError();
 }
