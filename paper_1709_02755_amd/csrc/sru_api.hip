@@ -866,9 +866,13 @@ int sru_backward_lowrank(const float* X, const float* Q, const float* P, const f
     return hip_status(sru::to_bf16_launch(src, rows, cols, dst, false, stream, label));
   };
 
-  // 1. reverse gradient scan (dU in the products' operand type)
+  // 1. reverse gradient scan (dU in the products' operand type); the v/b
+  //    sums over the batch run with the dP product (in its split-K sum's
+  //    launch when it has one)
   sru::ScanBwdArgs a{U,   X,    C,   dH,      dc_last, v_f,  v_r,  b_f,  b_r,  c0,
                      pad_mask, dU, bf16, dxh, partial, dc0, dv_f, dv_r, db_f, db_r};
+  a.defer_vb = true;
+  gp.vb = sru::scan_backward_vb(scan_shape(s, direction, op), a);
   if (int e = hip_status(sru::scan_backward_launch(scan_shape(s, direction, op), a, stream)))
     return e;
   // 2. dT = dU P (bf16: as dU (P^T)^T, written in bf16 only)

@@ -150,3 +150,33 @@ def test_lowrank_stack_wiring_equals_plain_calls():
             assert torch.equal(st.fw[li][key], fws[li][key]), (li, key)
         for key in ("dX", "dQ", "dP", "dv_f", "dv_r", "db_f", "db_r"):
             assert torch.equal(st.bw[li][key], bws[li][key]), (li, key)
+
+
+@pytest.mark.parametrize("case", [
+    (256, 16, 512, 512, 128, O.DIR_FWD, False, O.GEMM_BF16),  # dP split: in its split-K sum
+    (30, 5, 64, 96, 24, O.DIR_BI, True, O.GEMM_FP32),
+])
+def test_lowrank_vb_sums_same_bits_as_standalone_scan(case):
+    """The low-rank backward sums the v/b gradients over the batch inside the
+    dP product's launches; the standalone backward scan sums them in its own
+    launch.  Both run the same fixed-order sum: identical bits."""
+    L, B, d_in, d, dp, direction, masked, gemm = case
+    print(f"lowrank vb sums L={L} B={B} d_in={d_in} d={d} dp={dp} dir={direction} "
+          f"gemm={gemm}", flush=True)
+    rng = np.random.default_rng(L + dp)
+    c = random_layer_case(rng, L, B, d_in, d, direction, masked=masked, c0=True, dc_last=True,
+                          bias_scale=0.5)
+    ndir, k = c["W"].shape[:2]
+    Q = dev((rng.uniform(-1, 1, (d_in, dp)) * np.sqrt(3.0 / d_in)).astype(np.float32))
+    P = dev((rng.uniform(-1, 1, (ndir, k, d, dp)) * np.sqrt(3.0 / dp)).astype(np.float32))
+    X = dev(c["X"])
+    p = [dev(c[key]) for key in ("v_f", "v_r", "b_f", "b_r")]
+    kw = dict(c0=dev(c["c0"]), direction=direction, mask=dev(c["mask"]))
+    fw = sru.forward_lowrank(X, Q, P, *p, gemm_dtype=gemm, **kw)
+    bw = sru.backward_lowrank(X, Q, P, *p, fw["T"], fw["U"], fw["C"], dev(c["dH"]),
+                              dc_last=dev(c["dc_last"]), gemm_dtype=gemm, **kw)
+    sb = sru.scan_backward(fw["U"], X, fw["C"], dev(c["dH"]), *p, dc_last=dev(c["dc_last"]),
+                           **kw)
+    torch.cuda.synchronize()
+    for key in ("dv_f", "dv_r", "db_f", "db_r", "dc0"):
+        assert torch.equal(bw[key], sb[key]), key
