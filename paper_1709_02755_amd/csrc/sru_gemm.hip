@@ -1017,20 +1017,20 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
 
 // ---- fused projection + forward scan (inference: neither U nor C kept) ----
 // One workgroup per (direction, group of 64 hidden units, group of bb
-// sequences), bb = 4 or 8; its tile of U has 256 rows, the (step, sequence)
-// pairs of 256 / bb steps, and 256 columns, the four gate blocks of the 64
-// units (k = 4: block 3 is the highway input x_hat).  The MFMAs leave the
-// tile untransposed on 64 x 128 wave blocks, and the operand rows are mapped
-// so that a lane's accumulators are the scan's inputs: lane l of wave
-// (wm, wn) holds column l % 32 of each of its four 32-column MFMA blocks,
-// i.e. the four gates of unit 64 g + 32 wn + l % 32, and rows of one
+// sequences), bb = 2, 4 or 8; its tile of U has 256 rows, the (step,
+// sequence) pairs of 256 / bb steps, and 256 columns, the four gate blocks
+// of the 64 units (k = 4: block 3 is the highway input x_hat).  The MFMAs
+// leave the tile untransposed on 64 x 128 wave blocks, and the operand rows
+// are mapped so that a lane's accumulators are the scan's inputs: lane l of
+// wave (wm, wn) holds column l % 32 of each of its four 32-column MFMA
+// blocks, i.e. the four gates of unit 64 g + 32 wn + l % 32, and rows of one
 // sequence (l / 32 picks one of the wave's two), 16 consecutive steps per
 // 32-row block, so 32 steps in all.  The lane then runs Eq. 1-4 over those
 // steps from its own registers: U is neither written to memory nor staged.
-// With bb = 4 a sequence's 64 steps lie in two waves (time chunks), which
-// scan one after the other and hand c over through LDS.  The scan arithmetic
-// is the forward scan kernel's, in the same order, so H equals the unfused
-// path's bit for bit.
+// A sequence's 256 / bb steps lie in 8 / bb waves (time chunks of 32 steps),
+// which scan one after the other and hand c over through LDS.  The scan
+// arithmetic is the forward scan kernel's, in the same order, so H equals
+// the unfused path's bit for bit.
 using FusedCfg = DCfg<256, 256, 64, 4, 2, 2, 3>;  // 8 waves of 64 x 128, A two K steps ahead
 
 template <bool B_>
@@ -1059,12 +1059,14 @@ __global__ __launch_bounds__(FusedCfg::THREADS, 1) void proj_scan_fwd_kernel(Fus
   const int L = a.L, Bs = a.B, d = a.d;
   const long long nfeat = (long long)a.ndir * d;
 
-  // wave -> (time chunk, sequence pair, column half wn): with two chunks,
-  // waves 0-3 scan the first and waves 4-7 the second, one wave per SIMD
+  // wave -> (time chunk, sequence pair, column half wn): the waves of one
+  // chunk are consecutive, so they sit on different SIMDs (with two chunks,
+  // waves 0-3 scan the first and waves 4-7 the second)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wn = wave & 1;
-  const int q2 = nchunk == 2 ? wave >> 2 : 0;
-  const int pair = nchunk == 2 ? (wave >> 1) & 1 : wave >> 1;
+  const int pairs = 4 / nchunk;
+  const int q2 = (wave >> 1) / pairs;
+  const int pair = (wave >> 1) % pairs;
   const int wm = pair * nchunk + q2;  // the wave's 64-row block of the tile
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(a.Xb, a.a_bytes);
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.Wb, a.b_bytes);
@@ -1772,7 +1774,7 @@ hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, b
 
 hipError_t proj_scan_forward_launch(const FusedFwdArgs& a, hipStream_t st) {
   // a tile holds 256 / bb steps of bb sequences, in time chunks of 32 steps
-  if ((a.bb != 4 && a.bb != 8) || a.L > 256 / a.bb) return hipErrorInvalidValue;
+  if ((a.bb != 2 && a.bb != 4 && a.bb != 8) || a.L > 256 / a.bb) return hipErrorInvalidValue;
   const int grid = a.ndir * a.ngroups * a.nbgroups;
   timing_before("proj_scan_fwd", st);
   hipLaunchKernelGGL(proj_scan_fwd_kernel, dim3(grid), dim3(FusedCfg::THREADS), 0, st, a);

@@ -265,7 +265,8 @@ def test_forward_without_u_needs_the_fused_path():
     assert lib.sru_forward_fused_available(4, 2, 64, 64, 0, 1) == 0   # k = 3
     assert lib.sru_forward_fused_available(4, 2, 60, 64, 0, 1) == 0   # d_in % 8
     assert lib.sru_forward_fused_available(4, 2, 64, 32, 0, 1) == 0   # d % 64
-    assert lib.sru_forward_fused_available(65, 2, 128, 64, 0, 1) == 0  # L > 64
+    assert lib.sru_forward_fused_available(128, 2, 128, 64, 0, 1) == 1
+    assert lib.sru_forward_fused_available(129, 2, 128, 64, 0, 1) == 0  # L > 128
     # U omitted: fp32 products, or C kept, leave U required
     assert _fwd(lib, d_in=128, d=64, U=None, C=None) == E_NULL
     assert _fwd(lib, d_in=128, d=64, gemm=1, U=None, C=FAKE) == E_NULL

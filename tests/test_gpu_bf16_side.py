@@ -118,7 +118,7 @@ def test_stack_wiring_equals_plain_calls():
 
 
 def test_inference_stack_with_bf16_weights():
-    """Inference at the fused kernel's shape (k = 4, L <= 64) with the
+    """Inference at the fused kernel's shape (k = 4, L <= 128) with the
     weights held in bf16 (rounded once) equals the stack that rounds them on
     every call, bit for bit; so does the allocation-free forward."""
     L, B, d_in, d = 24, 10, 64, 128

@@ -1,7 +1,7 @@
 """The fused projection + scan of inference (sru_forward with U and C
-omitted; k = 4 and at most 64 steps): H, c_last and the bf16 copy of H equal
+omitted; k = 4 and at most 128 steps): H, c_last and the bf16 copy of H equal
 the unfused call's bit for bit (the scan reads the same fp32 projections, in
-the same order), across tile plans of 4 and 8 sequences, ragged step and
+the same order), across tile plans of 2, 4 and 8 sequences, ragged step and
 sequence counts, every direction, padding, c0 and the gate variants; and
 against the oracle, the linear recurrence included."""
 
@@ -24,6 +24,8 @@ CASES = [
     (17, 11, 128, 64, O.DIR_BI, False, float(np.sqrt(3.0)), False),  # 8 per tile
     (1, 4, 256, 128, O.DIR_REV, False, 1.0, True),      # a single step
     (64, 80, 512, 2048, O.DIR_FWD, False, 1.0, False),  # the Transformer-FFN shape
+    (100, 5, 256, 128, O.DIR_REV, True, 1.0, False),    # 2 per tile, 4 chunks, ragged L and B
+    (128, 3, 128, 64, O.DIR_BI, True, 1.3, True),       # 2 per tile, both directions, variants
 ]
 
 
@@ -62,9 +64,9 @@ def test_fused_equals_unfused_bitwise(case):
     assert torch.equal(got["H_bf16"].view(torch.int16), ref["H_bf16"].view(torch.int16))
 
 
-@pytest.mark.parametrize("linear", [False, True])
-def test_fused_matches_oracle(linear):
-    L, B, d_in, d, direction = 60, 6, 192, 128, O.DIR_BI
+@pytest.mark.parametrize("linear,L", [(False, 60), (True, 60), (False, 96)])
+def test_fused_matches_oracle(linear, L):
+    B, d_in, d, direction = 6, 192, 128, O.DIR_BI
     c = _case(L, B, d_in, d, direction, True, 5 + linear)
     got = _run(c, direction, {}, fused=True, linear=linear)
     torch.cuda.synchronize()
@@ -79,9 +81,9 @@ def test_fused_matches_oracle(linear):
 
 def test_fused_not_available_keeps_u_required():
     """Where the fused kernel does not apply (fp32 products, k = 3, sequences
-    over 64 steps, d not a multiple of 64) U stays required."""
-    assert sru.fused_available(64, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
+    over 128 steps, d not a multiple of 64) U stays required."""
+    assert sru.fused_available(128, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
     assert not sru.fused_available(8, 2, 128, 64, O.DIR_FWD, O.GEMM_FP32)
     assert not sru.fused_available(8, 2, 64, 64, O.DIR_FWD, O.GEMM_BF16)   # k = 3
-    assert not sru.fused_available(65, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
+    assert not sru.fused_available(129, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
     assert not sru.fused_available(8, 2, 96, 32, O.DIR_FWD, O.GEMM_BF16)
