@@ -709,7 +709,7 @@ struct DCfg {
   static constexpr int OCC = LDS <= 80 * 1024 ? 2 : 1;  // workgroups per CU
   static_assert(SA == STAGES || SA == STAGES + 1, "A ring depth");
   static_assert(BK == 32 || BK == 64, "k per stage");
-  static_assert((WM == 128 && WN == 64) || (WM == 64 && WN == 128), "wave block");
+  static_assert((WM == 128 && WN == 64) || (WM == 64 && (WN == 96 || WN == 128)), "wave block");
   static_assert(A_BPW * 1024 * WAVES == A_OPB && B_BPW * 1024 * WAVES == B_OPB,
                 "whole 1 KiB load blocks per wave");
   static_assert(LDS <= 160 * 1024 && IPS * (SA - 1) < 64, "LDS and vmcnt");
@@ -1031,16 +1031,21 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
 // which scan one after the other and hand c over through LDS.  The scan
 // arithmetic is the forward scan kernel's, in the same order, so H equals
 // the unfused path's bit for bit.
-using FusedCfg = DCfg<256, 256, 64, 4, 2, 2, 3>;  // 8 waves of 64 x 128, A two K steps ahead
+// 8 waves of 64 x 32k, A two K steps ahead (a type of its own per k: two
+// kernels instantiating the main loop on one configuration type trip the
+// host compilation pass)
+template <int KB>
+struct FusedCfg : DCfg<256, 64 * KB, 64, 4, 2, 2, 3> {};
 
 template <bool B_>
 struct BoolC {
   static constexpr bool value = B_;
 };
 
-__global__ __launch_bounds__(FusedCfg::THREADS, 1) void proj_scan_fwd_kernel(FusedFwdArgs a) {
-  using C = FusedCfg;
-  constexpr int KB = 4;
+template <int KB>
+__global__ __launch_bounds__(512, 1) void proj_scan_fwd_kernel(FusedFwdArgs a) {
+  using C = FusedCfg<KB>;
+  static_assert(C::THREADS == 512, "8 waves");
   static_assert(C::FM == 2 && C::FN == KB, "a lane: 2 row blocks, one column block per gate");
   static_assert(C::WAVES_M == 4 && C::WAVES_N == 2, "wave rows and columns");
   __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
@@ -1072,13 +1077,13 @@ __global__ __launch_bounds__(FusedCfg::THREADS, 1) void proj_scan_fwd_kernel(Fus
   const __amdgpu_buffer_rsrc_t rb = make_rsrc(a.Wb, a.b_bytes);
   using OpA = DirectOperand<C::BM, false, C::A_BPW, C::BK>;
   using OpB = DirectOperand<C::BN, false, C::B_BPW, C::BK>;
-  // tile column 128 cw + 32 gate + u: gate block `gate` of unit 64 g + 32 cw + u
+  // tile column 32 k cw + 32 gate + u: gate block `gate` of unit 64 g + 32 cw + u
   OpB lb;
   lb.init_rows(
       wave, lane,
       [&](int col) -> long long {
-        return (long long)(dir * KB + ((col >> 5) & 3)) * d + g * 64 + (col >> 7) * 32 +
-               (col & 31);
+        const int cw = col / (32 * KB), gate = (col >> 5) % KB;
+        return (long long)(dir * KB + gate) * d + g * 64 + cw * 32 + (col & 31);
       },
       a.d_in);
   // tile row r: wave row r / 64 = (sequence pair, time chunk); in a 32-row
@@ -1101,7 +1106,20 @@ __global__ __launch_bounds__(FusedCfg::THREADS, 1) void proj_scan_fwd_kernel(Fus
   // this lane's scan: sequence sb, unit 64 g + 32 wn + lane % 32, time chunk q2
   const int sb = b0 + 2 * pair + (lane >> 5);
   const bool live = sb < Bs;
-  const long long fidx = (long long)dir * d + g * 64 + wn * 32 + (lane & 31);
+  const int unit = g * 64 + wn * 32 + (lane & 31);
+  const long long fidx = (long long)dir * d + unit;
+  // k = 3: the highway input x_t of the wave's chunk, loaded now so that it
+  // arrives while earlier chunks scan (steps past L re-read step L - 1)
+  float xr[32];
+  if constexpr (KB == 3) {
+    if (live) {
+      const float* xp = a.X + (long long)sb * a.d_in + unit;
+      const long long xs = (long long)Bs * a.d_in;
+#pragma unroll
+      for (int tt = 0; tt < 32; ++tt) xr[tt] = xp[min(32 * q2 + tt, L - 1) * xs];
+    }
+  }
+  (void)xr;
   float vf = 0.f, vr = 0.f, bf = 0.f, br = 0.f, c = 0.f;
   if (live) {
     if (!a.linear) {
@@ -1171,7 +1189,10 @@ __global__ __launch_bounds__(FusedCfg::THREADS, 1) void proj_scan_fwd_kernel(Fus
       const int tt = RV ? 31 - s : s;
       if (WHOLE || tt < nv) {
         const float u0 = acc[tt >> 4][0][tt & 15], u1 = acc[tt >> 4][1][tt & 15];
-        const float u2 = acc[tt >> 4][2][tt & 15], xh = acc[tt >> 4][3][tt & 15];
+        const float u2 = acc[tt >> 4][2][tt & 15];
+        float xh;
+        if constexpr (KB == 4) xh = acc[tt >> 4][3][tt & 15];
+        else xh = xr[tt];
         const float f = sigmoid_scaled(fmaf(vfs, c, fmaf(u1, kNegLog2e, bfs)));  // Eq. 1
         const float cn = fmaf(f, c, fmaf(-f, u0, u0));                           // Eq. 2
         const float rin = rn ? cn : c;
@@ -1773,11 +1794,17 @@ hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, b
 }
 
 hipError_t proj_scan_forward_launch(const FusedFwdArgs& a, hipStream_t st) {
-  // a tile holds 256 / bb steps of bb sequences, in time chunks of 32 steps
-  if ((a.bb != 2 && a.bb != 4 && a.bb != 8) || a.L > 256 / a.bb) return hipErrorInvalidValue;
+  // a tile holds 256 / bb steps of bb sequences, in time chunks of 32 steps;
+  // k = 3 reads x_t from X (d_in = d)
+  if ((a.bb != 2 && a.bb != 4 && a.bb != 8) || a.L > 256 / a.bb || (a.k != 3 && a.k != 4) ||
+      (a.k == 3 && (!a.X || a.d_in != a.d)))
+    return hipErrorInvalidValue;
   const int grid = a.ndir * a.ngroups * a.nbgroups;
   timing_before("proj_scan_fwd", st);
-  hipLaunchKernelGGL(proj_scan_fwd_kernel, dim3(grid), dim3(FusedCfg::THREADS), 0, st, a);
+  if (a.k == 3)
+    hipLaunchKernelGGL((proj_scan_fwd_kernel<3>), dim3(grid), dim3(512), 0, st, a);
+  else
+    hipLaunchKernelGGL((proj_scan_fwd_kernel<4>), dim3(grid), dim3(512), 0, st, a);
   timing_after(st);
   return hipGetLastError();
 }

@@ -82,13 +82,15 @@ size_t gemm_partial_bytes(int M, int N, int splits);
 hipError_t gemm_launch(const GemmDesc& g, hipStream_t stream);
 
 // ------------------------------------------- fused projection + forward scan
-// Inference with bf16 products and k = 4: U = X Wcat^T and Eq. 1-4 in one
-// kernel; U and C are not stored.  Needs d % 64 == 0, d_in % 8 == 0, 16-byte
-// aligned bf16 operands smaller than 2 GiB (a_bytes, b_bytes: their sizes).
+// Inference with bf16 products: U = X Wcat^T and Eq. 1-4 in one kernel; U
+// and C are not stored.  Needs k = 3 or 4, L <= 256 / bb, d % 64 == 0,
+// d_in % 8 == 0, 16-byte aligned bf16 operands smaller than 2 GiB (a_bytes,
+// b_bytes: their sizes).
 struct FusedFwdArgs {
   const uint16_t* Xb;  // X in bf16 [L*B, d_in]
   const uint16_t* Wb;  // Wcat in bf16 [ndir*k*d, d_in]
   unsigned a_bytes, b_bytes;
+  const float* X;      // X in fp32: the highway input x_t when k = 3
   const float* v_f;
   const float* v_r;
   const float* b_f;
@@ -98,7 +100,7 @@ struct FusedFwdArgs {
   float* H;
   uint16_t* Hb;
   float* c_last;
-  int L, B, d_in, d, ndir, direction;
+  int L, B, d_in, d, ndir, k, direction;
   int bb;                 // sequences per tile: a tile holds 256 / bb steps of each
   int ngroups, nbgroups;  // d / 64 unit groups; ceil(B / bb) sequence groups
   float alpha;

@@ -262,7 +262,7 @@ def test_forward_without_u_needs_the_fused_path():
     lib = sru.lib()
     assert lib.sru_forward_fused_available(4, 2, 128, 64, 0, 1) == 1
     assert lib.sru_forward_fused_available(4, 2, 128, 64, 0, 0) == 0  # fp32 products
-    assert lib.sru_forward_fused_available(4, 2, 64, 64, 0, 1) == 0   # k = 3
+    assert lib.sru_forward_fused_available(4, 2, 64, 64, 0, 1) == 1   # k = 3
     assert lib.sru_forward_fused_available(4, 2, 60, 64, 0, 1) == 0   # d_in % 8
     assert lib.sru_forward_fused_available(4, 2, 64, 32, 0, 1) == 0   # d % 64
     assert lib.sru_forward_fused_available(128, 2, 128, 64, 0, 1) == 1

@@ -1,7 +1,7 @@
 """The fused projection + scan of inference (sru_forward with U and C
-omitted; k = 4 and at most 128 steps): H, c_last and the bf16 copy of H equal
+omitted; at most 128 steps): H, c_last and the bf16 copy of H equal
 the unfused call's bit for bit (the scan reads the same fp32 projections, in
-the same order), across tile plans of 2, 4 and 8 sequences, ragged step and
+the same order), across k = 3 and 4, tile plans of 2, 4 and 8 sequences, ragged step and
 sequence counts, every direction, padding, c0 and the gate variants; and
 against the oracle, the linear recurrence included."""
 
@@ -26,6 +26,11 @@ CASES = [
     (64, 80, 512, 2048, O.DIR_FWD, False, 1.0, False),  # the Transformer-FFN shape
     (100, 5, 256, 128, O.DIR_REV, True, 1.0, False),    # 2 per tile, 4 chunks, ragged L and B
     (128, 3, 128, 64, O.DIR_BI, True, 1.3, True),       # 2 per tile, both directions, variants
+    # k = 3 (d_in = d): the highway input x_t read from X
+    (64, 9, 192, 192, O.DIR_FWD, True, 1.0, False),
+    (50, 6, 128, 128, O.DIR_REV, True, 1.7, True),
+    (100, 5, 128, 128, O.DIR_BI, True, 1.0, False),
+    (17, 11, 64, 64, O.DIR_BI, False, float(np.sqrt(3.0)), False),
 ]
 
 
@@ -64,9 +69,10 @@ def test_fused_equals_unfused_bitwise(case):
     assert torch.equal(got["H_bf16"].view(torch.int16), ref["H_bf16"].view(torch.int16))
 
 
-@pytest.mark.parametrize("linear,L", [(False, 60), (True, 60), (False, 96)])
-def test_fused_matches_oracle(linear, L):
-    B, d_in, d, direction = 6, 192, 128, O.DIR_BI
+@pytest.mark.parametrize("linear,L,d_in", [(False, 60, 192), (True, 60, 192), (False, 96, 192),
+                                           (False, 70, 128), (True, 40, 128)])
+def test_fused_matches_oracle(linear, L, d_in):
+    B, d, direction = 6, 128, O.DIR_BI
     c = _case(L, B, d_in, d, direction, True, 5 + linear)
     got = _run(c, direction, {}, fused=True, linear=linear)
     torch.cuda.synchronize()
@@ -80,10 +86,10 @@ def test_fused_matches_oracle(linear, L):
 
 
 def test_fused_not_available_keeps_u_required():
-    """Where the fused kernel does not apply (fp32 products, k = 3, sequences
-    over 128 steps, d not a multiple of 64) U stays required."""
+    """Where the fused kernel does not apply (fp32 products, sequences over
+    128 steps, d not a multiple of 64) U stays required."""
     assert sru.fused_available(128, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
+    assert sru.fused_available(8, 2, 64, 64, O.DIR_FWD, O.GEMM_BF16)   # k = 3
     assert not sru.fused_available(8, 2, 128, 64, O.DIR_FWD, O.GEMM_FP32)
-    assert not sru.fused_available(8, 2, 64, 64, O.DIR_FWD, O.GEMM_BF16)   # k = 3
     assert not sru.fused_available(129, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
     assert not sru.fused_available(8, 2, 96, 32, O.DIR_FWD, O.GEMM_BF16)
