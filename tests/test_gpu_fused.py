@@ -8,11 +8,13 @@ against the oracle, the linear recurrence included."""
 import numpy as np
 import pytest
 import torch
+from hypothesis import HealthCheck, Phase, given, settings
+from hypothesis import strategies as st
 
 from helpers import TOL_BF16, check, dev
 from oracle import sru_oracle as O
 from paper_1709_02755_amd import sru
-from paper_1709_02755_amd.workloads import random_layer_case
+from paper_1709_02755_amd.workloads import irregular_mask, random_layer_case
 
 pytestmark = pytest.mark.gpu
 
@@ -93,3 +95,46 @@ def test_fused_not_available_keeps_u_required():
     assert not sru.fused_available(8, 2, 128, 64, O.DIR_FWD, O.GEMM_FP32)
     assert not sru.fused_available(129, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
     assert not sru.fused_available(8, 2, 96, 32, O.DIR_FWD, O.GEMM_BF16)
+
+
+SETTINGS = dict(deadline=None, derandomize=True, database=None, phases=[Phase.generate],
+                suppress_health_check=list(HealthCheck))
+
+
+@st.composite
+def fused_cases(draw):
+    L = draw(st.integers(1, 128))
+    B = draw(st.integers(1, 12))
+    d = draw(st.sampled_from([64, 128]))
+    d_in = draw(st.sampled_from([d, 8, 72, 192]))  # d: k = 3, else k = 4
+    direction = draw(st.sampled_from([O.DIR_FWD, O.DIR_REV, O.DIR_BI]))
+    mask = draw(st.sampled_from(["none", "suffix", "irregular"]))
+    alpha = draw(st.sampled_from([1.0, 1.7]))
+    reset_new = draw(st.booleans())
+    seed = draw(st.integers(0, 2 ** 16))
+    return L, B, d_in, d, direction, mask, alpha, reset_new, seed
+
+
+@settings(max_examples=40, **SETTINGS)
+@given(case=fused_cases())
+def test_fused_equals_unfused_on_random_cases(case):
+    """Random small shapes up to 128 steps, k = 3 and 4, every direction,
+    padding pattern and gate variant: the fused kernel's H, c_last and bf16
+    H equal the separate product and scan's, bit for bit.  (The linear
+    recurrence's separate scan evaluates its gates another way; its fused
+    results are held to the oracle above.)"""
+    L, B, d_in, d, direction, mask, alpha, reset_new, seed = case
+    print(f"fused case {case}", flush=True)
+    rng = np.random.default_rng(seed)
+    c = random_layer_case(rng, L, B, d_in, d, direction, masked=mask == "suffix", c0=True,
+                          bias_scale=0.5, v_scale=0.8)
+    if mask == "irregular":
+        c["mask"] = irregular_mask(rng, L, B)
+    assert sru.fused_available(L, B, d_in, d, direction, O.GEMM_BF16)
+    gv = dict(highway_scale=alpha, reset_new=reset_new)
+    ref = _run(c, direction, gv, fused=False)
+    got = _run(c, direction, gv, fused=True)
+    torch.cuda.synchronize()
+    for k in ("H", "c_last"):
+        assert torch.equal(got[k], ref[k]), (k, case)
+    assert torch.equal(got["H_bf16"].view(torch.int16), ref["H_bf16"].view(torch.int16)), case
