@@ -127,22 +127,26 @@ sru::GemmDesc gemm_desc(int op, bool bf16, int M, int N, int K, const void* A, l
 
 // Where inference (U and C not kept) runs the projection and the scan as one
 // kernel: bf16 products, whole groups of 64 hidden units, whole 16-byte
-// chunks of X rows, operands within the 2 GiB byte range of buffer loads;
-// four gate blocks (k = 4: a tile's columns are exactly the gates of 64
-// units); and sequences of at most 128 steps, so that at least two
-// sequences share a tile (a wave's lanes scan two).  Every lane scans from
-// its own accumulators, about 23 ns a step; at 64 to 128 steps per tile the
-// fused kernel measured 1.3-2x faster than the separate product and scan.
-constexpr int kFusedMaxL = 128;
+// chunks of X rows, operands within the 2 GiB byte range of buffer loads.
+// Every lane scans from its own accumulators, about 23 ns a step, and a
+// workgroup carries c from one time block to the next, so any length runs;
+// it is the faster organisation at up to 128 steps (1.3-2x, measured), and
+// beyond that where tiles of two sequences give every CU a workgroup
+// (1.2-1.65x at 256-512 steps; even at 128 workgroups, slower below).
+constexpr int kFusedShortL = 128;
+constexpr long long kFusedMinGroups = 256;
 bool fused_ok(const Dims& s, int gemm_dtype) {
-  return gemm_dtype == SRU_GEMM_BF16 && s.L <= kFusedMaxL && s.d % 64 == 0 &&
-         s.d_in % 8 == 0 && 2 * s.M * s.d_in < (1LL << 31) && 2 * s.N * s.d_in < (1LL << 31);
+  const long long groups = (long long)s.ndir * (s.d / 64) * ((s.B + 1) / 2);
+  return gemm_dtype == SRU_GEMM_BF16 && (s.L <= kFusedShortL || groups >= kFusedMinGroups) &&
+         s.d % 64 == 0 && s.d_in % 8 == 0 && 2 * s.M * s.d_in < (1LL << 31) &&
+         2 * s.N * s.d_in < (1LL << 31);
 }
+
 // Sequences per fused tile: the tile holds 256 rows of (step, sequence)
-// pairs in time chunks of 32 steps: 2 sequences of up to 128 steps, 4 of up
-// to 64, or 8 of up to 32.
+// pairs in time chunks of 32 steps: 8 sequences of up to 32 steps, 4 of up
+// to 64, else 2 (longer sequences take several blocks of 128 steps).
 int fused_seqs_per_tile(int L) {
-  int bb = 1;
+  int bb = 2;
   while (bb < 8 && 256 / (2 * bb) >= L) bb *= 2;
   return bb;
 }

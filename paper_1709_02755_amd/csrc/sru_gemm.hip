@@ -1086,40 +1086,12 @@ __global__ __launch_bounds__(512, 1) void proj_scan_fwd_kernel(FusedFwdArgs a) {
         return (long long)(dir * KB + gate) * d + g * 64 + cw * 32 + (col & 31);
       },
       a.d_in);
-  // tile row r: wave row r / 64 = (sequence pair, time chunk); in a 32-row
-  // block, row rr is sequence (rr / 4) % 2 of the pair at step
-  // 4 (rr / 8) + rr % 4 of the block's 16 (the MFMA's row of element e)
-  OpA la;
-  la.init_rows(
-      wave, lane,
-      [&](int r) -> long long {
-        const int wr = r >> 6, rr = r & 31;
-        const int b = b0 + 2 * (wr / nchunk) + ((rr >> 2) & 1);
-        const int t = 32 * (wr % nchunk) + 16 * ((r >> 5) & 1) + 4 * (rr >> 3) + (rr & 3);
-        return t < L && b < Bs ? (long long)t * Bs + b : -1;
-      },
-      a.d_in);
-  floatx16 acc[C::FM][C::FN];
-  direct_mainloop<C, false>(smem, la, lb, ra, rb, a.d_in, a.d_in, 0, a.d_in, wave, lane,
-                            wm * C::WM, wn * C::WN, acc);
-
-  // this lane's scan: sequence sb, unit 64 g + 32 wn + lane % 32, time chunk q2
+  // this lane's scan: sequence sb, unit 64 g + 32 wn + lane % 32, time chunk
+  // q2 of every block; c carries over from block to block
   const int sb = b0 + 2 * pair + (lane >> 5);
   const bool live = sb < Bs;
   const int unit = g * 64 + wn * 32 + (lane & 31);
   const long long fidx = (long long)dir * d + unit;
-  // k = 3: the highway input x_t of the wave's chunk, loaded now so that it
-  // arrives while earlier chunks scan (steps past L re-read step L - 1)
-  float xr[32];
-  if constexpr (KB == 3) {
-    if (live) {
-      const float* xp = a.X + (long long)sb * a.d_in + unit;
-      const long long xs = (long long)Bs * a.d_in;
-#pragma unroll
-      for (int tt = 0; tt < 32; ++tt) xr[tt] = xp[min(32 * q2 + tt, L - 1) * xs];
-    }
-  }
-  (void)xr;
   float vf = 0.f, vr = 0.f, bf = 0.f, br = 0.f, c = 0.f;
   if (live) {
     if (!a.linear) {
@@ -1142,98 +1114,139 @@ __global__ __launch_bounds__(512, 1) void proj_scan_fwd_kernel(FusedFwdArgs a) {
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
   };
-  barrier();  // every wave is done with the operand stages: LDS now holds the hand-over of c
+  // hand-over of c between the waves of consecutive chunks, in LDS, which is
+  // free between a block's product and the next block's
   float* cx = reinterpret_cast<float*>(smem) + (pair * C::WAVES_N + wn) * 64 + lane;
 
-  // the 32 steps of time chunk q (scan order: backward for a reverse
-  // direction); steps at or past L are not computed.  A whole chunk runs
-  // without a branch between its steps, so the compiler can overlap one
-  // step's output (reset gate, h, stores) with the next step's chain.
-  auto scan_chunk = [&](auto rev_c, auto whole_c, auto hb_c, int q) {
-    constexpr bool RV = decltype(rev_c)::value, WHOLE = decltype(whole_c)::value;
-    constexpr bool HB = decltype(hb_c)::value;
-    const int tb = 32 * q;
-    const int nv = min(32, L - tb);
-    // padding bits of the chunk's steps: lane u of each half reads step
-    // tb + u of its sequence, and the ballot hands each half its 32 bits
-    unsigned mbits = 0;
-    if (a.mask) {
-      const int tm = tb + (lane & 31);
-      const bool pad = live && tm < L && a.mask[(long long)tm * Bs + sb] != 0;
-      mbits = (unsigned)(__ballot(pad) >> (32 * (lane >> 5)));
-    }
-    if (!live) return;
-    // output offset at the chunk's first step in scan order, moved one step
-    // at a time (the empty asm keeps the compiler from precomputing every
-    // step's offset)
-    const int tt0 = RV ? (WHOLE ? 31 : nv - 1) : 0;
-    long long o = ((long long)(tb + tt0) * Bs + sb) * nfeat + fidx;
-    const long long dstep = (RV ? -1LL : 1LL) * Bs * nfeat;
-    // A step carries c forward first (Eq. 1-2) and then finishes the
-    // previous step's output (Eq. 3-4, the store), which no longer lies on
-    // the chain from one c to the next.
-    float p_cn = 0.f, p_rin = 0.f, p_zr = 0.f, p_xh = 0.f;
-    bool p_pad = false, pend = false;
-    auto emit = [&]() {
-      const float r = sigmoid_scaled(fmaf(vrs, p_rin, p_zr));        // Eq. 3
-      float h = fmaf(r, p_cn, (1.0f - r) * (alpha * p_xh));          // Eq. 4 (Sec. 3.2)
-      h = p_pad ? 0.0f : h;
-      __builtin_nontemporal_store(h, a.H + o);
-      if constexpr (HB)
-        __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), a.Hb + o);
-      o += dstep;
-      asm volatile("" : "+v"(o));
-    };
+  const int TB = 32 * nchunk;  // steps per block
+  const int nblk = (L + TB - 1) / TB;
+  int prev = -1;  // the time chunk scanned last (-1: none yet)
+  for (int ib = 0; ib < nblk; ++ib) {
+    const int t0 = (rev ? nblk - 1 - ib : ib) * TB;  // blocks in the direction's order
+    // tile row r: wave row r / 64 = (sequence pair, time chunk); in a 32-row
+    // block, row rr is sequence (rr / 4) % 2 of the pair at step
+    // 4 (rr / 8) + rr % 4 of the block's 16 (the MFMA's row of element e)
+    OpA la;
+    la.init_rows(
+        wave, lane,
+        [&](int r) -> long long {
+          const int wr = r >> 6, rr = r & 31;
+          const int b = b0 + 2 * (wr / nchunk) + ((rr >> 2) & 1);
+          const int t =
+              t0 + 32 * (wr % nchunk) + 16 * ((r >> 5) & 1) + 4 * (rr >> 3) + (rr & 3);
+          return t < L && b < Bs ? (long long)t * Bs + b : -1;
+        },
+        a.d_in);
+    floatx16 acc[C::FM][C::FN];
+    direct_mainloop<C, false>(smem, la, lb, ra, rb, a.d_in, a.d_in, 0, a.d_in, wave, lane,
+                              wm * C::WM, wn * C::WN, acc);
+    // k = 3: the highway input x_t of the wave's chunk, loaded now so that it
+    // arrives while earlier chunks scan (steps past L re-read step L - 1)
+    float xr[32];
+    if constexpr (KB == 3) {
+      if (live) {
+        const float* xp = a.X + (long long)sb * a.d_in + unit;
+        const long long xs = (long long)Bs * a.d_in;
 #pragma unroll
-    for (int s = 0; s < 32; ++s) {
-      const int tt = RV ? 31 - s : s;
-      if (WHOLE || tt < nv) {
-        const float u0 = acc[tt >> 4][0][tt & 15], u1 = acc[tt >> 4][1][tt & 15];
-        const float u2 = acc[tt >> 4][2][tt & 15];
-        float xh;
-        if constexpr (KB == 4) xh = acc[tt >> 4][3][tt & 15];
-        else xh = xr[tt];
-        const float f = sigmoid_scaled(fmaf(vfs, c, fmaf(u1, kNegLog2e, bfs)));  // Eq. 1
-        const float cn = fmaf(f, c, fmaf(-f, u0, u0));                           // Eq. 2
-        const float rin = rn ? cn : c;
-        const bool pad = (mbits >> tt) & 1u;
-        c = pad ? c : cn;
-        if (WHOLE ? s > 0 : pend) emit();
-        p_cn = cn;
-        p_rin = rin;
-        p_zr = fmaf(u2, kNegLog2e, brs);
-        p_xh = xh;
-        p_pad = pad;
-        pend = true;
+        for (int tt = 0; tt < 32; ++tt) xr[tt] = xp[min(t0 + 32 * q2 + tt, L - 1) * xs];
       }
     }
-    if (pend) emit();
-  };
-  // one instantiation per (direction of time, whole chunk, bf16 copy of H)
-  auto scan_any = [&](auto rev_c, int q) {
-    const bool whole = L - 32 * q >= 32;
-    if (whole) {
-      if (a.Hb) scan_chunk(rev_c, BoolC<true>{}, BoolC<true>{}, q);
-      else scan_chunk(rev_c, BoolC<true>{}, BoolC<false>{}, q);
-    } else {
-      if (a.Hb) scan_chunk(rev_c, BoolC<false>{}, BoolC<true>{}, q);
-      else scan_chunk(rev_c, BoolC<false>{}, BoolC<false>{}, q);
+    (void)xr;
+    barrier();  // every wave is done with the operand stages
+
+    // the 32 steps of the chunk from step tb (scan order: backward for a
+    // reverse direction); steps at or past L are not computed.  A whole
+    // chunk runs without a branch between its steps, so the compiler can
+    // overlap one step's output (reset gate, h, stores) with the next step's
+    // chain.
+    auto scan_chunk = [&](auto rev_c, auto whole_c, auto hb_c, int tb) {
+      constexpr bool RV = decltype(rev_c)::value, WHOLE = decltype(whole_c)::value;
+      constexpr bool HB = decltype(hb_c)::value;
+      const int nv = min(32, L - tb);
+      // padding bits of the chunk's steps: lane u of each half reads step
+      // tb + u of its sequence, and the ballot hands each half its 32 bits
+      unsigned mbits = 0;
+      if (a.mask) {
+        const int tm = tb + (lane & 31);
+        const bool pad = live && tm < L && a.mask[(long long)tm * Bs + sb] != 0;
+        mbits = (unsigned)(__ballot(pad) >> (32 * (lane >> 5)));
+      }
+      if (!live) return;
+      // output offset at the chunk's first step in scan order, moved one
+      // step at a time (the empty asm keeps the compiler from precomputing
+      // every step's offset)
+      const int tt0 = RV ? (WHOLE ? 31 : nv - 1) : 0;
+      long long o = ((long long)(tb + tt0) * Bs + sb) * nfeat + fidx;
+      const long long dstep = (RV ? -1LL : 1LL) * Bs * nfeat;
+      // A step carries c forward first (Eq. 1-2) and then finishes the
+      // previous step's output (Eq. 3-4, the store), which no longer lies on
+      // the chain from one c to the next.
+      float p_cn = 0.f, p_rin = 0.f, p_zr = 0.f, p_xh = 0.f;
+      bool p_pad = false, pend = false;
+      auto emit = [&]() {
+        const float r = sigmoid_scaled(fmaf(vrs, p_rin, p_zr));        // Eq. 3
+        float h = fmaf(r, p_cn, (1.0f - r) * (alpha * p_xh));          // Eq. 4 (Sec. 3.2)
+        h = p_pad ? 0.0f : h;
+        __builtin_nontemporal_store(h, a.H + o);
+        if constexpr (HB)
+          __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), a.Hb + o);
+        o += dstep;
+        asm volatile("" : "+v"(o));
+      };
+#pragma unroll
+      for (int s = 0; s < 32; ++s) {
+        const int tt = RV ? 31 - s : s;
+        if (WHOLE || tt < nv) {
+          const float u0 = acc[tt >> 4][0][tt & 15], u1 = acc[tt >> 4][1][tt & 15];
+          const float u2 = acc[tt >> 4][2][tt & 15];
+          float xh;
+          if constexpr (KB == 4) xh = acc[tt >> 4][3][tt & 15];
+          else xh = xr[tt];
+          const float f = sigmoid_scaled(fmaf(vfs, c, fmaf(u1, kNegLog2e, bfs)));  // Eq. 1
+          const float cn = fmaf(f, c, fmaf(-f, u0, u0));                           // Eq. 2
+          const float rin = rn ? cn : c;
+          const bool pad = (mbits >> tt) & 1u;
+          c = pad ? c : cn;
+          if (WHOLE ? s > 0 : pend) emit();
+          p_cn = cn;
+          p_rin = rin;
+          p_zr = fmaf(u2, kNegLog2e, brs);
+          p_xh = xh;
+          p_pad = pad;
+          pend = true;
+        }
+      }
+      if (pend) emit();
+    };
+    // one instantiation per (direction of time, whole chunk, bf16 copy of H)
+    auto scan_any = [&](auto rev_c, int tb) {
+      const bool whole = L - tb >= 32;
+      if (whole) {
+        if (a.Hb) scan_chunk(rev_c, BoolC<true>{}, BoolC<true>{}, tb);
+        else scan_chunk(rev_c, BoolC<true>{}, BoolC<false>{}, tb);
+      } else {
+        if (a.Hb) scan_chunk(rev_c, BoolC<false>{}, BoolC<true>{}, tb);
+        else scan_chunk(rev_c, BoolC<false>{}, BoolC<false>{}, tb);
+      }
+    };
+    for (int i = 0; i < nchunk; ++i) {
+      const int q = rev ? nchunk - 1 - i : i;  // the chunk scanned now
+      if (nchunk > 1 && prev >= 0) {
+        // the wave of the previous chunk (of this block or the one before)
+        // hands its c over
+        if (q2 == prev) *cx = c;
+        barrier();
+        if (q2 == q) c = *cx;
+      }
+      if (q2 == q) {
+        if (rev) scan_any(BoolC<true>{}, t0 + 32 * q);
+        else scan_any(BoolC<false>{}, t0 + 32 * q);
+      }
+      prev = q;
     }
-  };
-  for (int i = 0; i < nchunk; ++i) {
-    const int q = rev ? nchunk - 1 - i : i;  // the chunk scanned now
-    if (i > 0) {
-      // the wave of the previous chunk hands its c over
-      if (q2 == (rev ? q + 1 : q - 1)) *cx = c;
-      barrier();
-      if (q2 == q) c = *cx;
-    }
-    if (q2 == q) {
-      if (rev) scan_any(BoolC<true>{}, q);
-      else scan_any(BoolC<false>{}, q);
-    }
+    barrier();  // the hand-over's LDS reads are done before the next block's loads
   }
-  if (live && a.c_last && q2 == (rev ? 0 : nchunk - 1)) a.c_last[(long long)sb * nfeat + fidx] = c;
+  if (live && a.c_last && q2 == prev) a.c_last[(long long)sb * nfeat + fidx] = c;
 }
 
 template <class C, int ADD, bool A_RC, bool B_RC, bool OB = false>
@@ -1796,7 +1809,7 @@ hipError_t to_bf16_launch(const float* src, int rows, int cols, uint16_t* dst, b
 hipError_t proj_scan_forward_launch(const FusedFwdArgs& a, hipStream_t st) {
   // a tile holds 256 / bb steps of bb sequences, in time chunks of 32 steps;
   // k = 3 reads x_t from X (d_in = d)
-  if ((a.bb != 2 && a.bb != 4 && a.bb != 8) || a.L > 256 / a.bb || (a.k != 3 && a.k != 4) ||
+  if ((a.bb != 2 && a.bb != 4 && a.bb != 8) || (a.k != 3 && a.k != 4) ||
       (a.k == 3 && (!a.X || a.d_in != a.d)))
     return hipErrorInvalidValue;
   const int grid = a.ndir * a.ngroups * a.nbgroups;

@@ -266,7 +266,8 @@ def test_forward_without_u_needs_the_fused_path():
     assert lib.sru_forward_fused_available(4, 2, 60, 64, 0, 1) == 0   # d_in % 8
     assert lib.sru_forward_fused_available(4, 2, 64, 32, 0, 1) == 0   # d % 64
     assert lib.sru_forward_fused_available(128, 2, 128, 64, 0, 1) == 1
-    assert lib.sru_forward_fused_available(129, 2, 128, 64, 0, 1) == 0  # L > 128
+    assert lib.sru_forward_fused_available(129, 2, 128, 64, 0, 1) == 0  # L > 128, 1 tile
+    assert lib.sru_forward_fused_available(1024, 32, 1024, 1024, 0, 1) == 1  # 256 tiles
     # U omitted: fp32 products, or C kept, leave U required
     assert _fwd(lib, d_in=128, d=64, U=None, C=None) == E_NULL
     assert _fwd(lib, d_in=128, d=64, gemm=1, U=None, C=FAKE) == E_NULL

@@ -1,9 +1,9 @@
 """The fused projection + scan of inference (sru_forward with U and C
-omitted; at most 128 steps): H, c_last and the bf16 copy of H equal
-the unfused call's bit for bit (the scan reads the same fp32 projections, in
-the same order), across k = 3 and 4, tile plans of 2, 4 and 8 sequences, ragged step and
-sequence counts, every direction, padding, c0 and the gate variants; and
-against the oracle, the linear recurrence included."""
+omitted): H, c_last and the bf16 copy of H equal the unfused call's bit for
+bit (the scan reads the same fp32 projections, in the same order), across
+k = 3 and 4, tile plans of 2, 4 and 8 sequences, several time blocks per
+tile, ragged step and sequence counts, every direction, padding, c0 and the
+gate variants; and against the oracle, the linear recurrence included."""
 
 import numpy as np
 import pytest
@@ -33,6 +33,11 @@ CASES = [
     (50, 6, 128, 128, O.DIR_REV, True, 1.7, True),
     (100, 5, 128, 128, O.DIR_BI, True, 1.0, False),
     (17, 11, 64, 64, O.DIR_BI, False, float(np.sqrt(3.0)), False),
+    # longer than 128 steps where tiles of two sequences fill the chip: time
+    # blocks of 128 steps, c carried from block to block
+    (300, 32, 1024, 1024, O.DIR_FWD, True, 1.0, False),  # 3 blocks, the last of 44 steps
+    (200, 16, 256, 2048, O.DIR_REV, True, 1.7, True),    # k = 4, reverse
+    (150, 16, 1024, 1024, O.DIR_BI, True, 1.0, False),   # both directions, 22-step block
 ]
 
 
@@ -89,8 +94,11 @@ def test_fused_matches_oracle(linear, L, d_in):
 
 def test_fused_not_available_keeps_u_required():
     """Where the fused kernel does not apply (fp32 products, sequences over
-    128 steps, d not a multiple of 64) U stays required."""
+    128 steps with too few tiles to fill the chip, d not a multiple of 64) U
+    stays required."""
     assert sru.fused_available(128, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
+    assert sru.fused_available(1024, 32, 1024, 1024, O.DIR_FWD, O.GEMM_BF16)  # 256 tiles
+    assert not sru.fused_available(1024, 30, 1024, 1024, O.DIR_FWD, O.GEMM_BF16)  # 240
     assert sru.fused_available(8, 2, 64, 64, O.DIR_FWD, O.GEMM_BF16)   # k = 3
     assert not sru.fused_available(8, 2, 128, 64, O.DIR_FWD, O.GEMM_FP32)
     assert not sru.fused_available(129, 2, 128, 64, O.DIR_FWD, O.GEMM_BF16)
