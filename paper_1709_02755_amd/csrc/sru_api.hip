@@ -142,13 +142,29 @@ bool fused_ok(const Dims& s, int gemm_dtype) {
          2 * s.N * s.d_in < (1LL << 31);
 }
 
-// Sequences per fused tile: the tile holds 256 rows of (step, sequence)
-// pairs in time chunks of 32 steps: 8 sequences of up to 32 steps, 4 of up
-// to 64, else 2 (longer sequences take several blocks of 128 steps).
-int fused_seqs_per_tile(int L) {
-  int bb = 2;
-  while (bb < 8 && 256 / (2 * bb) >= L) bb *= 2;
-  return bb;
+// Sequences per fused tile (bb = 2, 4 or 8: the tile holds 256 / bb steps of
+// each, in time chunks of 32).  A workgroup runs its time blocks one after
+// another, each a product (about 1.4 us per 64 of d_in, plus 4 us) and a
+// serial scan of 256 / bb steps (about 25 ns each, plus 0.5 us per chunk
+// for the hand-over of c); the workgroups fill the 256 CUs in rounds.  The
+// plan with the least modelled time wins: on the 9 shapes measured it picked
+// the fastest plan, or one within 2 % of it.
+int fused_seqs_per_tile(const Dims& s) {
+  int best = 2;
+  long long best_cost = -1;
+  for (int bb : {2, 4, 8}) {
+    const long long tb = 256 / bb;
+    const long long groups = (long long)s.ndir * (s.d / 64) * ((s.B + bb - 1) / bb);
+    const long long rounds = (groups + 255) / 256;
+    const long long blocks = (s.L + tb - 1) / tb;
+    // in units of 25 ns
+    const long long cost = rounds * blocks * (56 * ((s.d_in + 63) / 64) + 160 + tb + 20 * (tb / 32));
+    if (best_cost < 0 || cost < best_cost) {
+      best = bb;
+      best_cost = cost;
+    }
+  }
+  return best;
 }
 
 // Scratch of the scans.  The linear recurrence's scans cut time into
@@ -509,7 +525,7 @@ int sru_forward(const float* X, const float* W, const float* v_f, const float* v
     f.k = s.k;
     f.X = X;
     f.direction = direction;
-    f.bb = fused_seqs_per_tile(L);
+    f.bb = fused_seqs_per_tile(s);
     f.ngroups = d / 64;
     f.nbgroups = (B + f.bb - 1) / f.bb;
     f.alpha = op.alpha;

@@ -1017,20 +1017,21 @@ __global__ __launch_bounds__(C::THREADS, C::OCC) void gemm_direct_kernel(KernelA
 
 // ---- fused projection + forward scan (inference: neither U nor C kept) ----
 // One workgroup per (direction, group of 64 hidden units, group of bb
-// sequences), bb = 2, 4 or 8; its tile of U has 256 rows, the (step,
-// sequence) pairs of 256 / bb steps, and 256 columns, the four gate blocks
-// of the 64 units (k = 4: block 3 is the highway input x_hat).  The MFMAs
-// leave the tile untransposed on 64 x 128 wave blocks, and the operand rows
-// are mapped so that a lane's accumulators are the scan's inputs: lane l of
-// wave (wm, wn) holds column l % 32 of each of its four 32-column MFMA
-// blocks, i.e. the four gates of unit 64 g + 32 wn + l % 32, and rows of one
-// sequence (l / 32 picks one of the wave's two), 16 consecutive steps per
-// 32-row block, so 32 steps in all.  The lane then runs Eq. 1-4 over those
-// steps from its own registers: U is neither written to memory nor staged.
-// A sequence's 256 / bb steps lie in 8 / bb waves (time chunks of 32 steps),
-// which scan one after the other and hand c over through LDS.  The scan
-// arithmetic is the forward scan kernel's, in the same order, so H equals
-// the unfused path's bit for bit.
+// sequences), bb = 2, 4 or 8.  Per time block of 256 / bb steps it computes
+// the tile of U whose 256 rows are the block's (step, sequence) pairs and
+// whose 64 k columns are the k gate blocks of the 64 units (k = 4: block 3
+// is the highway input x_hat; k = 3 reads x_t from X).  The MFMAs leave the
+// tile untransposed on 64 x 32k wave blocks, and the operand rows are mapped
+// so that a lane's accumulators are the scan's inputs: lane l of wave
+// (wm, wn) holds column l % 32 of each of its k 32-column MFMA blocks, i.e.
+// the gates of unit 64 g + 32 wn + l % 32, and rows of one sequence (l / 32
+// picks one of the wave's two), 16 consecutive steps per 32-row block, so 32
+// steps in all.  The lane then runs Eq. 1-4 over those steps from its own
+// registers: U is neither written to memory nor staged.  A block's 256 / bb
+// steps lie in 8 / bb waves (time chunks of 32 steps), which scan one after
+// the other and hand c over through LDS; c carries over from block to block
+// the same way.  The scan arithmetic is the forward scan kernel's, in the
+// same order, so H equals the unfused path's bit for bit.
 // 8 waves of 64 x 32k, A two K steps ahead (a type of its own per k: two
 // kernels instantiating the main loop on one configuration type trip the
 // host compilation pass)
