@@ -158,7 +158,11 @@ SRU_API size_t sru_backward_workspace_bytes(int L, int B, int d_in, int d, int d
  *        X_bf16).
  */
 /* 1 when sru_forward accepts U = NULL with C = NULL for these sizes (the
- * fused projection + scan of inference), else 0. */
+ * fused projection + scan of inference), else 0: bf16 products, d % 64 == 0,
+ * d_in % 8 == 0, bf16 operands below 2 GiB, and either L <= 128 or
+ * ndir * (d / 64) * ceil(B / 2) >= 256 (enough tiles of two sequences to
+ * give every CU of the chip one; with fewer, the separate projection and
+ * scan are faster on long sequences). */
 SRU_API int sru_forward_fused_available(int L, int B, int d_in, int d, int direction,
                                         int gemm_dtype);
 
