@@ -118,3 +118,34 @@ def test_default_options_equal_no_options():
         outs.append(H)
     torch.cuda.synchronize()
     assert torch.equal(outs[0], outs[1])
+
+
+@pytest.mark.parametrize("gemm", [O.GEMM_FP32, O.GEMM_BF16])
+def test_layer_with_the_papers_reset_bias(gemm):
+    """The setting of the character-level language model experiments (Sec.
+    4): the reset gate's bias at -3, so the gate starts mostly closed and the
+    highway carries most of x, with the correction Sec. 3.2 gives for a
+    non-zero bias, alpha = sqrt(1 + 2 e^-3); a whole layer, forward and
+    backward, against the oracle."""
+    L, B, d, direction = 29, 5, 128, O.DIR_BI
+    c = _case(77 + gemm, L, B, d, d, direction, masked=True, c0=True, dc_last=True,
+              bias_scale=0.5)
+    c["b_r"] = np.full_like(c["b_r"], -3.0)
+    alpha = O.scaling_alpha(-3.0)
+    X, W = dev(c["X"]), dev(c["W"])
+    p = [dev(c[k]) for k in ("v_f", "v_r", "b_f", "b_r")]
+    c0, mask = dev(c["c0"]), dev(c["mask"])
+    fw = sru.forward(X, W, *p, c0=c0, direction=direction, mask=mask, gemm_dtype=gemm,
+                     highway_scale=alpha)
+    bw = sru.backward(X, W, *p, fw["U"], fw["C"], dev(c["dH"]), c0=c0, dc_last=dev(c["dc_last"]),
+                      direction=direction, mask=mask, gemm_dtype=gemm, highway_scale=alpha)
+    torch.cuda.synchronize()
+    args = (c["X"], c["W"], c["v_f"], c["v_r"], c["b_f"], c["b_r"])
+    rf = O.forward(*args, c["c0"], direction, c["mask"], gemm, alpha=alpha)
+    rb = O.backward(*args, c["dH"], c["c0"], direction, c["mask"], gemm, c["dc_last"], fw=rf,
+                    alpha=alpha)
+    tol = TOL_FP32 if gemm == O.GEMM_FP32 else TOL_BF16
+    for k in ("H", "C", "c_last"):
+        check(k, fw[k], rf[k], tol)
+    for k in ("dX", "dW", "dv_f", "dv_r", "db_f", "db_r", "dc0"):
+        check(k, bw[k], rb[k], tol)
