@@ -123,15 +123,25 @@ __global__ __launch_bounds__(kScanThreads) void scan_fwd_kernel(ScanShape s, Sca
 #pragma unroll
   for (int p = 0; p < PF; ++p) load(r0[p], r1[p], r2[p], rx[p], rm[p]);
 
-  int s0 = 0;
-  for (; s0 + PF <= L; s0 += PF) {
+  auto ring = [&]() {
 #pragma unroll
     for (int p = 0; p < PF; ++p) {
       step(r0[p], r1[p], r2[p], rx[p], rm[p]);
-      load(r0[p], r1[p], r2[p], rx[p], rm[p]);  // step s0 + p + PF (or the last)
+      load(r0[p], r1[p], r2[p], rx[p], rm[p]);  // PF steps ahead (or the last step)
       // keep each prefetch where it is: sunk loads shorten the distance
       __builtin_amdgcn_sched_barrier(0);
     }
+  };
+  // The first ring is peeled off the loop, so the loop is entered with the
+  // memory operations of a whole ring in flight, as on its back edge: the
+  // compiler derives each step's wait for its loads from both paths, and
+  // from the prologue's loads alone the ring's first step would wait for
+  // loads issued 3 steps back instead of PF (L 256, B 8, d 1024:
+  // 33.0 -> 31.9 us).
+  int s0 = 0;
+  if (PF <= L) {
+    ring();
+    for (s0 = PF; s0 + PF <= L; s0 += PF) ring();
   }
 #pragma unroll
   for (int p = 0; p < PF; ++p)
@@ -466,6 +476,12 @@ __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, Sca
 
 #pragma unroll
   for (int p = 0; p < PF; ++p) load(r0[p], r1[p], r2[p], rx[p], rdh[p], rcp[p], rm[p]);
+  // The loop is entered from the prologue, whose loads alone set the
+  // waits of the first steps of every ring (a lead of 3 steps, not PF, on
+  // the ring's first step).  With the first ring peeled off, every step
+  // waits for loads PF steps back, and the scan was slower: more memory
+  // operations per wave than the memory system serves best (L 256, B 64,
+  // d 1024: 92.5 -> 96.7 us; L 400, B 32, d 128: 72.0 -> 78.9 us).
   int i0 = 0;
   for (; i0 + PF <= L; i0 += PF) {
 #pragma unroll
