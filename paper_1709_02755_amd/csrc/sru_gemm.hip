@@ -500,11 +500,40 @@ __device__ __forceinline__ void write_tile_staged(const KernelArgs& g,
                                                   const floatx16 (&acc)[C::FM][C::FN],
                                                   unsigned char* smem, int m0, int n0, int wm0,
                                                   int wn0, int lane, int wave, int split) {
-  static_assert(C::WN == 64, "16 lanes per 256-byte staged row");
-  static_assert(C::WAVES * 32 * kStagePitch * 4 <= C::LDS, "staging fits the operand stages");
-  float* blk = reinterpret_cast<float*>(smem) + wave * 32 * kStagePitch;
+  static_assert(C::WN == 64 || C::WN == 96, "staged rows of 64 or 96 columns");
   float* out = g.out + (long long)split * g.split_stride;
   const int cl = 4 * (lane >> 5);
+  if constexpr (C::WN == 96) {
+    // 96-column wave blocks: rows of 24 16-byte chunks (pitch 100 floats, 4
+    // past a multiple of 32 banks as for 64 columns), read back as 12 passes
+    // of 64 consecutive chunks of the 32-row group (runs of 384 bytes)
+    static_assert(ADD == 0, "the 96-column tiles serve products without an addend");
+    constexpr int P = 100, CPR = 24;
+    static_assert(C::WAVES * 32 * P * 4 <= C::LDS, "staging fits the operand stages");
+    float* blk = reinterpret_cast<float*>(smem) + wave * 32 * P;
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          floatx4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e];
+          *reinterpret_cast<floatx4*>(blk + (lane & 31) * P + j * 32 + 8 * q + cl) = v;
+        }
+#pragma unroll
+      for (int s = 0; s < 32 * CPR / 64; ++s) {
+        const int ch = s * 64 + lane, r = ch / CPR, col = 4 * (ch % CPR);
+        const long long mrow = m0 + wm0 + i * 32 + r;
+        *reinterpret_cast<floatx4*>(out + mrow * g.ldo + n0 + wn0 + col) =
+            *reinterpret_cast<const floatx4*>(blk + r * P + col);
+      }
+    }
+    return;
+  }
+  static_assert(C::WAVES * 32 * kStagePitch * 4 <= C::LDS, "staging fits the operand stages");
+  float* blk = reinterpret_cast<float*>(smem) + wave * 32 * kStagePitch;
   const int rr = lane >> 4, cc = 4 * (lane & 15);  // read-back: rows rr + 4 s, columns cc..cc+3
 #pragma unroll
   for (int i = 0; i < C::FM; ++i) {
@@ -719,6 +748,7 @@ using DirectWide = DCfg<256, 256, 32, 2, 4, 4>;  // 8 waves, 1 workgroup per CU
 using DirectLine = DCfg<256, 256, 64, 2, 4, 2>;  // 8 waves, whole-line loads
 using DirectLineA3 = DCfg<256, 256, 64, 2, 4, 2, 3>;  // the same, A two K steps ahead (160 KiB)
 using DirectNarrow = DCfg<256, 128, 64, 2, 2, 2, 3>;  // 4 waves, whole-line loads, half the columns
+using DirectN96 = DCfg<256, 96, 64, 4, 1, 2, 3>;  // 4 waves of 64 x 96
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_t;
@@ -1627,9 +1657,25 @@ bool use_narrow(const GemmDesc& g) {
   return tiles < 256;
 }
 
+using CfgN96 = DirectN96;
+// A product that is never split and has no addend (U = X W^T), whose
+// 256 x 128 tiles still leave CUs idle and whose N is a whole number of
+// 96-column tiles that fill more of them, runs on 256 x 96 tiles (one GPU's
+// share of a batch: 2,048 tokens x 3,072 columns make 256 such tiles against
+// 192 of 256 x 128).
+bool use_n96(const GemmDesc& g) {
+  if (!use_narrow(g) || split_allowed(g) || g.add_count != 0 || g.N % CfgN96::BN != 0)
+    return false;
+  const long long tm = (g.M + CfgN96::BM - 1) / CfgN96::BM;
+  const long long t128 = tm * ((g.N + CfgNarrow::BN - 1) / CfgNarrow::BN);
+  const long long t96 = tm * (g.N / CfgN96::BN);
+  return t128 < 256 && t96 > t128 && t96 <= 256;
+}
+
 // The split count of the configuration gemm_launch runs g on.
 int direct_splits(const GemmDesc& g) {
   if (!g.a_kc || !g.b_kc) return direct_splits_cfg<CfgDirect>(g);
+  if (use_n96(g)) return 1;
   if (use_narrow(g)) return direct_splits_cfg<CfgNarrow>(g);
   return direct_splits_cfg<CfgDirectKC>(g);
 }
@@ -1649,6 +1695,7 @@ SRU_DIRECT_INST(CfgDirect, 1, false, true, false)
 SRU_DIRECT_INST(CfgDirect, 2, false, true, false)
 SRU_DIRECT_INST(CfgDirectKC, 0, false, false, true)
 SRU_DIRECT_INST(CfgNarrow, 0, false, false, false)
+SRU_DIRECT_INST(CfgN96, 0, false, false, false)
 SRU_DIRECT_INST(CfgNarrow, 1, false, false, false)
 SRU_DIRECT_INST(CfgNarrow, 2, false, false, false)
 SRU_DIRECT_INST(CfgNarrow, 0, false, false, true)
@@ -1694,6 +1741,7 @@ hipError_t launch_direct_cfg(const GemmDesc& g, hipStream_t st) {
   const int nwg = a.tiles_m * a.tiles_n * splits;
   timing_before(g.label ? g.label : !g.b_kc ? (g.a_kc ? "gemm_nn" : "gemm_tn") : "gemm_nt", st);
   if constexpr (OB) launch_direct<C, 0, A_RC, B_RC, true>(a, nwg, st);
+  else if constexpr (C::WN == 96) launch_direct<C, 0, A_RC, B_RC>(a, nwg, st);  // no addend
   else if (a.add_count == 2) launch_direct<C, 2, A_RC, B_RC>(a, nwg, st);
   else if (a.add_count == 1) launch_direct<C, 1, A_RC, B_RC>(a, nwg, st);
   else launch_direct<C, 0, A_RC, B_RC>(a, nwg, st);
@@ -1761,6 +1809,7 @@ hipError_t gemm_launch(const GemmDesc& g, hipStream_t st) {
     }
     if (!g.a_kc) return launch_direct_cfg<CfgDirect, true, true>(g, st);
     if (!g.b_kc) return launch_direct_cfg<CfgDirect, false, true>(g, st);
+    if (use_n96(g)) return launch_direct_cfg<CfgN96, false, false>(g, st);
     if (use_narrow(g)) return launch_direct_cfg<CfgNarrow, false, false>(g, st);
     return launch_direct_cfg<CfgDirectKC, false, false>(g, st);
   }

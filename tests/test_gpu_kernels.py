@@ -19,10 +19,13 @@ def _bf16(a):
 
 
 # (1500, 520, 200): six tile rows of 256, i.e. one whole group of four tile
-# rows and a partial one in the workgroup -> tile order
+# rows and a partial one in the workgroup -> tile order.  NT in bf16 runs
+# (2048, 768, 256) and (700, 480, 72) on 256 x 96 tiles (more of them than
+# 256 x 128 tiles give), the latter with a partial tile row and a partial
+# K step.
 GEMM_SHAPES = [(1, 1, 1), (7, 5, 3), (63, 65, 130), (130, 63, 65), (256, 256, 32),
                (257, 513, 96), (384, 128, 128), (1000, 300, 260), (2048, 768, 256),
-               (1500, 520, 200)]
+               (1500, 520, 200), (700, 480, 72)]
 
 
 @pytest.mark.parametrize("op", [sru.OP_NT, sru.OP_NN, sru.OP_TN])
@@ -44,6 +47,19 @@ def test_gemm_matches_matmul(op, dtype, shape):
     torch.cuda.synchronize()
     # products of bf16 values are exact in fp32: only accumulation order differs
     check("C", C, ref, TOL_FP32)
+
+
+def test_gemm_n96_tiles_at_the_shard_shape():
+    """U = X W^T of one GPU's share of the 6-layer d = 1024 batch (2,048
+    tokens): 256 tiles of 256 x 96, every workgroup a full tile."""
+    M, N, K = 2048, 3072, 1024
+    print(f"gemm NT bf16 M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(96)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    B = rng.standard_normal((N, K)).astype(np.float32)
+    C = sru.gemm(sru.OP_NT, dev(A), dev(B), M, N, K, sru.GEMM_BF16)
+    torch.cuda.synchronize()
+    check("C", C, _bf16(A) @ _bf16(B).T, TOL_FP32)
 
 
 @pytest.mark.parametrize("dtype", [sru.GEMM_FP32, sru.GEMM_BF16])
@@ -79,6 +95,10 @@ SCAN_CASES = [
     (33, 4, 128, 128, O.DIR_BI, False),
     (40, 5, 64, 64, O.DIR_FWD, True),
     (23, 2, 96, 48, O.DIR_REV, True),
+    # exactly one and two rings of 6 steps (the forward's first ring runs
+    # ahead of its loop; no tail)
+    (6, 3, 64, 64, O.DIR_FWD, False),
+    (12, 2, 128, 64, O.DIR_BI, True),
     # a wave on every SIMD (B*ndir*d >= 65536): the backward's shorter ring,
     # with a ragged tail (L % 4 != 0), k = 3 and 4
     (7, 64, 1024, 1024, O.DIR_FWD, True),
