@@ -915,6 +915,188 @@ __global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_lin_kernel(ScanSha
   }
 }
 
+// ------------------------------------- gated backward, time-parallel
+// Given the forward states C, the backward recurrence of the gated layer is
+// affine in the carried gradient: a step maps g to A g + B with A = f +
+// p_f v_f (p_f = (c_{t-1} - u0) f (1 - f)) and B = A (dh r) + dr v_r, or
+// A (dh r + dr v_r) when the reset gate reads c_t; a padded step is the
+// identity.  So the reverse scan splits into chunks like the linear
+// recurrence's (scan_bwd_lin_kernel): every wave folds its CH steps into one
+// map, a chunk's incoming gradient is the block's incoming gradient pushed
+// through the maps of the chunks before it, and every wave rescans its steps
+// with the sequential kernel's arithmetic from there.  The outputs of a step
+// are then those of scan_bwd_kernel for the same incoming gradient, which
+// differs from the sequential one by rounding only.  One workgroup per 64
+// lanes covers the whole sequence (no time segments), so this serves shapes
+// whose lane groups alone fill at least half the CUs and leave most SIMDs
+// without a wave; there the sequential scan waits on its serial chain.
+template <int KB, bool MASK, bool DUB, bool RN, int CH>
+__global__ __launch_bounds__(64 * kLinMaxWaves) void scan_bwd_tp_kernel(ScanShape s,
+                                                                        ScanBwdArgs a,
+                                                                        LinPlan pl) {
+  __shared__ float2 agg[2][kLinMaxWaves][64];
+  __shared__ float carry_lds[2][64];
+  Lane ln;
+  const bool live = decode_lane_lin(s, ln, blockIdx.x);
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int NW = blockDim.x >> 6;
+  const int L = s.L;
+  const int d = s.d;
+  const long long nfeat = (long long)s.ndir * s.d;
+  const long long u_step = (long long)s.B * s.ndir * KB * s.d;
+  const long long x_step = (long long)s.B * s.d_in;
+  const long long h_step = (long long)s.B * nfeat;
+  const long long u_off = ((long long)ln.b * s.ndir + ln.dir) * KB * s.d + ln.j;
+  const float* up = a.U + u_off;
+  using DuT = typename std::conditional<DUB, uint16_t, float>::type;
+  DuT* dup = static_cast<DuT*>(a.dU) + u_off;
+  const float* xp = KB == 3 ? a.X + (long long)ln.b * s.d_in + ln.j : nullptr;
+  const uint8_t* mp = MASK ? a.mask + ln.b : nullptr;
+  const float* cpp = a.C + ln.gid;
+  const float* dhp = a.dH + ln.gid;
+  // the forward's gate arithmetic (sigmoid_scaled), as in scan_bwd_kernel
+  const float vf = a.v_f[ln.fidx], vr = a.v_r[ln.fidx];
+  const float vfs = vf * kNegLog2e, vrs = vr * kNegLog2e;
+  const float bfs = a.b_f[ln.fidx] * kNegLog2e, brs = a.b_r[ln.fidx] * kNegLog2e;
+  const float alpha = s.alpha;
+  const float c0v = a.c0 ? a.c0[ln.gid] : 0.0f;
+  float sum_df_c = 0.f, sum_dr_c = 0.f, sum_df = 0.f, sum_dr = 0.f;
+  // time index of processing index i (reverse of the direction's order;
+  // clamped into range)
+  auto tproc = [&](int i) {
+    const int pos = L - 1 - (i < L ? i : L - 1);
+    return (long long)(ln.rev ? L - 1 - pos : pos);
+  };
+
+  int blk = 0;
+  for (int base = 0; base < L; base += NW * CH, ++blk) {
+    const int p = blk & 1;
+    const int i0 = base + w * CH;
+    float ru0[CH], rf[CH], rr[CH], rx[CH], rdh[CH], rc[CH + 1];
+    bool act[CH], pad[CH];
+#pragma unroll
+    for (int m = 0; m < CH; ++m) {
+      const long long t = tproc(i0 + m);
+      const float* u = up + t * u_step;
+      ru0[m] = __builtin_nontemporal_load(u);
+      rf[m] = __builtin_nontemporal_load(u + d);
+      rr[m] = __builtin_nontemporal_load(u + 2 * d);
+      if constexpr (KB == 4) rx[m] = __builtin_nontemporal_load(u + 3 * d);
+      else rx[m] = xp[t * x_step];
+      rdh[m] = __builtin_nontemporal_load(dhp + t * h_step);
+      rc[m] = cpp[t * h_step];
+      act[m] = i0 + m < L;
+      pad[m] = MASK ? mp[t * s.B] != 0 : false;
+    }
+    {
+      const int ie = i0 + CH;  // c_{t-1} of the chunk's last step
+      rc[CH] = ie < L ? cpp[tproc(ie) * h_step] : c0v;
+    }
+    // 1. this chunk's map on the carried gradient (f and r replace u1, u2)
+    float A = 1.0f, S = 0.0f;
+#pragma unroll
+    for (int m = 0; m < CH; ++m) {
+      const float c_t = rc[m];
+      const float c_p = i0 + m + 1 < L ? rc[m + 1] : c0v;
+      const float c_r = RN ? c_t : c_p;
+      const float f = sigmoid_scaled(fmaf(vfs, c_p, fmaf(rf[m], kNegLog2e, bfs)));
+      const float r = sigmoid_scaled(fmaf(vrs, c_r, fmaf(rr[m], kNegLog2e, brs)));
+      rf[m] = f;
+      rr[m] = r;
+      if (act[m] && !pad[m]) {
+        const float dh = rdh[m];
+        const float dr = dh * (c_t - alpha * rx[m]) * (r * (1.0f - r));
+        const float gf = fmaf((c_p - ru0[m]) * (f * (1.0f - f)), vf, f);
+        const float bm = RN ? gf * fmaf(dr, vr, dh * r) : fmaf(gf, dh * r, dr * vr);
+        S = fmaf(gf, S, bm);
+        A *= gf;
+      }
+    }
+    agg[p][w][lane] = make_float2(A, S);
+    lds_barrier();
+    // 2. incoming gradient of this chunk
+    float g = blk == 0 ? (a.dc_last ? a.dc_last[ln.gid] : 0.0f) : carry_lds[p ^ 1][lane];
+    for (int m = 0; m < w; ++m) {
+      const float2 q = agg[p][m][lane];
+      g = fmaf(q.x, g, q.y);
+    }
+    // 3. rescan: scan_bwd_kernel's step
+#pragma unroll
+    for (int m = 0; m < CH; ++m) {
+      if (i0 + m >= L) break;
+      const long long t = tproc(i0 + m);
+      const float f = rf[m], r = rr[m];
+      const float c_t = rc[m];
+      const float c_p = i0 + m + 1 < L ? rc[m + 1] : c0v;
+      const float c_r = RN ? c_t : c_p;
+      const bool pd = pad[m];
+      const float dhv = pd ? 0.0f : rdh[m];
+      const float rrv = r * (1.0f - r);
+      const float ff = f * (1.0f - f);
+      float dr = dhv * (c_t - alpha * rx[m]) * rrv;
+      const float gc = RN ? fmaf(dr, vr, fmaf(dhv, r, g)) : fmaf(dhv, r, g);
+      const float pf = (c_p - ru0[m]) * ff;
+      float df = gc * pf;
+      float du0 = gc * (1.0f - f);
+      float dx = dhv * (1.0f - r) * alpha;
+      if constexpr (MASK) {
+        dr = pd ? 0.0f : dr;
+        df = pd ? 0.0f : df;
+        du0 = pd ? 0.0f : du0;
+        dx = pd ? 0.0f : dx;
+      }
+      sum_df_c = fmaf(df, c_p, sum_df_c);
+      sum_dr_c = fmaf(dr, c_r, sum_dr_c);
+      sum_df += df;
+      sum_dr += dr;
+      const float gf = fmaf(pf, vf, f);
+      const float gn = RN ? gc * gf : fmaf(gc, gf, dr * vr);
+      g = pd ? g : gn;
+      if (live) {
+        DuT* du = dup + t * u_step;
+        // bf16 dU through the cache, as in scan_bwd_kernel
+        auto put = [](float v, DuT* q) {
+          if constexpr (DUB) *q = __builtin_bit_cast(uint16_t, (__bf16)v);
+          else __builtin_nontemporal_store(v, q);
+        };
+        put(du0, du);
+        put(df, du + d);
+        put(dr, du + 2 * d);
+        if constexpr (KB == 4) put(dx, du + 3 * d);
+        else __builtin_nontemporal_store(dx, a.dxh + ln.gid + t * h_step);
+      }
+    }
+    const int w_last = (min(L - base, NW * CH) - 1) / CH;
+    if (w == w_last) {
+      carry_lds[p][lane] = g;
+      if (base + NW * CH >= L && live && a.dc0) a.dc0[ln.gid] = g;
+    }
+  }
+  // fixed-order sum of the waves' v/b sums (agg is free: every wave is past
+  // its last read of it once it reaches this barrier)
+  lds_barrier();
+  agg[0][w][lane] = make_float2(sum_df_c, sum_dr_c);
+  agg[1][w][lane] = make_float2(sum_df, sum_dr);
+  lds_barrier();
+  if (w == 0 && live) {
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    for (int m = 0; m < NW; ++m) {
+      const float2 q = agg[0][m][lane], q2 = agg[1][m][lane];
+      s0 += q.x;
+      s1 += q.y;
+      s2 += q2.x;
+      s3 += q2.y;
+    }
+    // one row of partials per sequence, as scan_bwd_kernel writes
+    float* part = a.partial + (long long)ln.b * 4 * nfeat + ln.fidx;
+    part[0] = s0;
+    part[nfeat] = s1;
+    part[2 * nfeat] = s2;
+    part[3 * nfeat] = s3;
+  }
+}
+
 // Sum of the per-sequence partials over b, in a fixed order (deterministic):
 // vb_sum_block, 64 outputs per workgroup of 4 waves.  The loads of a lane
 // are independent, so a launch costs about one memory round trip.  The same
@@ -1045,6 +1227,18 @@ hipError_t fwd_dispatch_c(const ScanShape& s, const ScanFwdArgs& a, hipStream_t 
              : fwd_dispatch<KB, MASK, false, false>(s, a, st);
 }
 
+// Where the gated backward runs time-parallel (scan_bwd_tp_kernel): fewer
+// lanes than one wave per SIMD, but lane groups for at least half the CUs
+// (one workgroup per group then covers the sequence without segments).
+// Smaller shapes keep the sequential scan, whose results do not depend on
+// how a sequence is cut into calls.
+constexpr long long kTpMinLanes = 128 * 64;
+bool bwd_tp_ok(const ScanShape& s) {
+  const long long lanes = (long long)s.B * s.ndir * s.d;
+  return !s.linear && lanes >= kTpMinLanes && lanes < kFullLanes &&
+         lin_plan(s, kBwdLinCH).nseg == 1;
+}
+
 template <int KB, bool MASK, int PF>
 void bwd_launch(const ScanShape& s, const ScanBwdArgs& a, int grid, hipStream_t st) {
   if (a.du_bf16 && s.reset_new)
@@ -1082,6 +1276,21 @@ hipError_t bwd_dispatch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t st
     else
       hipLaunchKernelGGL((scan_bwd_lin_kernel<KB, MASK, false, kBwdLinCH>),
                          dim3(pl.groups * pl.nseg), dim3(64 * pl.nw), 0, st, s, a, pl);
+    timing_after(st);
+    return hipGetLastError();
+  }
+  if (bwd_tp_ok(s)) {
+    const LinPlan pl = lin_plan(s, kBwdLinCH);
+    const dim3 g(pl.groups), b(64 * pl.nw);
+    timing_before("scan_bwd", st);
+    if (a.du_bf16 && s.reset_new)
+      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, true, true, kBwdLinCH>), g, b, 0, st, s, a, pl);
+    else if (a.du_bf16)
+      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, true, false, kBwdLinCH>), g, b, 0, st, s, a, pl);
+    else if (s.reset_new)
+      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, false, true, kBwdLinCH>), g, b, 0, st, s, a, pl);
+    else
+      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, false, false, kBwdLinCH>), g, b, 0, st, s, a, pl);
     timing_after(st);
     return hipGetLastError();
   }

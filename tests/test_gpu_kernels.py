@@ -99,6 +99,12 @@ SCAN_CASES = [
     # ahead of its loop; no tail)
     (6, 3, 64, 64, O.DIR_FWD, False),
     (12, 2, 128, 64, O.DIR_BI, True),
+    # 8,192 lanes: the backward runs time-parallel (chunks of 8 steps per
+    # wave, 8 or 16 waves per block): one partial block; two blocks, the
+    # second partial; k = 4 in both directions
+    (37, 8, 1024, 1024, O.DIR_FWD, True),
+    (150, 16, 512, 512, O.DIR_REV, True),
+    (21, 4, 512, 1024, O.DIR_BI, False),
     # a wave on every SIMD (B*ndir*d >= 65536): the backward's shorter ring,
     # with a ragged tail (L % 4 != 0), k = 3 and 4
     (7, 64, 1024, 1024, O.DIR_FWD, True),

@@ -165,6 +165,43 @@ def test_chunked_backward_carry_on_gpu(direction, gemm):
         check(k, ga[k] + gs[k], host(fb[k]), tol)
 
 
+@pytest.mark.parametrize("direction", [O.DIR_FWD, O.DIR_REV])
+def test_chunked_backward_carry_time_parallel(direction):
+    """The same chunked back-propagation at 8,192 lanes, where the backward
+    scan runs time-parallel: a chunk's incoming gradient is composed from
+    maps, so the calls agree with the one-call layer to fp32 rounding rather
+    than bit for bit.  H is still bit for bit (the forward is sequential)."""
+    L, B, d, h = 50, 8, 1024, 21
+    print(f"chunked backward, time-parallel scan, dir={direction}", flush=True)
+    c = random_layer_case(np.random.default_rng(31 + direction), L, B, d, d, direction,
+                          masked=True, c0=True, dc_last=True, bias_scale=0.5)
+    X, W, mask = dev(c["X"]), dev(c["W"]), dev(c["mask"])
+    p = [dev(c[k]) for k in ("v_f", "v_r", "b_f", "b_r")]
+    c0, dcl, dH = dev(c["c0"]), dev(c["dc_last"]), dev(c["dH"])
+    kw = dict(direction=direction, gemm_dtype=O.GEMM_FP32)
+    full = sru.forward(X, W, *p, c0=c0, mask=mask, **kw)
+    fb = sru.backward(X, W, *p, full["U"], full["C"], dH, c0=c0, dc_last=dcl, mask=mask, **kw)
+    first, second = (slice(0, h), slice(h, L)) if direction == O.DIR_FWD else (slice(h, L),
+                                                                               slice(0, h))
+    part = lambda t, s: t[s].contiguous()
+    fa = sru.forward(part(X, first), W, *p, c0=c0, mask=part(mask, first), **kw)
+    fs = sru.forward(part(X, second), W, *p, c0=fa["c_last"], mask=part(mask, second), **kw)
+    gs = sru.backward(part(X, second), W, *p, fs["U"], fs["C"], part(dH, second), c0=fa["c_last"],
+                      dc_last=dcl, mask=part(mask, second), **kw)
+    ga = sru.backward(part(X, first), W, *p, fa["U"], fa["C"], part(dH, first), c0=c0,
+                      dc_last=gs["dc0"], mask=part(mask, first), **kw)
+    torch.cuda.synchronize()
+    H = torch.empty_like(full["H"])
+    H[first], H[second] = fa["H"], fs["H"]
+    dX = torch.empty_like(fb["dX"])
+    dX[first], dX[second] = ga["dX"], gs["dX"]
+    assert torch.equal(H, full["H"])
+    check("dX", dX, host(fb["dX"]), TOL_FP32)
+    check("dc0", ga["dc0"], host(fb["dc0"]), TOL_FP32)
+    for k in ("dW", "dv_f", "dv_r", "db_f", "db_r"):
+        check(k, ga[k] + gs[k], host(fb[k]), TOL_FP32)
+
+
 def test_layers_on_two_streams_equal_serial():
     """Two layers enqueued at once on two streams (default priority) give the
     same bits as the same calls one after the other: the library keeps no

@@ -24,6 +24,7 @@ SCAN_CASES = [
     (40, 5, 128, 128, O.DIR_BI, True),
     (11, 64, 1024, 1024, O.DIR_REV, True),  # a wave on every SIMD: shorter backward ring
     (10, 32, 512, 1024, O.DIR_BI, True),  # k = 4, both directions, 256-unit workgroups
+    (45, 8, 1024, 1024, O.DIR_FWD, True),  # 8,192 lanes: the time-parallel backward
 ]
 
 
