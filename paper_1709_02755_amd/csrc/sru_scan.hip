@@ -1119,6 +1119,7 @@ constexpr int kBwdPFFull = 4;
 constexpr int kFullLanes = 256 * 4 * 64;  // one wave on each of the 1024 SIMDs
 constexpr int kFwdLinCH = 12;
 constexpr int kBwdLinCH = 8;
+constexpr int kBwdTpCH = 8;  // steps per wave chunk of the time-parallel gated backward
 
 // Plan of the chunked scans: waves per workgroup so that the launch holds
 // about 4096 waves (4 per SIMD), at most 16 per workgroup and no more chunks
@@ -1236,7 +1237,7 @@ constexpr long long kTpMinLanes = 128 * 64;
 bool bwd_tp_ok(const ScanShape& s) {
   const long long lanes = (long long)s.B * s.ndir * s.d;
   return !s.linear && lanes >= kTpMinLanes && lanes < kFullLanes &&
-         lin_plan(s, kBwdLinCH).nseg == 1;
+         lin_plan(s, kBwdTpCH).nseg == 1;
 }
 
 template <int KB, bool MASK, int PF>
@@ -1280,17 +1281,17 @@ hipError_t bwd_dispatch(const ScanShape& s, const ScanBwdArgs& a, hipStream_t st
     return hipGetLastError();
   }
   if (bwd_tp_ok(s)) {
-    const LinPlan pl = lin_plan(s, kBwdLinCH);
+    const LinPlan pl = lin_plan(s, kBwdTpCH);
     const dim3 g(pl.groups), b(64 * pl.nw);
     timing_before("scan_bwd", st);
     if (a.du_bf16 && s.reset_new)
-      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, true, true, kBwdLinCH>), g, b, 0, st, s, a, pl);
+      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, true, true, kBwdTpCH>), g, b, 0, st, s, a, pl);
     else if (a.du_bf16)
-      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, true, false, kBwdLinCH>), g, b, 0, st, s, a, pl);
+      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, true, false, kBwdTpCH>), g, b, 0, st, s, a, pl);
     else if (s.reset_new)
-      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, false, true, kBwdLinCH>), g, b, 0, st, s, a, pl);
+      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, false, true, kBwdTpCH>), g, b, 0, st, s, a, pl);
     else
-      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, false, false, kBwdLinCH>), g, b, 0, st, s, a, pl);
+      hipLaunchKernelGGL((scan_bwd_tp_kernel<KB, MASK, false, false, kBwdTpCH>), g, b, 0, st, s, a, pl);
     timing_after(st);
     return hipGetLastError();
   }
