@@ -54,6 +54,13 @@ struct Dims {
   long long M, N, nfeat;
 };
 
+// dX runs after dW when it is large: the layer below's backward scan reads
+// it as dH next, and then still finds much of it in the caches (measured:
+// L 256, B 64, d 1024 and L 128, B 128, d 2048 ran 0.6 % and 1.1 % faster
+// per step; with dX of 8 MB, at B 8, 0.8 % slower, so small ones keep dX
+// first)
+bool dx_last(const Dims& s) { return 4LL * s.M * s.d_in > kDxLastBytes; }
+
 // Shape checks shared by every layer entry point.  Sizes must be positive,
 // products must fit the 32-bit indices the kernels use for tokens, columns
 // and lanes, and no tensor may exceed kMaxElems elements.
@@ -209,10 +216,15 @@ sru::GemmDesc dw_desc(const Dims& s, bool bf16, const void* dU, const void* X, f
 
 // Backward workspace layout:
 //   [dU (fp32, or bf16 in bf16 mode) | dxh (k = 3) | v/b partials |
-//    Wcat^T and X in bf16 (bf16 mode) | dW split partials]
+//    Wcat^T and X in bf16 (bf16 mode) | split partials]
+// The split partials of dW and dX share one region, each product's sum
+// running before the other product starts; when both are split and dX runs
+// first, dX's sum runs in dW's split-sum launch (one launch less), and dX's
+// partials then follow dW's.
 struct BwdLayout {
-  size_t dU, dxh, partial, wt, xb, splitk, total;
+  size_t dU, dxh, partial, wt, xb, splitk, splitk_dx, total;
   int splits, splits_dx;
+  bool joint_sum;
 };
 
 // dX = dU Wcat (+ highway): NN on Wcat in fp32 mode; in bf16 mode NT on the
@@ -256,9 +268,17 @@ BwdLayout bwd_layout(const Dims& s, int gemm_dtype) {
   if (bf16) off += align_up(2 * (size_t)s.M * (size_t)s.d_in);
   w.splits = sru::gemm_splits(dw_desc(s, bf16, nullptr, nullptr, nullptr));
   w.splits_dx = sru::gemm_splits(dx_desc(s, bf16, nullptr, nullptr, nullptr, nullptr, nullptr));
-  w.splitk = off;  // shared by the dX and dW partials (they run one after the other)
-  off += align_up(std::max(sru::gemm_partial_bytes((int)s.N, s.d_in, w.splits),
-                           sru::gemm_partial_bytes((int)s.M, s.d_in, w.splits_dx)));
+  w.joint_sum = w.splits > 1 && w.splits_dx > 1 && !dx_last(s);
+  const size_t pw = sru::gemm_partial_bytes((int)s.N, s.d_in, w.splits);
+  const size_t px = sru::gemm_partial_bytes((int)s.M, s.d_in, w.splits_dx);
+  w.splitk = off;
+  if (w.joint_sum) {
+    w.splitk_dx = off + align_up(pw);
+    off += align_up(pw) + align_up(px);
+  } else {
+    w.splitk_dx = off;  // shared: the products run one after the other
+    off += align_up(std::max(pw, px));
+  }
   w.total = off;
   return w;
 }
@@ -625,8 +645,8 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
   //    operands row-contiguous; dX reads Wcat^T rounded to bf16 into the
   //    workspace (a transposed copy of W_bf16 when the caller holds it, else
   //    rounded from W), both operands K-contiguous, so it runs at the speed
-  //    of the projection.  dX's split partials (if any) and dW's share one
-  //    region; each product's sum runs before the other product starts.
+  //    of the projection.  Split partials: see BwdLayout (with both
+  //    products split and dX first, one launch sums both).
   auto run_dw = [&]() -> int {
     if (bf16 && !X_bf16) {
       if (int e = hip_status(sru::to_bf16_launch(X, (int)s.M, d_in, xb, false, stream, "bf16_x")))
@@ -634,6 +654,15 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
     }
     return hip_status(sru::gemm_launch(gw, stream));
   };
+  sru::GemmDesc gx = dx_desc(s, bf16, dU, W, wt, dX, dxh);
+  gx.partials = reinterpret_cast<float*>(ws + lay.splitk_dx);
+  // split as planned, else (a plan that differs at run time) not at all
+  if (sru::gemm_splits(gx) > lay.splits_dx) gx.kc_split = false;
+  if (lay.joint_sum && sru::gemm_splits(gx) > 1 && sru::gemm_splits(gw) > 1) {
+    // dX runs first; its split sum runs in dW's split-sum launch
+    gx.defer_sum = true;
+    gw.extra = sru::gemm_split_sum(gx);
+  }
   auto run_dx = [&]() -> int {
     if (bf16) {
       const hipError_t te = W_bf16
@@ -641,18 +670,9 @@ int sru_backward(const float* X, const float* W, const float* v_f, const float* 
           : sru::to_bf16_t_launch(W, false, (int)s.N, d_in, wt, stream, "bf16_wt");
       if (int e = hip_status(te)) return e;
     }
-    sru::GemmDesc gx = dx_desc(s, bf16, dU, W, wt, dX, dxh);
-    gx.partials = splitk;
-    // split as planned, else (a plan that differs at run time) not at all
-    if (sru::gemm_splits(gx) > lay.splits_dx) gx.kc_split = false;
     return hip_status(sru::gemm_launch(gx, stream));
   };
-  // dX last when it is large: the layer below's backward scan reads it as
-  // dH next, and then still finds much of it in the caches (measured:
-  // L 256, B 64, d 1024 and L 128, B 128, d 2048 ran 0.6 % and 1.1 % faster
-  // per step; with dX of 8 MB, at B 8, 0.8 % slower, so small ones keep dX
-  // first)
-  if (4LL * s.M * d_in > kDxLastBytes) {
+  if (dx_last(s)) {
     if (int e = run_dw()) return e;
     return run_dx();
   }

@@ -1313,57 +1313,100 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 // the same sequence of additions, so the result is bit-identical.  Blocks
 // from `main_blocks` on run the v/b sums of the backward pass instead
 // (vb_sum_block: the same bits as their own launch).
-__global__ __launch_bounds__(256) void splitk_reduce4_kernel(const float* __restrict__ part,
-                                                             int splits, int M, int N,
-                                                             float* C, long long ldc,
-                                                             const float* add, long long add_ld,
-                                                             long long add_off, int add_count,
-                                                             unsigned main_blocks, VbSum vb) {
-  if (blockIdx.x >= main_blocks) {
-    __shared__ float red[256];
-    vb_sum_block(vb.partial, vb.rows, vb.nfeat, vb.qlo, vb.out, blockIdx.x - main_blocks, red);
-    return;
-  }
-  const long long total = (long long)M * N;
-  const long long i = ((long long)blockIdx.x * 256 + threadIdx.x) * 4;
+__device__ __forceinline__ void split_sum4_block(const SplitSum& j, unsigned blk) {
+  const long long total = (long long)j.M * j.N;
+  const long long i = ((long long)blk * 256 + threadIdx.x) * 4;
   if (i >= total) return;
-  const int m = (int)(i / N);
-  const int n = (int)(i - (long long)m * N);
+  const int m = (int)(i / j.N);
+  const int n = (int)(i - (long long)m * j.N);
   floatx4 s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
-  for (int z = 0; z < splits; ++z) s += *reinterpret_cast<const floatx4*>(part + z * total + i);
-  if (add_count > 0) {
-    const float* ar = add + (long long)m * add_ld + n;
+  for (int z = 0; z < j.splits; ++z)
+    s += *reinterpret_cast<const floatx4*>(j.part + z * total + i);
+  if (j.add_count > 0) {
+    const float* ar = j.add + (long long)m * j.add_ld + n;
     s += *reinterpret_cast<const floatx4*>(ar);
-    if (add_count > 1) s += *reinterpret_cast<const floatx4*>(ar + add_off);
+    if (j.add_count > 1) s += *reinterpret_cast<const floatx4*>(ar + j.add_off);
   }
-  *reinterpret_cast<floatx4*>(C + (long long)m * ldc + n) = s;
+  *reinterpret_cast<floatx4*>(j.C + (long long)m * j.ldc + n) = s;
 }
 
-hipError_t launch_splitk_reduce(const float* part, int splits, int M, int N, float* C,
-                                long long ldc, const float* add, long long add_ld,
-                                long long add_off, int add_count, const VbSum& vb,
-                                hipStream_t st) {
-  const long long total = (long long)M * N;
-  auto al16 = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
-  const bool vec = N % 4 == 0 && ldc % 4 == 0 && al16(part) && al16(C) &&
-                   (add_count == 0 || (add_ld % 4 == 0 && add_off % 4 == 0 && al16(add)));
-  timing_before("splitk_reduce", st);
-  if (vec) {
-    const long long groups = total / 4;
-    const unsigned main_blocks = (unsigned)((groups + 255) / 256);
-    const unsigned extra = vb.partial ? (unsigned)vb_sum_blocks(vb) : 0u;
-    hipLaunchKernelGGL(splitk_reduce4_kernel, dim3(main_blocks + extra), dim3(256), 0, st, part,
-                       splits, M, N, C, ldc, add, add_ld, add_off, add_count, main_blocks, vb);
+// Blocks [0, n1) sum j1, [n1, n1 + n2) sum j2 (another product's deferred
+// split sum: one launch instead of two), the rest the v/b sums.
+__global__ __launch_bounds__(256) void splitk_reduce4_kernel(SplitSum j1, unsigned n1,
+                                                             SplitSum j2, unsigned n2,
+                                                             VbSum vb) {
+  const unsigned b = blockIdx.x;
+  if (b < n1) {
+    split_sum4_block(j1, b);
+  } else if (b < n1 + n2) {
+    split_sum4_block(j2, b - n1);
   } else {
-    const int grid = (int)std::min<long long>((total + 255) / 256, 8192);
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, st, part, splits, M, N,
-                       C, ldc, add, add_ld, add_off, add_count);
+    __shared__ float red[256];
+    vb_sum_block(vb.partial, vb.rows, vb.nfeat, vb.qlo, vb.out, b - n1 - n2, red);
   }
+}
+
+bool split_sum_vec(const SplitSum& j) {
+  auto al16 = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  return j.N % 4 == 0 && j.ldc % 4 == 0 && al16(j.part) && al16(j.C) &&
+         (j.add_count == 0 || (j.add_ld % 4 == 0 && j.add_off % 4 == 0 && al16(j.add)));
+}
+
+// Split sum j (if j.part), the deferred split sum `extra` (if extra.part) and
+// the v/b sums (if vb.partial), in one launch where the rows allow 16-byte
+// accesses.
+hipError_t launch_splitk_reduce(const SplitSum& j, const SplitSum& extra, const VbSum& vb,
+                                hipStream_t st) {
+  const bool vec = (!j.part || split_sum_vec(j)) && (!extra.part || split_sum_vec(extra));
+  if (!vec) {
+    // one element per thread, each sum in its own launch
+    for (const SplitSum* q : {&extra, &j}) {
+      if (!q->part) continue;
+      const long long total = (long long)q->M * q->N;
+      const int grid = (int)std::min<long long>((total + 255) / 256, 8192);
+      timing_before("splitk_reduce", st);
+      hipLaunchKernelGGL(splitk_reduce_kernel, dim3(grid), dim3(256), 0, st, q->part, q->splits,
+                         q->M, q->N, q->C, q->ldc, q->add, q->add_ld, q->add_off, q->add_count);
+      timing_after(st);
+      if (hipError_t e = hipGetLastError()) return e;
+    }
+    return vb.partial ? vb_sum_launch(vb, st) : hipSuccess;
+  }
+  auto blocks = [](const SplitSum& q) {
+    return q.part ? (unsigned)(((long long)q.M * q.N / 4 + 255) / 256) : 0u;
+  };
+  const unsigned n1 = blocks(j), n2 = blocks(extra);
+  const unsigned nv = vb.partial ? (unsigned)vb_sum_blocks(vb) : 0u;
+  if (n1 + n2 + nv == 0) return hipSuccess;
+  timing_before(n1 + n2 > 0 ? "splitk_reduce" : "reduce_vb", st);
+  hipLaunchKernelGGL(splitk_reduce4_kernel, dim3(n1 + n2 + nv), dim3(256), 0, st, j, n1, extra,
+                     n2, vb);
   timing_after(st);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || vec || !vb.partial) return e;
-  return vb_sum_launch(vb, st);
+  return hipGetLastError();
+}
+
+SplitSum split_sum_of(const GemmDesc& g, int splits) {
+  SplitSum j;
+  j.part = g.partials;
+  j.splits = splits;
+  j.M = g.M;
+  j.N = g.N;
+  j.C = g.C;
+  j.ldc = g.ldc;
+  j.add = g.add;
+  j.add_ld = g.add_ld;
+  j.add_off = g.add_off;
+  j.add_count = g.add_count;
+  return j;
+}
+
+// After a product: its split sum (unless deferred), the deferred split sum
+// of an earlier product, and the v/b sums, in one launch.
+hipError_t finish_product(const GemmDesc& g, int splits, hipStream_t st) {
+  if (splits > 1 && g.defer_sum) return hipSuccess;
+  const SplitSum own = splits > 1 ? split_sum_of(g, splits) : SplitSum{};
+  return launch_splitk_reduce(own, g.extra, g.vb, st);
 }
 
 // fp32 -> bf16 conversions (RNE).  Plain copy: 8 elements per thread (two
@@ -1551,9 +1594,7 @@ hipError_t launch_cfg(const GemmDesc& g, hipStream_t st) {
   timing_after(st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (a.splits == 1) return g.vb.partial ? vb_sum_launch(g.vb, st) : hipSuccess;
-  return launch_splitk_reduce(g.partials, a.splits, g.M, g.N, g.C, g.ldc, g.add, g.add_ld,
-                              g.add_off, g.add_count, g.vb, st);
+  return finish_product(g, a.splits, st);
 }
 
 // ---- the direct path: plan (shared by workspace sizing and launch) ----
@@ -1748,9 +1789,7 @@ hipError_t launch_direct_cfg(const GemmDesc& g, hipStream_t st) {
   timing_after(st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (splits == 1) return g.vb.partial ? vb_sum_launch(g.vb, st) : hipSuccess;
-  return launch_splitk_reduce(g.partials, a.splits, g.M, g.N, g.C, g.ldc, g.add, g.add_ld,
-                              g.add_off, g.add_count, g.vb, st);
+  return finish_product(g, splits, st);
 }
 
 // Operand-type combinations that are instantiated: fp32 x fp32 for every
@@ -1793,6 +1832,8 @@ int gemm_splits(const GemmDesc& g) {
   const int kps = ((kt + s - 1) / s) * bk;
   return (g.K + kps - 1) / kps;
 }
+
+SplitSum gemm_split_sum(const GemmDesc& g) { return split_sum_of(g, gemm_splits(g)); }
 
 size_t gemm_partial_bytes(int M, int N, int splits) {
   return splits > 1 ? sizeof(float) * (size_t)splits * (size_t)M * (size_t)N : 0;

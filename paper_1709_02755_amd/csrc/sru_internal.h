@@ -21,6 +21,19 @@ struct VbSum {
 inline int vb_sum_blocks(const VbSum& v) { return ((4 - v.qlo) * v.nfeat + 63) / 64; }
 hipError_t vb_sum_launch(const VbSum& v, hipStream_t stream);
 
+// A split-K sum: partials [splits, M, N] (fp32) summed in split order into
+// C (row pitch ldc), plus up to two addend rows (add, add + add_off; pitch
+// add_ld).
+struct SplitSum {
+  const float* part = nullptr;
+  int splits = 0, M = 0, N = 0;
+  float* C = nullptr;
+  long long ldc = 0;
+  const float* add = nullptr;
+  long long add_ld = 0, add_off = 0;
+  int add_count = 0;
+};
+
 // ----------------------------------------------------------------- GEMM
 // C[M,N] = sum_k A(m,k) B(n,k), fp32 result, MFMA compute.
 //   A(m,k) = a_kc ? A[m*lda + k] : A[k*lda + m]
@@ -59,7 +72,18 @@ struct GemmDesc {
   // v/b sums to run with this product (vb.partial != nullptr): in the same
   // launch as the split-K sum when there is one, else right after the product
   VbSum vb;
+  // defer_sum: a split product leaves its split sum to a later product's
+  // launch (the caller hands gemm_split_sum(this) to that product as
+  // `extra`, and keeps the two products' partials apart).  extra: another
+  // product's deferred split sum, run in the same launch as this product's
+  // (on its own when this product is not split).
+  bool defer_sum;
+  SplitSum extra;
 };
+
+// The split sum gemm_launch would run after g (its partials, split count,
+// output and addend).
+SplitSum gemm_split_sum(const GemmDesc& g);
 
 // fp32 -> bf16 (RNE) copy of a [rows, cols] matrix; transposed ([cols, rows])
 // when `transpose`.
