@@ -214,11 +214,13 @@ SRU_API int sru_forward_noalloc(const float* X, const float* W,
  *   copy, made in the workspace).  NULL: rounded into the workspace.  W
  *   may be NULL when W_bf16 is given (weights held in bf16, as in
  *   sru_forward); dW is still written in fp32.
- * A sequence cut into consecutive calls (c_last -> c0 forward, dc0 ->
- * dc_last backward) gives one call's results bit for bit, except with
- * 8,192 to 65,535 lanes (B * ndir * d): there the reverse scan runs in
- * time-parallel chunks (the gradient recurrence is affine given C), and
- * the calls agree with one call to fp32 rounding.
+ * With the gated recurrence, a sequence cut into consecutive calls
+ * (c_last -> c0 forward, dc0 -> dc_last backward) gives one call's results
+ * bit for bit, except the backward with 8,192 to 65,535 lanes
+ * (B * ndir * d): there the reverse scan runs in time-parallel chunks (the
+ * gradient recurrence is affine given C), and the calls agree with one
+ * call to fp32 rounding, as the linear recurrence's chunked scans do at
+ * every size.
  */
 SRU_API int sru_backward(const float* X, const float* W,
                  const float* v_f, const float* v_r, const float* b_f, const float* b_r,
