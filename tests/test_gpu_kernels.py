@@ -105,6 +105,7 @@ SCAN_CASES = [
     (37, 8, 1024, 1024, O.DIR_FWD, True),
     (150, 16, 512, 512, O.DIR_REV, True),
     (21, 4, 512, 1024, O.DIR_BI, False),
+    (19, 65, 127, 127, O.DIR_REV, True),  # 8,255 lanes: a partial last lane group
     # a wave on every SIMD (B*ndir*d >= 65536): the backward's shorter ring,
     # with a ragged tail (L % 4 != 0), k = 3 and 4
     (7, 64, 1024, 1024, O.DIR_FWD, True),
