@@ -109,9 +109,41 @@ def _inputs(case):
     return c
 
 
+@st.composite
+def time_parallel_cases(draw):
+    """Gated layers with 8,192 to 65,535 lanes (B * ndir * d), where the
+    backward scan runs in time-parallel chunks; short sequences keep the
+    oracle fast."""
+    direction = draw(st.sampled_from([O.DIR_FWD, O.DIR_REV, O.DIR_BI]))
+    ndir = 2 if direction == O.DIR_BI else 1
+    d = draw(st.sampled_from([128, 256, 512]))
+    lo = -(-8192 // (ndir * d))
+    B = draw(st.integers(lo, min(65535 // (ndir * d), lo + 24)))
+    k4 = draw(st.booleans())
+    return dict(
+        L=draw(st.integers(1, 24)), B=B, d=d,
+        d_in=draw(st.sampled_from([64, 96, 200])) if k4 else d, direction=direction,
+        mask=draw(st.sampled_from(["none", "lengths", "irregular"])),
+        gemm=draw(st.sampled_from([O.GEMM_FP32, O.GEMM_BF16])),
+        alpha=draw(st.sampled_from([1.0, float(np.sqrt(3.0)), 0.6])),
+        reset_new=draw(st.booleans()), linear=False,
+        c0=draw(st.booleans()), dc_last=draw(st.booleans()),
+        seed=draw(st.integers(0, 2 ** 31 - 1)))
+
+
 @settings(max_examples=150, **SETTINGS)
 @given(case=layer_cases())
 def test_layer_equals_oracle_on_random_cases(case):
+    check_layer_case(case)
+
+
+@settings(max_examples=25, **SETTINGS)
+@given(case=time_parallel_cases())
+def test_time_parallel_layer_equals_oracle_on_random_cases(case):
+    check_layer_case(case)
+
+
+def check_layer_case(case):
     print(f"property case {case}", flush=True)
     c = _inputs(case)
     direction, gemm, linear = case["direction"], case["gemm"], case["linear"]
