@@ -216,7 +216,7 @@ SRU_API int sru_forward_noalloc(const float* X, const float* W,
  *   sru_forward); dW is still written in fp32.
  * With the gated recurrence, a sequence cut into consecutive calls
  * (c_last -> c0 forward, dc0 -> dc_last backward) gives one call's results
- * bit for bit, except the backward with 8,192 to 65,535 lanes
+ * bit for bit, except the backward with 8,192 to 32,767 lanes
  * (B * ndir * d): there the reverse scan runs in time-parallel chunks (the
  * gradient recurrence is affine given C), and the calls agree with one
  * call to fp32 rounding, as the linear recurrence's chunked scans do at

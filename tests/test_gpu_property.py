@@ -111,14 +111,14 @@ def _inputs(case):
 
 @st.composite
 def time_parallel_cases(draw):
-    """Gated layers with 8,192 to 65,535 lanes (B * ndir * d), where the
+    """Gated layers with 8,192 to 32,767 lanes (B * ndir * d), where the
     backward scan runs in time-parallel chunks; short sequences keep the
     oracle fast."""
     direction = draw(st.sampled_from([O.DIR_FWD, O.DIR_REV, O.DIR_BI]))
     ndir = 2 if direction == O.DIR_BI else 1
     d = draw(st.sampled_from([128, 256, 512]))
     lo = -(-8192 // (ndir * d))
-    B = draw(st.integers(lo, min(65535 // (ndir * d), lo + 24)))
+    B = draw(st.integers(lo, min(32767 // (ndir * d), lo + 24)))
     k4 = draw(st.booleans())
     return dict(
         L=draw(st.integers(1, 24)), B=B, d=d,
