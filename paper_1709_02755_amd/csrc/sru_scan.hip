@@ -350,6 +350,160 @@ __global__ __launch_bounds__(kRingThreads) void scan_fwd_ring_kernel(ScanShape s
 //   v/b sums += (df c_p, dr c_p, df, dr);  g <- gc f + df v_f + dr v_r
 // A padded step writes zeros and leaves g unchanged.
 // DUB: store dU as bf16 (RNE), the operand type of bf16 matrix products.
+// ----------------------------------------- forward scan, narrow LDS ring
+// The same recurrence and arithmetic again (results equal bit for bit), for
+// few lanes, where each step of the register-ring scan waits on the one
+// before.  A workgroup owns 64 consecutive hidden units of one (sequence,
+// direction): one consumer wave runs the recurrence from LDS, one producer
+// wave streams its inputs into a ring of kNrSlots groups of kNrSteps steps.
+// A producer load covers four steps of one input segment (16 lanes x 16
+// bytes per step), so a group takes 4 loads per segment and three groups
+// stay in flight within the 63 loads vmcnt counts; the two waves meet at
+// one barrier per group.  Mask bytes: lanes 0-15 load one step's byte each
+// into their dword of the group's mask slot.
+constexpr int kNrUnits = 64;
+constexpr int kNrSteps = 16;  // steps per hand-off
+constexpr int kNrSlots = 4;   // groups in the ring
+
+template <int KB, bool MASK, bool STORE_C, bool STORE_HB, bool RN>
+__global__ __launch_bounds__(128) void scan_fwd_nring_kernel(ScanShape s, ScanFwdArgs a,
+                                                             unsigned u_bytes, unsigned x_bytes,
+                                                             unsigned m_bytes) {
+  constexpr int NSEG = 4;  // U blocks 0-2 and x (k = 3), or U blocks 0-3 (k = 4)
+  constexpr int STEPB = kNrUnits * 4;        // one segment of one step
+  constexpr int SEGB = kNrSteps * STEPB;     // one segment of a group
+  constexpr int SLOTB = NSEG * SEGB;
+  constexpr int IPG = NSEG * (kNrSteps / 4) + (MASK ? 1 : 0);  // loads per group
+  static_assert((kNrSlots - 1) * IPG < 64, "vmcnt counts at most 63 loads");
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[kNrSlots * SLOTB];
+  __shared__ __attribute__((aligned(256))) unsigned mring[kNrSlots][64];
+
+  const int nblk = s.d / kNrUnits;
+  const int jb = blockIdx.x % nblk;
+  const int bd = blockIdx.x / nblk;
+  const int dir = bd % s.ndir;
+  const int b = bd / s.ndir;
+  const bool rev = s.direction == 1 || (s.direction == 2 && dir == 1);
+  const int L = s.L;
+  const int G = (L + kNrSteps - 1) / kNrSteps;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+
+  if (wave == 1) {
+    // ---- producer
+    const __amdgpu_buffer_rsrc_t ru = ring_rsrc(a.U, u_bytes);
+    const __amdgpu_buffer_rsrc_t rx = ring_rsrc(KB == 3 ? a.X : a.U, KB == 3 ? x_bytes : u_bytes);
+    const __amdgpu_buffer_rsrc_t rm =
+        ring_rsrc(MASK ? static_cast<const void*>(a.mask) : static_cast<const void*>(a.U),
+                  MASK ? m_bytes : u_bytes);
+    const unsigned u_step = (unsigned)s.B * s.ndir * KB * s.d * 4u;
+    const unsigned x_step = (unsigned)s.B * s.d_in * 4u;
+    const int sub = lane >> 4;                    // step of the four an instruction loads
+    const unsigned uc = (unsigned)(lane & 15) * 16u;  // the lane's four units
+    const unsigned u_base =
+        (unsigned)((((long long)b * s.ndir + dir) * KB * s.d + jb * kNrUnits) * 4) + uc;
+    const unsigned x_base = (unsigned)(((long long)b * s.d_in + jb * kNrUnits) * 4) + uc;
+    const unsigned seg = (unsigned)s.d * 4u;
+    auto issue = [&](int gi) {
+      unsigned char* slot = ring + (gi % kNrSlots) * SLOTB;
+#pragma unroll
+      for (int k4 = 0; k4 < kNrSteps / 4; ++k4) {
+        const int step = gi * kNrSteps + 4 * k4 + sub;
+        const bool in = step < L;
+        const unsigned t = in ? (unsigned)(rev ? L - 1 - step : step) : 0u;
+        const unsigned oob = in ? 0u : kRingOOB;
+        const unsigned uo = (t * u_step + u_base) | oob;
+#pragma unroll
+        for (int q = 0; q < KB; ++q)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              ru, (lds_t*)(slot + q * SEGB + k4 * 4 * STEPB), 16, uo + q * seg, 0, 0, 0);
+        if constexpr (KB == 3)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(
+              rx, (lds_t*)(slot + 3 * SEGB + k4 * 4 * STEPB), 16, (t * x_step + x_base) | oob, 0,
+              0, 0);
+      }
+      if constexpr (MASK) {
+        const int step = gi * kNrSteps + lane;
+        const bool in = lane < kNrSteps && step < L;
+        const unsigned t = in ? (unsigned)(rev ? L - 1 - step : step) : 0u;
+        const unsigned mo = in ? t * (unsigned)s.B + (unsigned)b : kRingOOB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rm, (lds_t*)(&mring[gi % kNrSlots][0]), 1, mo, 0,
+                                                 0, 0);
+      }
+    };
+    for (int gi = 0; gi < kNrSlots - 1 && gi < G; ++gi) issue(gi);
+    for (int g = 0; g < G; ++g) {
+      // group g has landed once at most the groups issued after it remain
+      const int later = min(kNrSlots - 2, G - 1 - g);
+      if (later >= 2) __builtin_amdgcn_s_waitcnt(ring_vm_wait(2 * IPG));
+      else if (later == 1) __builtin_amdgcn_s_waitcnt(ring_vm_wait(IPG));
+      else __builtin_amdgcn_s_waitcnt(ring_vm_wait(0));
+      ring_barrier();
+      // the slot of group g - 1, which the consumer finished before the barrier
+      if (g + kNrSlots - 1 < G) issue(g + kNrSlots - 1);
+    }
+    return;
+  }
+
+  // ---- consumer: unit j of (b, dir), lane gid of the [B, ndir*d] state
+  const int j = jb * kNrUnits + lane;
+  const int fidx = dir * s.d + j;
+  const long long nfeat = (long long)s.ndir * s.d;
+  const long long gid = (long long)b * nfeat + fidx;
+  const long long h_step = (long long)s.B * nfeat;
+  const long long t0 = rev ? L - 1 : 0;
+  const long long sh = rev ? -h_step : h_step;
+  float* hp = a.H + gid + t0 * h_step;
+  float* cp = STORE_C ? a.C + gid + t0 * h_step : nullptr;
+  uint16_t* hbp = STORE_HB ? a.Hb + gid + t0 * h_step : nullptr;
+  const float vfs = a.v_f[fidx] * kNegLog2e, vrs = a.v_r[fidx] * kNegLog2e;
+  const float bfs = a.b_f[fidx] * kNegLog2e, brs = a.b_r[fidx] * kNegLog2e;
+  const float alpha = s.alpha;
+  float c = a.c0 ? a.c0[gid] : 0.0f;
+
+  auto step = [&](float u0, float u1, float u2, float xh, unsigned mk) {
+    const float f = sigmoid_scaled(fmaf(vfs, c, fmaf(u1, kNegLog2e, bfs)));  // Eq. 1
+    const float cn = fmaf(f, c, fmaf(-f, u0, u0));                           // Eq. 2
+    const float r = sigmoid_scaled(fmaf(vrs, RN ? cn : c, fmaf(u2, kNegLog2e, brs)));  // Eq. 3
+    float h = fmaf(r, cn, (1.0f - r) * (alpha * xh));  // Eq. 4 (Sec. 3.2)
+    if constexpr (MASK) {
+      const bool pad = mk != 0;
+      c = pad ? c : cn;
+      h = pad ? 0.0f : h;
+    } else {
+      c = cn;
+    }
+    // plain stores, as in the register-ring scan at few lanes
+    *hp = h;
+    if constexpr (STORE_C) *cp = c;
+    if constexpr (STORE_HB) *hbp = __builtin_bit_cast(uint16_t, (__bf16)h);
+    hp += sh;
+    if constexpr (STORE_C) cp += sh;
+    if constexpr (STORE_HB) hbp += sh;
+  };
+
+  const int Gfull = L / kNrSteps;
+  for (int g = 0; g < G; ++g) {
+    ring_barrier();
+    const unsigned char* slot = ring + (g % kNrSlots) * SLOTB + lane * 4;
+    const unsigned* mslot = mring[g % kNrSlots];
+    auto rd = [&](int q, int st) {
+      return *reinterpret_cast<const float*>(slot + q * SEGB + st * STEPB);
+    };
+    if (g < Gfull) {
+#pragma unroll
+      for (int st = 0; st < kNrSteps; ++st)
+        step(rd(0, st), rd(1, st), rd(2, st), rd(3, st), MASK ? (mslot[st] & 0xFFu) : 0u);
+    } else {
+#pragma unroll
+      for (int st = 0; st < kNrSteps; ++st)
+        if (g * kNrSteps + st < L)
+          step(rd(0, st), rd(1, st), rd(2, st), rd(3, st), MASK ? (mslot[st] & 0xFFu) : 0u);
+    }
+  }
+  if (a.c_last) a.c_last[gid] = c;
+}
+
 template <int KB, bool MASK, bool DUB, bool RN, int PF>
 __global__ __launch_bounds__(kScanThreads) void scan_bwd_kernel(ScanShape s, ScanBwdArgs a) {
   Lane ln;
@@ -1180,12 +1334,35 @@ bool ring_ok(const ScanShape& s, long long u_bytes, long long x_bytes) {
          (long long)s.L * s.B < (long long)kRingOOB;
 }
 
+// Where the narrow LDS ring runs: fewer lanes than one wave per SIMD (there
+// each step of the register-ring scan waits on the one before), whole groups
+// of 64 units, operands inside the 2 GiB range of buffer offsets.
+bool nring_ok(const ScanShape& s, long long u_bytes, long long x_bytes) {
+  const long long lanes = (long long)s.B * s.ndir * s.d;
+  return !s.linear && s.d % kNrUnits == 0 && lanes < kFullLanes &&
+         u_bytes < (long long)kRingOOB && x_bytes < (long long)kRingOOB &&
+         (long long)s.L * s.B < (long long)kRingOOB;
+}
+
 template <int KB, bool MASK, bool STORE_C, bool STORE_HB>
 hipError_t fwd_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st) {
   const int lanes = s.B * s.ndir * s.d;
   const int grid = (lanes + kScanThreads - 1) / kScanThreads;
   const long long u_bytes = 4LL * s.L * s.B * s.ndir * KB * s.d;
   const long long x_bytes = KB == 3 ? 4LL * s.L * s.B * s.d_in : 0;
+  if (nring_ok(s, u_bytes, x_bytes)) {
+    const int ngrid = s.B * s.ndir * (s.d / kNrUnits);
+    const unsigned m_bytes = (unsigned)((long long)s.L * s.B);
+    timing_before("scan_fwd", st);
+    if (s.reset_new)
+      hipLaunchKernelGGL((scan_fwd_nring_kernel<KB, MASK, STORE_C, STORE_HB, true>), dim3(ngrid),
+                         dim3(128), 0, st, s, a, (unsigned)u_bytes, (unsigned)x_bytes, m_bytes);
+    else
+      hipLaunchKernelGGL((scan_fwd_nring_kernel<KB, MASK, STORE_C, STORE_HB, false>), dim3(ngrid),
+                         dim3(128), 0, st, s, a, (unsigned)u_bytes, (unsigned)x_bytes, m_bytes);
+    timing_after(st);
+    return hipGetLastError();
+  }
   if (ring_ok(s, u_bytes, x_bytes)) {
     const int rgrid = s.B * s.ndir * (s.d / kRingUnits);
     const unsigned m_bytes = (unsigned)((long long)s.L * s.B);
