@@ -473,10 +473,11 @@ __global__ __launch_bounds__(128) void scan_fwd_nring_kernel(ScanShape s, ScanFw
     } else {
       c = cn;
     }
-    // plain stores, as in the register-ring scan at few lanes
-    *hp = h;
-    if constexpr (STORE_C) *cp = c;
-    if constexpr (STORE_HB) *hbp = __builtin_bit_cast(uint16_t, (__bf16)h);
+    // non-temporal stores: the consumer never waits for them (plain ones
+    // measured 2-3 % slower here)
+    __builtin_nontemporal_store(h, hp);
+    if constexpr (STORE_C) __builtin_nontemporal_store(c, cp);
+    if constexpr (STORE_HB) __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, (__bf16)h), hbp);
     hp += sh;
     if constexpr (STORE_C) cp += sh;
     if constexpr (STORE_HB) hbp += sh;
