@@ -1351,7 +1351,11 @@ hipError_t fwd_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st
   const int grid = (lanes + kScanThreads - 1) / kScanThreads;
   const long long u_bytes = 4LL * s.L * s.B * s.ndir * KB * s.d;
   const long long x_bytes = KB == 3 ? 4LL * s.L * s.B * s.d_in : 0;
-  if (nring_ok(s, u_bytes, x_bytes)) {
+  // the LDS rings load 16 bytes per lane from U and x: their bases must be
+  // 16-byte aligned (the interface asks 4 bytes of fp32 tensors)
+  auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  const bool al = al16(a.U) && (KB != 3 || al16(a.X));
+  if (al && nring_ok(s, u_bytes, x_bytes)) {
     const int ngrid = s.B * s.ndir * (s.d / kNrUnits);
     const unsigned m_bytes = (unsigned)((long long)s.L * s.B);
     timing_before("scan_fwd", st);
@@ -1364,7 +1368,7 @@ hipError_t fwd_dispatch(const ScanShape& s, const ScanFwdArgs& a, hipStream_t st
     timing_after(st);
     return hipGetLastError();
   }
-  if (ring_ok(s, u_bytes, x_bytes)) {
+  if (al && ring_ok(s, u_bytes, x_bytes)) {
     const int rgrid = s.B * s.ndir * (s.d / kRingUnits);
     const unsigned m_bytes = (unsigned)((long long)s.L * s.B);
     timing_before("scan_fwd", st);

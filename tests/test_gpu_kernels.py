@@ -199,6 +199,31 @@ def test_scan_backward_on_oracle_states(case):
         check(k, out[k], bw[k], TOL_FP32)
 
 
+@pytest.mark.parametrize("L,B,d", [(20, 8, 1024), (9, 64, 1024)])
+def test_scan_forward_on_unaligned_inputs(L, B, d):
+    """U and x need only 4-byte alignment.  The LDS-ring scans (8,192 lanes:
+    the narrow ring; 65,536: the wide one) load 16 bytes per lane, so inputs
+    that start 4 bytes past a 16-byte boundary take the register-ring scan;
+    the results are the same bits."""
+    print(f"scan_fwd unaligned L={L} B={B} d={d}", flush=True)
+    c = _case(L + B + d, L, B, d, d, O.DIR_FWD, masked=True, c0=True, bias_scale=0.5)
+    U = torch.randn(L, B, 1, 3, d, device="cuda")
+    X = dev(c["X"])
+    p = [dev(c[k]) for k in ("v_f", "v_r", "b_f", "b_r")]
+    def shifted(t):
+        buf = torch.empty(t.numel() + 1, device="cuda")
+        v = buf[1:].view(t.shape)
+        v.copy_(t)
+        return v
+    Us, Xs = shifted(U), shifted(X)
+    assert Us.data_ptr() % 16 == 4 and Xs.data_ptr() % 16 == 4
+    a = sru.scan_forward(U, X, *p, dev(c["c0"]), O.DIR_FWD, dev(c["mask"]))
+    b = sru.scan_forward(Us, Xs, *p, dev(c["c0"]), O.DIR_FWD, dev(c["mask"]))
+    torch.cuda.synchronize()
+    for k in ("H", "C", "c_last"):
+        assert torch.equal(a[k], b[k]), k
+
+
 def test_scan_saturation_exact_and_finite():
     """b_f = +100 keeps c = c0 exactly; b_f = -100 gives c = u0 exactly;
     b_r = +100 gives h = c exactly; no NaN anywhere (sigma saturates)."""
